@@ -1,0 +1,257 @@
+#!/usr/bin/env python3
+"""Benchmark of the three-stage W4A16 decoder layer on one MI355X.
+
+One step = the whole hot path once on the Llama-3-8B-shaped layer (hidden 4096,
+32/8 heads, head_dim 128, FFN 14336, W4A16 group 128, RoPE base 5e5):
+    prefill     T = 512 tokens
+    prefill_kv  T = 128 new tokens over a 1024-token history
+    decode      B = 1 at context 2048
+The steps rotate over several device copies of the layer (each with its own
+KV cache) so that the working set exceeds the 256 MB Infinity Cache and the
+weights stream from HBM, as they do across the layers of a real model.
+
+Printed: one JSON line.  ``value`` is decode layer-steps/s (the stage the
+paper measures); prefill and prefill_kv TFLOP/s are under ``stages``.  The
+roofline object covers the kernel that takes the largest share of a step (the
+prefill gate/up GEMM); the decode gate/up GEMV is reported beside it.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0            # MI355X HBM3E
+PEAK_MFMA_TFLOPS = 2500.0        # dense bf16 / fp16 MFMA
+
+WORKLOAD = dict(name="llama8b", prefill_T=512, pkv_T=128, pkv_L=1024, decode_B=1, decode_ctx=2048)
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+# ---------------------------------------------------------------- algorithmic work
+
+def linear_shapes(cfg):
+    from paper_2607_15865_amd import synth
+    return [cfg.linear_shape(n) for n in synth.LINEARS]
+
+
+def weight_bytes(cfg, names=None):
+    from paper_2607_15865_amd import synth
+    tot = 0
+    for n in (names or synth.LINEARS):
+        K, N = cfg.linear_shape(n)
+        tot += N * K // 2 + 2 * N * math.ceil(K / cfg.group_size)
+    return tot
+
+
+def stage_flops(cfg, M, T, L, B):
+    """2 * rows * weights of the seven linears + attention on causal pairs."""
+    params = sum(K * N for K, N in linear_shapes(cfg))
+    attn = 4 * cfg.head_dim * cfg.n_heads * B * (T * L + T * (T + 1) / 2)
+    return 2 * M * params + attn
+
+
+def stage_bytes(cfg, M, T, L, B):
+    """Weights (int4 + fp16 scales) + norm weights + KV read of the history
+    and the new entries + KV write + fp32 hidden states in and out."""
+    kv_row = 2 * 2 * cfg.n_kv_heads * cfg.head_dim          # K and V, bf16
+    return (weight_bytes(cfg) + 4 * cfg.hidden + kv_row * B * (L + T) + kv_row * B * T
+            + 8 * M * cfg.hidden)
+
+
+# ---------------------------------------------------------------- CPU baseline
+
+def cpu_baseline(cfg, w):
+    """The oracle as it stands, one decode layer-step on this workload."""
+    import numpy as np
+    from oracle import layer as O
+    from paper_2607_15865_amd import synth
+    threads = None
+    try:
+        import threadpoolctl
+        info = threadpoolctl.threadpool_info()
+        threads = max([i.get("num_threads", 1) for i in info] or [1])
+    except Exception:
+        pass
+    ctx = WORKLOAD["decode_ctx"]
+    rng = np.random.default_rng(0)
+    kc = O.bf16_to_f64(synth.bf16_bits(rng.standard_normal((1, cfg.n_kv_heads, ctx + 1, cfg.head_dim))))
+    vc = O.bf16_to_f64(synth.bf16_bits(rng.standard_normal((1, cfg.n_kv_heads, ctx + 1, cfg.head_dim))))
+    x = O.bf16_to_f64(synth.activations(cfg, synth.TID_X_DECODE, 1))
+    t0 = time.perf_counter()
+    O.decode(w, cfg, x, [ctx], kc, vc, [ctx])
+    dt = time.perf_counter() - t0
+    return {"value": 1.0 / dt, "unit": "layer-steps/s", "cores": threads or os.cpu_count(),
+            "kind": "oracle",
+            "sample": f"1 decode layer-step of the {WORKLOAD['name']}-shaped layer at context {ctx}, B=1, "
+                      f"fp64 numpy including the oracle's per-call weight dequantisation ({dt:.1f} s)"}
+
+
+# ---------------------------------------------------------------- main
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--copies", type=int, default=8, help="device copies of the layer (rotation)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: the layer's single-GPU kernels; --gpus {args.gpus} is not supported "
+              "(multi-GPU sharding is described in DESIGN.md, not built)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    from paper_2607_15865_amd import binding, synth
+
+    cfg = synth.CONFIGS[WORKLOAD["name"]]
+    Tp, Tk, Lk = WORKLOAD["prefill_T"], WORKLOAD["pkv_T"], WORKLOAD["pkv_L"]
+    Bd, ctx = WORKLOAD["decode_B"], WORKLOAD["decode_ctx"]
+    log(f"bench: generating the {cfg.name} layer")
+    w = synth.make_layer(cfg)
+    layers, caches = [], []
+    kb, vb = synth.kv_fill(cfg, 1)
+    for i in range(args.copies):
+        layers.append(binding.Layer(cfg, w))
+        k = torch.from_numpy(kb.view(np.int16)).cuda()
+        v = torch.from_numpy(vb.view(np.int16)).cuda()
+        caches.append((k, v))
+    log(f"bench: {args.copies} device copies created")
+
+    def f32(bits):
+        u = bits.astype(np.uint32) << 16
+        return torch.from_numpy(u.view(np.float32).copy()).cuda()
+
+    xp = f32(synth.activations(cfg, synth.TID_X_PREFILL, Tp))
+    xk = f32(synth.activations(cfg, synth.TID_X_PREFILL_KV, Tk))
+    xd = f32(synth.activations(cfg, synth.TID_X_DECODE, Bd))
+    yp, yk, yd = torch.empty_like(xp), torch.empty_like(xk), torch.empty_like(xd)
+    pp = torch.arange(Tp, dtype=torch.int32, device="cuda")
+    pk = torch.arange(Lk, Lk + Tk, dtype=torch.int32, device="cuda")
+    pd = torch.full((Bd,), ctx, dtype=torch.int32, device="cuda")
+    cd = torch.full((Bd,), ctx, dtype=torch.int32, device="cuda")
+    ws_bytes = max(binding.layer_workspace_size(layers[0].handle, 0, 1, Tp, 0),
+                   binding.layer_workspace_size(layers[0].handle, 1, 1, Tk, Lk),
+                   binding.layer_workspace_size(layers[0].handle, 2, Bd, 1, ctx))
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.current_stream()
+    sp = stream.cuda_stream
+
+    PREFILL_GU, DECODE_GU = 5, 4
+
+    def step(i, ev=None):
+        lay = layers[i % len(layers)].handle
+        k, v = caches[i % len(layers)]
+        if ev: ev[0].record(stream)
+        binding.check(binding.layer_prefill(lay, xp, pp, Tp, k, v, yp, ws, ws_bytes, sp))
+        if ev: ev[1].record(stream)
+        binding.check(binding.layer_prefill_kv(lay, xk, pk, Tk, Lk, k, v, yk, ws, ws_bytes, sp))
+        if ev: ev[2].record(stream)
+        binding.check(binding.layer_decode(lay, xd, pd, cd, ctx, None, Bd, k, v, yd, ws, ws_bytes, sp))
+        if ev: ev[3].record(stream)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    log(f"bench: {args.warmup} warmup steps done")
+
+    for lay in layers:
+        binding.check(binding.layer_profile_kernel(lay.handle, 0, PREFILL_GU))
+        binding.check(binding.layer_profile_kernel(lay.handle, 2, DECODE_GU))
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(i, evs[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    log(f"bench: {args.steps} timed steps in {wall:.3f} s")
+
+    st_ms = np.zeros(3)
+    for e in evs:
+        for j in range(3):
+            st_ms[j] += e[j].elapsed_time(e[j + 1])
+    st_ms /= args.steps
+    gu_ms, gu_n, dgu_ms, dgu_n = 0.0, 0, 0.0, 0
+    for lay in layers:
+        rc, ms, n = binding.layer_profile_read(lay.handle, 0)
+        binding.check(rc)
+        gu_ms += ms; gu_n += n
+        rc, ms, n = binding.layer_profile_read(lay.handle, 2)
+        binding.check(rc)
+        dgu_ms += ms; dgu_n += n
+        binding.layer_profile_kernel(lay.handle, 0, -1)
+        binding.layer_profile_kernel(lay.handle, 2, -1)
+
+    fl_p = stage_flops(cfg, Tp, Tp, 0, 1)
+    fl_k = stage_flops(cfg, Tk, Tk, Lk, 1)
+    by_d = stage_bytes(cfg, Bd, 1, ctx, Bd)
+    dec_s = st_ms[2] * 1e-3
+    stages = {
+        "prefill": {"T": Tp, "ms": round(st_ms[0], 4), "gflop": round(fl_p / 1e9, 2),
+                    "tflops": round(fl_p / (st_ms[0] * 1e-3) / 1e12, 1),
+                    "frac_mfma": round(fl_p / (st_ms[0] * 1e-3) / 1e12 / PEAK_MFMA_TFLOPS, 4)},
+        "prefill_kv": {"T": Tk, "hist": Lk, "ms": round(st_ms[1], 4), "gflop": round(fl_k / 1e9, 2),
+                       "tflops": round(fl_k / (st_ms[1] * 1e-3) / 1e12, 1),
+                       "frac_mfma": round(fl_k / (st_ms[1] * 1e-3) / 1e12 / PEAK_MFMA_TFLOPS, 4)},
+        "decode": {"B": Bd, "ctx": ctx, "us": round(st_ms[2] * 1e3, 2), "mbytes": round(by_d / 1e6, 2),
+                   "layer_steps_per_s": round(1.0 / dec_s, 1),
+                   "gbps": round(by_d / dec_s / 1e9, 1),
+                   "frac_hbm": round(by_d / dec_s / 1e9 / PEAK_HBM_GBS, 4)},
+    }
+    gu_flop = 2.0 * Tp * cfg.hidden * 2 * cfg.ffn
+    gu_avg = gu_ms / max(gu_n, 1)
+    roofline = {"kernel": "prefill gate/up W4 GEMM (512 x 28672 x 4096, SwiGLU epilogue)",
+                "bound": "mfma", "achieved": round(gu_flop / (gu_avg * 1e-3) / 1e12, 1),
+                "peak": PEAK_MFMA_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(gu_flop / (gu_avg * 1e-3) / 1e12 / PEAK_MFMA_TFLOPS, 4),
+                "avg_us": round(gu_avg * 1e3, 2), "launches": gu_n, "traffic": None}
+    dgu_bytes = weight_bytes(cfg, ["gate", "up"])
+    dgu_avg = dgu_ms / max(dgu_n, 1)
+    roofline_decode = {"kernel": "decode gate/up W4 GEMV (1 x 28672 x 4096, RMSNorm prologue)",
+                       "bound": "hbm", "achieved": round(dgu_bytes / (dgu_avg * 1e-3) / 1e9, 1),
+                       "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                       "frac": round(dgu_bytes / (dgu_avg * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+                       "avg_us": round(dgu_avg * 1e3, 2), "launches": dgu_n, "traffic": None}
+    out = {
+        "metric": "decode layer-steps/s (+ prefill/prefill_kv TFLOP/s) of a W4A16 Llama-3-8B-shaped layer",
+        "value": round(1.0 / dec_s, 1),
+        "unit": "layer-steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(wall * 1e3 / args.steps, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "llama8b-shaped W4A16 layer: prefill T=512; prefill_kv T=128 over 1024; "
+                               "decode B=1 at ctx 2048",
+                   "hidden": cfg.hidden, "heads": f"{cfg.n_heads}/{cfg.n_kv_heads}", "head_dim": cfg.head_dim,
+                   "ffn": cfg.ffn, "group": cfg.group_size, "rotation_copies": args.copies},
+        "stages": stages,
+        "roofline": roofline,
+        "roofline_decode": roofline_decode,
+    }
+    if not args.no_cpu_baseline:
+        log("bench: timing the CPU oracle (one decode layer-step)")
+        out["cpu_baseline"] = cpu_baseline(cfg, w)
+    print(json.dumps(out), flush=True)
+    for lay in layers:
+        lay.close()
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,230 @@
+/*
+ * w4layer.h -- C ABI of the MI355X (gfx950) three-stage W4A16 decoder layer.
+ *
+ * One Transformer decoder block (RMSNorm, q/k/v projections, RoPE from a
+ * precomputed cos/sin table, grouped-query causal attention, o_proj +
+ * residual, RMSNorm, SwiGLU MLP + residual; Sec. 3.1, Listings 1-2 of the
+ * paper) with 4-bit group-quantised weights and bf16 activations (W4BF16,
+ * Sec. 5.1), statically specialised into the paper's three stages
+ * (Sec. 4.1, Table 1):
+ *
+ *   layer_prefill     a whole prompt, no history             (Sec. 4.2)
+ *   layer_prefill_kv  a new chunk after a history cache       (Sec. 4.3)
+ *   layer_decode      one token per sequence against a cache  (Sec. 4.4)
+ *
+ * plus the KV-cache calls kv_layout / kv_append (the in-place Concat of
+ * Sec. 4.6.3).
+ *
+ * Conventions shared by every call
+ *   - Return value 0 on success, a negative W4_E* code on failure; the
+ *     message of the last failure on the calling thread is layer_last_error().
+ *   - Arguments are validated on the host before any HIP call; a call that
+ *     fails validation has launched nothing and touched no buffer.
+ *   - Pointers documented as "device" are HIP device pointers on the current
+ *     device; "host" pointers are ordinary host memory.
+ *   - Stage calls are asynchronous on the given stream (a hipStream_t passed
+ *     as void*, NULL = default stream), allocate nothing and do not
+ *     synchronise.  The caller owns every buffer it passes and must keep it
+ *     alive until the stream has drained.
+ *   - Device-side values (positions, context lengths) are trusted: an
+ *     out-of-range value there is undefined behaviour.
+ *
+ * Numerics
+ *   - Hidden states x and y are fp32 (the block interface of Listing 3 is f32);
+ *     the residual stream is never rounded.
+ *   - The block's intermediate activations -- the normalised matmul inputs,
+ *     q/k after RoPE, v, the attention output and the MLP hidden
+ *     activation -- are rounded once to bf16 (round to nearest even), which
+ *     is the W4BF16 precision; the K/V cache holds bf16.
+ *   - Weights are used exactly: W[k][n] = s[k/G][n] * (q[k][n] - z), sums in
+ *     fp32.
+ */
+#ifndef W4LAYER_H
+#define W4LAYER_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- error codes --------------------------------------------------------- */
+#define W4_OK             0
+#define W4_EINVAL        -1  /* null pointer, bad dimension or argument      */
+#define W4_EUNSUPPORTED  -2  /* shape or device this library does not handle */
+#define W4_ECAPACITY     -3  /* would exceed max_seq or max_batch             */
+#define W4_EWORKSPACE    -4  /* workspace missing or smaller than required   */
+#define W4_EHIP          -5  /* a HIP runtime call or launch failed          */
+
+/* ---- types ---------------------------------------------------------------- */
+
+/* Shape of one decoder layer.  Supported: head_dim 64 or 128; n_heads a
+ * multiple of n_kv_heads; group_size in {32, 64, 128, 256}; hidden a multiple
+ * of 128 and of group_size; n_heads*head_dim a multiple of 128 and of
+ * group_size; ffn a multiple of 8; max_seq >= 1; 1 <= max_batch <= 64.
+ * rms_eps is added inside the square root of RMSNorm; RoPE uses the
+ * rotate-half pairing (i, i + head_dim/2) with angle pos * rope_base^(-2i/d). */
+typedef struct layer_config {
+    int32_t hidden;
+    int32_t n_heads;
+    int32_t n_kv_heads;
+    int32_t head_dim;
+    int32_t ffn;
+    int32_t group_size;
+    float   rms_eps;
+    float   rope_base;
+    int32_t max_seq;     /* capacity of the KV cache and of the RoPE table */
+    int32_t max_batch;   /* largest decode batch                            */
+} layer_config;
+
+/* One quantised linear y[M][N] = x[M][K] * W[K][N] in the canonical
+ * GPTQ-style format that the paper compiles straight through (Sec. 3.2).
+ * All pointers are host pointers, read only during layer_create.
+ *   qweight  int32 [K/8][N]: code k = 8r + j of column n in bits 4j..4j+3 of
+ *            word [r][n];
+ *   scales   fp16 bit patterns [ceil(K/G)][N]: scale of group g = k / G;
+ *   zeros    uint8 [ceil(K/G)][N] zero points in 0..15, or NULL for 8. */
+typedef struct qlinear_host {
+    const int32_t*  qweight;
+    const uint16_t* scales;
+    const uint8_t*  zeros;
+} qlinear_host;
+
+/* All weights of one layer (host pointers).  K x N of each linear, with
+ * H = hidden, Q = n_heads*head_dim, V = n_kv_heads*head_dim, F = ffn:
+ * q: H x Q, k: H x V, v: H x V, o: Q x H, gate: H x F, up: H x F, down: F x H.
+ * attn_norm / mlp_norm: bf16 bit patterns [hidden] (the RMSNorm weights). */
+typedef struct layer_weights_host {
+    const uint16_t* attn_norm;
+    const uint16_t* mlp_norm;
+    qlinear_host q, k, v, o, gate, up, down;
+} layer_weights_host;
+
+typedef struct layer_s* layer_t;
+
+/* Layout of a K or V cache: bf16 [batch][n_kv_heads][max_seq][head_dim],
+ * strides in elements (stride of head_dim is 1), bytes = size of one cache. */
+typedef struct kv_desc {
+    int32_t batch;
+    int32_t n_kv_heads;
+    int32_t max_seq;
+    int32_t head_dim;
+    int64_t stride_b;
+    int64_t stride_h;
+    int64_t stride_s;
+    size_t  bytes;
+} kv_desc;
+
+/* ---- lifetime ------------------------------------------------------------ */
+
+/* Validate cfg, repack the host weights into the private device layout,
+ * upload them and the fp32 cos/sin table (max_seq x head_dim/2, computed in
+ * double precision on the host: the table of Sec. 4.6.2) to the current
+ * device.  Synchronous.  On success *out owns all device memory of the layer;
+ * the handle is immutable afterwards, so stage calls on different streams
+ * may share it.  Errors: W4_EINVAL (null), W4_EUNSUPPORTED (shape, or the
+ * current device is not gfx950), W4_EHIP (allocation or copy failed). */
+int layer_create(const layer_config* cfg, const layer_weights_host* w, layer_t* out);
+
+/* Free the layer's device memory.  The caller must have drained every stream
+ * that uses it.  NULL is accepted.  Synchronous. */
+int layer_destroy(layer_t layer);
+
+/* The KV-cache layout for a batch of sequences (pure host computation). */
+int kv_layout(const layer_config* cfg, int32_t batch, kv_desc* out);
+
+/* Bytes of device workspace a stage call needs: stage 0 prefill (batch 1,
+ * T tokens), 1 prefill_kv (batch 1, T tokens, history up to max_ctx), 2
+ * decode (batch sequences, context up to max_ctx).  Returns 0 for invalid
+ * arguments. */
+size_t layer_workspace_size(layer_t layer, int32_t stage, int32_t batch, int32_t T, int32_t max_ctx);
+
+/* ---- the three stages (all device pointers; asynchronous on stream) ---- */
+
+/* Prefill (Sec. 4.2): T >= 1 prompt tokens of one sequence, no history.
+ *   x        fp32 [T][hidden] hidden states in;
+ *   pos      int32 [T] position_ids (RoPE angles), 0 <= pos < max_seq;
+ *   k_cache, v_cache  bf16 [n_kv_heads][max_seq][head_dim] of this sequence
+ *            (batch entry of a kv_layout cache); slots 0..T-1 are written,
+ *            no other slot is touched;
+ *   y        fp32 [T][hidden] out (must not alias x);
+ *   ws       workspace of at least layer_workspace_size(layer, 0, 1, T, 0).
+ * Errors: W4_EINVAL, W4_ECAPACITY (T > max_seq), W4_EWORKSPACE, W4_EHIP. */
+int layer_prefill(layer_t layer, const float* x, const int32_t* pos, int32_t T,
+                  void* k_cache, void* v_cache, float* y,
+                  void* ws, size_t ws_bytes, void* stream);
+
+/* Prefill_kv (Sec. 4.3): T >= 1 new tokens after hist_len >= 0 cached ones.
+ * Reads cache slots 0..hist_len-1, writes slots hist_len..hist_len+T-1, and
+ * the new token t attends to slots 0..hist_len+t.  With hist_len = 0 this is
+ * exactly layer_prefill.  Other arguments as for layer_prefill; ws of at
+ * least layer_workspace_size(layer, 1, 1, T, hist_len).
+ * Errors: as layer_prefill, W4_ECAPACITY if hist_len + T > max_seq. */
+int layer_prefill_kv(layer_t layer, const float* x, const int32_t* pos, int32_t T, int32_t hist_len,
+                     void* k_cache, void* v_cache, float* y,
+                     void* ws, size_t ws_bytes, void* stream);
+
+/* Decode (Sec. 4.4): one new token for each of B sequences.
+ *   x         fp32 [B][hidden];
+ *   pos       int32 [B] position ids;
+ *   ctx_lens  int32 [B] device: cached tokens of sequence b; its new token
+ *             is written to slot ctx_lens[b] and attends to slots
+ *             0..ctx_lens[b]; every ctx_lens[b] must be <= max_ctx;
+ *   max_ctx   host upper bound of ctx_lens, max_ctx + 1 <= max_seq;
+ *   attn_mask fp32 [B][max_seq] device, added to the score of slot j (0 to
+ *             attend, -inf to mask), or NULL for none; a row whose visible
+ *             slots are all -inf produces a zero attention output;
+ *   k_cache, v_cache  bf16 caches in the kv_layout(cfg, B) layout;
+ *   y         fp32 [B][hidden] out;
+ *   ws        at least layer_workspace_size(layer, 2, B, 1, max_ctx).
+ * Errors: W4_EINVAL, W4_ECAPACITY (B > max_batch or max_ctx + 1 > max_seq),
+ * W4_EWORKSPACE, W4_EHIP. */
+int layer_decode(layer_t layer, const float* x, const int32_t* pos, const int32_t* ctx_lens,
+                 int32_t max_ctx, const float* attn_mask, int32_t B,
+                 void* k_cache, void* v_cache, float* y,
+                 void* ws, size_t ws_bytes, void* stream);
+
+/* ---- KV cache -------------------------------------------------------------- */
+
+/* In-place Concat (Sec. 4.6.3): copy new keys/values k_new, v_new (bf16
+ * [B][T][n_kv_heads][head_dim], device) into cache slots
+ * slot_start[b] .. slot_start[b]+T-1 of sequence b (caches in the layout of
+ * *desc).  slot_start is a host array [B].  Bit-exact copy; no other slot is
+ * touched.  Errors: W4_EINVAL, W4_ECAPACITY (slot range outside the cache or
+ * B > desc->batch), W4_EHIP. */
+int kv_append(const kv_desc* desc, void* k_cache, void* v_cache,
+              const void* k_new, const void* v_new, int32_t B, int32_t T,
+              const int32_t* slot_start, void* stream);
+
+/* ---- diagnostics ------------------------------------------------------- */
+
+/* Dequantise linear `which` (0..6 = q, k, v, o, gate, up, down) from the
+ * device copy of the weights into out, fp32 [K][N] device, in the order of
+ * the canonical format: out[k][n] = s[k/G][n] * (q[k][n] - z).  Exact (the
+ * product fits fp32).  Uses the same unpacking code as the stage kernels.
+ * Errors: W4_EINVAL, W4_EHIP. */
+int layer_debug_dequant(layer_t layer, int32_t which, float* out, void* stream);
+
+/* Per-kernel timing for measurement (diagnostics, not for concurrent use).
+ * layer_profile_kernel selects, for one stage, the kernel to time (stage 0 and
+ * 1, prefill and prefill_kv: 0 rmsnorm, 1 qkv GEMM, 2 attention, 3 o_proj
+ * GEMM, 4 rmsnorm, 5 gate/up GEMM, 6 down GEMM; stage 2, decode: 0 qkv GEMV,
+ * 1 attention (split + combine), 3 o_proj GEMV, 4 gate/up GEMV, 5 down GEMV);
+ * kernel < 0 switches timing of that stage off.  While selected, each stage
+ * call records a HIP event pair around that launch on the call's stream (at
+ * most 4096 pairs per stage until the next read).  layer_profile_read waits
+ * for the recorded events of a stage, returns the summed duration in
+ * *total_ms and the number of timed launches in *launches, and clears the
+ * record.  A layer_prefill_kv call with hist_len 0 counts as stage 0.
+ * Errors: W4_EINVAL, W4_EHIP. */
+int layer_profile_kernel(layer_t layer, int32_t stage, int32_t kernel);
+int layer_profile_read(layer_t layer, int32_t stage, float* total_ms, int32_t* launches);
+
+/* Message of the last failed call on this thread ("" if none). */
+const char* layer_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* W4LAYER_H */

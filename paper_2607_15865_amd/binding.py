@@ -1,0 +1,286 @@
+"""Thin ctypes binding of libw4layer.so (include/w4layer.h).
+
+Argument marshalling only: every step of the layer runs in the HIP kernels of
+the library.  Tensors are torch tensors on the GPU (PyTorch provides device
+memory and streams); the functions keep the C names and return the C status
+codes, and ``check`` turns a non-zero code into a ``W4Error``.
+
+Importing this module loads the library and raises if it is missing: there is
+no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+from typing import Optional
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libw4layer.so")
+HEADER = os.path.join(os.path.dirname(HERE), "include", "w4layer.h")
+
+W4_OK, W4_EINVAL, W4_EUNSUPPORTED, W4_ECAPACITY, W4_EWORKSPACE, W4_EHIP = 0, -1, -2, -3, -4, -5
+STAGE_PREFILL, STAGE_PREFILL_KV, STAGE_DECODE = 0, 1, 2
+LINEAR_INDEX = {"q": 0, "k": 1, "v": 2, "o": 3, "gate": 4, "up": 5, "down": 6}
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"{LIB_PATH} is not built; run python -m paper_2607_15865_amd.build "
+                      "(the layer has no CPU fallback)")
+# torch ships its own HIP runtime under the same soname (libamdhip64.so.7) as
+# the system one the library links; whichever loads first serves the whole
+# process.  Load torch's first so that torch and the library share it.
+import torch  # noqa: E402,F401
+
+_lib = ctypes.CDLL(LIB_PATH)
+
+
+class W4Error(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"w4layer error {code}: {msg}")
+        self.code = code
+
+
+class layer_config(ctypes.Structure):
+    _fields_ = [("hidden", ctypes.c_int32), ("n_heads", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("ffn", ctypes.c_int32), ("group_size", ctypes.c_int32),
+                ("rms_eps", ctypes.c_float), ("rope_base", ctypes.c_float),
+                ("max_seq", ctypes.c_int32), ("max_batch", ctypes.c_int32)]
+
+
+class qlinear_host(ctypes.Structure):
+    _fields_ = [("qweight", ctypes.c_void_p), ("scales", ctypes.c_void_p), ("zeros", ctypes.c_void_p)]
+
+
+class layer_weights_host(ctypes.Structure):
+    _fields_ = [("attn_norm", ctypes.c_void_p), ("mlp_norm", ctypes.c_void_p)] + \
+               [(n, qlinear_host) for n in ("q", "k", "v", "o", "gate", "up", "down")]
+
+
+class kv_desc(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32), ("max_seq", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("stride_b", ctypes.c_int64), ("stride_h", ctypes.c_int64),
+                ("stride_s", ctypes.c_int64), ("bytes", ctypes.c_size_t)]
+
+
+_P = ctypes.c_void_p
+_I = ctypes.c_int32
+_SIG = {
+    "layer_create": (ctypes.c_int, [ctypes.POINTER(layer_config), ctypes.POINTER(layer_weights_host), ctypes.POINTER(_P)]),
+    "layer_destroy": (ctypes.c_int, [_P]),
+    "kv_layout": (ctypes.c_int, [ctypes.POINTER(layer_config), _I, ctypes.POINTER(kv_desc)]),
+    "layer_workspace_size": (ctypes.c_size_t, [_P, _I, _I, _I, _I]),
+    "layer_prefill": (ctypes.c_int, [_P, _P, _P, _I, _P, _P, _P, _P, ctypes.c_size_t, _P]),
+    "layer_prefill_kv": (ctypes.c_int, [_P, _P, _P, _I, _I, _P, _P, _P, _P, ctypes.c_size_t, _P]),
+    "layer_decode": (ctypes.c_int, [_P, _P, _P, _P, _I, _P, _I, _P, _P, _P, _P, ctypes.c_size_t, _P]),
+    "kv_append": (ctypes.c_int, [ctypes.POINTER(kv_desc), _P, _P, _P, _P, _I, _I, _P, _P]),
+    "layer_debug_dequant": (ctypes.c_int, [_P, _I, _P, _P]),
+    "layer_profile_kernel": (ctypes.c_int, [_P, _I, _I]),
+    "layer_profile_read": (ctypes.c_int, [_P, _I, ctypes.POINTER(ctypes.c_float), ctypes.POINTER(ctypes.c_int32)]),
+    "layer_last_error": (ctypes.c_char_p, []),
+}
+for _name, (_res, _args) in _SIG.items():
+    _f = getattr(_lib, _name)
+    _f.restype = _res
+    _f.argtypes = _args
+
+
+def declared_functions() -> list:
+    """Names of the functions include/w4layer.h declares."""
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[\w]+\s*\**\s+\**(\w+)\s*\(", text, flags=re.M)))
+
+
+def exported(name: str) -> bool:
+    try:
+        getattr(_lib, name)
+        return True
+    except AttributeError:
+        return False
+
+
+def layer_last_error() -> str:
+    return (_lib.layer_last_error() or b"").decode()
+
+
+def check(rc: int) -> int:
+    if rc != W4_OK:
+        raise W4Error(rc, layer_last_error())
+    return rc
+
+
+def make_config(cfg) -> layer_config:
+    """layer_config from any object with the LayerConfig attribute names."""
+    return layer_config(cfg.hidden, cfg.n_heads, cfg.n_kv_heads, cfg.head_dim, cfg.ffn, cfg.group_size,
+                        cfg.rms_eps, cfg.rope_base, cfg.max_seq, cfg.max_batch)
+
+
+def _ptr(t) -> Optional[int]:
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    if isinstance(t, np.ndarray):
+        return t.ctypes.data
+    return t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+# ------------------------------------------------------------ C-named calls
+
+def layer_create(cfg, weights: dict):
+    """weights: the canonical host format (numpy arrays): for each linear a
+    dict with qweight int32 [K/8][N], scales fp16 [ceil(K/G)][N], optional
+    zeros uint8; attn_norm / mlp_norm bf16 bit patterns (uint16)."""
+    keep = []
+
+    def arr(a, dtype):
+        a = np.ascontiguousarray(a)
+        if a.dtype != dtype:
+            a = a.view(dtype) if a.dtype.itemsize == np.dtype(dtype).itemsize else a.astype(dtype)
+        keep.append(a)
+        return a.ctypes.data
+
+    wh = layer_weights_host()
+    wh.attn_norm = arr(weights["attn_norm"], np.uint16)
+    wh.mlp_norm = arr(weights["mlp_norm"], np.uint16)
+    for name in ("q", "k", "v", "o", "gate", "up", "down"):
+        lin = weights[name]
+        z = lin.get("zeros")
+        setattr(wh, name, qlinear_host(arr(lin["qweight"], np.int32), arr(lin["scales"], np.uint16),
+                                       None if z is None else arr(z, np.uint8)))
+    c = make_config(cfg)
+    h = _P()
+    rc = _lib.layer_create(ctypes.byref(c), ctypes.byref(wh), ctypes.byref(h))
+    return rc, h.value
+
+
+def layer_destroy(handle) -> int:
+    return _lib.layer_destroy(handle)
+
+
+def kv_layout(cfg, batch: int):
+    d = kv_desc()
+    rc = _lib.kv_layout(ctypes.byref(make_config(cfg)), batch, ctypes.byref(d))
+    return rc, d
+
+
+def layer_workspace_size(handle, stage: int, batch: int, T: int, max_ctx: int) -> int:
+    return _lib.layer_workspace_size(handle, stage, batch, T, max_ctx)
+
+
+def layer_prefill(handle, x, pos, T, k_cache, v_cache, y, ws, ws_bytes, stream=None) -> int:
+    return _lib.layer_prefill(handle, _ptr(x), _ptr(pos), T, _ptr(k_cache), _ptr(v_cache), _ptr(y), _ptr(ws),
+                              ws_bytes, _stream(stream))
+
+
+def layer_prefill_kv(handle, x, pos, T, hist_len, k_cache, v_cache, y, ws, ws_bytes, stream=None) -> int:
+    return _lib.layer_prefill_kv(handle, _ptr(x), _ptr(pos), T, hist_len, _ptr(k_cache), _ptr(v_cache), _ptr(y),
+                                 _ptr(ws), ws_bytes, _stream(stream))
+
+
+def layer_decode(handle, x, pos, ctx_lens, max_ctx, attn_mask, B, k_cache, v_cache, y, ws, ws_bytes,
+                 stream=None) -> int:
+    return _lib.layer_decode(handle, _ptr(x), _ptr(pos), _ptr(ctx_lens), max_ctx, _ptr(attn_mask), B,
+                             _ptr(k_cache), _ptr(v_cache), _ptr(y), _ptr(ws), ws_bytes, _stream(stream))
+
+
+def kv_append(desc: kv_desc, k_cache, v_cache, k_new, v_new, B, T, slot_start, stream=None) -> int:
+    ss = np.ascontiguousarray(np.asarray(slot_start, dtype=np.int32))
+    return _lib.kv_append(ctypes.byref(desc), _ptr(k_cache), _ptr(v_cache), _ptr(k_new), _ptr(v_new), B, T,
+                          ss.ctypes.data, _stream(stream))
+
+
+def layer_debug_dequant(handle, which, out, stream=None) -> int:
+    if isinstance(which, str):
+        which = LINEAR_INDEX[which]
+    return _lib.layer_debug_dequant(handle, which, _ptr(out), _stream(stream))
+
+
+def layer_profile_kernel(handle, stage: int, kernel: int) -> int:
+    return _lib.layer_profile_kernel(handle, stage, kernel)
+
+
+def layer_profile_read(handle, stage: int):
+    ms = ctypes.c_float()
+    n = ctypes.c_int32()
+    rc = _lib.layer_profile_read(handle, stage, ctypes.byref(ms), ctypes.byref(n))
+    return rc, ms.value, n.value
+
+
+# ------------------------------------------------------------ convenience
+
+class Layer:
+    """Owns a layer handle plus reusable workspace; methods raise W4Error."""
+
+    def __init__(self, cfg, weights: dict):
+        import torch
+        self.cfg = cfg
+        rc, self.handle = layer_create(cfg, weights)
+        check(rc)
+        self._ws = torch.empty(0, dtype=torch.uint8, device="cuda")
+
+    def close(self):
+        if self.handle:
+            layer_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def workspace(self, stage, batch, T, max_ctx):
+        import torch
+        n = layer_workspace_size(self.handle, stage, batch, T, max_ctx)
+        if n == 0:
+            raise W4Error(W4_EINVAL, "invalid workspace query")
+        if self._ws.numel() < n:
+            self._ws = torch.empty(n, dtype=torch.uint8, device="cuda")
+        return self._ws, self._ws.numel()
+
+    def new_cache(self, batch: int, fill_bits: Optional[int] = None):
+        """A K and a V cache in the kv_layout(cfg, batch) layout (uint16 bf16
+        bit patterns), optionally filled with one bit pattern."""
+        import torch
+        rc, d = kv_layout(self.cfg, batch)
+        check(rc)
+        shape = (batch, d.n_kv_heads, d.max_seq, d.head_dim)
+        k = torch.empty(shape, dtype=torch.int16, device="cuda")
+        v = torch.empty(shape, dtype=torch.int16, device="cuda")
+        if fill_bits is not None:
+            val = int(np.array([fill_bits], dtype=np.uint16).view(np.int16)[0])
+            k.fill_(val)
+            v.fill_(val)
+        return k, v
+
+    def prefill(self, x, pos, k_cache, v_cache, y, stream=None):
+        ws, n = self.workspace(STAGE_PREFILL, 1, x.shape[0], 0)
+        check(layer_prefill(self.handle, x, pos, x.shape[0], k_cache, v_cache, y, ws, n, stream))
+
+    def prefill_kv(self, x, pos, hist_len, k_cache, v_cache, y, stream=None):
+        ws, n = self.workspace(STAGE_PREFILL_KV, 1, x.shape[0], hist_len)
+        check(layer_prefill_kv(self.handle, x, pos, x.shape[0], hist_len, k_cache, v_cache, y, ws, n, stream))
+
+    def decode(self, x, pos, ctx_lens, max_ctx, k_cache, v_cache, y, attn_mask=None, stream=None):
+        B = x.shape[0]
+        ws, n = self.workspace(STAGE_DECODE, B, 1, max_ctx)
+        check(layer_decode(self.handle, x, pos, ctx_lens, max_ctx, attn_mask, B, k_cache, v_cache, y, ws, n, stream))
+
+    def debug_dequant(self, which):
+        import torch
+        K, N = self.cfg.linear_shape(which)
+        out = torch.empty((K, N), dtype=torch.float32, device="cuda")
+        check(layer_debug_dequant(self.handle, which, out))
+        return out

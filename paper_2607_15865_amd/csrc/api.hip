@@ -1,0 +1,700 @@
+// C ABI of the three-stage W4A16 decoder layer (declared in include/w4layer.h):
+// argument validation, weight repacking into the tiled device layout, the
+// workspace plan and the kernel sequence of each stage.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstdarg>
+#include <cstring>
+#include <string>
+#include <thread>
+#include <vector>
+
+#include "../../include/w4layer.h"
+#include "common.h"
+#include "launch.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+int fail(int code, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return code;
+}
+
+#define HIP_TRY(call)                                                                        \
+    do {                                                                                     \
+        hipError_t e_ = (call);                                                              \
+        if (e_ != hipSuccess) return fail(W4_EHIP, "%s: %s", #call, hipGetErrorString(e_)); \
+    } while (0)
+
+int round_up(int a, int b) { return (a + b - 1) / b * b; }
+
+struct DevBuf {
+    void* p = nullptr;
+    ~DevBuf() { if (p) (void)hipFree(p); }
+};
+
+// Canonical host linear (see qlinear_host) with its logical shape.
+struct HostLin {
+    const int32_t* qw;
+    const uint16_t* sc;
+    const uint8_t* z;
+    int K, N;
+};
+
+struct ColSrc {        // where a device column comes from
+    const HostLin* lin;  // null: padding column
+    int n;
+};
+
+struct Repacked {
+    std::vector<uint32_t> qw;
+    std::vector<uint16_t> scales;
+    std::vector<float> ratios, slast;
+    std::vector<uint8_t> zeros;
+};
+
+inline bool f16_is_zero(uint16_t b) { return (b & 0x7FFFu) == 0; }
+inline double f16_value(uint16_t b) {
+    const int e = (b >> 10) & 0x1F, f = b & 0x3FF;
+    const double v = (e == 0) ? std::ldexp((double)f, -24) : std::ldexp(1.0 + f / 1024.0, e - 15);
+    return (b & 0x8000u) ? -v : v;
+}
+
+// Repack columns [c0, c1) of a device linear.
+void repack_cols(const std::vector<ColSrc>& cols, int K_pad, int G, bool has_zeros, Repacked& R, int c0, int c1) {
+    const int KG = K_pad / G, KB = K_pad / 64;
+    std::vector<uint8_t> code(K_pad);
+    std::vector<uint16_t> s(KG);
+    std::vector<uint8_t> z(KG);
+    std::vector<char> dead(KG);
+    for (int nd = c0; nd < c1; nd++) {
+        const ColSrc& cs = cols[nd];
+        const HostLin* L = cs.lin;
+        const int ng = L ? (L->K + G - 1) / G : 0;
+        for (int g = 0; g < KG; g++) {
+            s[g] = (L && g < ng) ? L->sc[(size_t)g * L->N + cs.n] : 0;
+            z[g] = (L && L->z && g < ng) ? L->z[(size_t)g * L->N + cs.n] : 8;
+            dead[g] = f16_is_zero(s[g]);
+        }
+        // non-zero stand-in scales for groups that contribute nothing
+        uint16_t first = 0x3C00;
+        for (int g = 0; g < KG; g++)
+            if (!dead[g]) { first = s[g]; break; }
+        uint16_t prev = first;
+        for (int g = 0; g < KG; g++) {
+            if (dead[g]) s[g] = prev; else prev = s[g];
+        }
+        for (int k = 0; k < K_pad; k++) {
+            const int g = k / G;
+            uint8_t cv = z[g];
+            if (L && k < L->K && !dead[g]) {
+                const uint32_t w = (uint32_t)L->qw[(size_t)(k / 8) * L->N + cs.n];
+                cv = (w >> (4 * (k % 8))) & 0xF;
+            }
+            code[k] = cv;
+        }
+        const int nb = nd / 32, cc = nd % 32;
+        for (int kb = 0; kb < KB; kb++)
+            for (int hh = 0; hh < 2; hh++)
+                for (int si = 0; si < 4; si++) {
+                    const int k0 = kb * 64 + si * 16 + hh * 8;
+                    uint32_t w = 0;
+                    for (int j = 0; j < 8; j++) w |= (uint32_t)code[k0 + j] << (4 * (j / 2) + 16 * (j % 2));
+                    R.qw[(((size_t)nb * KB + kb) * 64 + hh * 32 + cc) * 4 + si] = w;
+                }
+        for (int g = 0; g < KG; g++) {
+            R.scales[(size_t)nd * KG + g] = s[g];
+            R.ratios[(size_t)nd * KG + g] = g == 0 ? 1.0f : (float)(f16_value(s[g - 1]) / f16_value(s[g]));
+            if (has_zeros) R.zeros[(size_t)nd * KG + g] = z[g];
+        }
+        R.slast[nd] = (float)f16_value(s[KG - 1]);
+    }
+}
+
+}  // namespace
+
+struct DevLinearOwned {
+    DevLinear d{};
+    DevBuf qw, scales, ratios, slast, zeros, colmap_a, colmap_b, colmap_c;
+};
+
+struct Profiler {          // one timed kernel per stage
+    static constexpr int kMax = 4096;
+    int kernel[3] = {-1, -1, -1};
+    std::vector<hipEvent_t> ev[3];   // 2 per recorded launch
+    int used[3] = {0, 0, 0};
+    ~Profiler() {
+        for (auto& v : ev)
+            for (auto e : v) (void)hipEventDestroy(e);
+    }
+};
+
+struct layer_s {
+    layer_config cfg{};
+    int F_pad = 0;
+    DevLinearOwned qkv, o, gu, down;
+    DevBuf attn_norm, mlp_norm, rope_cos, rope_sin;
+    int device = 0;
+    Profiler prof;
+};
+
+namespace {
+
+int upload(DevBuf& b, const void* src, size_t bytes) {
+    if (bytes == 0) return 0;
+    HIP_TRY(hipMalloc(&b.p, bytes));
+    HIP_TRY(hipMemcpy(b.p, src, bytes, hipMemcpyHostToDevice));
+    return 0;
+}
+
+int build_linear(DevLinearOwned& out, const std::vector<ColSrc>& cols, int K, int K_pad, int G, bool has_zeros) {
+    const int N_dev = (int)cols.size();
+    const int KG = K_pad / G;
+    Repacked R;
+    R.qw.resize((size_t)N_dev * K_pad / 8);
+    R.scales.resize((size_t)N_dev * KG);
+    R.ratios.resize((size_t)N_dev * KG);
+    R.slast.resize(N_dev);
+    if (has_zeros) R.zeros.resize((size_t)N_dev * KG);
+    const int nth = std::max(1, std::min(16, (int)std::thread::hardware_concurrency()));
+    std::vector<std::thread> th;
+    const int per = (N_dev / 32 + nth - 1) / nth * 32;
+    for (int i = 0; i < nth; i++) {
+        const int c0 = i * per, c1 = std::min(N_dev, (i + 1) * per);
+        if (c0 >= c1) break;
+        th.emplace_back(repack_cols, std::cref(cols), K_pad, G, has_zeros, std::ref(R), c0, c1);
+    }
+    for (auto& t : th) t.join();
+    int rc;
+    if ((rc = upload(out.qw, R.qw.data(), R.qw.size() * 4))) return rc;
+    if ((rc = upload(out.scales, R.scales.data(), R.scales.size() * 2))) return rc;
+    if ((rc = upload(out.ratios, R.ratios.data(), R.ratios.size() * 4))) return rc;
+    if ((rc = upload(out.slast, R.slast.data(), R.slast.size() * 4))) return rc;
+    if (has_zeros && (rc = upload(out.zeros, R.zeros.data(), R.zeros.size()))) return rc;
+    DevLinear& d = out.d;
+    d.qw = (const uint32_t*)out.qw.p;
+    d.scales = (const uint16_t*)out.scales.p;
+    d.ratios = (const float*)out.ratios.p;
+    d.slast = (const float*)out.slast.p;
+    d.zeros = has_zeros ? (const uint8_t*)out.zeros.p : nullptr;
+    d.K = K;
+    d.N = N_dev;
+    d.K_pad = K_pad;
+    d.N_dev = N_dev;
+    d.KG = KG;
+    return 0;
+}
+
+int validate_config(const layer_config* c) {
+    if (!c) return fail(W4_EINVAL, "null config");
+    if (c->hidden <= 0 || c->n_heads <= 0 || c->n_kv_heads <= 0 || c->ffn <= 0 || c->max_seq <= 0 ||
+        c->max_batch <= 0)
+        return fail(W4_EINVAL, "non-positive dimension in config");
+    if (!(c->rms_eps >= 0.f) || !(c->rope_base > 0.f)) return fail(W4_EINVAL, "bad rms_eps or rope_base");
+    if (c->head_dim != 64 && c->head_dim != 128) return fail(W4_EUNSUPPORTED, "head_dim must be 64 or 128");
+    if (c->n_heads % c->n_kv_heads) return fail(W4_EUNSUPPORTED, "n_heads must be a multiple of n_kv_heads");
+    if (c->n_heads / c->n_kv_heads > 8) return fail(W4_EUNSUPPORTED, "at most 8 query heads per kv head");
+    const int G = c->group_size;
+    if (G != 32 && G != 64 && G != 128 && G != 256) return fail(W4_EUNSUPPORTED, "group_size must be 32, 64, 128 or 256");
+    const int KP = std::max(64, G);
+    if (c->hidden % 128 || c->hidden % KP) return fail(W4_EUNSUPPORTED, "hidden must be a multiple of 128 and of group_size");
+    const int qd = c->n_heads * c->head_dim;
+    if (qd % 128 || qd % KP) return fail(W4_EUNSUPPORTED, "n_heads*head_dim must be a multiple of 128 and of group_size");
+    if (c->ffn % 8) return fail(W4_EUNSUPPORTED, "ffn must be a multiple of 8");
+    if (c->max_batch > 64) return fail(W4_EUNSUPPORTED, "max_batch above 64");
+    if (c->hidden > 16384 || round_up(c->ffn, KP) > 65536) return fail(W4_EUNSUPPORTED, "hidden or ffn too large");
+    return 0;
+}
+
+int check_device() {
+    int dev = 0;
+    HIP_TRY(hipGetDevice(&dev));
+    hipDeviceProp_t prop;
+    HIP_TRY(hipGetDeviceProperties(&prop, dev));
+    if (std::strncmp(prop.gcnArchName, "gfx950", 6) != 0)
+        return fail(W4_EUNSUPPORTED, "device %d is %s, this library is built for gfx950", dev, prop.gcnArchName);
+    return 0;
+}
+
+// ---- workspace plan
+struct Carve {
+    size_t off = 0;
+    size_t take(size_t bytes) {
+        const size_t o = off;
+        off += (bytes + 255) / 256 * 256;
+        return o;
+    }
+};
+
+struct PrefillWs { size_t xn1, q, attn, h, xn2, g, total; };
+PrefillWs plan_prefill(const layer_s* L, int T) {
+    const layer_config& c = L->cfg;
+    const size_t qd = (size_t)c.n_heads * c.head_dim;
+    Carve cv;
+    PrefillWs w;
+    w.xn1 = cv.take((size_t)T * c.hidden * 2);
+    w.q = cv.take((size_t)T * qd * 2);
+    w.attn = cv.take((size_t)T * qd * 2);
+    w.h = cv.take((size_t)T * c.hidden * 4);
+    w.xn2 = cv.take((size_t)T * c.hidden * 2);
+    w.g = cv.take((size_t)T * L->F_pad * 2);
+    w.total = cv.off;
+    return w;
+}
+
+constexpr int DEC_MAX_CHUNKS = 32;
+int decode_chunk(int max_ctx) {
+    const int keys = max_ctx + 1;
+    int ch = 64 * ((keys + 64 * DEC_MAX_CHUNKS - 1) / (64 * DEC_MAX_CHUNKS));
+    return std::min(512, std::max(64, ch));
+}
+
+struct DecodeWs { size_t q, part, attn, h, g, total; int chunk, nchunks; };
+DecodeWs plan_decode(const layer_s* L, int B, int max_ctx) {
+    const layer_config& c = L->cfg;
+    const size_t qd = (size_t)c.n_heads * c.head_dim;
+    DecodeWs w;
+    w.chunk = decode_chunk(max_ctx);
+    w.nchunks = (max_ctx + 1 + w.chunk - 1) / w.chunk;
+    Carve cv;
+    w.q = cv.take((size_t)B * qd * 2);
+    w.part = cv.take((size_t)B * c.n_heads * w.nchunks * (c.head_dim + 2) * 4);
+    w.attn = cv.take((size_t)B * qd * 2);
+    w.h = cv.take((size_t)B * c.hidden * 4);
+    w.g = cv.take((size_t)B * L->F_pad * 2);
+    w.total = cv.off;
+    return w;
+}
+
+int gemv_ksplit(const DevLinear& W, int want_blocks, int B) {
+    const int pairs = W.N_dev / 64, KB = W.K_pad / 64;
+    int ks = std::max(1, std::min(KB, (want_blocks + pairs - 1) / pairs));
+    // activation slice of B rows must fit the LDS budget (128 KB)
+    while ((long long)B * ((KB + ks - 1) / ks) * 64 * 2 > 128 * 1024 && ks < KB) ks++;
+    return ks;
+}
+
+// Event pair around kernel `k` of `stage` when it is the profiled one.
+struct ProfScope {
+    layer_s* L;
+    int stage;
+    bool on = false;
+    hipStream_t st;
+    ProfScope(layer_s* L_, int stage_, int k, hipStream_t s) : L(L_), stage(stage_), st(s) {
+        Profiler& p = L->prof;
+        if (p.kernel[stage] == k && p.used[stage] < Profiler::kMax) {
+            auto& ev = p.ev[stage];
+            if ((int)ev.size() < 2 * (p.used[stage] + 1)) {
+                hipEvent_t a, b;
+                if (hipEventCreate(&a) != hipSuccess) return;
+                if (hipEventCreate(&b) != hipSuccess) { (void)hipEventDestroy(a); return; }
+                ev.push_back(a);
+                ev.push_back(b);
+            }
+            on = hipEventRecord(ev[2 * p.used[stage]], st) == hipSuccess;
+        }
+    }
+    ~ProfScope() {
+        if (on) {
+            Profiler& p = L->prof;
+            if (hipEventRecord(p.ev[stage][2 * p.used[stage] + 1], st) == hipSuccess) p.used[stage]++;
+        }
+    }
+};
+
+EpiArgs base_epi(const layer_s* L) {
+    EpiArgs e{};
+    const layer_config& c = L->cfg;
+    e.rope_cos = (const float*)L->rope_cos.p;
+    e.rope_sin = (const float*)L->rope_sin.p;
+    e.nq = c.n_heads;
+    e.nkv = c.n_kv_heads;
+    e.head_dim = c.head_dim;
+    e.F_pad = L->F_pad;
+    return e;
+}
+
+int run_prefill(layer_s* L, const float* x, const int32_t* pos, int T, int hist, void* kc, void* vc, float* y,
+                void* ws, size_t ws_bytes, void* stream_) {
+    if (!L) return fail(W4_EINVAL, "null layer");
+    if (!x || !pos || !kc || !vc || !y || !ws) return fail(W4_EINVAL, "null pointer argument");
+    if (T < 1 || hist < 0) return fail(W4_EINVAL, "T must be >= 1 and hist_len >= 0");
+    if ((const void*)x == (const void*)y) return fail(W4_EINVAL, "x and y must not alias");
+    const layer_config& c = L->cfg;
+    if ((long long)hist + T > c.max_seq) return fail(W4_ECAPACITY, "hist_len + T = %lld exceeds max_seq %d", (long long)hist + T, c.max_seq);
+    const PrefillWs w = plan_prefill(L, T);
+    if (ws_bytes < w.total) return fail(W4_EWORKSPACE, "workspace %zu bytes, need %zu", ws_bytes, w.total);
+    hipStream_t st = (hipStream_t)stream_;
+    char* base = (char*)ws;
+    f16* xn1 = (f16*)(base + w.xn1);
+    uint16_t* q = (uint16_t*)(base + w.q);
+    f16* attn = (f16*)(base + w.attn);
+    float* h = (float*)(base + w.h);
+    f16* xn2 = (f16*)(base + w.xn2);
+    f16* g = (f16*)(base + w.g);
+    const int H = c.hidden, d = c.head_dim, qd = c.n_heads * d;
+
+    int rc = 0;
+    const int stage = hist > 0 ? 1 : 0;
+    { ProfScope ps(L, stage, 0, st); rc |= launch_rmsnorm(x, (const uint16_t*)L->attn_norm.p, c.rms_eps, T, H, xn1, st); }
+    EpiArgs e = base_epi(L);
+    e.q_out = q;
+    e.k_cache = (uint16_t*)kc;
+    e.v_cache = (uint16_t*)vc;
+    e.cache_stride_b = 0;
+    e.cache_stride_h = (long long)c.max_seq * d;
+    e.pos = pos;
+    e.slot_base = hist;
+    { ProfScope ps(L, stage, 1, st); rc |= launch_gemm_w4(EPI_QKV, xn1, T, H, L->qkv.d, e, st); }
+    AttnPrefillArgs aa{};
+    aa.q = q;
+    aa.k_cache = (const uint16_t*)kc;
+    aa.v_cache = (const uint16_t*)vc;
+    aa.cache_stride_h = (long long)c.max_seq * d;
+    aa.out = attn;
+    aa.T = T;
+    aa.L = hist;
+    aa.nq = c.n_heads;
+    aa.nkv = c.n_kv_heads;
+    aa.d = d;
+    aa.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)d));
+    { ProfScope ps(L, stage, 2, st); rc |= launch_attn_prefill(aa, st); }
+    EpiArgs eo = base_epi(L);
+    eo.resid = x;
+    eo.out_f32 = h;
+    { ProfScope ps(L, stage, 3, st); rc |= launch_gemm_w4(EPI_RESID, attn, T, qd, L->o.d, eo, st); }
+    { ProfScope ps(L, stage, 4, st); rc |= launch_rmsnorm(h, (const uint16_t*)L->mlp_norm.p, c.rms_eps, T, H, xn2, st); }
+    EpiArgs eg = base_epi(L);
+    eg.act_out = g;
+    { ProfScope ps(L, stage, 5, st); rc |= launch_gemm_w4(EPI_SWIGLU, xn2, T, H, L->gu.d, eg, st); }
+    EpiArgs ed = base_epi(L);
+    ed.resid = h;
+    ed.out_f32 = y;
+    { ProfScope ps(L, stage, 6, st); rc |= launch_gemm_w4(EPI_RESID, g, T, L->F_pad, L->down.d, ed, st); }
+    if (rc) return fail(W4_EHIP, "kernel launch failed: %s", hipGetErrorString(hipGetLastError()));
+    return W4_OK;
+}
+
+}  // namespace
+
+// =================================================================== C ABI
+
+extern "C" {
+
+const char* layer_last_error(void) { return g_err.c_str(); }
+
+int kv_layout(const layer_config* cfg, int32_t batch, kv_desc* out) {
+    if (!cfg || !out) return fail(W4_EINVAL, "null argument");
+    if (batch < 1) return fail(W4_EINVAL, "batch must be >= 1");
+    if (cfg->n_kv_heads <= 0 || cfg->max_seq <= 0 || cfg->head_dim <= 0) return fail(W4_EINVAL, "bad config");
+    out->batch = batch;
+    out->n_kv_heads = cfg->n_kv_heads;
+    out->max_seq = cfg->max_seq;
+    out->head_dim = cfg->head_dim;
+    out->stride_s = cfg->head_dim;
+    out->stride_h = (int64_t)cfg->max_seq * cfg->head_dim;
+    out->stride_b = out->stride_h * cfg->n_kv_heads;
+    out->bytes = (size_t)out->stride_b * batch * 2;
+    return W4_OK;
+}
+
+int layer_create(const layer_config* cfg, const layer_weights_host* w, layer_t* out) {
+    int rc;
+    if ((rc = validate_config(cfg))) return rc;
+    if (!w || !out) return fail(W4_EINVAL, "null argument");
+    const qlinear_host* lins[7] = {&w->q, &w->k, &w->v, &w->o, &w->gate, &w->up, &w->down};
+    for (int i = 0; i < 7; i++)
+        if (!lins[i]->qweight || !lins[i]->scales) return fail(W4_EINVAL, "null weight pointer (linear %d)", i);
+    if (!w->attn_norm || !w->mlp_norm) return fail(W4_EINVAL, "null norm weight");
+    if ((rc = check_device())) return rc;
+    const bool zq = w->q.zeros || w->k.zeros || w->v.zeros || w->o.zeros || w->gate.zeros || w->up.zeros || w->down.zeros;
+    if (zq && !(w->q.zeros && w->k.zeros && w->v.zeros && w->o.zeros && w->gate.zeros && w->up.zeros && w->down.zeros))
+        return fail(W4_EINVAL, "zero points must be given for all seven linears or for none");
+
+    const layer_config& c = *cfg;
+    const int H = c.hidden, d = c.head_dim, nq = c.n_heads, nkv = c.n_kv_heads, F = c.ffn, G = c.group_size;
+    const int KP = std::max(64, G);
+    const int qd = nq * d, kvd = nkv * d;
+    const int F_pad = round_up(F, KP);
+
+    // scales must be finite
+    auto finite_scales = [&](const qlinear_host& q, int K, int N) {
+        const size_t n = (size_t)((K + G - 1) / G) * N;
+        for (size_t i = 0; i < n; i++)
+            if (((q.scales[i] >> 10) & 0x1F) == 0x1F) return false;
+        return true;
+    };
+    HostLin hq{w->q.qweight, w->q.scales, w->q.zeros, H, qd}, hk{w->k.qweight, w->k.scales, w->k.zeros, H, kvd},
+        hv{w->v.qweight, w->v.scales, w->v.zeros, H, kvd}, ho{w->o.qweight, w->o.scales, w->o.zeros, qd, H},
+        hg{w->gate.qweight, w->gate.scales, w->gate.zeros, H, F}, hu{w->up.qweight, w->up.scales, w->up.zeros, H, F},
+        hd{w->down.qweight, w->down.scales, w->down.zeros, F, H};
+    const HostLin* all[7] = {&hq, &hk, &hv, &ho, &hg, &hu, &hd};
+    for (int i = 0; i < 7; i++)
+        if (!finite_scales(*lins[i], all[i]->K, all[i]->N)) return fail(W4_EINVAL, "non-finite scale in linear %d", i);
+
+    layer_s* L = new layer_s();
+    L->cfg = c;
+    L->F_pad = F_pad;
+    (void)hipGetDevice(&L->device);
+
+    // fused q|k|v with the RoPE block order inside each head
+    std::vector<ColSrc> cq(qd + 2 * kvd);
+    std::vector<int32_t> mq(qd), mk(kvd), mv(kvd);
+    for (int nd = 0; nd < qd + 2 * kvd; nd++) {
+        int local = nd;
+        const HostLin* src = &hq;
+        std::vector<int32_t>* map = &mq;
+        if (local >= qd + kvd) { local -= qd + kvd; src = &hv; map = &mv; }
+        else if (local >= qd) { local -= qd; src = &hk; map = &mk; }
+        const int head = local / d, p = (local % d) / 32;
+        const int dim = 32 * rope_block(p, d) + local % 32;
+        cq[nd] = ColSrc{src, head * d + dim};
+        (*map)[head * d + dim] = nd;
+    }
+    std::vector<ColSrc> co(H), cd(H);
+    std::vector<int32_t> mo(H), md(H);
+    for (int n = 0; n < H; n++) { co[n] = ColSrc{&ho, n}; cd[n] = ColSrc{&hd, n}; mo[n] = n; md[n] = n; }
+    std::vector<ColSrc> cgu(2 * F_pad);
+    std::vector<int32_t> mg(F), mu(F);
+    for (int nd = 0; nd < 2 * F_pad; nd++) {
+        const int j2 = nd / 32, j = j2 / 2, which = j2 % 2, f = 32 * j + nd % 32;
+        if (f < F) {
+            cgu[nd] = ColSrc{which ? &hu : &hg, f};
+            (which ? mu : mg)[f] = nd;
+        } else {
+            cgu[nd] = ColSrc{nullptr, 0};
+        }
+    }
+    if ((rc = build_linear(L->qkv, cq, H, H, G, zq)) || (rc = build_linear(L->o, co, qd, qd, G, zq)) ||
+        (rc = build_linear(L->gu, cgu, H, H, G, zq)) || (rc = build_linear(L->down, cd, F, F_pad, G, zq)) ||
+        (rc = upload(L->qkv.colmap_a, mq.data(), mq.size() * 4)) || (rc = upload(L->qkv.colmap_b, mk.data(), mk.size() * 4)) ||
+        (rc = upload(L->qkv.colmap_c, mv.data(), mv.size() * 4)) || (rc = upload(L->o.colmap_a, mo.data(), mo.size() * 4)) ||
+        (rc = upload(L->gu.colmap_a, mg.data(), mg.size() * 4)) || (rc = upload(L->gu.colmap_b, mu.data(), mu.size() * 4)) ||
+        (rc = upload(L->down.colmap_a, md.data(), md.size() * 4)) ||
+        (rc = upload(L->attn_norm, w->attn_norm, (size_t)H * 2)) || (rc = upload(L->mlp_norm, w->mlp_norm, (size_t)H * 2))) {
+        delete L;
+        return rc;
+    }
+    // RoPE cos/sin table, computed in double (Sec. 4.6.2)
+    std::vector<float> tc((size_t)c.max_seq * (d / 2)), ts(tc.size());
+    for (int p = 0; p < c.max_seq; p++)
+        for (int i = 0; i < d / 2; i++) {
+            const double ang = (double)p * std::pow((double)c.rope_base, -2.0 * i / d);
+            tc[(size_t)p * (d / 2) + i] = (float)std::cos(ang);
+            ts[(size_t)p * (d / 2) + i] = (float)std::sin(ang);
+        }
+    if ((rc = upload(L->rope_cos, tc.data(), tc.size() * 4)) || (rc = upload(L->rope_sin, ts.data(), ts.size() * 4))) {
+        delete L;
+        return rc;
+    }
+    *out = L;
+    return W4_OK;
+}
+
+int layer_destroy(layer_t layer) {
+    if (!layer) return W4_OK;
+    (void)hipDeviceSynchronize();
+    delete layer;
+    return W4_OK;
+}
+
+size_t layer_workspace_size(layer_t L, int32_t stage, int32_t batch, int32_t T, int32_t max_ctx) {
+    if (!L) return 0;
+    if (stage == 0 || stage == 1) {
+        if (T < 1) return 0;
+        return plan_prefill(L, T).total;
+    }
+    if (stage == 2) {
+        if (batch < 1 || max_ctx < 0) return 0;
+        return plan_decode(L, batch, max_ctx).total;
+    }
+    return 0;
+}
+
+int layer_prefill(layer_t L, const float* x, const int32_t* pos, int32_t T, void* kc, void* vc, float* y, void* ws,
+                  size_t ws_bytes, void* stream) {
+    return run_prefill(L, x, pos, T, 0, kc, vc, y, ws, ws_bytes, stream);
+}
+
+int layer_prefill_kv(layer_t L, const float* x, const int32_t* pos, int32_t T, int32_t hist_len, void* kc, void* vc,
+                     float* y, void* ws, size_t ws_bytes, void* stream) {
+    return run_prefill(L, x, pos, T, hist_len, kc, vc, y, ws, ws_bytes, stream);
+}
+
+int layer_decode(layer_t L, const float* x, const int32_t* pos, const int32_t* ctx_lens, int32_t max_ctx,
+                 const float* attn_mask, int32_t B, void* kc, void* vc, float* y, void* ws, size_t ws_bytes,
+                 void* stream) {
+    if (!L) return fail(W4_EINVAL, "null layer");
+    if (!x || !pos || !ctx_lens || !kc || !vc || !y || !ws) return fail(W4_EINVAL, "null pointer argument");
+    if (B < 1 || max_ctx < 0) return fail(W4_EINVAL, "B must be >= 1 and max_ctx >= 0");
+    if ((const void*)x == (const void*)y) return fail(W4_EINVAL, "x and y must not alias");
+    const layer_config& c = L->cfg;
+    if (B > c.max_batch) return fail(W4_ECAPACITY, "B = %d exceeds max_batch %d", B, c.max_batch);
+    if (B > 8) return fail(W4_EUNSUPPORTED, "decode batch above 8");
+    if ((long long)max_ctx + 1 > c.max_seq) return fail(W4_ECAPACITY, "max_ctx + 1 = %lld exceeds max_seq %d", (long long)max_ctx + 1, c.max_seq);
+    const DecodeWs w = plan_decode(L, B, max_ctx);
+    if (ws_bytes < w.total) return fail(W4_EWORKSPACE, "workspace %zu bytes, need %zu", ws_bytes, w.total);
+    hipStream_t st = (hipStream_t)stream;
+    char* base = (char*)ws;
+    uint16_t* q = (uint16_t*)(base + w.q);
+    float* part = (float*)(base + w.part);
+    f16* attn = (f16*)(base + w.attn);
+    float* h = (float*)(base + w.h);
+    f16* g = (f16*)(base + w.g);
+    const int H = c.hidden, d = c.head_dim, qd = c.n_heads * d;
+    const long long sh = (long long)c.max_seq * d, sb = sh * c.n_kv_heads;
+    int rc = 0;
+
+    GemvArgs a1{};
+    a1.W = L->qkv.d;
+    a1.x_f32 = x;
+    a1.gamma = (const uint16_t*)L->attn_norm.p;
+    a1.eps = c.rms_eps;
+    a1.B = B;
+    a1.ksplit = 1;
+    a1.ep = base_epi(L);
+    a1.ep.q_out = q;
+    a1.ep.k_cache = (uint16_t*)kc;
+    a1.ep.v_cache = (uint16_t*)vc;
+    a1.ep.cache_stride_b = sb;
+    a1.ep.cache_stride_h = sh;
+    a1.ep.pos = pos;
+    a1.ep.slot_dev = ctx_lens;
+    a1.copy_src = x;
+    a1.copy_dst = h;
+    a1.copy_n = B * H;
+    { ProfScope ps(L, 2, 0, st); rc |= launch_gemv_w4(EPI_QKV, true, a1, st); }
+
+    AttnDecodeArgs ad{};
+    ad.q = q;
+    ad.k_cache = (const uint16_t*)kc;
+    ad.v_cache = (const uint16_t*)vc;
+    ad.stride_b = sb;
+    ad.stride_h = sh;
+    ad.ctx_lens = ctx_lens;
+    ad.mask = attn_mask;
+    ad.max_seq = c.max_seq;
+    ad.part = part;
+    ad.out = attn;
+    ad.B = B;
+    ad.nq = c.n_heads;
+    ad.nkv = c.n_kv_heads;
+    ad.d = d;
+    ad.chunk = w.chunk;
+    ad.nchunks = w.nchunks;
+    ad.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)d));
+    { ProfScope ps(L, 2, 1, st); rc |= launch_attn_decode(ad, st); }
+
+    GemvArgs a2{};
+    a2.W = L->o.d;
+    a2.x_f16 = attn;
+    a2.ldx = qd;
+    a2.B = B;
+    a2.ksplit = gemv_ksplit(L->o.d, 512, B);
+    a2.ep = base_epi(L);
+    a2.ep.out_f32 = h;
+    { ProfScope ps(L, 2, 3, st); rc |= launch_gemv_w4(EPI_RESID, false, a2, st); }
+
+    GemvArgs a3{};
+    a3.W = L->gu.d;
+    a3.x_f32 = h;
+    a3.gamma = (const uint16_t*)L->mlp_norm.p;
+    a3.eps = c.rms_eps;
+    a3.B = B;
+    a3.ksplit = 1;
+    a3.ep = base_epi(L);
+    a3.ep.act_out = g;
+    a3.copy_src = h;
+    a3.copy_dst = y;
+    a3.copy_n = B * H;
+    { ProfScope ps(L, 2, 4, st); rc |= launch_gemv_w4(EPI_SWIGLU, true, a3, st); }
+
+    GemvArgs a4{};
+    a4.W = L->down.d;
+    a4.x_f16 = g;
+    a4.ldx = L->F_pad;
+    a4.B = B;
+    a4.ksplit = gemv_ksplit(L->down.d, 512, B);
+    a4.ep = base_epi(L);
+    a4.ep.out_f32 = y;
+    { ProfScope ps(L, 2, 5, st); rc |= launch_gemv_w4(EPI_RESID, false, a4, st); }
+    if (rc) return fail(W4_EHIP, "kernel launch failed: %s", hipGetErrorString(hipGetLastError()));
+    return W4_OK;
+}
+
+int kv_append(const kv_desc* desc, void* kc, void* vc, const void* k_new, const void* v_new, int32_t B, int32_t T,
+              const int32_t* slot_start, void* stream) {
+    if (!desc || !kc || !vc || !k_new || !v_new || !slot_start) return fail(W4_EINVAL, "null argument");
+    if (B < 1 || T < 1) return fail(W4_EINVAL, "B and T must be >= 1");
+    if (desc->head_dim % 8 || desc->head_dim <= 0 || desc->n_kv_heads <= 0 || desc->stride_s != desc->head_dim)
+        return fail(W4_EINVAL, "bad kv_desc");
+    if (B > desc->batch || B > 64) return fail(W4_ECAPACITY, "B = %d exceeds the cache batch", B);
+    for (int b = 0; b < B; b++)
+        if (slot_start[b] < 0 || (long long)slot_start[b] + T > desc->max_seq)
+            return fail(W4_ECAPACITY, "slots %d..%d of sequence %d outside max_seq %d", slot_start[b], slot_start[b] + T - 1, b, desc->max_seq);
+    if (launch_kv_append((uint16_t*)kc, (uint16_t*)vc, (const uint16_t*)k_new, (const uint16_t*)v_new, B, T,
+                         desc->n_kv_heads, desc->head_dim, desc->stride_b, desc->stride_h, slot_start,
+                         (hipStream_t)stream))
+        return fail(W4_EHIP, "kv_append launch failed: %s", hipGetErrorString(hipGetLastError()));
+    return W4_OK;
+}
+
+int layer_debug_dequant(layer_t L, int32_t which, float* out, void* stream) {
+    if (!L || !out) return fail(W4_EINVAL, "null argument");
+    if (which < 0 || which > 6) return fail(W4_EINVAL, "which must be 0..6");
+    const layer_config& c = L->cfg;
+    const int H = c.hidden, qd = c.n_heads * c.head_dim, kvd = c.n_kv_heads * c.head_dim, F = c.ffn;
+    const DevLinearOwned* dl;
+    const void* map;
+    int K, N;
+    switch (which) {
+        case 0: dl = &L->qkv; map = L->qkv.colmap_a.p; K = H; N = qd; break;
+        case 1: dl = &L->qkv; map = L->qkv.colmap_b.p; K = H; N = kvd; break;
+        case 2: dl = &L->qkv; map = L->qkv.colmap_c.p; K = H; N = kvd; break;
+        case 3: dl = &L->o; map = L->o.colmap_a.p; K = qd; N = H; break;
+        case 4: dl = &L->gu; map = L->gu.colmap_a.p; K = H; N = F; break;
+        case 5: dl = &L->gu; map = L->gu.colmap_b.p; K = H; N = F; break;
+        default: dl = &L->down; map = L->down.colmap_a.p; K = F; N = H; break;
+    }
+    if (launch_debug_dequant(dl->d, (const int32_t*)map, K, N, out, (hipStream_t)stream))
+        return fail(W4_EHIP, "debug dequant launch failed: %s", hipGetErrorString(hipGetLastError()));
+    return W4_OK;
+}
+
+int layer_profile_kernel(layer_t L, int32_t stage, int32_t kernel) {
+    if (!L) return fail(W4_EINVAL, "null layer");
+    if (stage < 0 || stage > 2) return fail(W4_EINVAL, "stage must be 0..2");
+    L->prof.kernel[stage] = kernel < 0 ? -1 : kernel;
+    L->prof.used[stage] = 0;
+    return W4_OK;
+}
+
+int layer_profile_read(layer_t L, int32_t stage, float* total_ms, int32_t* launches) {
+    if (!L || !total_ms || !launches) return fail(W4_EINVAL, "null argument");
+    if (stage < 0 || stage > 2) return fail(W4_EINVAL, "stage must be 0..2");
+    Profiler& p = L->prof;
+    double tot = 0.0;
+    for (int i = 0; i < p.used[stage]; i++) {
+        HIP_TRY(hipEventSynchronize(p.ev[stage][2 * i + 1]));
+        float ms = 0.f;
+        HIP_TRY(hipEventElapsedTime(&ms, p.ev[stage][2 * i], p.ev[stage][2 * i + 1]));
+        tot += ms;
+    }
+    *total_ms = (float)tot;
+    *launches = p.used[stage];
+    p.used[stage] = 0;
+    return W4_OK;
+}
+
+}  // extern "C"

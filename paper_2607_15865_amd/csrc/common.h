@@ -1,0 +1,156 @@
+// Shared device helpers and the private device layout of the W4A16 layer.
+//
+// Device weight layout (written once by layer_create, read by every stage):
+//
+//   A linear with K rows and N columns is stored as "tiles" of 32 columns x
+//   64 rows (k).  Tile (nb, kb) is 1 KB: 64 lanes x 4 words, so one wave
+//   reads a whole tile with one 16-byte load per lane.  Lane l holds column
+//   32*nb + (l % 32) and, for h = l / 32, the words that cover
+//   k = 64*kb + 16*s + 8*h + (0..7) for s = 0..3 (word s of the lane).
+//   Inside a word the eight 4-bit codes of k0..k0+7 sit at bit offsets
+//   0, 16, 4, 20, 8, 24, 12, 28, so ((w >> 4p) & 0x000F000F) holds the codes
+//   of k0+2p (low half) and k0+2p+1 (high half).  OR-ing 0x64006400 makes the
+//   fp16 pair (1024 + q) exactly, and subtracting 1024 + z leaves the exact
+//   code minus zero point.  This pair order is the operand order of the
+//   32x32x16 MFMA, so a lane's word s is its B fragment of k16 step s.
+//
+//   Tile index: nb * (K_pad / 64) + kb (column strips contiguous along k).
+//   Scales: fp16 [N_dev][K_pad / G]; ratios for the prefill GEMM: fp32
+//   [N_dev][K_pad / G] with ratio[n][g] = s[g-1][n] / s[g][n] (g >= 1), and the
+//   last scale as fp32 [N_dev].  Zero points (optional): uint8 [N_dev][K_pad/G].
+//
+//   K_pad is K rounded up to max(64, G); padded rows and groups carry the zero
+//   point code (weight 0).  A group whose scale is 0 is stored with all codes
+//   at the zero point and a non-zero stand-in scale, so every scale is
+//   non-zero (the ratios are finite) and the group still contributes 0.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+typedef _Float16 f16;
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+#define W4_TILE_N 32
+#define W4_TILE_K 64
+#define W4_TILE_WORDS 256   // 64 lanes x 4 words
+
+// Column permutation inside a head for the fused q/k/v weight: the head's
+// dims are cut into blocks of 32 and stored as pairs (b, b + d/64) so that a
+// RoPE pair (i, i + d/2) lands in the same lane of two adjacent 32-column
+// tiles.  Device block p of a head holds dim block rope_block(p).
+__host__ __device__ inline int rope_block(int p, int head_dim) {
+    int nb = head_dim / 32;          // 2 or 4
+    int half = nb / 2;
+    return (p % 2 == 0) ? (p / 2) : (p / 2 + half);
+}
+
+// ---------------------------------------------------------------- numerics
+
+// fp32 -> bf16 -> fp32, round to nearest even (finite inputs).
+__device__ __forceinline__ float round_bf16(float x) {
+    uint32_t u = __float_as_uint(x);
+    u += 0x7FFFu + ((u >> 16) & 1u);
+    return __uint_as_float(u & 0xFFFF0000u);
+}
+
+__device__ __forceinline__ uint16_t bf16_bits_rne(float x) {
+    uint32_t u = __float_as_uint(x);
+    u += 0x7FFFu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+
+__device__ __forceinline__ float bf16_bits_to_f32(uint16_t b) {
+    return __uint_as_float(((uint32_t)b) << 16);
+}
+
+// Activation store: the value rounded to bf16 and held as fp16 (exact for
+// the bf16 values inside the fp16 range), the operand type of the W4 MFMA.
+__device__ __forceinline__ f16 act_f16(float x) {
+    return (f16)round_bf16(x);
+}
+
+// Exact (code - zero) fp16 pair p (0..3) of a weight word; zoff2 is the
+// packed fp16 pair (-(1024+z), -(1024+z)).
+__device__ __forceinline__ f16x2 dequant_pair(uint32_t w, int p, f16x2 zoff2) {
+    uint32_t v = ((w >> (4 * p)) & 0x000F000Fu) | 0x64006400u;
+    return __builtin_bit_cast(f16x2, v) + zoff2;
+}
+
+__device__ __forceinline__ f16x8 dequant_word(uint32_t w, f16x2 zoff2) {
+    f16x2 a = dequant_pair(w, 0, zoff2), b = dequant_pair(w, 1, zoff2);
+    f16x2 c = dequant_pair(w, 2, zoff2), d = dequant_pair(w, 3, zoff2);
+    f16x8 r;
+    r[0] = a[0]; r[1] = a[1]; r[2] = b[0]; r[3] = b[1];
+    r[4] = c[0]; r[5] = c[1]; r[6] = d[0]; r[7] = d[1];
+    return r;
+}
+
+__device__ __forceinline__ f16x2 zero_offset_pair(const uint8_t* zeros, size_t idx) {
+    f16 z = (f16)(-(1024.0f + (zeros ? (float)zeros[idx] : 8.0f)));
+    f16x2 r; r[0] = z; r[1] = z;
+    return r;
+}
+
+// Reinterpret a 32-bit word as a bf16 pair.  Always pass a scalar: clang
+// miscompiles __builtin_bit_cast applied directly to an ext_vector element
+// with a loop index (it reads element 0).
+__device__ __forceinline__ bf16x2 as_bf16x2(uint32_t u) {
+    bf16x2 r;
+    __builtin_memcpy(&r, &u, 4);
+    return r;
+}
+
+__device__ __forceinline__ float silu(float z) { return z / (1.0f + __expf(-z)); }
+
+// wave-level reductions (64 lanes)
+__device__ __forceinline__ float wave_sum(float v) {
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+    return v;
+}
+__device__ __forceinline__ float wave_max(float v) {
+    for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+    return v;
+}
+
+// ---------------------------------------------------------------- layouts
+
+struct DevLinear {
+    const uint32_t* qw;      // tiles
+    const uint16_t* scales;  // fp16 bits [N_dev][KG]
+    const float* ratios;     // [N_dev][KG]
+    const float* slast;      // [N_dev]
+    const uint8_t* zeros;    // [N_dev][KG] or null
+    int K, N;                // logical
+    int K_pad, N_dev, KG;    // padded rows, device columns, groups
+};
+
+// Epilogue kinds shared by the GEMM (prefill) and GEMV (decode).
+enum EpiKind { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2 };
+
+// Everything an epilogue needs.
+struct EpiArgs {
+    // QKV
+    uint16_t* q_out;          // bf16 [M][nq][d]
+    uint16_t* k_cache;        // bf16 base of the cache
+    uint16_t* v_cache;
+    long long cache_stride_b; // elements between sequences (decode)
+    long long cache_stride_h; // elements between kv heads
+    const int32_t* pos;       // [M] position ids
+    const int32_t* slot_dev;  // decode: [B] device slots (ctx_lens); null in prefill
+    int slot_base;            // prefill: slot of row 0 (hist_len)
+    const float* rope_cos;    // [max_seq][d/2]
+    const float* rope_sin;
+    int nq, nkv, head_dim;
+    // RESID
+    const float* resid;       // fp32 [M][N]
+    float* out_f32;           // fp32 [M][N]
+    // SWIGLU
+    f16* act_out;             // fp16 [M][F_pad]
+    int F_pad;
+};

@@ -1,0 +1,102 @@
+// Row RMSNorm (prefill), the in-place KV append, and the debug dequantiser.
+#include "common.h"
+#include "launch.h"
+
+namespace {
+
+// top.RMSNorm (Sec. 2.2): y = x / sqrt(mean(x^2) + eps) * gamma over a row,
+// rounded to bf16 and held as fp16 (the matmul operand).  One block per row.
+__global__ void __launch_bounds__(256) rmsnorm_kernel(const float* __restrict__ x, const uint16_t* __restrict__ gamma,
+                                                      float eps, int H, f16* __restrict__ out) {
+    __shared__ float part[4];
+    const int row = blockIdx.x, tid = threadIdx.x;
+    const float* xr = x + (size_t)row * H;
+    float ss = 0.f;
+    for (int k = tid * 4; k < H; k += 1024) {
+        const float4 v = *reinterpret_cast<const float4*>(xr + k);
+        ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+    }
+    ss = wave_sum(ss);
+    if ((tid & 63) == 0) part[tid >> 6] = ss;
+    __syncthreads();
+    const float tot = part[0] + part[1] + part[2] + part[3];
+    const float rinv = 1.0f / sqrtf(tot / (float)H + eps);
+    f16* orow = out + (size_t)row * H;
+    for (int k = tid; k < H; k += 256) orow[k] = act_f16(xr[k] * rinv * bf16_bits_to_f32(gamma[k]));
+}
+
+struct SlotStarts { int32_t v[64]; };
+
+// Copy new K/V rows [B][T][nkv][d] into cache slots start_b + t.
+__global__ void kv_append_kernel(uint16_t* __restrict__ kc, uint16_t* __restrict__ vc,
+                                 const uint16_t* __restrict__ kn, const uint16_t* __restrict__ vn,
+                                 int B, int T, int nkv, int d, long long sb, long long sh, SlotStarts st) {
+    const int segs = d / 8;
+    const long long total = (long long)B * T * nkv * segs;
+    for (long long i = blockIdx.x * (long long)blockDim.x + threadIdx.x; i < total;
+         i += (long long)gridDim.x * blockDim.x) {
+        const int seg = (int)(i % segs);
+        long long r = i / segs;
+        const int g = (int)(r % nkv); r /= nkv;
+        const int t = (int)(r % T);
+        const int b = (int)(r / T);
+        const size_t src = (((size_t)b * T + t) * nkv + g) * d + seg * 8;
+        const size_t dst = (size_t)b * sb + (size_t)g * sh + (size_t)(st.v[b] + t) * d + seg * 8;
+        *reinterpret_cast<u32x4*>(kc + dst) = *reinterpret_cast<const u32x4*>(kn + src);
+        *reinterpret_cast<u32x4*>(vc + dst) = *reinterpret_cast<const u32x4*>(vn + src);
+    }
+}
+
+// out[k][n] = s * (code - zero) for logical column n (device column
+// col_map[n]), read from the tiled layout with the same unpacking as the
+// stage kernels.
+__global__ void debug_dequant_kernel(DevLinear W, const int32_t* __restrict__ col_map, int K, int N,
+                                     float* __restrict__ out) {
+    const long long total = (long long)K * N;
+    const int KB = W.K_pad / 64;
+    const int G = W.K_pad / W.KG;
+    for (long long i = blockIdx.x * (long long)blockDim.x + threadIdx.x; i < total;
+         i += (long long)gridDim.x * blockDim.x) {
+        const int k = (int)(i / N), n = (int)(i % N);
+        const int nd = col_map[n];
+        const int nt = nd / 32, cc = nd % 32;
+        const int kb = k / 64, kr = k % 64;
+        const int s = kr / 16, hh = (kr % 16) / 8, j = kr % 8;
+        const int lane = hh * 32 + cc;
+        const uint32_t w = W.qw[(((size_t)nt * KB + kb) * 64 + lane) * 4 + s];
+        const int g = k / G;
+        const f16x2 pr = dequant_pair(w, j / 2, zero_offset_pair(W.zeros, (size_t)nd * W.KG + g));
+        const float qz = (float)pr[j % 2];
+        const float sc = (float)__builtin_bit_cast(f16, W.scales[(size_t)nd * W.KG + g]);
+        out[i] = qz * sc;
+    }
+}
+
+}  // namespace
+
+int launch_rmsnorm(const float* x, const uint16_t* gamma, float eps, int M, int H, f16* out, hipStream_t stream) {
+    hipLaunchKernelGGL(rmsnorm_kernel, dim3(M), dim3(256), 0, stream, x, gamma, eps, H, out);
+    return hipGetLastError() == hipSuccess ? 0 : -1;
+}
+
+int launch_kv_append(uint16_t* k_cache, uint16_t* v_cache, const uint16_t* k_new, const uint16_t* v_new,
+                     int B, int T, int nkv, int d, long long stride_b, long long stride_h,
+                     const int32_t* slot_start_host, hipStream_t stream) {
+    SlotStarts st;
+    for (int b = 0; b < 64; b++) st.v[b] = b < B ? slot_start_host[b] : 0;
+    const long long total = (long long)B * T * nkv * (d / 8);
+    int blocks = (int)((total + 255) / 256);
+    if (blocks > 4096) blocks = 4096;
+    if (blocks < 1) blocks = 1;
+    hipLaunchKernelGGL(kv_append_kernel, dim3(blocks), dim3(256), 0, stream, k_cache, v_cache, k_new, v_new,
+                       B, T, nkv, d, stride_b, stride_h, st);
+    return hipGetLastError() == hipSuccess ? 0 : -1;
+}
+
+int launch_debug_dequant(const DevLinear& W, const int32_t* col_map, int K, int N, float* out, hipStream_t stream) {
+    const long long total = (long long)K * N;
+    int blocks = (int)((total + 255) / 256);
+    if (blocks > 8192) blocks = 8192;
+    hipLaunchKernelGGL(debug_dequant_kernel, dim3(blocks), dim3(256), 0, stream, W, col_map, K, N, out);
+    return hipGetLastError() == hipSuccess ? 0 : -1;
+}

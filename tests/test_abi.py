@@ -1,0 +1,86 @@
+"""The C ABI on the host, no GPU needed: the library loads and exports every
+function include/w4layer.h declares, the KV layout arithmetic, and the
+argument validation that happens before any HIP call."""
+import os
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+LIB = os.path.join(ROOT, "paper_2607_15865_amd", "libw4layer.so")
+
+if not os.path.exists(LIB):  # the driver builds first; build here if it has not
+    from paper_2607_15865_amd import build as _b
+    _b.build()
+
+from paper_2607_15865_amd import binding as B  # noqa: E402
+from paper_2607_15865_amd import synth  # noqa: E402
+from conftest import read_golden  # noqa: E402
+
+
+def test_every_declared_function_is_exported():
+    names = B.declared_functions()
+    assert {"layer_prefill", "layer_prefill_kv", "layer_decode", "kv_append", "kv_layout",
+            "layer_create", "layer_destroy", "layer_workspace_size"} <= set(names)
+    missing = [n for n in names if not B.exported(n)]
+    assert not missing, missing
+
+
+def test_kv_layout_strides():
+    cfg = synth.CONFIGS["llama8b"]
+    rc, d = B.kv_layout(cfg, 3)
+    assert rc == 0
+    assert (d.batch, d.n_kv_heads, d.max_seq, d.head_dim) == (3, 8, 4096, 128)
+    assert d.stride_s == 128 and d.stride_h == 4096 * 128 and d.stride_b == 8 * 4096 * 128
+    assert d.bytes == 3 * 8 * 4096 * 128 * 2
+    assert B.kv_layout(cfg, 0)[0] == B.W4_EINVAL
+
+
+def test_kv_bytes_of_the_paper_example():
+    """The worked example of Sec. 2.3: 32 layers, 100 tokens, 2 kv heads,
+    head_dim 128 -> K and V of 100 * 2 * 128 bf16 values per layer."""
+    cfg = synth.replace(synth.CONFIGS["llama8b"], n_kv_heads=2, max_seq=100)
+    rc, d = B.kv_layout(cfg, 1)
+    assert rc == 0
+    assert 32 * 2 * d.bytes == 32 * 2 * 100 * 2 * 128 * 2
+
+
+def test_stage_calls_validate_before_any_hip_call():
+    assert B.layer_prefill(None, 1, 1, 4, 1, 1, 2, 1, 1 << 20, 0) == B.W4_EINVAL
+    assert B.layer_prefill_kv(None, 1, 1, 4, 0, 1, 1, 2, 1, 1 << 20, 0) == B.W4_EINVAL
+    assert B.layer_decode(None, 1, 1, 1, 8, None, 1, 1, 1, 2, 1, 1 << 20, 0) == B.W4_EINVAL
+    assert "null layer" in B.layer_last_error()
+    assert B.layer_workspace_size(None, 0, 1, 16, 0) == 0
+    assert B.layer_debug_dequant(None, 0, 1, stream=0) == B.W4_EINVAL
+    assert B.layer_profile_kernel(None, 0, 1) == B.W4_EINVAL
+
+
+def test_kv_append_validation():
+    cfg = synth.CONFIGS["tiny"]
+    rc, d = B.kv_layout(cfg, 2)
+    assert B.kv_append(d, 1, 1, 1, 1, 2, 4, [0, cfg.max_seq - 3], stream=0) == B.W4_ECAPACITY
+    assert B.kv_append(d, 1, 1, 1, 1, 3, 4, [0, 0, 0], stream=0) == B.W4_ECAPACITY
+    assert B.kv_append(d, 1, 1, 1, 1, 2, 0, [0, 0], stream=0) == B.W4_EINVAL
+    assert B.kv_append(d, 1, 1, 1, 1, 2, 4, [-1, 0], stream=0) == B.W4_ECAPACITY
+
+
+@pytest.mark.parametrize("field,value,code", [
+    ("head_dim", 96, B.W4_EUNSUPPORTED), ("n_kv_heads", 3, B.W4_EUNSUPPORTED),
+    ("group_size", 48, B.W4_EUNSUPPORTED), ("hidden", 200, B.W4_EUNSUPPORTED),
+    ("ffn", 690, B.W4_EUNSUPPORTED), ("hidden", 0, B.W4_EINVAL), ("max_seq", 0, B.W4_EINVAL),
+    ("n_heads", 36, B.W4_EUNSUPPORTED)])
+def test_layer_create_rejects_bad_configs(field, value, code):
+    cfg = synth.replace(synth.CONFIGS["tiny"], **{field: value})
+    w = synth.make_layer(synth.CONFIGS["tiny"])
+    rc, h = B.layer_create(cfg, w)
+    assert rc == code, (field, value, rc, B.layer_last_error())
+    assert not h
+
+
+def test_bandwidth_utilisation_definition():
+    """Bandwidth utilisation as Sec. 5.1 defines it (tokens/s x model size /
+    peak bandwidth) reproduces Table 2 within its printed rounding."""
+    for row in read_golden("table2_bw_util.txt"):
+        size, tps, printed = float(row[1]), float(row[2]), float(row[3])
+        util = 100.0 * tps * size / 64.0
+        assert abs(util - printed) < 0.5, row

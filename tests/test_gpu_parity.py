@@ -1,0 +1,218 @@
+"""Parity of the three stages on the GPU against the CPU oracle, element by
+element on the same seeded inputs: y (fp32) and the new cache entries, within
+max-abs 2e-2 and relative Frobenius 1e-2.  Sizes run from the tiny layer
+(several tiles and ragged tails) to the full Qwen/Llama-shaped layers, where
+the oracle evaluates a sample of rows."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import layer as O
+from paper_2607_15865_amd import synth
+from gpu_helpers import (assert_parity, bits_to_torch_f32, cache_values, device_layer, host_layer, log,
+                         oracle_weights, to_cache_bits)
+
+pytestmark = pytest.mark.gpu
+
+
+def _x(cfg, tid, rows):
+    bits = synth.activations(cfg, tid, rows)
+    return bits, O.bf16_to_f64(bits)
+
+
+def _check_new_kv(k, v, ok, ov, start, T, seq=0, rows=None):
+    gk = cache_values(k)[seq][:, start:start + T, :].transpose(1, 0, 2)
+    gv = cache_values(v)[seq][:, start:start + T, :].transpose(1, 0, 2)
+    if rows is not None:
+        gk, gv, ok, ov = gk[rows], gv[rows], ok[rows], ov[rows]
+    assert_parity(gk, ok, "new K")
+    assert_parity(gv, ov, "new V")
+    flips = np.mean(gk != ok)
+    log(f"  new K entries differing from the oracle's bf16 value: {flips:.2e}")
+    assert flips < 0.05
+
+
+PREFILL_CASES = [("tiny", 32, None), ("tiny", 1, None), ("tiny", 77, None), ("qwen05b", 256, None),
+                 ("llama8b", 512, None), ("qwen7b", 2048, [0, 1, 2, 3, 7, 31, 32, 127, 128, 129, 511, 1000, 1023,
+                                                          1024, 1535, 2000, 2046, 2047])]
+
+
+@pytest.mark.parametrize("name,T,rows", PREFILL_CASES)
+def test_prefill(name, T, rows):
+    cfg, w = host_layer(name)
+    W = oracle_weights(name)
+    lay = device_layer(name)
+    log(f"prefill {name} T={T}")
+    xb, xv = _x(cfg, synth.TID_X_PREFILL, T)
+    pos = np.arange(T)
+    k, v = lay.new_cache(1, 0)
+    x = bits_to_torch_f32(xb)
+    y = torch.empty_like(x)
+    lay.prefill(x, torch.from_numpy(pos.astype(np.int32)).cuda(), k, v, y)
+    torch.cuda.synchronize()
+    yo, ko, vo = O.prefill(w, cfg, xv, pos, rows=rows, W=W)
+    gy = y.cpu().numpy().astype(np.float64)
+    assert_parity(gy if rows is None else gy[rows], yo, "y")
+    _check_new_kv(k, v, ko, vo, 0, T)
+
+
+PKV_CASES = [("tiny", 16, 32), ("tiny", 5, 100), ("qwen05b", 64, 256), ("llama8b", 128, 1024)]
+
+
+@pytest.mark.parametrize("name,T,L", PKV_CASES)
+def test_prefill_kv(name, T, L):
+    """History = the oracle's own prefill of L tokens (bf16 values), given to
+    both sides; then a chunk of T new tokens."""
+    cfg, w = host_layer(name)
+    W = oracle_weights(name)
+    lay = device_layer(name)
+    log(f"prefill_kv {name} T={T} L={L}")
+    xh_bits, xh = _x(cfg, synth.TID_X_PREFILL, L)
+    _, kh, vh = O.prefill(w, cfg, xh, np.arange(L), rows=[L - 1], W=W)
+    kc = np.zeros((cfg.n_kv_heads, cfg.max_seq, cfg.head_dim))
+    kc = O.cache_write(kc, kh, 0)
+    vc = O.cache_write(np.zeros_like(kc), vh, 0)
+    k = torch.from_numpy(to_cache_bits(kc)[None]).cuda()
+    v = torch.from_numpy(to_cache_bits(vc)[None]).cuda()
+    xb, xv = _x(cfg, synth.TID_X_PREFILL_KV, T)
+    pos = np.arange(L, L + T)
+    x = bits_to_torch_f32(xb)
+    y = torch.empty_like(x)
+    lay.prefill_kv(x, torch.from_numpy(pos.astype(np.int32)).cuda(), L, k, v, y)
+    torch.cuda.synchronize()
+    yo, ko, vo = O.prefill_kv(w, cfg, xv, pos, kc, vc, L, W=W)
+    assert_parity(y.cpu().numpy(), yo, "y")
+    _check_new_kv(k, v, ko, vo, L, T)
+
+
+DECODE_CASES = [("tiny", 1, [48]), ("tiny", 4, [0, 9, 64, 126]), ("qwen05b", 1, [512]), ("llama8b", 1, [2048]),
+                ("qwen7b", 1, [8192]), ("qwen7b", 8, [8192, 17, 4000, 8191, 1, 2048, 6000, 8100])]
+
+
+@pytest.mark.parametrize("name,B,ctx", DECODE_CASES)
+def test_decode(name, B, ctx):
+    """Decode against an N(0,1) bf16 cache (the synthetic cache of the decode
+    workloads)."""
+    cfg, w = host_layer(name)
+    W = oracle_weights(name)
+    lay = device_layer(name)
+    log(f"decode {name} B={B} ctx={ctx}")
+    kb, vb = synth.kv_fill(cfg, B)
+    kc, vc = O.bf16_to_f64(kb), O.bf16_to_f64(vb)
+    ctx = np.array(ctx, dtype=np.int32)
+    pos = ctx.copy()
+    xb, xv = _x(cfg, synth.TID_X_DECODE, B)
+    k = torch.from_numpy(kb.view(np.int16)).cuda()
+    v = torch.from_numpy(vb.view(np.int16)).cuda()
+    x = bits_to_torch_f32(xb)
+    y = torch.empty_like(x)
+    ctx_d = torch.from_numpy(ctx).cuda()
+    lay.decode(x, torch.from_numpy(pos).cuda(), ctx_d, int(ctx.max()), k, v, y)
+    torch.cuda.synchronize()
+    yo, ko, vo = O.decode(w, cfg, xv, pos, kc, vc, ctx, W=W)
+    assert_parity(y.cpu().numpy(), yo, "y")
+    gk, gv = cache_values(k), cache_values(v)
+    gkn = np.stack([gk[b][:, ctx[b], :] for b in range(B)])
+    gvn = np.stack([gv[b][:, ctx[b], :] for b in range(B)])
+    assert_parity(gkn, ko, "new K")
+    assert_parity(gvn, vo, "new V")
+
+
+def test_decode_mask():
+    """The external decode mask: all-zero equals no mask; -inf at slot j
+    removes key j; a row with every visible slot masked gives a zero
+    attention output (y = h)."""
+    name = "qwen05b"
+    cfg, w = host_layer(name)
+    W = oracle_weights(name)
+    lay = device_layer(name)
+    B = 3
+    kb, vb = synth.kv_fill(cfg, B)
+    kc, vc = O.bf16_to_f64(kb), O.bf16_to_f64(vb)
+    ctx = np.array([300, 511, 64], dtype=np.int32)
+    xb, xv = _x(cfg, synth.TID_X_DECODE, B)
+    mask = np.zeros((B, cfg.max_seq), dtype=np.float32)
+    rng = np.random.default_rng(5)
+    mask[0, rng.choice(300, 40, replace=False)] = -np.inf
+    mask[1, :] = rng.normal(0, 2, cfg.max_seq).astype(np.float32)
+    mask[2, :65] = -np.inf
+    outs = []
+    for m in (None, np.zeros_like(mask), mask):
+        k = torch.from_numpy(kb.view(np.int16)).cuda()
+        v = torch.from_numpy(vb.view(np.int16)).cuda()
+        x = bits_to_torch_f32(xb)
+        y = torch.empty_like(x)
+        md = None if m is None else torch.from_numpy(m).cuda()
+        lay.decode(x, torch.from_numpy(ctx).cuda(), torch.from_numpy(ctx).cuda(), int(ctx.max()), k, v, y, md)
+        torch.cuda.synchronize()
+        outs.append(y.cpu().numpy())
+    assert np.array_equal(outs[0], outs[1]) or np.max(np.abs(outs[0] - outs[1])) < 1e-5
+    yo, _, _ = O.decode(w, cfg, xv, ctx, kc, vc, ctx, mask.astype(np.float64), W=W)
+    assert_parity(outs[2], yo, "y masked")
+
+
+def test_decode_batch_rows_match_single():
+    name = "tiny"
+    cfg, w = host_layer(name)
+    lay = device_layer(name)
+    B = 8
+    kb, vb = synth.kv_fill(cfg, B)
+    ctx = np.array([3, 100, 50, 127 - 1, 0, 64, 65, 31], dtype=np.int32)
+    xb, _ = _x(cfg, synth.TID_X_DECODE, B)
+    x = bits_to_torch_f32(xb)
+
+    def run(sel):
+        k = torch.from_numpy(kb[sel].view(np.int16).copy()).cuda()
+        v = torch.from_numpy(vb[sel].view(np.int16).copy()).cuda()
+        c = torch.from_numpy(ctx[sel].copy()).cuda()
+        y = torch.empty((len(sel), cfg.hidden), dtype=torch.float32, device="cuda")
+        lay.decode(x[sel].contiguous(), c, c, int(ctx[sel].max()), k, v, y)
+        torch.cuda.synchronize()
+        return y.cpu().numpy()
+
+    yall = run(list(range(B)))
+    for b in range(B):
+        yb = run([b])
+        assert np.max(np.abs(yb[0] - yall[b])) < 1e-4, b
+
+
+def test_chain_prefill_prefill_kv_decode():
+    """The paper's runtime order (Sec. 4.5) on the GPU's own caches: prefill 32
+    tokens, prefill_kv 16 more, then 16 decode steps, against the oracle
+    running the same chain on its own caches."""
+    name = "tiny"
+    cfg, w = host_layer(name)
+    W = oracle_weights(name)
+    lay = device_layer(name)
+    P, C, D = 32, 16, 16
+    k, v = lay.new_cache(1, 0)
+    kc = np.zeros((cfg.n_kv_heads, cfg.max_seq, cfg.head_dim))
+    vc = np.zeros_like(kc)
+    xb, xv = _x(cfg, synth.TID_X_PREFILL, P)
+    x = bits_to_torch_f32(xb)
+    y = torch.empty_like(x)
+    lay.prefill(x, torch.arange(P, dtype=torch.int32, device="cuda"), k, v, y)
+    yo, ko, vo = O.prefill(w, cfg, xv, np.arange(P), W=W)
+    kc, vc = O.cache_write(kc, ko, 0), O.cache_write(vc, vo, 0)
+    assert_parity(y.cpu().numpy(), yo, "prefill y")
+    xb, xv = _x(cfg, synth.TID_X_PREFILL_KV, C)
+    x = bits_to_torch_f32(xb)
+    y = torch.empty_like(x)
+    lay.prefill_kv(x, torch.arange(P, P + C, dtype=torch.int32, device="cuda"), P, k, v, y)
+    yo, ko, vo = O.prefill_kv(w, cfg, xv, np.arange(P, P + C), kc, vc, P, W=W)
+    kc, vc = O.cache_write(kc, ko, P), O.cache_write(vc, vo, P)
+    assert_parity(y.cpu().numpy(), yo, "prefill_kv y")
+    for s in range(D):
+        t = P + C + s
+        xb = synth.activations(cfg, synth.TID_X_DECODE + 1000 * s, 1)
+        x = bits_to_torch_f32(xb)
+        y = torch.empty_like(x)
+        td = torch.tensor([t], dtype=torch.int32, device="cuda")
+        lay.decode(x, td, td, t, k, v, y)
+        yo, ko, vo = O.decode(w, cfg, O.bf16_to_f64(xb), [t], kc[None], vc[None], [t], W=W)
+        kc, vc = O.cache_write(kc, ko, t), O.cache_write(vc, vo, t)
+        assert_parity(y.cpu().numpy(), yo, f"decode step {s} y")
+    torch.cuda.synchronize()
+    n = P + C + D
+    assert_parity(cache_values(k)[0][:, :n], kc[:, :n], "cache K")
+    assert_parity(cache_values(v)[0][:, :n], vc[:, :n], "cache V")
