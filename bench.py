@@ -148,7 +148,7 @@ def main():
     stream = torch.cuda.current_stream()
     sp = stream.cuda_stream
 
-    PREFILL_GU, DECODE_GU = 5, 4
+    PREFILL_GU, DECODE_FUSED = 5, 6
 
     def step(i, ev=None):
         lay = layers[i % len(layers)].handle
@@ -168,7 +168,7 @@ def main():
 
     for lay in layers:
         binding.check(binding.layer_profile_kernel(lay.handle, 0, PREFILL_GU))
-        binding.check(binding.layer_profile_kernel(lay.handle, 2, DECODE_GU))
+        binding.check(binding.layer_profile_kernel(lay.handle, 2, DECODE_FUSED))
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -217,12 +217,11 @@ def main():
                 "peak": PEAK_MFMA_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(gu_flop / (gu_avg * 1e-3) / 1e12 / PEAK_MFMA_TFLOPS, 4),
                 "avg_us": round(gu_avg * 1e3, 2), "launches": gu_n, "traffic": None}
-    dgu_bytes = weight_bytes(cfg, ["gate", "up"])
     dgu_avg = dgu_ms / max(dgu_n, 1)
-    roofline_decode = {"kernel": "decode gate/up W4 GEMV (1 x 28672 x 4096, RMSNorm prologue)",
-                       "bound": "hbm", "achieved": round(dgu_bytes / (dgu_avg * 1e-3) / 1e9, 1),
+    roofline_decode = {"kernel": "persistent decode kernel (whole decode step, B=1, ctx 2048)",
+                       "bound": "hbm", "achieved": round(by_d / (dgu_avg * 1e-3) / 1e9, 1),
                        "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                       "frac": round(dgu_bytes / (dgu_avg * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+                       "frac": round(by_d / (dgu_avg * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
                        "avg_us": round(dgu_avg * 1e3, 2), "launches": dgu_n, "traffic": None}
     out = {
         "metric": "decode layer-steps/s (+ prefill/prefill_kv TFLOP/s) of a W4A16 Llama-3-8B-shaped layer",

@@ -206,11 +206,35 @@ int kv_append(const kv_desc* desc, void* k_cache, void* v_cache,
  * Errors: W4_EINVAL, W4_EHIP. */
 int layer_debug_dequant(layer_t layer, int32_t which, float* out, void* stream);
 
+/* Decode implementation (tuning / testing): 0 automatic (default), 1 a
+ * sequence of kernels, 2 one persistent cooperative launch with one block per
+ * CU (used automatically for B <= 4 when its on-chip working set fits; calls
+ * of that path on one layer must not run concurrently, since they share the
+ * layer's grid-barrier state).  Both compute the same result.  With 2, a
+ * decode call the persistent path cannot serve fails with W4_EUNSUPPORTED.
+ * Errors: W4_EINVAL. */
+int layer_set_decode_path(layer_t layer, int32_t path);
+
+/* Diagnostics of the persistent decode path: durations in microseconds of
+ * its five phases in the last completed call (q/k/v, attention, o_proj,
+ * gate/up, down; measured by block 0 between grid barriers, the last one up
+ * to the end of the last block) into us_out[5], and the error flag raised by
+ * a grid-barrier timeout (0 = none) into *error_flag (nullable).  Waits for
+ * the device.  Errors: W4_EINVAL, W4_EHIP. */
+int layer_decode_phase_times(layer_t layer, float* us_out, int32_t* error_flag);
+
+/* Raw wall-clock stamps of the last persistent decode call (diagnostics):
+ * [0..5] phase boundaries as above, then for phase p (0..4) and block j the
+ * block's arrival at the barrier that ends the phase at [8 + p*nblocks + j].
+ * Copies min(n, 8 + 5*1024) values.  Waits for the device. */
+int layer_debug_decode_stamps(layer_t layer, uint64_t* out, int32_t n);
+
 /* Per-kernel timing for measurement (diagnostics, not for concurrent use).
  * layer_profile_kernel selects, for one stage, the kernel to time (stage 0 and
  * 1, prefill and prefill_kv: 0 rmsnorm, 1 qkv GEMM, 2 attention, 3 o_proj
  * GEMM, 4 rmsnorm, 5 gate/up GEMM, 6 down GEMM; stage 2, decode: 0 qkv GEMV,
- * 1 attention (split + combine), 3 o_proj GEMV, 4 gate/up GEMV, 5 down GEMV);
+ * 1 attention (split + combine), 3 o_proj GEMV, 4 gate/up GEMV, 5 down GEMV,
+ * 6 the whole persistent decode launch);
  * kernel < 0 switches timing of that stage off.  While selected, each stage
  * call records a HIP event pair around that launch on the call's stream (at
  * most 4096 pairs per stage until the next read).  layer_profile_read waits

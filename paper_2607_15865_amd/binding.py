@@ -76,6 +76,9 @@ _SIG = {
     "layer_decode": (ctypes.c_int, [_P, _P, _P, _P, _I, _P, _I, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "kv_append": (ctypes.c_int, [ctypes.POINTER(kv_desc), _P, _P, _P, _P, _I, _I, _P, _P]),
     "layer_debug_dequant": (ctypes.c_int, [_P, _I, _P, _P]),
+    "layer_set_decode_path": (ctypes.c_int, [_P, _I]),
+    "layer_decode_phase_times": (ctypes.c_int, [_P, _P, _P]),
+    "layer_debug_decode_stamps": (ctypes.c_int, [_P, _P, _I]),
     "layer_profile_kernel": (ctypes.c_int, [_P, _I, _I]),
     "layer_profile_read": (ctypes.c_int, [_P, _I, ctypes.POINTER(ctypes.c_float), ctypes.POINTER(ctypes.c_int32)]),
     "layer_last_error": (ctypes.c_char_p, []),
@@ -207,6 +210,23 @@ def layer_debug_dequant(handle, which, out, stream=None) -> int:
     return _lib.layer_debug_dequant(handle, which, _ptr(out), _stream(stream))
 
 
+def layer_decode_phase_times(handle):
+    us = (ctypes.c_float * 5)()
+    err = ctypes.c_int32()
+    rc = _lib.layer_decode_phase_times(handle, ctypes.cast(us, ctypes.c_void_p), ctypes.cast(ctypes.pointer(err), ctypes.c_void_p))
+    return rc, list(us), err.value
+
+
+def layer_debug_decode_stamps(handle, n: int = 8 + 5 * 1024):
+    out = np.zeros(n, dtype=np.uint64)
+    rc = _lib.layer_debug_decode_stamps(handle, out.ctypes.data, n)
+    return rc, out
+
+
+def layer_set_decode_path(handle, path: int) -> int:
+    return _lib.layer_set_decode_path(handle, path)
+
+
 def layer_profile_kernel(handle, stage: int, kernel: int) -> int:
     return _lib.layer_profile_kernel(handle, stage, kernel)
 
@@ -277,6 +297,10 @@ class Layer:
         B = x.shape[0]
         ws, n = self.workspace(STAGE_DECODE, B, 1, max_ctx)
         check(layer_decode(self.handle, x, pos, ctx_lens, max_ctx, attn_mask, B, k_cache, v_cache, y, ws, n, stream))
+
+    def set_decode_path(self, path: int):
+        """0 automatic, 1 separate kernels, 2 one persistent launch."""
+        check(layer_set_decode_path(self.handle, path))
 
     def debug_dequant(self, which):
         import torch

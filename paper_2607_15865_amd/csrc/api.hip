@@ -14,6 +14,7 @@
 
 #include "../../include/w4layer.h"
 #include "common.h"
+#include "decode_fused.h"
 #include "launch.h"
 
 namespace {
@@ -147,6 +148,13 @@ struct layer_s {
     DevBuf attn_norm, mlp_norm, rope_cos, rope_sin;
     int device = 0;
     Profiler prof;
+    // persistent decode: barrier, completion counters and error flag (zeroed)
+    DevBuf sync;
+    unsigned *bar = nullptr, *cnt_qkv = nullptr, *cnt_gu = nullptr, *cnt_attn = nullptr, *cnt_o = nullptr,
+             *cnt_down = nullptr;
+    int* err = nullptr;
+    unsigned long long* stamps = nullptr;
+    int decode_path = 0;   // 0 auto, 1 separate kernels, 2 persistent
 };
 
 namespace {
@@ -193,6 +201,8 @@ int build_linear(DevLinearOwned& out, const std::vector<ColSrc>& cols, int K, in
     d.K_pad = K_pad;
     d.N_dev = N_dev;
     d.KG = KG;
+    d.lgG = 0;
+    while ((1 << d.lgG) < G) d.lgG++;
     return 0;
 }
 
@@ -275,6 +285,66 @@ DecodeWs plan_decode(const layer_s* L, int B, int max_ctx) {
     w.g = cv.take((size_t)B * L->F_pad * 2);
     w.total = cv.off;
     return w;
+}
+
+// ---- persistent decode plan
+struct FusedPlan {
+    bool ok = false;
+    int nblocks = 0, chunk = 0, nchunk = 0;
+    int tpw_qkv = 0, tpw_o = 0, tpw_gu = 0, tpw_down = 0, segmax_qkv = 0, segmax_gu = 0, segmax_o = 0, segmax_down = 0;
+    size_t lds_act = 0, lds_bytes = 0;
+    size_t h, part_qkv, part_gu, part_o, part_down, q_fin, kv_new, apart, A, g, total;
+};
+
+FusedPlan plan_fused(const layer_s* L, int B, int max_ctx, bool query_device) {
+    FusedPlan p;
+    const layer_config& c = L->cfg;
+    if (B > 4 || L->decode_path == 1) return p;
+    const int d = c.head_dim, qd = c.n_heads * d, r = c.n_heads / c.n_kv_heads;
+    const size_t act = (size_t)B * std::max(std::max(c.hidden, qd), L->F_pad) * 2;
+    p.lds_act = (act + 255) / 256 * 256;
+    p.nblocks = 256;
+    if (query_device) {
+        int dev = 0, cus = 0;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+            return p;
+        p.nblocks = cus;
+    }
+    const int per_group = std::max(1, p.nblocks / (B * c.n_kv_heads));
+    int ch = (max_ctx + 1 + per_group - 1) / per_group;
+    ch = std::max(16, std::min(512, (ch + 15) / 16 * 16));
+    p.chunk = ch;
+    p.nchunk = (max_ctx + 1 + ch - 1) / ch;
+    const size_t attn_lds = (size_t)(8 * ch + 8 * 8 * d + 16) * 4;
+    p.lds_bytes = std::max(p.lds_act + 256, attn_lds);
+    if (p.lds_bytes > 160 * 1024) return p;
+    if (query_device && decode_fused_blocks(d, B, p.lds_bytes) != p.nblocks) return p;
+    const int nw = p.nblocks * 8;
+    auto tpw = [&](const DevLinear& W) { const long long T = (long long)(W.N_dev / 32) * (W.K_pad / 64); return (int)((T + nw - 1) / nw); };
+    p.tpw_qkv = tpw(L->qkv.d);
+    p.tpw_o = tpw(L->o.d);
+    p.tpw_gu = tpw(L->gu.d);
+    p.tpw_down = tpw(L->down.d);
+    p.segmax_qkv = (L->qkv.d.K_pad / 64 + p.tpw_qkv - 1) / p.tpw_qkv + 1;
+    p.segmax_gu = (L->gu.d.K_pad / 64 + p.tpw_gu - 1) / p.tpw_gu + 1;
+    p.segmax_o = (L->o.d.K_pad / 64 + p.tpw_o - 1) / p.tpw_o + 1;
+    p.segmax_down = (L->down.d.K_pad / 64 + p.tpw_down - 1) / p.tpw_down + 1;
+    Carve cv;
+    p.h = cv.take((size_t)B * c.hidden * 4);
+    p.part_qkv = cv.take((size_t)(L->qkv.d.N_dev / 32) * p.segmax_qkv * B * 32 * 4);
+    p.part_gu = cv.take((size_t)(L->gu.d.N_dev / 32) * p.segmax_gu * B * 32 * 4);
+    p.part_o = cv.take((size_t)(L->o.d.N_dev / 32) * p.segmax_o * B * 32 * 4);
+    p.part_down = cv.take((size_t)(L->down.d.N_dev / 32) * p.segmax_down * B * 32 * 4);
+    p.q_fin = cv.take((size_t)B * qd * 2);
+    p.kv_new = cv.take((size_t)B * 2 * c.n_kv_heads * d * 2);
+    p.apart = cv.take((size_t)B * c.n_heads * p.nchunk * (d + 2) * 4);
+    p.A = cv.take((size_t)B * qd * 2);
+    p.g = cv.take((size_t)B * L->F_pad * 2);
+    p.total = cv.off;
+    (void)r;
+    p.ok = true;
+    return p;
 }
 
 int gemv_ksplit(const DevLinear& W, int want_blocks, int B) {
@@ -498,6 +568,22 @@ int layer_create(const layer_config* cfg, const layer_weights_host* w, layer_t* 
         delete L;
         return rc;
     }
+    {
+        const size_t n_bar = 4096, n_qkv = (size_t)(qd + 2 * kvd) / 64, n_gu = (size_t)F_pad / 32,
+                     n_attn = (size_t)c.max_batch * nkv, n_col = (size_t)H / 32;
+        const size_t words = n_bar + n_qkv + n_gu + n_attn + 2 * n_col + 64 + 16 + 2 * (8 + 5 * 1024);
+        std::vector<unsigned> zero(words, 0u);
+        if ((rc = upload(L->sync, zero.data(), words * 4))) { delete L; return rc; }
+        unsigned* base = (unsigned*)L->sync.p;
+        L->bar = base;
+        L->cnt_qkv = base + n_bar;
+        L->cnt_gu = L->cnt_qkv + n_qkv;
+        L->cnt_attn = L->cnt_gu + n_gu;
+        L->cnt_o = L->cnt_attn + n_attn;
+        L->cnt_down = L->cnt_o + n_col;
+        L->err = (int*)(L->cnt_down + n_col);
+        L->stamps = (unsigned long long*)(((uintptr_t)(L->cnt_down + n_col + 16) + 63) & ~(uintptr_t)63);
+    }
     *out = L;
     return W4_OK;
 }
@@ -517,7 +603,10 @@ size_t layer_workspace_size(layer_t L, int32_t stage, int32_t batch, int32_t T, 
     }
     if (stage == 2) {
         if (batch < 1 || max_ctx < 0) return 0;
-        return plan_decode(L, batch, max_ctx).total;
+        size_t n = plan_decode(L, batch, max_ctx).total;
+        const FusedPlan fp = plan_fused(L, batch, max_ctx, true);
+        if (fp.ok) n = std::max(n, fp.total);
+        return n;
     }
     return 0;
 }
@@ -543,9 +632,51 @@ int layer_decode(layer_t L, const float* x, const int32_t* pos, const int32_t* c
     if (B > c.max_batch) return fail(W4_ECAPACITY, "B = %d exceeds max_batch %d", B, c.max_batch);
     if (B > 8) return fail(W4_EUNSUPPORTED, "decode batch above 8");
     if ((long long)max_ctx + 1 > c.max_seq) return fail(W4_ECAPACITY, "max_ctx + 1 = %lld exceeds max_seq %d", (long long)max_ctx + 1, c.max_seq);
+    hipStream_t st = (hipStream_t)stream;
+    const FusedPlan fp = plan_fused(L, B, max_ctx, true);
+    if (L->decode_path == 2 && !fp.ok) return fail(W4_EUNSUPPORTED, "persistent decode not possible for this shape/batch");
+    if (fp.ok) {
+        if (ws_bytes < fp.total) return fail(W4_EWORKSPACE, "workspace %zu bytes, need %zu", ws_bytes, fp.total);
+        char* base = (char*)ws;
+        DecodeFusedArgs a{};
+        a.qkv = L->qkv.d; a.o = L->o.d; a.gu = L->gu.d; a.down = L->down.d;
+        a.attn_norm = (const uint16_t*)L->attn_norm.p;
+        a.mlp_norm = (const uint16_t*)L->mlp_norm.p;
+        a.eps = c.rms_eps;
+        a.rope_cos = (const float*)L->rope_cos.p;
+        a.rope_sin = (const float*)L->rope_sin.p;
+        a.H = c.hidden; a.nq = c.n_heads; a.nkv = c.n_kv_heads; a.d = c.head_dim; a.F_pad = L->F_pad; a.B = B;
+        a.x = x; a.pos = pos; a.ctx_lens = ctx_lens; a.mask = attn_mask; a.max_seq = c.max_seq;
+        a.k_cache = (uint16_t*)kc; a.v_cache = (uint16_t*)vc;
+        a.sh = (long long)c.max_seq * c.head_dim; a.sb = a.sh * c.n_kv_heads;
+        a.y = y;
+        a.h = (float*)(base + fp.h);
+        a.part_qkv = (float*)(base + fp.part_qkv);
+        a.part_gu = (float*)(base + fp.part_gu);
+        a.part_o = (float*)(base + fp.part_o);
+        a.part_down = (float*)(base + fp.part_down);
+        a.q_fin = (uint16_t*)(base + fp.q_fin);
+        a.kv_new = (uint16_t*)(base + fp.kv_new);
+        a.apart = (float*)(base + fp.apart);
+        a.A = (f16*)(base + fp.A);
+        a.g = (f16*)(base + fp.g);
+        a.bar = L->bar; a.cnt_qkv = L->cnt_qkv; a.cnt_gu = L->cnt_gu; a.cnt_attn = L->cnt_attn; a.err = L->err;
+        a.cnt_o = L->cnt_o; a.cnt_down = L->cnt_down; a.stamps = L->stamps;
+        a.tpw_qkv = fp.tpw_qkv; a.tpw_o = fp.tpw_o; a.tpw_gu = fp.tpw_gu; a.tpw_down = fp.tpw_down;
+        a.segmax_qkv = fp.segmax_qkv; a.segmax_gu = fp.segmax_gu; a.segmax_o = fp.segmax_o;
+        a.segmax_down = fp.segmax_down;
+        a.chunk = fp.chunk; a.nchunk = fp.nchunk;
+        a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)c.head_dim));
+        a.nblocks = fp.nblocks;
+        a.lds_act = fp.lds_act;
+        a.lds_bytes = fp.lds_bytes;
+        int rc;
+        { ProfScope ps(L, 2, 6, st); rc = launch_decode_fused(a, st); }
+        if (rc) return fail(W4_EHIP, "persistent decode launch failed: %s", hipGetErrorString(hipGetLastError()));
+        return W4_OK;
+    }
     const DecodeWs w = plan_decode(L, B, max_ctx);
     if (ws_bytes < w.total) return fail(W4_EWORKSPACE, "workspace %zu bytes, need %zu", ws_bytes, w.total);
-    hipStream_t st = (hipStream_t)stream;
     char* base = (char*)ws;
     uint16_t* q = (uint16_t*)(base + w.q);
     float* part = (float*)(base + w.part);
@@ -669,6 +800,34 @@ int layer_debug_dequant(layer_t L, int32_t which, float* out, void* stream) {
     }
     if (launch_debug_dequant(dl->d, (const int32_t*)map, K, N, out, (hipStream_t)stream))
         return fail(W4_EHIP, "debug dequant launch failed: %s", hipGetErrorString(hipGetLastError()));
+    return W4_OK;
+}
+
+int layer_decode_phase_times(layer_t L, float* us_out, int32_t* error_flag) {
+    if (!L || !us_out) return fail(W4_EINVAL, "null argument");
+    unsigned long long ts[6];
+    int err = 0;
+    HIP_TRY(hipDeviceSynchronize());
+    HIP_TRY(hipMemcpy(ts, L->stamps, sizeof ts, hipMemcpyDeviceToHost));
+    HIP_TRY(hipMemcpy(&err, L->err, sizeof err, hipMemcpyDeviceToHost));
+    int khz = 0;
+    HIP_TRY(hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, L->device));
+    for (int i = 0; i < 5; i++) us_out[i] = khz > 0 ? (float)((double)(ts[i + 1] - ts[i]) * 1000.0 / khz) : 0.f;
+    if (error_flag) *error_flag = err;
+    return W4_OK;
+}
+
+int layer_debug_decode_stamps(layer_t L, uint64_t* out, int32_t n) {
+    if (!L || !out || n < 0) return fail(W4_EINVAL, "bad argument");
+    HIP_TRY(hipDeviceSynchronize());
+    HIP_TRY(hipMemcpy(out, L->stamps, (size_t)std::min(n, 8 + 5 * 1024) * 8, hipMemcpyDeviceToHost));
+    return W4_OK;
+}
+
+int layer_set_decode_path(layer_t L, int32_t path) {
+    if (!L) return fail(W4_EINVAL, "null layer");
+    if (path < 0 || path > 2) return fail(W4_EINVAL, "path must be 0, 1 or 2");
+    L->decode_path = path;
     return W4_OK;
 }
 

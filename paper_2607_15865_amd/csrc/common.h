@@ -128,6 +128,7 @@ struct DevLinear {
     const uint8_t* zeros;    // [N_dev][KG] or null
     int K, N;                // logical
     int K_pad, N_dev, KG;    // padded rows, device columns, groups
+    int lgG;                 // log2 of the group size (a power of two)
 };
 
 // Epilogue kinds shared by the GEMM (prefill) and GEMV (decode).

@@ -34,7 +34,7 @@ __global__ void __launch_bounds__(256) gemm_w4_kernel(const f16* __restrict__ X,
     const int n0 = blockIdx.x * BN;
     const int h = lane >> 5, c = lane & 31;
     const int KB = W.K_pad / BK;
-    const int G = W.K_pad / W.KG;          // group size in k
+    const int Gm1 = (1 << W.lgG) - 1;      // group size in k, minus one
 
     // weight tiles of this wave: n-tiles nt0, nt0 + 1
     const int nt0 = (n0 + wn * 64) / 32;
@@ -89,8 +89,8 @@ __global__ void __launch_bounds__(256) gemm_w4_kernel(const f16* __restrict__ X,
 #pragma unroll
         for (int s = 0; s < 4; s++) {
             const int k = kb * BK + s * 16;
-            if (k % G == 0 && k > 0) {
-                const int g = k / G;
+            if ((k & Gm1) == 0 && k > 0) {
+                const int g = k >> W.lgG;
                 const float r0 = W.ratios[(size_t)col0 * W.KG + g];
                 const float r1 = W.ratios[(size_t)col1 * W.KG + g];
 #pragma unroll

@@ -38,8 +38,6 @@ __global__ void __launch_bounds__(NW * 64) gemv_w4_kernel(GemvArgs a) {
     const int kb_hi = (int)((long long)(blockIdx.y + 1) * KB / a.ksplit);
     const int klo = kb_lo * 64, klen = (kb_hi - kb_lo) * 64;
     const int B = a.B;
-    const int G = W.K_pad / W.KG;
-
     f16* xs = reinterpret_cast<f16*>(smem);                        // [B][klen]
     float* red = reinterpret_cast<float*>(smem + (size_t)MAXB * klen * 2);  // [NSUB][2][MAXB][32]
     float* rinv = red + NSUB * 2 * MAXB * 32;                        // [MAXB]
@@ -110,7 +108,7 @@ __global__ void __launch_bounds__(NW * 64) gemv_w4_kernel(GemvArgs a) {
 #pragma unroll
             for (int s = 0; s < 4; s++) {
                 const int k = kb * 64 + s * 16 + h * 8;
-                const int g = k / G;
+                const int g = (kb * 64 + s * 16) >> W.lgG;
                 if (g != cur_g) {
 #pragma unroll
                     for (int b = 0; b < MAXB; b++) { acc[b] += sc * gacc[b]; gacc[b] = 0.f; }

@@ -54,7 +54,6 @@ __global__ void debug_dequant_kernel(DevLinear W, const int32_t* __restrict__ co
                                      float* __restrict__ out) {
     const long long total = (long long)K * N;
     const int KB = W.K_pad / 64;
-    const int G = W.K_pad / W.KG;
     for (long long i = blockIdx.x * (long long)blockDim.x + threadIdx.x; i < total;
          i += (long long)gridDim.x * blockDim.x) {
         const int k = (int)(i / N), n = (int)(i % N);
@@ -64,7 +63,7 @@ __global__ void debug_dequant_kernel(DevLinear W, const int32_t* __restrict__ co
         const int s = kr / 16, hh = (kr % 16) / 8, j = kr % 8;
         const int lane = hh * 32 + cc;
         const uint32_t w = W.qw[(((size_t)nt * KB + kb) * 64 + lane) * 4 + s];
-        const int g = k / G;
+        const int g = k >> W.lgG;
         const f16x2 pr = dequant_pair(w, j / 2, zero_offset_pair(W.zeros, (size_t)nd * W.KG + g));
         const float qz = (float)pr[j % 2];
         const float sc = (float)__builtin_bit_cast(f16, W.scales[(size_t)nd * W.KG + g]);
