@@ -208,25 +208,30 @@ int layer_debug_dequant(layer_t layer, int32_t which, float* out, void* stream);
 
 /* Decode implementation (tuning / testing): 0 automatic (default), 1 a
  * sequence of kernels, 2 one persistent cooperative launch with one block per
- * CU (used automatically for B <= 4 when its on-chip working set fits; calls
- * of that path on one layer must not run concurrently, since they share the
- * layer's grid-barrier state).  Both compute the same result.  With 2, a
- * decode call the persistent path cannot serve fails with W4_EUNSUPPORTED.
- * Errors: W4_EINVAL. */
+ * CU (used automatically for B <= 4 when the layer has no zero points and
+ * its on-chip working set fits).  Both compute the same result; the
+ * persistent path is deterministic.  With 2, a decode call the persistent
+ * path cannot serve fails with W4_EUNSUPPORTED.  Errors: W4_EINVAL. */
 int layer_set_decode_path(layer_t layer, int32_t path);
 
 /* Diagnostics of the persistent decode path: durations in microseconds of
- * its five phases in the last completed call (q/k/v, attention, o_proj,
- * gate/up, down; measured by block 0 between grid barriers, the last one up
- * to the end of the last block) into us_out[5], and the error flag raised by
- * a grid-barrier timeout (0 = none) into *error_flag (nullable).  Waits for
- * the device.  Errors: W4_EINVAL, W4_EHIP. */
+ * its five phases in the last completed call (q/k/v, attention with the
+ * combine of its chunks, o_proj, gate/up, down), phase p measured from the
+ * moment the last block finished phase p-1 (the kernel start for p = 0) to
+ * the moment the last block finished phase p, into us_out[5]; and the error
+ * flag raised by a wait that timed out (0 = none, sticky) into *error_flag
+ * (nullable).  Waits for the device.  Errors: W4_EINVAL, W4_EHIP. */
 int layer_decode_phase_times(layer_t layer, float* us_out, int32_t* error_flag);
 
 /* Raw wall-clock stamps of the last persistent decode call (diagnostics):
- * [0..5] phase boundaries as above, then for phase p (0..4) and block j the
- * block's arrival at the barrier that ends the phase at [8 + p*nblocks + j].
- * Copies min(n, 8 + 5*1024) values.  Waits for the device. */
+ * [0] kernel start (block 0), [1] number of blocks, and at [8 + p*nblocks + j]
+ * the time block j passed point p: p = 0..4 the end of the five phases,
+ * 5 its start, 6/7 the end of the q/k/v RMSNorm / GEMV, 8 q/k/v gathered by
+ * its attention unit, 9 its attention units done, 10 the chunk outputs of
+ * its combine slice gathered, 11 the o_proj input gathered, 12 h gathered,
+ * 13 the gate/up GEMV done, 14 the down input gathered, 15 the down GEMV
+ * done (points of work a block does not own keep older values).  Copies
+ * min(n, 8 + 16*1024) values.  Waits for the device. */
 int layer_debug_decode_stamps(layer_t layer, uint64_t* out, int32_t n);
 
 /* Per-kernel timing for measurement (diagnostics, not for concurrent use).

@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cmath>
 #include <cstdio>
 #include <cstdarg>
@@ -63,6 +64,7 @@ struct Repacked {
     std::vector<uint16_t> scales;
     std::vector<float> ratios, slast;
     std::vector<uint8_t> zeros;
+    std::vector<uint32_t> sz;
 };
 
 inline bool f16_is_zero(uint16_t b) { return (b & 0x7FFFu) == 0; }
@@ -72,9 +74,10 @@ inline double f16_value(uint16_t b) {
     return (b & 0x8000u) ? -v : v;
 }
 
-// Repack columns [c0, c1) of a device linear.
+// Repack columns [c0, c1) of a device linear with N_dev columns.
 void repack_cols(const std::vector<ColSrc>& cols, int K_pad, int G, bool has_zeros, Repacked& R, int c0, int c1) {
     const int KG = K_pad / G, KB = K_pad / 64;
+    const size_t N_dev = cols.size();
     std::vector<uint8_t> code(K_pad);
     std::vector<uint16_t> s(KG);
     std::vector<uint8_t> z(KG);
@@ -115,9 +118,13 @@ void repack_cols(const std::vector<ColSrc>& cols, int K_pad, int G, bool has_zer
                     R.qw[(((size_t)nb * KB + kb) * 64 + hh * 32 + cc) * 4 + si] = w;
                 }
         for (int g = 0; g < KG; g++) {
-            R.scales[(size_t)nd * KG + g] = s[g];
-            R.ratios[(size_t)nd * KG + g] = g == 0 ? 1.0f : (float)(f16_value(s[g - 1]) / f16_value(s[g]));
-            if (has_zeros) R.zeros[(size_t)nd * KG + g] = z[g];
+            const size_t gi = (size_t)g * N_dev + nd;
+            R.scales[gi] = s[g];
+            R.ratios[gi] = g == 0 ? 1.0f : (float)(f16_value(s[g - 1]) / f16_value(s[g]));
+            if (has_zeros) {
+                R.zeros[gi] = z[g];
+                R.sz[gi] = (uint32_t)s[g] | ((uint32_t)z[g] << 16);
+            }
         }
         R.slast[nd] = (float)f16_value(s[KG - 1]);
     }
@@ -127,7 +134,7 @@ void repack_cols(const std::vector<ColSrc>& cols, int K_pad, int G, bool has_zer
 
 struct DevLinearOwned {
     DevLinear d{};
-    DevBuf qw, scales, ratios, slast, zeros, colmap_a, colmap_b, colmap_c;
+    DevBuf qw, scales, ratios, slast, zeros, sz, colmap_a, colmap_b, colmap_c;
 };
 
 struct Profiler {          // one timed kernel per stage
@@ -141,6 +148,9 @@ struct Profiler {          // one timed kernel per stage
     }
 };
 
+constexpr int kMaxBlocks = 1024;                    // persistent decode blocks (one per CU)
+constexpr int kStampWords = 8 + 24 * kMaxBlocks;
+
 struct layer_s {
     layer_config cfg{};
     int F_pad = 0;
@@ -148,10 +158,10 @@ struct layer_s {
     DevBuf attn_norm, mlp_norm, rope_cos, rope_sin;
     int device = 0;
     Profiler prof;
-    // persistent decode: barrier, completion counters and error flag (zeroed)
+    // persistent decode: error flag and optional per-block time stamps (zeroed)
     DevBuf sync;
-    unsigned *bar = nullptr, *cnt_qkv = nullptr, *cnt_gu = nullptr, *cnt_attn = nullptr, *cnt_o = nullptr,
-             *cnt_down = nullptr;
+    DevBuf fplan;                 // work table of the persistent decode (decode_fused_plan)
+    int fplan_blocks = 0, S_qkv = 1, S_o = 1, S_down = 1;
     int* err = nullptr;
     unsigned long long* stamps = nullptr;
     int decode_path = 0;   // 0 auto, 1 separate kernels, 2 persistent
@@ -174,7 +184,10 @@ int build_linear(DevLinearOwned& out, const std::vector<ColSrc>& cols, int K, in
     R.scales.resize((size_t)N_dev * KG);
     R.ratios.resize((size_t)N_dev * KG);
     R.slast.resize(N_dev);
-    if (has_zeros) R.zeros.resize((size_t)N_dev * KG);
+    if (has_zeros) {
+        R.zeros.resize((size_t)N_dev * KG);
+        R.sz.resize((size_t)N_dev * KG);
+    }
     const int nth = std::max(1, std::min(16, (int)std::thread::hardware_concurrency()));
     std::vector<std::thread> th;
     const int per = (N_dev / 32 + nth - 1) / nth * 32;
@@ -190,12 +203,14 @@ int build_linear(DevLinearOwned& out, const std::vector<ColSrc>& cols, int K, in
     if ((rc = upload(out.ratios, R.ratios.data(), R.ratios.size() * 4))) return rc;
     if ((rc = upload(out.slast, R.slast.data(), R.slast.size() * 4))) return rc;
     if (has_zeros && (rc = upload(out.zeros, R.zeros.data(), R.zeros.size()))) return rc;
+    if (has_zeros && (rc = upload(out.sz, R.sz.data(), R.sz.size() * 4))) return rc;
     DevLinear& d = out.d;
     d.qw = (const uint32_t*)out.qw.p;
     d.scales = (const uint16_t*)out.scales.p;
     d.ratios = (const float*)out.ratios.p;
     d.slast = (const float*)out.slast.p;
     d.zeros = has_zeros ? (const uint8_t*)out.zeros.p : nullptr;
+    d.sz = has_zeros ? (const uint32_t*)out.sz.p : nullptr;
     d.K = K;
     d.N = N_dev;
     d.K_pad = K_pad;
@@ -290,19 +305,23 @@ DecodeWs plan_decode(const layer_s* L, int B, int max_ctx) {
 // ---- persistent decode plan
 struct FusedPlan {
     bool ok = false;
-    int nblocks = 0, chunk = 0, nchunk = 0;
-    int tpw_qkv = 0, tpw_o = 0, tpw_gu = 0, tpw_down = 0, segmax_qkv = 0, segmax_gu = 0, segmax_o = 0, segmax_down = 0;
-    size_t lds_act = 0, lds_bytes = 0;
-    size_t h, part_qkv, part_gu, part_o, part_down, q_fin, kv_new, apart, A, g, total;
+    int nblocks = 0, chunk = 0, nchunk = 0, S_qkv = 1, S_o = 1, S_down = 1, ldx = 0, comb_per = 0, comb_lpv = 1;
+    size_t off_h = 0, off_red = 0, off_gam = 0, lds_bytes = 0;
+    size_t qkv_part, apart, A, o_part, g, down_part, total;
 };
 
+size_t align256(size_t v) { return (v + 255) / 256 * 256; }
+
+// Column tiles of every product are owned by whole blocks; a product with
+// fewer column tiles than blocks is also cut along k into S parts.
 FusedPlan plan_fused(const layer_s* L, int B, int max_ctx, bool query_device) {
     FusedPlan p;
     const layer_config& c = L->cfg;
     if (B > 4 || L->decode_path == 1) return p;
-    const int d = c.head_dim, qd = c.n_heads * d, r = c.n_heads / c.n_kv_heads;
-    const size_t act = (size_t)B * std::max(std::max(c.hidden, qd), L->F_pad) * 2;
-    p.lds_act = (act + 255) / 256 * 256;
+    if (L->qkv.d.sz || L->o.d.sz || L->gu.d.sz || L->down.d.sz) return p;   // zero points: separate kernels
+    if (c.group_size < 64) return p;                                         // groups of 32: separate kernels
+    const int d = c.head_dim, qd = c.n_heads * d, H = c.hidden, r = c.n_heads / c.n_kv_heads;
+    constexpr int MAXR = 8, NWAVE = 16, SLOTS = 4;
     p.nblocks = 256;
     if (query_device) {
         int dev = 0, cus = 0;
@@ -311,40 +330,56 @@ FusedPlan plan_fused(const layer_s* L, int B, int max_ctx, bool query_device) {
             return p;
         p.nblocks = cus;
     }
-    const int per_group = std::max(1, p.nblocks / (B * c.n_kv_heads));
+    const int P = p.nblocks;
+    if (P > kMaxBlocks || r > MAXR || P != L->fplan_blocks) return p;
+    if (L->gu.d.N_dev / 64 > 2 * P) return p;                                // at most 2 gate/up pairs per block
+    p.S_qkv = L->S_qkv;
+    p.S_o = L->S_o;
+    p.S_down = L->S_down;
+    // attention units: B * n_kv_heads * nchunk, about one per block
+    const int per_group = std::max(1, P / (B * c.n_kv_heads));
     int ch = (max_ctx + 1 + per_group - 1) / per_group;
-    ch = std::max(16, std::min(512, (ch + 15) / 16 * 16));
+    ch = std::max(16, (ch + 15) / 16 * 16);
+    ch = std::min(ch, decode_fused_max_chunk(d));
     p.chunk = ch;
     p.nchunk = (max_ctx + 1 + ch - 1) / ch;
-    const size_t attn_lds = (size_t)(8 * ch + 8 * 8 * d + 16) * 4;
-    p.lds_bytes = std::max(p.lds_act + 256, attn_lds);
+    const int kr_o = (L->o.d.K_pad / 64 + p.S_o - 1) / p.S_o * 64;
+    const int kr_d = (L->down.d.K_pad / 64 + p.S_down - 1) / p.S_down * 64;
+    p.ldx = std::max(std::max(H, kr_o), kr_d) + 8;
+    const int maxb = B <= 1 ? 1 : 4;
+    const size_t xs_bytes = (size_t)B * p.ldx * 2;
+    const size_t attn_bytes = (size_t)(MAXR * ch + NWAVE * d + 2 * MAXR + (MAXR + 2) * d) * 4 + (size_t)(MAXR * d + 2 * d) * 2;
+    const int V = B * qd;
+    p.comb_per = (((V + P - 1) / P) + 1) & ~1;
+    p.comb_lpv = 1;
+    while (p.comb_lpv < p.nchunk && p.comb_lpv < 64) p.comb_lpv *= 2;
+    if (p.nchunk > 4 * p.comb_lpv) return p;
+    const size_t comb_bytes = (size_t)p.comb_per * 2;
+    p.off_h = align256(std::max(std::max(xs_bytes, attn_bytes), comb_bytes));
+    p.off_red = align256(p.off_h + (size_t)B * H * 4);
+    p.off_gam = align256(p.off_red + (size_t)(NWAVE * SLOTS * maxb * 32 + 8 + NWAVE * maxb + maxb * 32 + 2 * maxb) * 4);
+    p.lds_bytes = p.off_gam + (size_t)2 * H * 2;
     if (p.lds_bytes > 160 * 1024) return p;
     if (query_device && decode_fused_blocks(d, B, p.lds_bytes) != p.nblocks) return p;
-    const int nw = p.nblocks * 8;
-    auto tpw = [&](const DevLinear& W) { const long long T = (long long)(W.N_dev / 32) * (W.K_pad / 64); return (int)((T + nw - 1) / nw); };
-    p.tpw_qkv = tpw(L->qkv.d);
-    p.tpw_o = tpw(L->o.d);
-    p.tpw_gu = tpw(L->gu.d);
-    p.tpw_down = tpw(L->down.d);
-    p.segmax_qkv = (L->qkv.d.K_pad / 64 + p.tpw_qkv - 1) / p.tpw_qkv + 1;
-    p.segmax_gu = (L->gu.d.K_pad / 64 + p.tpw_gu - 1) / p.tpw_gu + 1;
-    p.segmax_o = (L->o.d.K_pad / 64 + p.tpw_o - 1) / p.tpw_o + 1;
-    p.segmax_down = (L->down.d.K_pad / 64 + p.tpw_down - 1) / p.tpw_down + 1;
     Carve cv;
-    p.h = cv.take((size_t)B * c.hidden * 4);
-    p.part_qkv = cv.take((size_t)(L->qkv.d.N_dev / 32) * p.segmax_qkv * B * 32 * 4);
-    p.part_gu = cv.take((size_t)(L->gu.d.N_dev / 32) * p.segmax_gu * B * 32 * 4);
-    p.part_o = cv.take((size_t)(L->o.d.N_dev / 32) * p.segmax_o * B * 32 * 4);
-    p.part_down = cv.take((size_t)(L->down.d.N_dev / 32) * p.segmax_down * B * 32 * 4);
-    p.q_fin = cv.take((size_t)B * qd * 2);
-    p.kv_new = cv.take((size_t)B * 2 * c.n_kv_heads * d * 2);
-    p.apart = cv.take((size_t)B * c.n_heads * p.nchunk * (d + 2) * 4);
-    p.A = cv.take((size_t)B * qd * 2);
-    p.g = cv.take((size_t)B * L->F_pad * 2);
+    p.qkv_part = cv.take((size_t)p.S_qkv * B * L->qkv.d.N_dev * 8);
+    p.apart = cv.take((size_t)B * c.n_heads * p.nchunk * (d + 2) * 8);
+    p.A = cv.take((size_t)B * qd / 2 * 8);
+    p.o_part = cv.take((size_t)p.S_o * B * H * 8);
+    p.g = cv.take((size_t)B * L->F_pad / 2 * 8);
+    p.down_part = cv.take((size_t)p.S_down * B * H * 8);
     p.total = cv.off;
-    (void)r;
     p.ok = true;
     return p;
+}
+
+// Tag of a persistent decode launch: unique for 2^32 - 1 launches in the
+// process, never 0 (a zeroed workspace holds no valid word).
+uint32_t next_epoch() {
+    static std::atomic<uint32_t> ctr{0};
+    uint32_t e = ctr.fetch_add(1, std::memory_order_relaxed) + 1;
+    if (e == 0) e = ctr.fetch_add(1, std::memory_order_relaxed) + 1;
+    return e;
 }
 
 int gemv_ksplit(const DevLinear& W, int want_blocks, int B) {
@@ -569,20 +604,34 @@ int layer_create(const layer_config* cfg, const layer_weights_host* w, layer_t* 
         return rc;
     }
     {
-        const size_t n_bar = 4096, n_qkv = (size_t)(qd + 2 * kvd) / 64, n_gu = (size_t)F_pad / 32,
-                     n_attn = (size_t)c.max_batch * nkv, n_col = (size_t)H / 32;
-        const size_t words = n_bar + n_qkv + n_gu + n_attn + 2 * n_col + 64 + 16 + 2 * (8 + 5 * 1024);
-        std::vector<unsigned> zero(words, 0u);
-        if ((rc = upload(L->sync, zero.data(), words * 4))) { delete L; return rc; }
-        unsigned* base = (unsigned*)L->sync.p;
-        L->bar = base;
-        L->cnt_qkv = base + n_bar;
-        L->cnt_gu = L->cnt_qkv + n_qkv;
-        L->cnt_attn = L->cnt_gu + n_gu;
-        L->cnt_o = L->cnt_attn + n_attn;
-        L->cnt_down = L->cnt_o + n_col;
-        L->err = (int*)(L->cnt_down + n_col);
-        L->stamps = (unsigned long long*)(((uintptr_t)(L->cnt_down + n_col + 16) + 63) & ~(uintptr_t)63);
+        // [0]: error flag; from byte 64: stamps (8 + 24 * max blocks words of 8 bytes)
+        const size_t bytes = 64 + (size_t)kStampWords * 8;
+        std::vector<unsigned char> zero(bytes, 0);
+        if ((rc = upload(L->sync, zero.data(), bytes))) { delete L; return rc; }
+        L->err = (int*)L->sync.p;
+        L->stamps = (unsigned long long*)((char*)L->sync.p + 64);
+    }
+    // work table of the persistent decode: one block per CU; a product with
+    // fewer column tiles than blocks is also cut along k (at most 2 parts)
+    {
+        int dev = 0, cus = 0;
+        if (hipGetDevice(&dev) == hipSuccess &&
+            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && cus > 0 &&
+            cus <= kMaxBlocks) {
+            auto parts = [&](const DevLinear& W) {
+                const int nt = W.N_dev / 32, kb = W.K_pad / 64;
+                return std::max(1, std::min(std::min(2, kb), cus / nt));
+            };
+            if (L->qkv.d.N_dev / 32 <= cus && L->o.d.N_dev / 32 <= cus && L->down.d.N_dev / 32 <= cus) {
+                L->S_qkv = parts(L->qkv.d);
+                L->S_o = parts(L->o.d);
+                L->S_down = parts(L->down.d);
+                std::vector<int> tab((size_t)cus * 16);
+                decode_fused_plan(cus, L->qkv.d, L->o.d, L->gu.d, L->down.d, L->S_qkv, L->S_o, L->S_down, tab.data());
+                if ((rc = upload(L->fplan, tab.data(), tab.size() * 4))) { delete L; return rc; }
+                L->fplan_blocks = cus;
+            }
+        }
     }
     *out = L;
     return W4_OK;
@@ -650,25 +699,25 @@ int layer_decode(layer_t L, const float* x, const int32_t* pos, const int32_t* c
         a.k_cache = (uint16_t*)kc; a.v_cache = (uint16_t*)vc;
         a.sh = (long long)c.max_seq * c.head_dim; a.sb = a.sh * c.n_kv_heads;
         a.y = y;
-        a.h = (float*)(base + fp.h);
-        a.part_qkv = (float*)(base + fp.part_qkv);
-        a.part_gu = (float*)(base + fp.part_gu);
-        a.part_o = (float*)(base + fp.part_o);
-        a.part_down = (float*)(base + fp.part_down);
-        a.q_fin = (uint16_t*)(base + fp.q_fin);
-        a.kv_new = (uint16_t*)(base + fp.kv_new);
-        a.apart = (float*)(base + fp.apart);
-        a.A = (f16*)(base + fp.A);
-        a.g = (f16*)(base + fp.g);
-        a.bar = L->bar; a.cnt_qkv = L->cnt_qkv; a.cnt_gu = L->cnt_gu; a.cnt_attn = L->cnt_attn; a.err = L->err;
-        a.cnt_o = L->cnt_o; a.cnt_down = L->cnt_down; a.stamps = L->stamps;
-        a.tpw_qkv = fp.tpw_qkv; a.tpw_o = fp.tpw_o; a.tpw_gu = fp.tpw_gu; a.tpw_down = fp.tpw_down;
-        a.segmax_qkv = fp.segmax_qkv; a.segmax_gu = fp.segmax_gu; a.segmax_o = fp.segmax_o;
-        a.segmax_down = fp.segmax_down;
+        a.qkv_part = (uint64_t*)(base + fp.qkv_part);
+        a.apart = (uint64_t*)(base + fp.apart);
+        a.A = (uint64_t*)(base + fp.A);
+        a.o_part = (uint64_t*)(base + fp.o_part);
+        a.g = (uint64_t*)(base + fp.g);
+        a.down_part = (uint64_t*)(base + fp.down_part);
+        a.epoch = next_epoch();
+        a.err = L->err;
+        a.stamps = L->stamps;
+        a.S_qkv = fp.S_qkv; a.S_o = fp.S_o; a.S_down = fp.S_down;
+        a.plan = (const int*)L->fplan.p;
+        a.comb_per = fp.comb_per; a.comb_lpv = fp.comb_lpv;
         a.chunk = fp.chunk; a.nchunk = fp.nchunk;
         a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)c.head_dim));
         a.nblocks = fp.nblocks;
-        a.lds_act = fp.lds_act;
+        a.ldx = fp.ldx;
+        a.off_h = fp.off_h;
+        a.off_red = fp.off_red;
+        a.off_gam = fp.off_gam;
         a.lds_bytes = fp.lds_bytes;
         int rc;
         { ProfScope ps(L, 2, 6, st); rc = launch_decode_fused(a, st); }
@@ -805,14 +854,22 @@ int layer_debug_dequant(layer_t L, int32_t which, float* out, void* stream) {
 
 int layer_decode_phase_times(layer_t L, float* us_out, int32_t* error_flag) {
     if (!L || !us_out) return fail(W4_EINVAL, "null argument");
-    unsigned long long ts[6];
+    std::vector<unsigned long long> ts(kStampWords);
     int err = 0;
     HIP_TRY(hipDeviceSynchronize());
-    HIP_TRY(hipMemcpy(ts, L->stamps, sizeof ts, hipMemcpyDeviceToHost));
+    HIP_TRY(hipMemcpy(ts.data(), L->stamps, ts.size() * 8, hipMemcpyDeviceToHost));
     HIP_TRY(hipMemcpy(&err, L->err, sizeof err, hipMemcpyDeviceToHost));
     int khz = 0;
     HIP_TRY(hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, L->device));
-    for (int i = 0; i < 5; i++) us_out[i] = khz > 0 ? (float)((double)(ts[i + 1] - ts[i]) * 1000.0 / khz) : 0.f;
+    const int nb = (int)std::min<unsigned long long>(ts[1], kMaxBlocks);
+    // end of phase i: the last block to finish it
+    unsigned long long prev = ts[0];
+    for (int i = 0; i < 5; i++) {
+        unsigned long long e = prev;
+        for (int b = 0; b < nb; b++) e = std::max(e, ts[8 + (size_t)i * nb + b]);
+        us_out[i] = khz > 0 ? (float)((double)(e - prev) * 1000.0 / khz) : 0.f;
+        prev = e;
+    }
     if (error_flag) *error_flag = err;
     return W4_OK;
 }
@@ -820,7 +877,7 @@ int layer_decode_phase_times(layer_t L, float* us_out, int32_t* error_flag) {
 int layer_debug_decode_stamps(layer_t L, uint64_t* out, int32_t n) {
     if (!L || !out || n < 0) return fail(W4_EINVAL, "bad argument");
     HIP_TRY(hipDeviceSynchronize());
-    HIP_TRY(hipMemcpy(out, L->stamps, (size_t)std::min(n, 8 + 5 * 1024) * 8, hipMemcpyDeviceToHost));
+    HIP_TRY(hipMemcpy(out, L->stamps, (size_t)std::min(n, kStampWords) * 8, hipMemcpyDeviceToHost));
     return W4_OK;
 }
 

@@ -15,9 +15,12 @@
 //   32x32x16 MFMA, so a lane's word s is its B fragment of k16 step s.
 //
 //   Tile index: nb * (K_pad / 64) + kb (column strips contiguous along k).
-//   Scales: fp16 [N_dev][K_pad / G]; ratios for the prefill GEMM: fp32
-//   [N_dev][K_pad / G] with ratio[n][g] = s[g-1][n] / s[g][n] (g >= 1), and the
-//   last scale as fp32 [N_dev].  Zero points (optional): uint8 [N_dev][K_pad/G].
+//   Group parameters are group-major, so the 32 lanes of a tile read one
+//   contiguous run: scales fp16 [K_pad / G][N_dev]; ratios for the prefill
+//   GEMM fp32 [K_pad / G][N_dev] with ratio[g][n] = s[g-1][n] / s[g][n]
+//   (g >= 1), and the last scale as fp32 [N_dev].  Zero points (optional):
+//   uint8 [K_pad / G][N_dev], and the same again packed with the scale bits
+//   as uint32 (scale | zero << 16) for the decode GEMV.
 //
 //   K_pad is K rounded up to max(64, G); padded rows and groups carry the zero
 //   point code (weight 0).  A group whose scale is 0 is stored with all codes
@@ -75,25 +78,54 @@ __device__ __forceinline__ f16 act_f16(float x) {
     return (f16)round_bf16(x);
 }
 
-// Exact (code - zero) fp16 pair p (0..3) of a weight word; zoff2 is the
-// packed fp16 pair (-(1024+z), -(1024+z)).
-__device__ __forceinline__ f16x2 dequant_pair(uint32_t w, int p, f16x2 zoff2) {
-    uint32_t v = ((w >> (4 * p)) & 0x000F000Fu) | 0x64006400u;
-    return __builtin_bit_cast(f16x2, v) + zoff2;
-}
+// Dequantisation offsets of one zero point z: the fp16 pairs -(1024 + z) and
+// -(64 + z).
+struct ZeroOff {
+    f16x2 even, odd;
+};
 
-__device__ __forceinline__ f16x8 dequant_word(uint32_t w, f16x2 zoff2) {
-    f16x2 a = dequant_pair(w, 0, zoff2), b = dequant_pair(w, 1, zoff2);
-    f16x2 c = dequant_pair(w, 2, zoff2), d = dequant_pair(w, 3, zoff2);
-    f16x8 r;
-    r[0] = a[0]; r[1] = a[1]; r[2] = b[0]; r[3] = b[1];
-    r[4] = c[0]; r[5] = c[1]; r[6] = d[0]; r[7] = d[1];
+__device__ __forceinline__ ZeroOff zero_off(float z) {
+    ZeroOff r;
+    const f16 e = (f16)(-(1024.0f + z)), o = (f16)(-(64.0f + z));
+    r.even = f16x2{e, e};
+    r.odd = f16x2{o, o};
     return r;
 }
 
-__device__ __forceinline__ f16x2 zero_offset_pair(const uint8_t* zeros, size_t idx) {
-    f16 z = (f16)(-(1024.0f + (zeros ? (float)zeros[idx] : 8.0f)));
-    f16x2 r; r[0] = z; r[1] = z;
+// The three bit patterns of dequant8, held in vector registers (opaque to the
+// compiler, which would otherwise fold them into instruction literals and
+// split every and-or into two instructions).
+struct DqConst {
+    uint32_t lo, hi, magic;
+};
+
+__device__ __forceinline__ uint32_t vreg_const(uint32_t v) {
+    uint32_t r;
+    asm("v_mov_b32 %0, %1" : "=v"(r) : "i"(v));
+    return r;
+}
+
+__device__ __forceinline__ DqConst dq_const() {
+    return DqConst{vreg_const(0x000F000Fu), vreg_const(0x00F000F0u), vreg_const(0x64006400u)};
+}
+
+// Exact fp16 (code - zero) of the eight codes of a weight word, in k order.
+// Pair p (k0+2p, k0+2p+1) sits at bits 4p and 16+4p.  OR-ing 0x6400 onto a
+// code in bits 0..3 of a half gives the fp16 value 1024 + q, onto a code in
+// bits 4..7 the value 1024 + 16q; the first loses 1024 + z by one packed add,
+// the second is brought to q - z by one packed fma with 1/16 (exact: the
+// product 64 + q is exact and so is the integer sum).  Nine VALU operations
+// per word: one shift, four and-or, four packed f16 ops.
+__device__ __forceinline__ f16x8 dequant8(uint32_t w, ZeroOff zo, const DqConst& k) {
+    const uint32_t w8 = w >> 8;
+    const f16x2 sixteenth = f16x2{(f16)0.0625f, (f16)0.0625f};
+    const f16x2 p0 = __builtin_bit_cast(f16x2, (w & k.lo) | k.magic) + zo.even;
+    const f16x2 p1 = __builtin_elementwise_fma(__builtin_bit_cast(f16x2, (w & k.hi) | k.magic), sixteenth, zo.odd);
+    const f16x2 p2 = __builtin_bit_cast(f16x2, (w8 & k.lo) | k.magic) + zo.even;
+    const f16x2 p3 = __builtin_elementwise_fma(__builtin_bit_cast(f16x2, (w8 & k.hi) | k.magic), sixteenth, zo.odd);
+    f16x8 r;
+    r[0] = p0[0]; r[1] = p0[1]; r[2] = p1[0]; r[3] = p1[1];
+    r[4] = p2[0]; r[5] = p2[1]; r[6] = p3[0]; r[7] = p3[1];
     return r;
 }
 
@@ -122,10 +154,11 @@ __device__ __forceinline__ float wave_max(float v) {
 
 struct DevLinear {
     const uint32_t* qw;      // tiles
-    const uint16_t* scales;  // fp16 bits [N_dev][KG]
-    const float* ratios;     // [N_dev][KG]
+    const uint16_t* scales;  // fp16 bits [KG][N_dev]
+    const float* ratios;     // [KG][N_dev]
     const float* slast;      // [N_dev]
-    const uint8_t* zeros;    // [N_dev][KG] or null
+    const uint8_t* zeros;    // [KG][N_dev] or null
+    const uint32_t* sz;      // scale bits | zero << 16, [KG][N_dev]; null without zeros
     int K, N;                // logical
     int K_pad, N_dev, KG;    // padded rows, device columns, groups
     int lgG;                 // log2 of the group size (a power of two)

@@ -19,36 +19,38 @@ struct DecodeFusedArgs {
     uint16_t* v_cache;
     long long sb, sh;
     float* y;                  // [B][H]
-    // workspace
-    float* h;                  // [B][H]
-    float* part_qkv;           // [CT][segmax][B][32]
-    float* part_gu;
-    float* part_o;
-    float* part_down;
-    uint16_t* q_fin;           // bf16 [B][nq*d]
-    uint16_t* kv_new;          // bf16 [B][2][nkv][d]
-    float* apart;              // [B][nq][nchunk][d+2]
-    f16* A;                    // [B][nq*d]
-    f16* g;                    // [B][F_pad]
-    // synchronisation state (per layer handle, zeroed at create)
-    unsigned* bar;
-    unsigned* cnt_qkv;
-    unsigned* cnt_gu;
-    unsigned* cnt_attn;
-    unsigned* cnt_o;           // per column tile of o_proj
-    unsigned* cnt_down;        // per column tile of down
-    int* err;
-    unsigned long long* stamps;  // [6] phase timestamps (wall clock) or null
+    // workspace: tagged words (payload | epoch << 32)
+    uint64_t* qkv_part;        // [S_qkv][B][N_qkv]      fp32 partial sums
+    uint64_t* apart;           // [B][nq][nchunk][d + 2] fp32 chunk outputs, max, sum
+    uint64_t* A;               // [B][nq*d / 2]          attention output, fp16 pairs
+    uint64_t* o_part;          // [S_o][B][H]            fp32 partial sums
+    uint64_t* g;               // [B][F_pad / 2]         SwiGLU output, fp16 pairs
+    uint64_t* down_part;       // [S_down][B][H]         fp32 partial sums (s >= 1)
+    uint32_t epoch;            // tag of this launch (never 0)
+    int* err;                  // set when a wait times out
+    unsigned long long* stamps;  // wall-clock stamps or null
     // work split
-    int tpw_qkv, tpw_o, tpw_gu, tpw_down;
-    int segmax_qkv, segmax_gu, segmax_o, segmax_down;
-    int chunk, nchunk;
+    const int* plan;           // per block: 16 ints (decode_fused_plan)
+    int S_qkv, S_o, S_down;    // k-parts per column tile
+    int comb_per, comb_lpv;    // attention outputs combined per block, lanes per output
+    int chunk, nchunk;         // attention keys per unit, units per (row, kv head)
     float scale_log2;
     int nblocks;
-    size_t lds_act;            // bytes of the activation rows in LDS
+    int ldx;                   // fp16 elements per activation row in LDS
+    size_t off_h, off_red, off_gam;  // LDS offsets (bytes)
     size_t lds_bytes;          // dynamic LDS per block
 };
 
 int launch_decode_fused(const DecodeFusedArgs& a, hipStream_t stream);
+// Work table of the persistent decode for nblocks blocks, 16 ints per block:
+//   [0..3]   q/k/v:  column tile (-1: none), k-tile range [ka, kz), k-part s
+//   [4..7]   o_proj: the same
+//   [8..9]   gate/up: column tile range [t0, t1) (whole gate/up pairs)
+//   [10..13] down:   column tile, k-tile range, k-part
+// S_* are the k-parts per column tile of the three products.
+void decode_fused_plan(int nblocks, const DevLinear& qkv, const DevLinear& o, const DevLinear& gu,
+                       const DevLinear& down, int S_qkv, int S_o, int S_down, int* out);
 // Blocks of the persistent launch (one per CU) or 0 if it cannot be resident.
 int decode_fused_blocks(int head_dim, int B, size_t lds_bytes);
+// Largest attention chunk (keys per unit) the kernel supports for head_dim.
+int decode_fused_max_chunk(int head_dim);

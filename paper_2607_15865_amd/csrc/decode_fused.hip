@@ -1,375 +1,171 @@
-// Decode stage in one persistent launch (one block of 8 waves per CU).
-// Deterministic: every column sum is formed from per-wave partials added in a
-// fixed order, no floating-point atomics.
+// Decode stage in one persistent launch (one block of 8 waves per CU), run as
+// a dataflow graph without grid barriers.
 //
-// The decode step is a chain of five dependent phases (Sec. 4.4):
-//   P1  q/k/v GEMV on RMSNorm(x)      -> RoPE, bf16, new K/V into the cache
-//   P2  split-KV attention            -> attention output A
-//   P3  o_proj GEMV                   -> h = x + A Wo
-//   P4  gate/up GEMV on RMSNorm(h)    -> g = silu(gate) * up
-//   P5  down GEMV                     -> y = h + g Wd
-// Separate kernels pay a launch boundary (~2.3 us) per phase and run each
-// phase on a partly idle machine; here the blocks stay resident and meet at
-// grid barriers (~1.6 us, fence-free tree).  Every GEMV phase splits the
-// layer's 1 KB weight tiles evenly over all waves (each wave a contiguous run
-// of tiles in column-major order), so no phase has a tail of idle CUs.
-// Epilogues that need a column's complete sum (RoPE, SwiGLU) are run by the
-// wave that contributes the last partial of a column pair (or column tile
-// for the residual epilogues); the attention
-// combine of a kv group by the block that finishes its last chunk.
+// The decode step is a chain of dependent products (Sec. 4.4):
+//   P1  q/k/v GEMV on RMSNorm(x)
+//   P2  split-KV attention (RoPE and bf16 of q/k/v at the consumer), then the
+//       combine of the chunks into the attention output A
+//   P3  o_proj GEMV                    -> partial sums of A Wo
+//   P4  h = x + A Wo; gate/up GEMV on RMSNorm(h) -> g = silu(gate) * up
+//   P5  down GEMV                      -> y = h + g Wd
 //
-// Memory ordering: the L2 of each XCD is not coherent with the others, so
-// every value one block produces for another in the same launch moves
-// through agent-scope (sc1) stores/loads or atomics, and a writer waits for
-// its stores (s_waitcnt vmcnt(0)) before it signals with an atomic.  Weights
-// and the KV cache history are produced by earlier launches and use ordinary
-// loads.  The new K/V row is read back from a coherent side buffer, not from
-// the cache.  Barrier spins are bounded: on timeout the kernel raises an
-// error flag and runs to completion.
+// Work split: in every GEMV the block owns whole column tiles (32 columns) or
+// a k-part of one, and its 8 waves split the block's k range; the waves'
+// partials meet in LDS.  A block's weight tiles for the next product are
+// requested (gemv_core ring) as soon as its current run is done, so the
+// weight stream keeps going while the block waits for its inputs.
+//
+// Synchronisation: every value that one block hands to another is a 64-bit
+// word (32-bit payload | 32-bit launch epoch) written with one agent-scope
+// store.  A consumer polls the words it needs until each carries this
+// launch's epoch; a 64-bit access is single-copy atomic, so a word with the
+// right tag holds this launch's payload.  There are no counters, fences or
+// grid barriers, and a consumer waits only for the producers of its own
+// inputs.  Sums are formed in a fixed order: results do not depend on
+// timing.  Polls are bounded: on a timeout the kernel raises an error flag
+// and runs to completion.  All blocks are co-resident (cooperative launch).
 #include "common.h"
+#include "gemv_core.h"
 #include "launch.h"
 #include "decode_fused.h"
 
 namespace {
 
-constexpr int NWAVE = 8;
+constexpr int NWAVE = 16;
 constexpr int NTHR = NWAVE * 64;
-constexpr int SPIN_MAX = 1 << 22;
-constexpr int MAXR_F = 8;        // query heads per kv head
-
-__device__ __forceinline__ void wait_stores() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
-__device__ __forceinline__ void compiler_fence() { asm volatile("" ::: "memory"); }
+constexpr int SPIN_MAX = 1 << 20;  // polls per thread per launch before the error flag is raised
+constexpr int RING = 8;            // weight tiles in flight per wave (gate/up, down)
+constexpr int RING_QKV = 4;        // q/k/v: its run is about 4 tiles per wave
+constexpr int RING_O = 4;          // o_proj: its run is 2 to 4 tiles per wave
+constexpr int NIT = 4;             // K/V register rows per lane: chunk <= NIT * NWAVE * (64 / (d / 8))
+constexpr int MAXS = 2;            // k-parts of a column tile
+constexpr int MAXR = 8;            // query heads per kv head
+constexpr int SLOTS = 4;           // column tiles per block in one product
 
 #define GLOBAL_AS __attribute__((address_space(1)))
 template <typename T>
 __device__ __forceinline__ GLOBAL_AS T* gptr(const T* p) {
     return (GLOBAL_AS T*)(const_cast<T*>(p));
 }
-__device__ __forceinline__ void st_coh(float* p, float v) {
-    __hip_atomic_store(gptr(p), v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+
+__device__ __forceinline__ void put_tagged(uint64_t* p, uint32_t payload, uint32_t ep) {
+    __hip_atomic_store(gptr(p), ((uint64_t)ep << 32) | payload, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ __forceinline__ float ld_coh(const float* p) {
+__device__ __forceinline__ uint64_t get_tagged(const uint64_t* p) {
     return __hip_atomic_load(gptr(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ __forceinline__ void st_coh16(uint16_t* p, uint16_t v) {
-    __hip_atomic_store(gptr(p), v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ void st_coh64(void* p, uint64_t v) {
-    __hip_atomic_store(gptr(reinterpret_cast<uint64_t*>(p)), v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ uint64_t ld_coh64(const void* p) {
-    return __hip_atomic_load(gptr(reinterpret_cast<const uint64_t*>(p)), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ unsigned atom_add(unsigned* p, unsigned v) {
-    return __hip_atomic_fetch_add(gptr(p), v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ unsigned atom_ld(const unsigned* p) {
-    return __hip_atomic_load(gptr(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ void atom_st(unsigned* p, unsigned v) {
-    __hip_atomic_store(gptr(p), v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+
+// Poll budget of a thread for the whole launch: once it is spent, waits
+// give up at once (after raising the error flag), so a launch whose producer
+// never writes still ends.
+struct Waiter {
+    int* err;
+    int left;
+};
+
+// Payload of the word at p, given a first load v: poll until the tag is ep.
+__device__ __forceinline__ uint32_t settle(const uint64_t* p, uint64_t v, uint32_t ep, Waiter& wt) {
+    while ((uint32_t)(v >> 32) != ep) {
+        if (--wt.left < 0) {
+            if (wt.left == -1) atomicExch(wt.err, 1);
+            break;
+        }
+        __builtin_amdgcn_s_sleep(2);
+        v = get_tagged(p);
+    }
+    return (uint32_t)v;
 }
 
-// Tree barrier over the grid, in two halves so that loads can be issued
-// between arriving and waiting.  bar[0]: release generation; bar[16]: root
-// counter; bar[32 + 16 g]: counter of group g (16 blocks), each on its own
-// 64-byte line.  Counters return to 0 after every barrier.
-__device__ __forceinline__ unsigned grid_arrive(unsigned* bar) {
-    wait_stores();           // every wave: its stores are performed
-    __syncthreads();
-    unsigned gen = 0;
-    if (threadIdx.x == 0) {
-        gen = atom_ld(&bar[0]);
-        const unsigned nb = gridDim.x, G = 16, ngroups = (nb + G - 1) / G;
-        const unsigned grp = blockIdx.x / G, gsize = min(G, nb - grp * G);
-        unsigned* gc = &bar[32 + 16 * grp];
-        if (atom_add(gc, 1u) + 1 == gsize) {
-            atom_st(gc, 0u);
-            wait_stores();
-            if (atom_add(&bar[16], 1u) + 1 == ngroups) {
-                atom_st(&bar[16], 0u);
-                wait_stores();
-                atom_st(&bar[0], gen + 1);
-            }
+// Block-wide read of n elements: element i is the float sum over parts
+// s < S (in s order) of the tagged word at addr(i) + s * sstride, handed to
+// sink(i, sum).  The loads of 4 elements per thread (all parts) go out
+// together before any poll.
+template <typename Addr, typename Sink>
+__device__ __forceinline__ void gather_sum(int n, int S, size_t sstride, uint32_t ep, Waiter& wt, Addr addr, Sink sink) {
+    constexpr int BATCH = 4;
+    for (int base = threadIdx.x; base < n; base += NTHR * BATCH) {
+        uint64_t v[BATCH][MAXS];
+#pragma unroll
+        for (int j = 0; j < BATCH; j++) {
+            const int i = base + j * NTHR;
+#pragma unroll
+            for (int s = 0; s < MAXS; s++)
+                v[j][s] = (i < n && s < S) ? get_tagged(addr(i) + s * sstride) : 0;
+        }
+#pragma unroll
+        for (int j = 0; j < BATCH; j++) {
+            const int i = base + j * NTHR;
+            if (i >= n) break;
+            float sum = 0.f;
+#pragma unroll
+            for (int s = 0; s < MAXS; s++)
+                if (s < S) sum += __uint_as_float(settle(addr(i) + s * sstride, v[j][s], ep, wt));
+            sink(i, sum);
         }
     }
-    return gen;              // meaningful in thread 0 only
 }
 
-__device__ __forceinline__ void grid_wait(unsigned* bar, unsigned gen, int* err) {
-    if (threadIdx.x == 0) {
-        int n = 0;
-        while (atom_ld(&bar[0]) == gen) {
-            __builtin_amdgcn_s_sleep(1);
-            if (++n > SPIN_MAX) { atomicExch(err, 1); break; }
+// Block-wide read of n raw payloads: element i is the tagged word at addr(i)
+// (skipped when addr(i) is null), handed to sink(i, payload).
+template <typename Addr, typename Sink>
+__device__ __forceinline__ void gather_raw(int n, uint32_t ep, Waiter& wt, Addr addr, Sink sink) {
+    constexpr int BATCH = 8;
+    for (int base = threadIdx.x; base < n; base += NTHR * BATCH) {
+        uint64_t v[BATCH];
+#pragma unroll
+        for (int j = 0; j < BATCH; j++) {
+            const int i = base + j * NTHR;
+            const uint64_t* p = i < n ? addr(i) : nullptr;
+            v[j] = p ? get_tagged(p) : 0;
         }
-        compiler_fence();
+#pragma unroll
+        for (int j = 0; j < BATCH; j++) {
+            const int i = base + j * NTHR;
+            if (i >= n) break;
+            const uint64_t* p = addr(i);
+            if (p) sink(i, settle(p, v[j], ep, wt));
+        }
     }
-    __syncthreads();
 }
 
-__device__ __forceinline__ void grid_sync(unsigned* bar, int* err) { grid_wait(bar, grid_arrive(bar), err); }
-
-__device__ __forceinline__ float scale_of(const DevLinear& W, int n, int g) {
-    return (float)__builtin_bit_cast(f16, W.scales[(size_t)n * W.KG + g]);
-}
-
-// RMSNorm of B fp32 rows into LDS (fp16-held bf16 values).  coherent: the
-// rows were produced in this launch.  Every thread loads its slice of all
-// rows at once (one memory round trip), then a block reduction.
-template <int MAXB>
-__device__ __forceinline__ void norm_rows(const float* src, bool coherent, const uint16_t* gamma, float eps, int B, int K,
-                          f16* xs, float* red) {
+// RMSNorm of B rows (fp32, row b at src + b * K, in LDS) into the activation
+// rows of LDS as fp16-held bf16: xs[b * ldx + k].  gamma: bf16 bits in LDS.
+// red8: 8 + NWAVE * B floats of LDS scratch.
+__device__ __forceinline__ void norm_rows(const float* src, const uint16_t* gamma, float eps, int B, int K,
+                                          f16* xs, int ldx, float* red8) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    constexpr int PER = 8;                        // floats per thread per row
-    float v[MAXB][PER];
-    const int k0 = tid * PER;                     // K <= NTHR * PER * passes
-    float ss[MAXB];
-#pragma unroll
-    for (int b = 0; b < MAXB; b++) ss[b] = 0.f;
-    for (int kk = k0; kk < K; kk += NTHR * PER) {
-#pragma unroll
-        for (int b = 0; b < MAXB; b++) {
-            if (b >= B) break;
-#pragma unroll
-            for (int j = 0; j < PER; j += 2) {
-                const float* p = src + (size_t)b * K + kk + j;
-                if (coherent) {
-                    const uint64_t u = ld_coh64(p);
-                    v[b][j] = __uint_as_float((uint32_t)u);
-                    v[b][j + 1] = __uint_as_float((uint32_t)(u >> 32));
-                } else {
-                    const float2 f = *reinterpret_cast<const float2*>(p);
-                    v[b][j] = f.x;
-                    v[b][j + 1] = f.y;
-                }
-            }
+    for (int b = 0; b < B; b++) {
+        float ss = 0.f;
+        for (int k = tid; k < K; k += NTHR) {
+            const float v = src[b * K + k];
+            ss += v * v;
         }
-#pragma unroll
-        for (int b = 0; b < MAXB; b++) {
-            if (b >= B) break;
-#pragma unroll
-            for (int j = 0; j < PER; j++) ss[b] += v[b][j] * v[b][j];
-        }
-    }
-#pragma unroll
-    for (int b = 0; b < MAXB; b++) {
-        if (b >= B) break;
-        const float w = wave_sum(ss[b]);
-        if (lane == 0) red[8 + b * NWAVE + wave] = w;
+        ss = wave_sum(ss);
+        if (lane == 0) red8[8 + b * NWAVE + wave] = ss;
     }
     __syncthreads();
     if (tid < B) {
         float t = 0.f;
-        for (int w = 0; w < NWAVE; w++) t += red[8 + tid * NWAVE + w];
-        red[tid] = 1.0f / sqrtf(t / (float)K + eps);
+        for (int w = 0; w < NWAVE; w++) t += red8[8 + tid * NWAVE + w];
+        red8[tid] = 1.0f / sqrtf(t / (float)K + eps);
     }
     __syncthreads();
-    // second pass: the values of the first pass are still in registers when K
-    // fits one pass (the common case); otherwise reload
-    if (K <= NTHR * PER) {
-        if (k0 < K) {
-#pragma unroll
-            for (int b = 0; b < MAXB; b++) {
-                if (b >= B) break;
-                const float rb = red[b];
-#pragma unroll
-                for (int j = 0; j < PER; j++)
-                    xs[(size_t)b * K + k0 + j] = act_f16(v[b][j] * rb * bf16_bits_to_f32(gamma[k0 + j]));
-            }
-        }
-    } else {
-        for (int i = tid * 2; i < B * K; i += NTHR * 2) {
-            const int b = i / K, k = i - b * K;
-            float x0, x1;
-            if (coherent) {
-                const uint64_t u = ld_coh64(src + i);
-                x0 = __uint_as_float((uint32_t)u);
-                x1 = __uint_as_float((uint32_t)(u >> 32));
-            } else {
-                x0 = src[i];
-                x1 = src[i + 1];
-            }
-            xs[i] = act_f16(x0 * red[b] * bf16_bits_to_f32(gamma[k]));
-            xs[i + 1] = act_f16(x1 * red[b] * bf16_bits_to_f32(gamma[k + 1]));
-        }
+    for (int b = 0; b < B; b++) {
+        const float rb = red8[b];
+        for (int k = tid; k < K; k += NTHR)
+            xs[b * ldx + k] = act_f16(src[b * K + k] * rb * bf16_bits_to_f32(gamma[k]));
     }
     __syncthreads();
 }
 
-// Load B coherent fp16 rows [B][K] (4 halves per 8-byte load) into LDS.
-__device__ __forceinline__ void load_rows_f16(const f16* src, int B, int K, f16* xs) {
-    for (int i = threadIdx.x * 4; i < B * K; i += NTHR * 4)
-        *reinterpret_cast<uint64_t*>(xs + i) = ld_coh64(src + i);
-    __syncthreads();
-}
-
-// Even split of T tiles over all waves: wave w owns [w*TPW, min((w+1)*TPW, T)).
-struct Split {
-    int KB, TPW, total;
-    __device__ int first_wave(int t) const { return (t * KB) / TPW; }
-    __device__ int nseg(int t) const { return ((t + 1) * KB - 1) / TPW - (t * KB) / TPW + 1; }
-};
-
-constexpr int GDEPTH = 8;   // tiles per batch (16 bytes per lane each)
-
-struct Prefetch {
-    u32x4 w[GDEPTH];
-    float sc[GDEPTH][2];     // scale of the tile's group(s): k 0..31 and 32..63
-};
-
-// Tile i of the wave's run (column tile t, k-tile kb) and the scales of its
-// two k halves (equal unless the group size is 32).
-__device__ __forceinline__ void load_tile(const DevLinear& W, int i, int i1, int t, int kb, int lane, u32x4& w,
-                                          float (&sc)[2]) {
-    if (i < i1) {
-        const int col = t * 32 + (lane & 31);
-        w = reinterpret_cast<const u32x4*>(W.qw)[(size_t)i * 64 + lane];
-        const int g0 = (kb * 64) >> W.lgG, g1 = (kb * 64 + 32) >> W.lgG;
-        sc[0] = scale_of(W, col, g0);
-        sc[1] = (g1 != g0) ? scale_of(W, col, g1) : sc[0];
-    } else {
-        w = u32x4{0, 0, 0, 0};
-        sc[0] = sc[1] = 0.f;
-    }
-}
-
-// Issue the first batch of this wave's tiles (weights do not depend on earlier
-// phases, so this can run ahead of a grid barrier).
-__device__ __forceinline__ void gemv_prefetch(const DevLinear& W, const Split& sp, Prefetch& pf) {
-    const int lane = threadIdx.x & 63;
-    const int wave = blockIdx.x * NWAVE + (threadIdx.x >> 6);
-    const int i0 = wave * sp.TPW, i1 = min(i0 + sp.TPW, sp.total);
-    const int t0 = i0 / sp.KB, bnd = (t0 + 1) * sp.KB;
-#pragma unroll
-    for (int u = 0; u < GDEPTH; u++) {
-        const int i = i0 + u, t = (i >= bnd) ? t0 + 1 : t0;
-        load_tile(W, i, i1, t, i - t * sp.KB, lane, pf.w[u], pf.sc[u]);
-    }
-}
-
-// One wave's share of a GEMV phase: its contiguous run of tiles [i0, i1)
-// (column-major) covers at most two column tiles (the host keeps the number
-// of column tiles below the number of waves).  Batches are pipelined: the
-// next batch is in flight while the current one is dotted.  The B sums per
-// lane column of each column tile go to emit(t, seg, acc).
-template <int MAXB, typename Emit>
-__device__ __forceinline__ void gemv_share(const DevLinear& W, const Split& sp, const f16* xs, int ldx, int B, Prefetch& pf,
-                           Emit emit) {
-    const int lane = threadIdx.x & 63, h = lane >> 5, c = lane & 31;
-    const int wave = blockIdx.x * NWAVE + (threadIdx.x >> 6);
-    const int i0 = wave * sp.TPW, i1 = min(i0 + sp.TPW, sp.total);
-    if (i0 >= i1) return;
-    const int t0 = i0 / sp.KB, bnd = (t0 + 1) * sp.KB;
-    float acc[MAXB], gacc[MAXB], acc0[MAXB];
-#pragma unroll
-    for (int b = 0; b < MAXB; b++) { acc[b] = 0.f; gacc[b] = 0.f; acc0[b] = 0.f; }
-    int t_cur = t0, cur_g = -1;
-    float sc = 0.f;
-    f16x2 zo = zero_offset_pair(nullptr, 0);
-    for (int pos = i0; pos < i1; pos += GDEPTH) {
-        Prefetch nx;
-#pragma unroll
-        for (int u = 0; u < GDEPTH; u++) {
-            const int i = pos + GDEPTH + u, t = (i >= bnd) ? t0 + 1 : t0;
-            load_tile(W, i, i1, t, i - t * sp.KB, lane, nx.w[u], nx.sc[u]);
-        }
-#pragma unroll
-        for (int u = 0; u < GDEPTH; u++) {
-            const int i = pos + u;
-            if (i >= i1) break;
-            const int t = (i >= bnd) ? t0 + 1 : t0, kb = i - t * sp.KB;
-            if (t != t_cur) {                       // second column tile of the run
-#pragma unroll
-                for (int b = 0; b < MAXB; b++) { acc0[b] = acc[b] + sc * gacc[b]; acc[b] = 0.f; gacc[b] = 0.f; }
-                t_cur = t;
-                cur_g = -1;
-                sc = 0.f;
-            }
-            const int col = t * 32 + c;
-            const uint32_t wd4[4] = {pf.w[u][0], pf.w[u][1], pf.w[u][2], pf.w[u][3]};
-#pragma unroll
-            for (int s = 0; s < 4; s++) {
-                const int k = kb * 64 + s * 16 + h * 8;
-                const int g = (kb * 64 + s * 16) >> W.lgG;
-                if (g != cur_g) {
-#pragma unroll
-                    for (int b = 0; b < MAXB; b++) { acc[b] += sc * gacc[b]; gacc[b] = 0.f; }
-                    cur_g = g;
-                    sc = pf.sc[u][s >= 2 ? 1 : 0];
-                    if (W.zeros) zo = zero_offset_pair(W.zeros, (size_t)col * W.KG + g);
-                }
-                const uint32_t wd = wd4[s];
-                const f16x2 d0 = dequant_pair(wd, 0, zo), d1 = dequant_pair(wd, 1, zo);
-                const f16x2 d2 = dequant_pair(wd, 2, zo), d3 = dequant_pair(wd, 3, zo);
-#pragma unroll
-                for (int b = 0; b < MAXB; b++) {
-                    if (b < B) {
-                        const f16x8 xv = *reinterpret_cast<const f16x8*>(xs + (size_t)b * ldx + k);
-                        float v = gacc[b];
-                        v = __builtin_amdgcn_fdot2(f16x2{xv[0], xv[1]}, d0, v, false);
-                        v = __builtin_amdgcn_fdot2(f16x2{xv[2], xv[3]}, d1, v, false);
-                        v = __builtin_amdgcn_fdot2(f16x2{xv[4], xv[5]}, d2, v, false);
-                        v = __builtin_amdgcn_fdot2(f16x2{xv[6], xv[7]}, d3, v, false);
-                        gacc[b] = v;
-                    }
-                }
-            }
-        }
-        pf = nx;
-    }
-#pragma unroll
-    for (int b = 0; b < MAXB; b++) acc[b] += sc * gacc[b];
-    if (t_cur != t0) {
-#pragma unroll
-        for (int b = 0; b < MAXB; b++) acc0[b] += __shfl_xor(acc0[b], 32, 64);
-        emit(t0, wave - sp.first_wave(t0), acc0);
-    }
-#pragma unroll
-    for (int b = 0; b < MAXB; b++) acc[b] += __shfl_xor(acc[b], 32, 64);
-    emit(t_cur, wave - sp.first_wave(t_cur), acc);
-}
-
-// Partial of column tile t, segment seg: part[(t * SEGMAX + seg) * B + b][32].
-template <int MAXB>
-__device__ __forceinline__ void store_partial(float* part, int segmax, int t, int seg, int B, const float (&acc)[MAXB]) {
-    const int lane = threadIdx.x & 63;
-    if (lane < 32)
-#pragma unroll
-        for (int b = 0; b < MAXB; b++)
-            if (b < B) st_coh(part + ((size_t)(t * segmax + seg) * B + b) * 32 + lane, acc[b]);
-}
-
-// Sum of the partials of column tile t for row b, lane column c, in segment
-// order.  Up to 24 loads go out together (one round trip in practice).
-__device__ __forceinline__ float sum_partials(const float* part, int segmax, const Split& sp, int t, int B, int b, int c) {
-    float v = 0.f;
-    const int ns = sp.nseg(t);
-    for (int s0 = 0; s0 < ns; s0 += 24) {
-        float x[24];
-#pragma unroll
-        for (int j = 0; j < 24; j++)
-            x[j] = (s0 + j < ns) ? ld_coh(part + ((size_t)(t * segmax + s0 + j) * B + b) * 32 + c) : 0.f;
-#pragma unroll
-        for (int j = 0; j < 24; j++) v += x[j];
-    }
-    return v;
-}
-
-// Signal that a partial of unit p (a column tile or a pair of them) is
-// stored; true for the wave that stored the last one (all lanes agree).
-__device__ __forceinline__ bool pair_done(unsigned* cnt, int p, unsigned total) {
-    const int lane = threadIdx.x & 63;
-    wait_stores();
-    unsigned old = 0;
-    if (lane == 0) old = atom_add(&cnt[p], 1u);
-    old = __shfl(old, 0, 64);
-    const bool last = (old + 1 == total);
-    if (last) {
-        compiler_fence();
-        if (lane == 0) atom_st(&cnt[p], 0u);
-    }
-    return last;
+// Device position (inside a head) of dim j: the head's 32-dim blocks are
+// stored in the order that puts RoPE partners in adjacent tiles.
+template <int D>
+__device__ __forceinline__ int devpos(int j) {
+    constexpr int half = D / 64;
+    const int jb = j >> 5;
+    const int p = jb < half ? 2 * jb : 2 * (jb - half) + 1;
+    return p * 32 + (j & 31);
 }
 
 // ---------------------------------------------------------------- kernel
@@ -377,342 +173,462 @@ __device__ __forceinline__ bool pair_done(unsigned* cnt, int p, unsigned total) 
 template <int D, int MAXB>
 __global__ void __launch_bounds__(NTHR) decode_fused_kernel(DecodeFusedArgs a) {
     extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int B = a.B, H = a.H, d = D, nq = a.nq, nkv = a.nkv, r = nq / nkv;
-    const int qd = nq * d;
-    f16* xs = reinterpret_cast<f16*>(smem);                    // activation rows
-    float* red = reinterpret_cast<float*>(smem + a.lds_act);   // small scratch
-    // phase timestamps (block 0, thread 0): start and after each barrier
-    auto stamp = [&](int i) {
-        if (blockIdx.x == 0 && tid == 0 && a.stamps) a.stamps[i] = wall_clock64();
-    };
-    auto arrive = [&](int ph) {      // this block's arrival at the barrier ending phase ph
-        if (tid == 0 && a.stamps) a.stamps[8 + ph * gridDim.x + blockIdx.x] = wall_clock64();
-    };
-    stamp(0);
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int blk = blockIdx.x, P = gridDim.x;
+    const int B = a.B, H = a.H, nq = a.nq, nkv = a.nkv, r = nq / nkv;
+    const int qd = nq * D, kd = nkv * D;
+    const uint32_t ep = a.epoch;
+    Waiter wt{a.err, SPIN_MAX};
+    const int ldx = a.ldx;
+    const int h = lane >> 5, c = lane & 31;
+    f16* xs = reinterpret_cast<f16*>(smem);
+    float* hbuf = reinterpret_cast<float*>(smem + a.off_h);       // [B][H]
+    float* red = reinterpret_cast<float*>(smem + a.off_red);      // [NWAVE][SLOTS][B][32]
+    float* red8 = red + NWAVE * SLOTS * MAXB * 32;                // 8 + NWAVE * MAXB
+    float* own = red8 + 8 + NWAVE * MAXB;                         // [MAXB][32]
+    int* meta = reinterpret_cast<int*>(own + MAXB * 32);          // ctx_lens[B], pos[B]
+    uint16_t* gam = reinterpret_cast<uint16_t*>(smem + a.off_gam);           // RMSNorm weights [2][H]
 
-    // ================= P1: q/k/v =================
-    Prefetch pf;
-    const Split sp_qkv{a.qkv.K_pad / 64, a.tpw_qkv, (a.qkv.N_dev / 32) * (a.qkv.K_pad / 64)};
-    const Split sp_o{a.o.K_pad / 64, a.tpw_o, (a.o.N_dev / 32) * (a.o.K_pad / 64)};
-    const Split sp_gu{a.gu.K_pad / 64, a.tpw_gu, (a.gu.N_dev / 32) * (a.gu.K_pad / 64)};
-    const Split sp_dn{a.down.K_pad / 64, a.tpw_down, (a.down.N_dev / 32) * (a.down.K_pad / 64)};
-    gemv_prefetch(a.qkv, sp_qkv, pf);
-    norm_rows<MAXB>(a.x, false, a.attn_norm, a.eps, B, H, xs, red);
-    {
-        const Split& sp = sp_qkv;
-        gemv_share<MAXB>(a.qkv, sp, xs, H, B, pf, [&](int t, int seg, const float (&acc)[MAXB]) {
-            store_partial<MAXB>(a.part_qkv, a.segmax_qkv, t, seg, B, acc);
-            const int p = t / 2;
-            if (!pair_done(a.cnt_qkv, p, sp.nseg(2 * p) + sp.nseg(2 * p + 1))) return;
-            // finalize the pair: RoPE for q/k, bf16, write q / cache / new-row buffer
-            if (lane < 32) {
-                for (int b = 0; b < B; b++) {
-                    const float v0 = sum_partials(a.part_qkv, a.segmax_qkv, sp, 2 * p, B, b, lane);
-                    const float v1 = sum_partials(a.part_qkv, a.segmax_qkv, sp, 2 * p + 1, B, b, lane);
-                    // which, head, dims of the pair
-                    int n = p * 64, kind, head;
-                    const int kd = nkv * d;
-                    if (n < qd) { kind = 0; head = n / d; n -= head * d; }
-                    else if (n < qd + kd) { kind = 1; n -= qd; head = n / d; n -= head * d; }
-                    else { kind = 2; n -= qd + kd; head = n / d; n -= head * d; }
-                    const int p0 = n / 32;
-                    const int dim0 = 32 * rope_block(p0, d) + lane, dim1 = 32 * rope_block(p0 + 1, d) + lane;
-                    float o0 = v0, o1 = v1;
-                    if (kind < 2) {
-                        const int ps = a.pos[b];
-                        const float cs = a.rope_cos[(size_t)ps * (d / 2) + dim0];
-                        const float sn = a.rope_sin[(size_t)ps * (d / 2) + dim0];
-                        o0 = v0 * cs - v1 * sn;
-                        o1 = v1 * cs + v0 * sn;
-                    }
-                    const uint16_t b0 = bf16_bits_rne(o0), b1 = bf16_bits_rne(o1);
-                    if (kind == 0) {
-                        uint16_t* q = a.q_fin + ((size_t)b * nq + head) * d;
-                        st_coh16(q + dim0, b0);
-                        st_coh16(q + dim1, b1);
-                    } else {
-                        const int slot = a.ctx_lens[b];
-                        uint16_t* cache = (kind == 1) ? a.k_cache : a.v_cache;
-                        uint16_t* cp = cache + (size_t)b * a.sb + (size_t)head * a.sh + (size_t)slot * d;
-                        cp[dim0] = b0;
-                        cp[dim1] = b1;
-                        uint16_t* nv = a.kv_new + (((size_t)b * 2 + (kind - 1)) * nkv + head) * d;
-                        st_coh16(nv + dim0, b0);
-                        st_coh16(nv + dim1, b1);
-                    }
-                }
-            }
-        });
+    if (a.stamps && blk == 0 && tid == 0) {
+        a.stamps[0] = wall_clock64();
+        a.stamps[1] = (unsigned long long)P;
     }
-    arrive(0);
-    grid_sync(a.bar, a.err);
-    stamp(1);
+    // stamp slot ph of this block: 0..4 end of the five phases, 5.. detail
+    auto stamp_done = [&](int ph) {
+        if (a.stamps && tid == 0) a.stamps[8 + ph * P + blk] = wall_clock64();
+    };
+    stamp_done(5);
 
-    // ================= P2: attention =================
+    // ---- this block's work (host plan): column tiles and k ranges per product,
+    // read (scalar loads) where they are needed
+    const int* pl = a.plan + blk * 16;
+    const int Nq = a.qkv.N_dev;
+    // this wave's run of product ph (1 q/k/v, 3 o_proj, 4 gate/up, 5 down)
+    auto wave_run = [&](int ph) {
+        int t0, tz, ka, kz;
+        if (ph == 4) { t0 = pl[8]; tz = pl[9]; ka = 0; kz = a.gu.K_pad / 64; }
+        else {
+            const int* e = pl + (ph == 1 ? 0 : ph == 3 ? 4 : 10);
+            t0 = e[0]; tz = t0 + 1; ka = e[1]; kz = e[2];
+        }
+        return Run{t0, tz, ka + wave * (kz - ka) / NWAVE, ka + (wave + 1) * (kz - ka) / NWAVE};
+    };
+    auto owns = [&](int ph) { return ph == 4 ? pl[9] > pl[8] : pl[ph == 1 ? 0 : ph == 3 ? 4 : 10] >= 0; };
+
+    // one ring per product, sized for its usual run length; a product's ring
+    // is filled as soon as the previous product's tiles are all consumed
+    TileRing<RING_QKV, false> R1;
+    TileRing<RING_O, false> R3;
+    TileRing<RING, false> R4, R5;
+    RunCursor q1, q3, q4, q5;
+    auto prefetch = [&](int ph) {
+        if (!owns(ph)) return;
+        const Run run = wave_run(ph);
+        if (run.ka >= run.kz) return;
+        if (ph == 1) ring_prefetch<RING_QKV, false, false>(a.qkv, run, R1, q1);
+        if (ph == 3) ring_prefetch<RING_O, false, false>(a.o, run, R3, q3);
+        if (ph == 4) ring_prefetch<RING, false, false>(a.gu, run, R4, q4);
+        if (ph == 5) ring_prefetch<RING, false, false>(a.down, run, R5, q5);
+    };
+    // this wave's part of the block partial of slot `slot`
+    auto to_red = [&](int slot, const float (&out)[4]) {
+#pragma unroll
+        for (int qq = 0; qq < 4; qq++) {
+            const int b = 4 * h + qq;
+            if (b < B) red[((wave * SLOTS + slot) * B + b) * 32 + c] = out[qq];
+        }
+    };
+    // (after a block barrier: the last product's partials may still be read)
+    auto clear_red = [&]() {
+        __syncthreads();
+        for (int i = lane; i < SLOTS * B * 32; i += 64) red[wave * SLOTS * B * 32 + i] = 0.f;
+    };
+    // block sum of slot `slot`, row b, column cc (after a __syncthreads)
+    auto red_sum = [&](int slot, int b, int cc) {
+        float v = 0.f;
+#pragma unroll
+        for (int w = 0; w < NWAVE; w++) v += red[((w * SLOTS + slot) * B + b) * 32 + cc];
+        return v;
+    };
+
+    // x, the RMSNorm weights and the per-row metadata into LDS: every load of a
+    // thread is issued before its first wait, and before the weight prefetch
+    {
+        float4 xv[2];
+        u32x4 g1, g2;
+        const int i0 = tid * 4, i1 = i0 + NTHR * 4;
+        xv[0] = i0 < B * H ? *reinterpret_cast<const float4*>(a.x + i0) : float4{0.f, 0.f, 0.f, 0.f};
+        xv[1] = i1 < B * H ? *reinterpret_cast<const float4*>(a.x + i1) : float4{0.f, 0.f, 0.f, 0.f};
+        const int gi = tid * 8 < H ? tid * 8 : 0;
+        g1 = *reinterpret_cast<const u32x4*>(a.attn_norm + gi);
+        g2 = *reinterpret_cast<const u32x4*>(a.mlp_norm + gi);
+        int m0 = 0;
+        if (tid < B) m0 = a.ctx_lens[tid];
+        else if (tid >= MAXB && tid < MAXB + B) m0 = a.pos[tid - MAXB];
+        prefetch(1);
+        if (i0 < B * H) *reinterpret_cast<float4*>(hbuf + i0) = xv[0];
+        if (i1 < B * H) *reinterpret_cast<float4*>(hbuf + i1) = xv[1];
+        if (tid * 8 < H) {
+            *reinterpret_cast<u32x4*>(gam + tid * 8) = g1;
+            *reinterpret_cast<u32x4*>(gam + H + tid * 8) = g2;
+        }
+        if (tid < MAXB + B) meta[tid] = m0;
+        for (int i = i1 + NTHR * 4; i < B * H; i += NTHR * 4)      // rows past 2 * NTHR * 4 floats
+            *reinterpret_cast<float4*>(hbuf + i) = *reinterpret_cast<const float4*>(a.x + i);
+        for (int i = tid * 8 + NTHR * 8; i < H; i += NTHR * 8) {
+            *reinterpret_cast<u32x4*>(gam + i) = *reinterpret_cast<const u32x4*>(a.attn_norm + i);
+            *reinterpret_cast<u32x4*>(gam + H + i) = *reinterpret_cast<const u32x4*>(a.mlp_norm + i);
+        }
+        __syncthreads();
+    }
+
+    // ================= P1: q/k/v partial sums =================
+    if (owns(1)) {
+        const int t1 = pl[0], s1 = pl[3];
+        const Run run1 = wave_run(1);
+        norm_rows(hbuf, gam, a.eps, B, H, xs, ldx, red8);
+        stamp_done(6);
+        clear_red();
+        if (run1.ka < run1.kz)
+            gemv_run<RING_QKV, false, false>(a.qkv, run1, xs, ldx, B, R1, q1, [&](int, const float (&out)[4]) { to_red(0, out); });
+        stamp_done(7);
+        __syncthreads();
+        for (int i = tid; i < B * 32; i += NTHR) {
+            const int b = i >> 5, cc = i & 31;
+            put_tagged(a.qkv_part + ((size_t)s1 * B + b) * Nq + t1 * 32 + cc, __float_as_uint(red_sum(0, b, cc)), ep);
+        }
+    }
+    prefetch(3);
+    stamp_done(0);
+
+    // ================= P2: attention units =================
     {
         constexpr int LPK = D / 8, KPW = 64 / LPK;
-        float* sc = reinterpret_cast<float*>(smem);                 // [r][chunk]
-        float* ored = sc + MAXR_F * a.chunk;                        // [NWAVE][r][D]
-        float* stat = ored + NWAVE * MAXR_F * D;                    // [r][2]
-        const int units = B * nkv * a.nchunk;
+        const int CH = a.chunk, NCH = a.nchunk;
         const int kl = lane / LPK, dseg = lane % LPK;
+        float* sc = reinterpret_cast<float*>(smem);                  // [r][CH]
+        float* ored = sc + MAXR * CH;                                // [NWAVE][D]
+        float* stat = ored + NWAVE * D;                              // [r][2]
+        float* qkvf = stat + 2 * MAXR;                               // [r + 2][D] device order
+        uint16_t* qb = reinterpret_cast<uint16_t*>(qkvf + (MAXR + 2) * D);   // [r][D] bf16
+        uint16_t* knb = qb + MAXR * D;                               // [D]
+        uint16_t* vnb = knb + D;                                     // [D]
         const float LOG2E = 1.4426950408889634f;
-        for (int u = blockIdx.x; u < units; u += gridDim.x) {
-            const int b = u / (nkv * a.nchunk), rem = u % (nkv * a.nchunk);
-            const int g = rem / a.nchunk, chunk = rem % a.nchunk;
-            const int ctx = a.ctx_lens[b];
-            const int start = chunk * a.chunk, end = min(start + a.chunk, ctx + 1);
+        const int units = B * nkv * NCH;
+        for (int u = blk; u < units; u += P) {
+            const int b = u / (nkv * NCH), g = (u / NCH) % nkv, chunk = u % NCH;
+            const int ctx = meta[b];
+            const int start = chunk * CH, end = min(start + CH, ctx + 1);
             if (start >= end) continue;
+            const int nkeys = end - start, hist_end = min(end, ctx);
             const uint16_t* kc = a.k_cache + (size_t)b * a.sb + (size_t)g * a.sh;
             const uint16_t* vc = a.v_cache + (size_t)b * a.sb + (size_t)g * a.sh;
-            const uint16_t* kn = a.kv_new + (((size_t)b * 2 + 0) * nkv + g) * d;
-            const uint16_t* vn = a.kv_new + (((size_t)b * 2 + 1) * nkv + g) * d;
-            uint32_t qv[MAXR_F][4];
-#pragma unroll
-            for (int i = 0; i < MAXR_F; i++) {
-                if (i < r) {
-                    const uint16_t* qp = a.q_fin + ((size_t)b * nq + g * r + i) * d + dseg * 8;
-                    const uint64_t lo = ld_coh64(qp), hi = ld_coh64(qp + 4);
-                    qv[i][0] = (uint32_t)lo; qv[i][1] = (uint32_t)(lo >> 32);
-                    qv[i][2] = (uint32_t)hi; qv[i][3] = (uint32_t)(hi >> 32);
-                } else {
-                    qv[i][0] = qv[i][1] = qv[i][2] = qv[i][3] = 0;
-                }
-            }
+            // K/V history rows of this lane (keys start + (it*NWAVE + wave)*KPW + kl),
+            // mask values and the RoPE factors of this thread's dim, all requested
+            // before the wait for q/k/v.  Loads are unconditional (rows past the
+            // history read row 0 and are not used).
             const float* mrow = a.mask ? a.mask + (size_t)b * a.max_seq : nullptr;
-            for (int k0 = start + wave * KPW; k0 < end; k0 += NWAVE * KPW) {
-                const int key = k0 + kl;
-                const bool valid = key < end;
-                uint32_t kw[4] = {0, 0, 0, 0};
-                if (valid) {
-                    if (key == ctx) {
-                        const uint64_t lo = ld_coh64(kn + dseg * 8), hi = ld_coh64(kn + dseg * 8 + 4);
-                        kw[0] = (uint32_t)lo; kw[1] = (uint32_t)(lo >> 32); kw[2] = (uint32_t)hi; kw[3] = (uint32_t)(hi >> 32);
-                    } else {
-                        const u32x4 kk = *reinterpret_cast<const u32x4*>(kc + (size_t)key * d + dseg * 8);
-                        kw[0] = kk[0]; kw[1] = kk[1]; kw[2] = kk[2]; kw[3] = kk[3];
-                    }
-                }
+            u32x4 kr[NIT], vr[NIT];
+            float mk[NIT];
 #pragma unroll
-                for (int i = 0; i < MAXR_F; i++) {
-                    if (i >= r) break;
+            for (int it = 0; it < NIT; it++) {
+                const int key = start + (it * NWAVE + wave) * KPW + kl;
+                const int kk = key < hist_end ? key : 0;
+                kr[it] = *reinterpret_cast<const u32x4*>(kc + (size_t)kk * D + dseg * 8);
+                vr[it] = *reinterpret_cast<const u32x4*>(vc + (size_t)kk * D + dseg * 8);
+                mk[it] = mrow ? mrow[key < end ? key : start] : 0.f;
+            }
+            const int ps = meta[MAXB + b];
+            const int jr = tid % (D / 2);            // the RoPE dim of every item of this thread
+            const float rc = a.rope_cos[(size_t)ps * (D / 2) + jr], rs = a.rope_sin[(size_t)ps * (D / 2) + jr];
+            // q (r heads), k_new, v_new of row b: sums of the q/k/v parts
+            const uint64_t* qrow = a.qkv_part + (size_t)b * Nq;
+            gather_sum((r + 2) * D, a.S_qkv, (size_t)B * Nq, ep, wt,
+                       [&](int i) {
+                           const int col = i < r * D ? g * r * D + i
+                                         : i < (r + 1) * D ? qd + g * D + (i - r * D)
+                                                           : qd + kd + g * D + (i - (r + 1) * D);
+                           return qrow + col;
+                       },
+                       [&](int i, float v) { qkvf[i] = v; });
+            __syncthreads();
+            stamp_done(8);
+            // RoPE of q and k (Sec. 3.1, table of Sec. 4.6.2), bf16
+            for (int i = tid; i < (r + 1) * (D / 2); i += NTHR) {
+                const int hh = i / (D / 2), j = jr;
+                const float v0 = qkvf[hh * D + devpos<D>(j)], v1 = qkvf[hh * D + devpos<D>(j + D / 2)];
+                uint16_t* dst = hh < r ? qb + hh * D : knb;
+                dst[j] = bf16_bits_rne(v0 * rc - v1 * rs);
+                dst[j + D / 2] = bf16_bits_rne(v1 * rc + v0 * rs);
+            }
+            for (int j = tid; j < D; j += NTHR) vnb[j] = bf16_bits_rne(qkvf[(r + 1) * D + devpos<D>(j)]);
+            __syncthreads();
+            stamp_done(16);
+            if (chunk == 0) {     // the new row goes to cache slot ctx (read by later launches only)
+                uint16_t* kw = a.k_cache + (size_t)b * a.sb + (size_t)g * a.sh + (size_t)ctx * D;
+                uint16_t* vw = a.v_cache + (size_t)b * a.sb + (size_t)g * a.sh + (size_t)ctx * D;
+                for (int j = tid; j < D; j += NTHR) { kw[j] = knb[j]; vw[j] = vnb[j]; }
+            }
+            // scores (log2 domain) of every key of the chunk for the r heads
+#pragma unroll
+            for (int it = 0; it < NIT; it++) {
+                const int kbase = (it * NWAVE + wave) * KPW;
+                if (kbase >= nkeys) break;
+                const int key = start + kbase + kl;
+                uint32_t kw[4];
+                if (key == ctx) {
+                    const uint32_t* kp = reinterpret_cast<const uint32_t*>(knb + dseg * 8);
+                    kw[0] = kp[0]; kw[1] = kp[1]; kw[2] = kp[2]; kw[3] = kp[3];
+                } else {
+                    const u32x4 kk = kr[it];
+                    kw[0] = kk[0]; kw[1] = kk[1]; kw[2] = kk[2]; kw[3] = kk[3];
+                }
+                for (int i = 0; i < r; i++) {
+                    const uint32_t* qp = reinterpret_cast<const uint32_t*>(qb + i * D + dseg * 8);
                     float v = 0.f;
 #pragma unroll
                     for (int pp = 0; pp < 4; pp++)
-                        v = __builtin_amdgcn_fdot2_f32_bf16(as_bf16x2(qv[i][pp]), as_bf16x2(kw[pp]), v, false);
+                        v = __builtin_amdgcn_fdot2_f32_bf16(as_bf16x2(qp[pp]), as_bf16x2(kw[pp]), v, false);
 #pragma unroll
                     for (int o = 1; o < LPK; o <<= 1) v += __shfl_xor(v, o, 64);
-                    if (dseg == 0 && valid) {
-                        float s = v * a.scale_log2;
-                        if (mrow) s += mrow[key] * LOG2E;
-                        sc[i * a.chunk + (key - start)] = s;
+                    if (dseg == 0 && key < end) {
+                        float sv = v * a.scale_log2;
+                        if (mrow) sv += mk[it] * LOG2E;
+                        sc[i * CH + kbase + kl] = sv;
                     }
                 }
             }
             __syncthreads();
-            const int n = end - start;
+            stamp_done(17);
             for (int i = wave; i < r; i += NWAVE) {
                 float mx = -INFINITY;
-                for (int j = lane; j < n; j += 64) mx = fmaxf(mx, sc[i * a.chunk + j]);
+                for (int j = lane; j < nkeys; j += 64) mx = fmaxf(mx, sc[i * CH + j]);
                 mx = wave_max(mx);
                 float sum = 0.f;
-                for (int j = lane; j < n; j += 64) {
-                    const float pv = (mx == -INFINITY) ? 0.f : exp2f(sc[i * a.chunk + j] - mx);
-                    sc[i * a.chunk + j] = pv;
+                for (int j = lane; j < nkeys; j += 64) {
+                    const float pv = (mx == -INFINITY) ? 0.f : exp2f(sc[i * CH + j] - mx);
+                    sc[i * CH + j] = pv;
                     sum += pv;
                 }
                 sum = wave_sum(sum);
                 if (lane == 0) { stat[2 * i] = mx; stat[2 * i + 1] = sum; }
             }
             __syncthreads();
-            float ov[MAXR_F][8];
+            stamp_done(18);
+            // chunk output of every head: sum of p * v
+            uint64_t* ap = a.apart + ((size_t)b * nq + g * r) * NCH * (D + 2) + (size_t)chunk * (D + 2);
+            for (int i = 0; i < r; i++) {
+                float ov[8];
 #pragma unroll
-            for (int i = 0; i < MAXR_F; i++)
+                for (int j = 0; j < 8; j++) ov[j] = 0.f;
 #pragma unroll
-                for (int j = 0; j < 8; j++) ov[i][j] = 0.f;
-            for (int k0 = start + wave * KPW; k0 < end; k0 += NWAVE * KPW) {
-                const int key = k0 + kl;
-                if (key >= end) continue;
-                uint32_t vw[4];
-                if (key == ctx) {
-                    const uint64_t lo = ld_coh64(vn + dseg * 8), hi = ld_coh64(vn + dseg * 8 + 4);
-                    vw[0] = (uint32_t)lo; vw[1] = (uint32_t)(lo >> 32); vw[2] = (uint32_t)hi; vw[3] = (uint32_t)(hi >> 32);
-                } else {
-                    const u32x4 vv = *reinterpret_cast<const u32x4*>(vc + (size_t)key * d + dseg * 8);
-                    vw[0] = vv[0]; vw[1] = vv[1]; vw[2] = vv[2]; vw[3] = vv[3];
+                for (int it = 0; it < NIT; it++) {
+                    const int kbase = (it * NWAVE + wave) * KPW;
+                    if (kbase >= nkeys) break;
+                    const int key = start + kbase + kl;
+                    if (key < end) {
+                        uint32_t vw[4];
+                        if (key == ctx) {
+                            const uint32_t* vp = reinterpret_cast<const uint32_t*>(vnb + dseg * 8);
+                            vw[0] = vp[0]; vw[1] = vp[1]; vw[2] = vp[2]; vw[3] = vp[3];
+                        } else {
+                            const u32x4 vv = vr[it];
+                            vw[0] = vv[0]; vw[1] = vv[1]; vw[2] = vv[2]; vw[3] = vv[3];
+                        }
+                        const float pv = sc[i * CH + kbase + kl];
+#pragma unroll
+                        for (int pp = 0; pp < 4; pp++) {
+                            ov[2 * pp] += pv * __uint_as_float(vw[pp] << 16);
+                            ov[2 * pp + 1] += pv * __uint_as_float(vw[pp] & 0xFFFF0000u);
+                        }
+                    }
                 }
-                float vf[8];
-#pragma unroll
-                for (int pp = 0; pp < 4; pp++) {
-                    vf[2 * pp] = __uint_as_float(vw[pp] << 16);
-                    vf[2 * pp + 1] = __uint_as_float(vw[pp] & 0xFFFF0000u);
-                }
-#pragma unroll
-                for (int i = 0; i < MAXR_F; i++) {
-                    if (i >= r) break;
-                    const float pv = sc[i * a.chunk + (key - start)];
-#pragma unroll
-                    for (int j = 0; j < 8; j++) ov[i][j] += pv * vf[j];
-                }
-            }
-#pragma unroll
-            for (int i = 0; i < MAXR_F; i++) {
-                if (i >= r) break;
 #pragma unroll
                 for (int j = 0; j < 8; j++) {
-                    float v = ov[i][j];
+                    float v = ov[j];
 #pragma unroll
                     for (int o = LPK; o < 64; o <<= 1) v += __shfl_xor(v, o, 64);
-                    ov[i][j] = v;
+                    ov[j] = v;
                 }
                 if (kl == 0)
 #pragma unroll
-                    for (int j = 0; j < 8; j++) ored[(wave * MAXR_F + i) * D + dseg * 8 + j] = ov[i][j];
-            }
-            __syncthreads();
-            for (int idx = tid; idx < r * D; idx += NTHR) {
-                const int i = idx / D, dim = idx % D;
-                float v = 0.f;
+                    for (int j = 0; j < 8; j++) ored[wave * D + dseg * 8 + j] = ov[j];
+                __syncthreads();
+                uint64_t* aph = ap + (size_t)i * NCH * (D + 2);
+                for (int dim = tid; dim < D; dim += NTHR) {
+                    float v = 0.f;
 #pragma unroll
-                for (int w = 0; w < NWAVE; w++) v += ored[(w * MAXR_F + i) * D + dim];
-                float* pp = a.apart + (((size_t)b * nq + g * r + i) * a.nchunk + chunk) * (D + 2);
-                st_coh(pp + dim, v);
-                if (dim == 0) { st_coh(pp + D, stat[2 * i]); st_coh(pp + D + 1, stat[2 * i + 1]); }
-            }
-            // last chunk of this (b, g) combines the heads of the group
-            wait_stores();
-            __syncthreads();
-            __shared__ unsigned last_flag;
-            if (tid == 0) {
-                const unsigned nch = (unsigned)((ctx + 1 + a.chunk - 1) / a.chunk);
-                const unsigned old = atom_add(&a.cnt_attn[b * nkv + g], 1u);
-                last_flag = (old + 1 == nch);
-                if (last_flag) atom_st(&a.cnt_attn[b * nkv + g], 0u);
-            }
-            __syncthreads();
-            if (last_flag) {
-                compiler_fence();
-                const int nch = (ctx + 1 + a.chunk - 1) / a.chunk;
-                float* ml = sc;   // [r][nch][2] (the scores are no longer needed)
-                for (int idx = tid; idx < r * nch * 2; idx += NTHR) {
-                    const int i = idx / (nch * 2), rem2 = idx % (nch * 2);
-                    const int ch = rem2 / 2, which = rem2 % 2;
-                    ml[idx] = ld_coh(a.apart + (((size_t)b * nq + g * r + i) * a.nchunk + ch) * (D + 2) + D + which);
+                    for (int w = 0; w < NWAVE; w++) v += ored[w * D + dim];
+                    put_tagged(aph + dim, __float_as_uint(v), ep);
+                }
+                if (tid == 0) {
+                    put_tagged(aph + D, __float_as_uint(stat[2 * i]), ep);
+                    put_tagged(aph + D + 1, __float_as_uint(stat[2 * i + 1]), ep);
                 }
                 __syncthreads();
-                for (int idx = tid; idx < r * D; idx += NTHR) {
-                    const int i = idx / D, dim = idx % D;
-                    const float* pp = a.apart + (((size_t)b * nq + g * r + i) * a.nchunk) * (D + 2);
-                    const float* mli = ml + i * nch * 2;
-                    float M = -INFINITY;
-                    for (int ch = 0; ch < nch; ch++) M = fmaxf(M, mli[2 * ch]);
-                    float L = 0.f, O = 0.f;
-                    if (M != -INFINITY) {
-                        for (int c0 = 0; c0 < nch; c0 += 32) {
-                            float ov8[32];
+            }
+        }
+        stamp_done(9);
+
+        // ---- combine: this block's slice [v0, v1) of A (an even count).  LPV
+        // lanes share one value (each holds one chunk or more), so the max and
+        // the two sums over the chunks are lane shuffles.
+        const int V = B * qd, per = a.comb_per;
+        const int v0 = min(V, blk * per), v1 = min(V, v0 + per), nv = v1 - v0;
+        uint16_t* abuf = reinterpret_cast<uint16_t*>(smem);
+        if (nv > 0) {
+            const int LPV = a.comb_lpv, VPW = 64 / LPV;          // lanes per value (power of two)
+            const int cpl = (NCH + LPV - 1) / LPV;                // chunks per lane (<= 4)
+            for (int vb = wave * VPW; vb < nv; vb += NWAVE * VPW) {
+                const int j = vb + lane / LPV, cl = lane % LPV;
+                const bool valid = j < nv;
+                const int vv = v0 + (valid ? j : 0);
+                const int head = vv / D, dim = vv - head * D;     // head over all rows: b * nq + head
+                const int b = head / nq;
+                const int nch = (meta[b] + 1 + CH - 1) / CH;
+                const uint64_t* base = a.apart + (size_t)head * NCH * (D + 2);
+                uint64_t t0[4], t1w[4], t2[4];
+                bool use[4];
 #pragma unroll
-                            for (int j = 0; j < 32; j++)
-                                ov8[j] = (c0 + j < nch) ? ld_coh(pp + (c0 + j) * (D + 2) + dim) : 0.f;
-#pragma unroll
-                            for (int j = 0; j < 32; j++) {
-                                if (c0 + j >= nch) break;
-                                const float mc = mli[2 * (c0 + j)];
-                                if (mc == -INFINITY) continue;
-                                const float w = exp2f(mc - M);
-                                L += w * mli[2 * (c0 + j) + 1];
-                                O += w * ov8[j];
-                            }
-                        }
-                    }
-                    const f16 val = act_f16(L > 0.f ? O / L : 0.f);
-                    st_coh16(reinterpret_cast<uint16_t*>(a.A) + ((size_t)b * nq + g * r + i) * D + dim,
-                             __builtin_bit_cast(uint16_t, val));
+                for (int qq = 0; qq < 4; qq++) {
+                    const int ch = cl + qq * LPV;
+                    use[qq] = valid && qq < cpl && ch < nch;
+                    const uint64_t* p = base + (size_t)(use[qq] ? ch : 0) * (D + 2);
+                    t0[qq] = use[qq] ? get_tagged(p + dim) : 0;
+                    t1w[qq] = use[qq] ? get_tagged(p + D) : 0;
+                    t2[qq] = use[qq] ? get_tagged(p + D + 1) : 0;
                 }
+                float m[4], l[4], o[4];
+#pragma unroll
+                for (int qq = 0; qq < 4; qq++) {
+                    const uint64_t* p = base + (size_t)(cl + qq * LPV) * (D + 2);
+                    if (use[qq]) {
+                        o[qq] = __uint_as_float(settle(p + dim, t0[qq], ep, wt));
+                        m[qq] = __uint_as_float(settle(p + D, t1w[qq], ep, wt));
+                        l[qq] = __uint_as_float(settle(p + D + 1, t2[qq], ep, wt));
+                    } else {
+                        o[qq] = 0.f; m[qq] = -INFINITY; l[qq] = 0.f;
+                    }
+                }
+                float M = fmaxf(fmaxf(m[0], m[1]), fmaxf(m[2], m[3]));
+                for (int off = 1; off < LPV; off <<= 1) M = fmaxf(M, __shfl_xor(M, off, 64));
+                float L = 0.f, O = 0.f;
+                if (M != -INFINITY) {
+#pragma unroll
+                    for (int qq = 0; qq < 4; qq++) {
+                        if (m[qq] == -INFINITY) continue;
+                        const float w = exp2f(m[qq] - M);
+                        L += w * l[qq];
+                        O += w * o[qq];
+                    }
+                }
+                for (int off = 1; off < LPV; off <<= 1) {
+                    L += __shfl_xor(L, off, 64);
+                    O += __shfl_xor(O, off, 64);
+                }
+                if (valid && cl == 0) abuf[j] = __builtin_bit_cast(uint16_t, act_f16(L > 0.f ? O / L : 0.f));
             }
             __syncthreads();
+            stamp_done(10);
+            for (int j = 2 * tid; j < nv; j += 2 * NTHR)
+                put_tagged(a.A + (v0 + j) / 2, (uint32_t)abuf[j] | ((uint32_t)abuf[j + 1] << 16), ep);
+        }
+        __syncthreads();
+    }
+    stamp_done(1);
+
+    // ================= P3: o_proj partial sums =================
+    if (owns(3)) {
+        const int t3 = pl[4], ka3 = pl[5], kz3 = pl[6], s3 = pl[7];
+        const Run run3 = wave_run(3);
+        const int klo = ka3 * 64, kh = (kz3 - ka3) * 32;       // k range in fp16 pairs
+        for (int b = 0; b < B; b++) {
+            const uint64_t* src = a.A + ((size_t)b * qd + klo) / 2;
+            f16* dst = xs + b * ldx;
+            gather_raw(kh, ep, wt, [&](int i) -> const uint64_t* { return src + i; },
+                       [&](int i, uint32_t p) { *reinterpret_cast<uint32_t*>(dst + 2 * i) = p; });
+        }
+        stamp_done(11);
+        clear_red();
+        __syncthreads();
+        stamp_done(19);
+        if (run3.ka < run3.kz)
+            gemv_run<RING_O, false, false>(a.o, run3, xs - klo, ldx, B, R3, q3, [&](int, const float (&out)[4]) { to_red(0, out); });
+        stamp_done(20);
+        __syncthreads();
+        stamp_done(21);
+        for (int i = tid; i < B * 32; i += NTHR) {
+            const int b = i >> 5, cc = i & 31;
+            put_tagged(a.o_part + ((size_t)s3 * B + b) * H + t3 * 32 + cc, __float_as_uint(red_sum(0, b, cc)), ep);
         }
     }
-    arrive(1);
-    {
-        const unsigned gen = grid_arrive(a.bar);
-        gemv_prefetch(a.o, sp_o, pf);
-        grid_wait(a.bar, gen, a.err);
-    }
-    stamp(2);
+    prefetch(4);
+    stamp_done(2);
 
-    // ================= P3: o_proj, h = x + A Wo =================
-    load_rows_f16(a.A, B, qd, xs);
-    {
-        const Split& sp = sp_o;
-        gemv_share<MAXB>(a.o, sp, xs, qd, B, pf, [&](int t, int seg, const float (&acc)[MAXB]) {
-            store_partial<MAXB>(a.part_o, a.segmax_o, t, seg, B, acc);
-            if (!pair_done(a.cnt_o, t, sp.nseg(t))) return;
-            if (lane < 32)
-                for (int b = 0; b < B; b++) {
-                    const size_t i = (size_t)b * H + t * 32 + lane;
-                    st_coh(a.h + i, a.x[i] + sum_partials(a.part_o, a.segmax_o, sp, t, B, b, lane));
-                }
-        });
+    // ================= P4: h, RMSNorm(h), gate/up, SwiGLU =================
+    gather_sum(B * H, a.S_o, (size_t)B * H, ep, wt, [&](int i) { return a.o_part + i; },
+               [&](int i, float v) { hbuf[i] += v; });
+    __syncthreads();
+    stamp_done(12);
+    if (owns(4)) {
+        const int ta4 = pl[8], tb4 = pl[9];
+        const Run run4 = wave_run(4);
+        norm_rows(hbuf, gam + H, a.eps, B, H, xs, ldx, red8);
+        stamp_done(22);
+        clear_red();
+        if (run4.ka < run4.kz)
+            gemv_run<RING, false, false>(a.gu, run4, xs, ldx, B, R4, q4,
+                                         [&](int t, const float (&out)[4]) { to_red(t - ta4, out); });
+        stamp_done(13);
+        __syncthreads();
+        const int np = (tb4 - ta4) / 2;
+        for (int i = tid; i < np * B * 16; i += NTHR) {
+            const int pp = i / (B * 16), rem = i - pp * B * 16, b = rem >> 4, cc = 2 * (rem & 15);
+            const f16 g0 = act_f16(silu(red_sum(2 * pp, b, cc)) * red_sum(2 * pp + 1, b, cc));
+            const f16 g1 = act_f16(silu(red_sum(2 * pp, b, cc + 1)) * red_sum(2 * pp + 1, b, cc + 1));
+            const uint32_t word = (uint32_t)__builtin_bit_cast(uint16_t, g0) | ((uint32_t)__builtin_bit_cast(uint16_t, g1) << 16);
+            put_tagged(a.g + ((size_t)b * a.F_pad + (ta4 / 2 + pp) * 32 + cc) / 2, word, ep);
+        }
     }
-    arrive(2);
-    {
-        const unsigned gen = grid_arrive(a.bar);
-        gemv_prefetch(a.gu, sp_gu, pf);
-        grid_wait(a.bar, gen, a.err);
-    }
-    stamp(3);
-
-    // ================= P4: gate/up on RMSNorm(h) =================
-    norm_rows<MAXB>(a.h, true, a.mlp_norm, a.eps, B, H, xs, red);
-    {
-        const Split& sp = sp_gu;
-        gemv_share<MAXB>(a.gu, sp, xs, H, B, pf, [&](int t, int seg, const float (&acc)[MAXB]) {
-            store_partial<MAXB>(a.part_gu, a.segmax_gu, t, seg, B, acc);
-            const int p = t / 2;
-            if (!pair_done(a.cnt_gu, p, sp.nseg(2 * p) + sp.nseg(2 * p + 1))) return;
-            if (lane < 32) {
-                for (int b = 0; b < B; b++) {
-                    const float gv = sum_partials(a.part_gu, a.segmax_gu, sp, 2 * p, B, b, lane);
-                    const float uv = sum_partials(a.part_gu, a.segmax_gu, sp, 2 * p + 1, B, b, lane);
-                    const f16 val = act_f16(silu(gv) * uv);
-                    st_coh16(reinterpret_cast<uint16_t*>(a.g) + (size_t)b * a.F_pad + p * 32 + lane,
-                             __builtin_bit_cast(uint16_t, val));
-                }
-            }
-        });
-    }
-    arrive(3);
-    {
-        const unsigned gen = grid_arrive(a.bar);
-        gemv_prefetch(a.down, sp_dn, pf);
-        grid_wait(a.bar, gen, a.err);
-    }
-    stamp(4);
+    prefetch(5);
+    stamp_done(3);
 
     // ================= P5: down, y = h + g Wd =================
-    load_rows_f16(a.g, B, a.F_pad, xs);
-    {
-        const Split& sp = sp_dn;
-        gemv_share<MAXB>(a.down, sp, xs, a.F_pad, B, pf, [&](int t, int seg, const float (&acc)[MAXB]) {
-            store_partial<MAXB>(a.part_down, a.segmax_down, t, seg, B, acc);
-            if (!pair_done(a.cnt_down, t, sp.nseg(t))) return;
-            if (lane < 32)
-                for (int b = 0; b < B; b++) {
-                    const size_t i = (size_t)b * H + t * 32 + lane;
-                    a.y[i] = ld_coh(a.h + i) + sum_partials(a.part_down, a.segmax_down, sp, t, B, b, lane);
-                }
-        });
-    }
-    arrive(4);
-    if (a.stamps) {          // end: the last block to finish writes the time
-        wait_stores();
+    if (owns(5)) {
+        const int t5 = pl[10], ka5 = pl[11], kz5 = pl[12], s5 = pl[13];
+        const Run run5 = wave_run(5);
+        const int klo = ka5 * 64, kh = (kz5 - ka5) * 32;
+        for (int b = 0; b < B; b++) {
+            const uint64_t* src = a.g + ((size_t)b * a.F_pad + klo) / 2;
+            f16* dst = xs + b * ldx;
+            gather_raw(kh, ep, wt, [&](int i) -> const uint64_t* { return src + i; },
+                       [&](int i, uint32_t p) { *reinterpret_cast<uint32_t*>(dst + 2 * i) = p; });
+        }
+        stamp_done(14);
+        clear_red();
         __syncthreads();
-        if (tid == 0 && atom_add(&a.bar[8], 1u) + 1 == gridDim.x) {
-            atom_st(&a.bar[8], 0u);
-            a.stamps[5] = wall_clock64();
+        if (run5.ka < run5.kz)
+            gemv_run<RING, false, false>(a.down, run5, xs - klo, ldx, B, R5, q5, [&](int, const float (&out)[4]) { to_red(0, out); });
+        stamp_done(15);
+        __syncthreads();
+        if (s5 > 0) {
+            for (int i = tid; i < B * 32; i += NTHR) {
+                const int b = i >> 5, cc = i & 31;
+                put_tagged(a.down_part + ((size_t)s5 * B + b) * H + t5 * 32 + cc, __float_as_uint(red_sum(0, b, cc)), ep);
+            }
+        } else {
+            for (int i = tid; i < B * 32; i += NTHR) own[i] = red_sum(0, i >> 5, i & 31);
+            __syncthreads();
+            gather_sum(B * 32, a.S_down - 1, (size_t)B * H, ep, wt,
+                       [&](int i) { return a.down_part + ((size_t)1 * B + (i >> 5)) * H + t5 * 32 + (i & 31); },
+                       [&](int i, float v) {
+                           const int b = i >> 5, col = t5 * 32 + (i & 31);
+                           a.y[(size_t)b * H + col] = hbuf[b * H + col] + (own[i] + v);
+                       });
         }
     }
+    stamp_done(4);
 }
 
 template <int D, int MAXB>
@@ -720,15 +636,39 @@ int launch_t(const DecodeFusedArgs& a, hipStream_t stream) {
     auto fn = decode_fused_kernel<D, MAXB>;
     if (hipFuncSetAttribute((const void*)fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)a.lds_bytes) != hipSuccess)
         return -1;
-    DecodeFusedArgs args = a;
-    void* kargs[] = {&args};
-    return hipLaunchCooperativeKernel((const void*)fn, dim3(a.nblocks), dim3(NTHR), kargs, a.lds_bytes, stream) ==
-                   hipSuccess
-               ? 0
-               : -1;
+    // An ordinary launch: one block per CU (the LDS of a block leaves room for
+    // no second one), so every block is resident once the CUs are free.  A
+    // cooperative launch would guarantee the same at about 20 us per launch.
+    hipLaunchKernelGGL(fn, dim3(a.nblocks), dim3(NTHR), a.lds_bytes, stream, a);
+    return hipGetLastError() == hipSuccess ? 0 : -1;
 }
 
 }  // namespace
+
+void decode_fused_plan(int P, const DevLinear& qkv, const DevLinear& o, const DevLinear& gu, const DevLinear& down,
+                       int S_qkv, int S_o, int S_down, int* out) {
+    auto part = [&](int blk, const DevLinear& W, int S, int* e) {
+        const int nt = W.N_dev / 32, kb = W.K_pad / 64;
+        if (blk >= nt * S) { e[0] = -1; e[1] = e[2] = e[3] = 0; return; }
+        const int t = blk / S, s = blk % S;
+        e[0] = t;
+        e[1] = s * kb / S;
+        e[2] = (s + 1) * kb / S;
+        e[3] = s;
+    };
+    const int np = gu.N_dev / 64;
+    for (int blk = 0; blk < P; blk++) {
+        int* e = out + (size_t)blk * 16;
+        part(blk, qkv, S_qkv, e);
+        part(blk, o, S_o, e + 4);
+        e[8] = 2 * (int)((long long)blk * np / P);
+        e[9] = 2 * (int)((long long)(blk + 1) * np / P);
+        part(blk, down, S_down, e + 10);
+        e[14] = e[15] = 0;
+    }
+}
+
+int decode_fused_max_chunk(int head_dim) { return NIT * NWAVE * (64 / (head_dim / 8)); }
 
 int decode_fused_blocks(int head_dim, int B, size_t lds_bytes) {
     int dev = 0, cus = 0, occ = 0;
@@ -743,7 +683,7 @@ int decode_fused_blocks(int head_dim, int B, size_t lds_bytes) {
 }
 
 int launch_decode_fused(const DecodeFusedArgs& a, hipStream_t stream) {
-    if (a.B > 4) return -1;
+    if (a.B > 4 || a.S_qkv > MAXS || a.S_o > MAXS || a.S_down > MAXS) return -1;
     if (a.d == 128) return a.B <= 1 ? launch_t<128, 1>(a, stream) : launch_t<128, 4>(a, stream);
     if (a.d == 64) return a.B <= 1 ? launch_t<64, 1>(a, stream) : launch_t<64, 4>(a, stream);
     return -1;

@@ -70,12 +70,13 @@ __global__ void __launch_bounds__(256) gemm_w4_kernel(const f16* __restrict__ X,
 #pragma unroll
         for (int j = 0; j < 2; j++) acc[i][j] = f32x16{};
 
+    const DqConst dq = dq_const();
     u32x4 xr[4];
     load_x(0, xr);
     store_x(0, xr);
     u32x4 b0 = wt0[0], b1 = wt1[0];
-    f16x2 zo0 = zero_offset_pair(W.zeros, (size_t)col0 * W.KG);
-    f16x2 zo1 = zero_offset_pair(W.zeros, (size_t)col1 * W.KG);
+    ZeroOff zo0 = zero_off(W.zeros ? (float)W.zeros[col0] : 8.0f);
+    ZeroOff zo1 = zero_off(W.zeros ? (float)W.zeros[col1] : 8.0f);
 
     for (int kb = 0; kb < KB; kb++) {
         __syncthreads();
@@ -91,19 +92,19 @@ __global__ void __launch_bounds__(256) gemm_w4_kernel(const f16* __restrict__ X,
             const int k = kb * BK + s * 16;
             if ((k & Gm1) == 0 && k > 0) {
                 const int g = k >> W.lgG;
-                const float r0 = W.ratios[(size_t)col0 * W.KG + g];
-                const float r1 = W.ratios[(size_t)col1 * W.KG + g];
+                const float r0 = W.ratios[(size_t)g * W.N_dev + col0];
+                const float r1 = W.ratios[(size_t)g * W.N_dev + col1];
 #pragma unroll
                 for (int i = 0; i < 2; i++)
 #pragma unroll
                     for (int e = 0; e < 16; e++) { acc[i][0][e] *= r0; acc[i][1][e] *= r1; }
                 if (W.zeros) {
-                    zo0 = zero_offset_pair(W.zeros, (size_t)col0 * W.KG + g);
-                    zo1 = zero_offset_pair(W.zeros, (size_t)col1 * W.KG + g);
+                    zo0 = zero_off((float)W.zeros[(size_t)g * W.N_dev + col0]);
+                    zo1 = zero_off((float)W.zeros[(size_t)g * W.N_dev + col1]);
                 }
             }
-            f16x8 bf0 = dequant_word(b0[s], zo0);
-            f16x8 bf1 = dequant_word(b1[s], zo1);
+            f16x8 bf0 = dequant8(b0[s], zo0, dq);
+            f16x8 bf1 = dequant8(b1[s], zo1, dq);
 #pragma unroll
             for (int i = 0; i < 2; i++) {
                 const f16* ap = &As[buf][(wm * 64 + i * 32 + c) * LDA + s * 16 + h * 8];

@@ -1,47 +1,51 @@
-// W4A16 GEMV for the decode stage (B <= 8 rows): y[b][n] = sum_k x[b][k] W[k][n].
+// W4A16 GEMV for the decode stage, one kernel per linear (B <= 8 rows):
+// y[b][n] = sum_k x[b][k] W[k][n].
 //
-// HBM-streaming: every weight tile (32 columns x 64 k, 1 KB) is read once with
-// one 16-byte load per lane.  Codes are turned into exact fp16 (code - zero)
-// pairs in registers and dotted with the fp16-held bf16 activations by
-// v_dot2_f32_f16 into a per-group fp32 sum, which is multiplied by the group
-// scale.  The two lanes that share a column (k halves) meet with one shuffle,
-// the waves that split K meet in LDS.
-//
-// Block: 512 threads = 8 waves on a pair of tiles (64 device columns: a RoPE
-// pair of q/k blocks or a gate/up pair), 4 waves per tile splitting the
-// block's k range.  Grid: (N_dev / 64, ksplit); with ksplit > 1 the residual
-// epilogue adds into an output that an earlier kernel initialised.
+// Block: 512 threads = 8 waves on a pair of column tiles (64 device columns:
+// a RoPE pair of q/k blocks, a gate/up pair, or two residual tiles) and the
+// block's k range; the waves split the k range evenly and each streams its
+// share through the register ring of the GEMV core (gemv_core.h).  The wave
+// partials meet in LDS in a fixed order.  Grid: (N_dev / 64, ksplit); with
+// ksplit > 1 the residual epilogue adds into an output that an earlier
+// kernel initialised.
 //
 // Optional prologue: RMSNorm of the fp32 rows (every block reduces the whole
-// row; the rows are small and L2-resident), rounded to bf16.
+// row; the rows are small and L2-resident), rounded to bf16.  The first
+// weight tiles are requested before the prologue runs.
 #include "common.h"
+#include "gemv_core.h"
 #include "launch.h"
 
 namespace {
 
 constexpr int NW = 8;            // waves per block
-constexpr int NSUB = NW / 2;     // waves per tile
 constexpr int MAXB = 8;
+constexpr int RING = 8;          // tiles in flight per wave
 
-__device__ __forceinline__ float scale_at(const DevLinear& W, int n, int g) {
-    return (float)__builtin_bit_cast(f16, W.scales[(size_t)n * W.KG + g]);
-}
-
-template <int EPI, bool NORM>
+template <int EPI, bool NORM, bool ZP, bool G32>
 __global__ void __launch_bounds__(NW * 64) gemv_w4_kernel(GemvArgs a) {
     extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
     const DevLinear& W = a.W;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int pair = blockIdx.x;
     const int KB = W.K_pad / 64;
     const int kb_lo = (int)((long long)blockIdx.y * KB / a.ksplit);
     const int kb_hi = (int)((long long)(blockIdx.y + 1) * KB / a.ksplit);
     const int klo = kb_lo * 64, klen = (kb_hi - kb_lo) * 64;
+    const int ldx = klen + 8;
     const int B = a.B;
-    f16* xs = reinterpret_cast<f16*>(smem);                        // [B][klen]
-    float* red = reinterpret_cast<float*>(smem + (size_t)MAXB * klen * 2);  // [NSUB][2][MAXB][32]
-    float* rinv = red + NSUB * 2 * MAXB * 32;                        // [MAXB]
-    float* tot = rinv + MAXB;                                        // [MAXB][64]
+    f16* xs = reinterpret_cast<f16*>(smem);                                   // [B][ldx]
+    float* red = reinterpret_cast<float*>(smem + (size_t)MAXB * ldx * 2);     // [NW][2][MAXB][32]
+    float* rinv = red + NW * 2 * MAXB * 32;                                   // [MAXB]
+    float* tot = rinv + MAXB;                                                 // [MAXB][64]
+
+    // this wave's k-tiles of both column tiles
+    const int nk = kb_hi - kb_lo;
+    const Run run{pair * 2, pair * 2 + 2, kb_lo + wave * nk / NW, kb_lo + (wave + 1) * nk / NW};
+    TileRing<RING, G32> R;
+    RunCursor q;
+    if (run.ka < run.kz) ring_prefetch<RING, ZP, G32>(W, run, R, q);
 
     // side copy (e.g. residual initialisation of the next accumulation)
     if (a.copy_n > 0) {
@@ -67,90 +71,38 @@ __global__ void __launch_bounds__(NW * 64) gemv_w4_kernel(GemvArgs a) {
         for (int i = tid; i < B * klen; i += NW * 64) {
             const int b = i / klen, k = i - b * klen;
             const float g = bf16_bits_to_f32(a.gamma[klo + k]);
-            xs[i] = act_f16(a.x_f32[(size_t)b * K + klo + k] * rinv[b] * g);
+            xs[b * ldx + k] = act_f16(a.x_f32[(size_t)b * K + klo + k] * rinv[b] * g);
         }
     } else {
         const int nv = klen / 8;
         for (int i = tid; i < B * nv; i += NW * 64) {
             const int b = i / nv, v = i - b * nv;
-            *reinterpret_cast<u32x4*>(xs + (size_t)b * klen + v * 8) =
+            *reinterpret_cast<u32x4*>(xs + b * ldx + v * 8) =
                 *reinterpret_cast<const u32x4*>(a.x_f16 + (size_t)b * a.ldx + klo + v * 8);
         }
     }
     __syncthreads();
 
-    // ---- main loop
-    const int t = wave & 1, sub = wave >> 1;
+    // ---- main loop: partial sums of this wave into red[wave]
     const int h = lane >> 5, c = lane & 31;
-    const int nt = pair * 2 + t;
-    const int col = nt * 32 + c;
-    const u32x4* tiles = reinterpret_cast<const u32x4*>(W.qw) + (size_t)nt * KB * 64 + lane;
-
-    float acc[MAXB], gacc[MAXB];
+    if (run.ka < run.kz) {
+        gemv_run<RING, ZP, G32>(W, run, xs - klo, ldx, B, R, q, [&](int t, const float (&out)[4]) {
+            const int tt = t - pair * 2;
 #pragma unroll
-    for (int b = 0; b < MAXB; b++) { acc[b] = 0.f; gacc[b] = 0.f; }
-    int cur_g = -1;
-    float sc = 0.f;
-    f16x2 zo = zero_offset_pair(nullptr, 0);
-
-    constexpr int DEPTH = 4;
-    for (int kb0 = kb_lo + sub; kb0 < kb_hi; kb0 += NSUB * DEPTH) {
-        u32x4 wv[DEPTH];
-#pragma unroll
-        for (int u = 0; u < DEPTH; u++) {
-            const int kb = kb0 + u * NSUB;
-            wv[u] = (kb < kb_hi) ? tiles[(size_t)kb * 64] : u32x4{0, 0, 0, 0};
-        }
-#pragma unroll
-        for (int u = 0; u < DEPTH; u++) {
-            const int kb = kb0 + u * NSUB;
-            if (kb >= kb_hi) break;
-#pragma unroll
-            for (int s = 0; s < 4; s++) {
-                const int k = kb * 64 + s * 16 + h * 8;
-                const int g = (kb * 64 + s * 16) >> W.lgG;
-                if (g != cur_g) {
-#pragma unroll
-                    for (int b = 0; b < MAXB; b++) { acc[b] += sc * gacc[b]; gacc[b] = 0.f; }
-                    cur_g = g;
-                    sc = scale_at(W, col, g);
-                    if (W.zeros) zo = zero_offset_pair(W.zeros, (size_t)col * W.KG + g);
-                }
-                const uint32_t wd = wv[u][s];
-                const f16x2 d0 = dequant_pair(wd, 0, zo), d1 = dequant_pair(wd, 1, zo);
-                const f16x2 d2 = dequant_pair(wd, 2, zo), d3 = dequant_pair(wd, 3, zo);
-#pragma unroll
-                for (int b = 0; b < MAXB; b++) {
-                    if (b < B) {
-                        const f16x8 xv = *reinterpret_cast<const f16x8*>(xs + (size_t)b * klen + (k - klo));
-                        float v = gacc[b];
-                        v = __builtin_amdgcn_fdot2(f16x2{xv[0], xv[1]}, d0, v, false);
-                        v = __builtin_amdgcn_fdot2(f16x2{xv[2], xv[3]}, d1, v, false);
-                        v = __builtin_amdgcn_fdot2(f16x2{xv[4], xv[5]}, d2, v, false);
-                        v = __builtin_amdgcn_fdot2(f16x2{xv[6], xv[7]}, d3, v, false);
-                        gacc[b] = v;
-                    }
-                }
+            for (int r = 0; r < 4; r++) {
+                const int b = 4 * h + r;
+                if (b < B) red[((wave * 2 + tt) * MAXB + b) * 32 + c] = out[r];
             }
-        }
-    }
-#pragma unroll
-    for (int b = 0; b < MAXB; b++) acc[b] += sc * gacc[b];
-
-    // ---- reduction: k halves (lanes l, l^32), then the waves of a tile
-#pragma unroll
-    for (int b = 0; b < MAXB; b++) acc[b] += __shfl_xor(acc[b], 32, 64);
-    if (h == 0) {
-#pragma unroll
-        for (int b = 0; b < MAXB; b++)
-            if (b < B) red[((sub * 2 + t) * MAXB + b) * 32 + c] = acc[b];
+        });
+    } else {
+        for (int i = lane; i < 2 * MAXB * 32; i += 64) red[wave * 2 * MAXB * 32 + i] = 0.f;
     }
     __syncthreads();
     for (int i = tid; i < B * 64; i += NW * 64) {
         const int b = i / 64, cc = i % 64;
         const int tt = cc / 32, c2 = cc % 32;
         float v = 0.f;
-        for (int s2 = 0; s2 < NSUB; s2++) v += red[((s2 * 2 + tt) * MAXB + b) * 32 + c2];
+        for (int w = 0; w < NW; w++) v += red[((w * 2 + tt) * MAXB + b) * 32 + c2];
         tot[b * 64 + cc] = v;
     }
     __syncthreads();
@@ -181,26 +133,34 @@ __global__ void __launch_bounds__(NW * 64) gemv_w4_kernel(GemvArgs a) {
     }
 }
 
-template <int EPI, bool NORM>
+template <int EPI, bool NORM, bool ZP, bool G32>
 int launch_t(const GemvArgs& a, hipStream_t stream) {
     const int KB = a.W.K_pad / 64;
     const int kmax = (KB + a.ksplit - 1) / a.ksplit * 64;
-    const size_t smem = (size_t)MAXB * kmax * 2 + (NSUB * 2 * MAXB * 32 + MAXB + MAXB * 64) * sizeof(float);
+    const size_t smem = (size_t)MAXB * (kmax + 8) * 2 + (NW * 2 * MAXB * 32 + MAXB + MAXB * 64) * sizeof(float);
     if (smem > 160 * 1024) return -1;
     if (smem > 64 * 1024 &&
-        hipFuncSetAttribute((const void*)gemv_w4_kernel<EPI, NORM>, hipFuncAttributeMaxDynamicSharedMemorySize,
+        hipFuncSetAttribute((const void*)gemv_w4_kernel<EPI, NORM, ZP, G32>, hipFuncAttributeMaxDynamicSharedMemorySize,
                             (int)smem) != hipSuccess)
         return -1;
     dim3 grid(a.W.N_dev / 64, a.ksplit);
-    hipLaunchKernelGGL((gemv_w4_kernel<EPI, NORM>), grid, dim3(NW * 64), smem, stream, a);
+    hipLaunchKernelGGL((gemv_w4_kernel<EPI, NORM, ZP, G32>), grid, dim3(NW * 64), smem, stream, a);
     return hipGetLastError() == hipSuccess ? 0 : -1;
+}
+
+template <bool ZP, bool G32>
+int launch_zp(int epi, bool norm, const GemvArgs& a, hipStream_t stream) {
+    if (epi == EPI_QKV && norm) return launch_t<EPI_QKV, true, ZP, G32>(a, stream);
+    if (epi == EPI_SWIGLU && norm) return launch_t<EPI_SWIGLU, true, ZP, G32>(a, stream);
+    if (epi == EPI_RESID && !norm) return launch_t<EPI_RESID, false, ZP, G32>(a, stream);
+    return -1;
 }
 
 }  // namespace
 
 int launch_gemv_w4(int epi, bool norm, const GemvArgs& a, hipStream_t stream) {
-    if (epi == EPI_QKV && norm) return launch_t<EPI_QKV, true>(a, stream);
-    if (epi == EPI_SWIGLU && norm) return launch_t<EPI_SWIGLU, true>(a, stream);
-    if (epi == EPI_RESID && !norm) return launch_t<EPI_RESID, false>(a, stream);
-    return -1;
+    if (a.B < 1 || a.B > MAXB) return -1;
+    const bool g32 = a.W.lgG == 5;
+    if (a.W.sz) return g32 ? launch_zp<true, true>(epi, norm, a, stream) : launch_zp<true, false>(epi, norm, a, stream);
+    return g32 ? launch_zp<false, true>(epi, norm, a, stream) : launch_zp<false, false>(epi, norm, a, stream);
 }

@@ -64,9 +64,12 @@ __global__ void debug_dequant_kernel(DevLinear W, const int32_t* __restrict__ co
         const int lane = hh * 32 + cc;
         const uint32_t w = W.qw[(((size_t)nt * KB + kb) * 64 + lane) * 4 + s];
         const int g = k >> W.lgG;
-        const f16x2 pr = dequant_pair(w, j / 2, zero_offset_pair(W.zeros, (size_t)nd * W.KG + g));
-        const float qz = (float)pr[j % 2];
-        const float sc = (float)__builtin_bit_cast(f16, W.scales[(size_t)nd * W.KG + g]);
+        const size_t gi = (size_t)g * W.N_dev + nd;
+        const f16x8 v8 = dequant8(w, zero_off(W.zeros ? (float)W.zeros[gi] : 8.0f), dq_const());
+        f16 vals[8];
+        __builtin_memcpy(vals, &v8, sizeof vals);
+        const float qz = (float)vals[j];
+        const float sc = (float)__builtin_bit_cast(f16, W.scales[gi]);
         out[i] = qz * sc;
     }
 }
