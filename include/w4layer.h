@@ -226,12 +226,15 @@ int layer_decode_phase_times(layer_t layer, float* us_out, int32_t* error_flag);
 /* Raw wall-clock stamps of the last persistent decode call (diagnostics):
  * [0] kernel start (block 0), [1] number of blocks, and at [8 + p*nblocks + j]
  * the time block j passed point p: p = 0..4 the end of the five phases,
- * 5 its start, 6/7 the end of the q/k/v RMSNorm / GEMV, 8 q/k/v gathered by
- * its attention unit, 9 its attention units done, 10 the chunk outputs of
- * its combine slice gathered, 11 the o_proj input gathered, 12 h gathered,
- * 13 the gate/up GEMV done, 14 the down input gathered, 15 the down GEMV
- * done (points of work a block does not own keep older values).  Copies
- * min(n, 8 + 16*1024) values.  Waits for the device. */
+ * 5 its start, 23 the end of its prologue, 6/7 the end of the q/k/v RMSNorm /
+ * GEMV, 8 q/k/v gathered by its attention unit, 16 RoPE applied, 17 scores
+ * done, 18 softmax statistics done, 9 its attention units done, 10 the chunk
+ * outputs of its combine slice gathered, 11 the o_proj input gathered, 19
+ * o_proj GEMV started, 20/21 its wave / all waves done, 12 h gathered, 22 the
+ * MLP RMSNorm done, 13/24 the gate/up GEMV done in wave 0 / all waves, 14 the
+ * down input gathered, 15 the down GEMV done (points of work a block does not
+ * own keep older values).  Copies min(n, 8 + 32*1024) values.  Waits for the
+ * device. */
 int layer_debug_decode_stamps(layer_t layer, uint64_t* out, int32_t n);
 
 /* Per-kernel timing for measurement (diagnostics, not for concurrent use).

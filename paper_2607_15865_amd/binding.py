@@ -217,7 +217,7 @@ def layer_decode_phase_times(handle):
     return rc, list(us), err.value
 
 
-def layer_debug_decode_stamps(handle, n: int = 8 + 24 * 1024):
+def layer_debug_decode_stamps(handle, n: int = 8 + 32 * 1024):
     out = np.zeros(n, dtype=np.uint64)
     rc = _lib.layer_debug_decode_stamps(handle, out.ctypes.data, n)
     return rc, out

@@ -149,7 +149,7 @@ struct Profiler {          // one timed kernel per stage
 };
 
 constexpr int kMaxBlocks = 1024;                    // persistent decode blocks (one per CU)
-constexpr int kStampWords = 8 + 24 * kMaxBlocks;
+constexpr int kStampWords = 8 + 32 * kMaxBlocks;
 
 struct layer_s {
     layer_config cfg{};
@@ -162,6 +162,9 @@ struct layer_s {
     DevBuf sync;
     DevBuf fplan;                 // work table of the persistent decode (decode_fused_plan)
     int fplan_blocks = 0, S_qkv = 1, S_o = 1, S_down = 1;
+    // prefill GEMM split-K tile counters (zero between calls) and the CU count
+    DevBuf gemm_cnt;
+    int num_cus = 256;
     int* err = nullptr;
     unsigned long long* stamps = nullptr;
     int decode_path = 0;   // 0 auto, 1 separate kernels, 2 persistent
@@ -262,18 +265,28 @@ struct Carve {
     }
 };
 
-struct PrefillWs { size_t xn1, q, attn, h, xn2, g, total; };
+constexpr int kGemmCounters = 1024;     // split-K tiles of one GEMM (at most about one per CU)
+
+struct PrefillWs {
+    size_t xn1, q, attn, h, xn2, g, part, total;
+    GemmPlan qkv, o, gu, down;
+};
 PrefillWs plan_prefill(const layer_s* L, int T) {
     const layer_config& c = L->cfg;
     const size_t qd = (size_t)c.n_heads * c.head_dim;
     Carve cv;
     PrefillWs w;
+    w.qkv = gemm_w4_plan(T, L->qkv.d, L->num_cus);
+    w.o = gemm_w4_plan(T, L->o.d, L->num_cus);
+    w.gu = gemm_w4_plan(T, L->gu.d, L->num_cus);
+    w.down = gemm_w4_plan(T, L->down.d, L->num_cus);
     w.xn1 = cv.take((size_t)T * c.hidden * 2);
     w.q = cv.take((size_t)T * qd * 2);
     w.attn = cv.take((size_t)T * qd * 2);
     w.h = cv.take((size_t)T * c.hidden * 4);
     w.xn2 = cv.take((size_t)T * c.hidden * 2);
     w.g = cv.take((size_t)T * L->F_pad * 2);
+    w.part = cv.take(std::max(std::max(w.qkv.part_bytes, w.o.part_bytes), std::max(w.gu.part_bytes, w.down.part_bytes)));
     w.total = cv.off;
     return w;
 }
@@ -348,7 +361,7 @@ FusedPlan plan_fused(const layer_s* L, int B, int max_ctx, bool query_device) {
     p.ldx = std::max(std::max(H, kr_o), kr_d) + 8;
     const int maxb = B <= 1 ? 1 : 4;
     const size_t xs_bytes = (size_t)B * p.ldx * 2;
-    const size_t attn_bytes = (size_t)(MAXR * ch + NWAVE * d + 2 * MAXR + (MAXR + 2) * d) * 4 + (size_t)(MAXR * d + 2 * d) * 2;
+    const size_t attn_bytes = (size_t)(MAXR * ch + NWAVE * MAXR * d + 2 * MAXR + (MAXR + 2) * d) * 4 + (size_t)(MAXR * d + 2 * d) * 2;
     const int V = B * qd;
     p.comb_per = (((V + P - 1) / P) + 1) & ~1;
     p.comb_lpv = 1;
@@ -448,7 +461,11 @@ int run_prefill(layer_s* L, const float* x, const int32_t* pos, int T, int hist,
     float* h = (float*)(base + w.h);
     f16* xn2 = (f16*)(base + w.xn2);
     f16* g = (f16*)(base + w.g);
+    float* part = (float*)(base + w.part);
+    unsigned* cnt = (unsigned*)L->gemm_cnt.p;
     const int H = c.hidden, d = c.head_dim, qd = c.n_heads * d;
+    for (const GemmPlan* gp : {&w.qkv, &w.o, &w.gu, &w.down})
+        if (gp->S > 1 && gp->tiles > kGemmCounters) return fail(W4_EUNSUPPORTED, "split-K tile count above %d", kGemmCounters);
 
     int rc = 0;
     const int stage = hist > 0 ? 1 : 0;
@@ -461,7 +478,7 @@ int run_prefill(layer_s* L, const float* x, const int32_t* pos, int T, int hist,
     e.cache_stride_h = (long long)c.max_seq * d;
     e.pos = pos;
     e.slot_base = hist;
-    { ProfScope ps(L, stage, 1, st); rc |= launch_gemm_w4(EPI_QKV, xn1, T, H, L->qkv.d, e, st); }
+    { ProfScope ps(L, stage, 1, st); rc |= launch_gemm_w4(EPI_QKV, xn1, H, L->qkv.d, e, w.qkv, T, part, cnt, st); }
     AttnPrefillArgs aa{};
     aa.q = q;
     aa.k_cache = (const uint16_t*)kc;
@@ -478,15 +495,15 @@ int run_prefill(layer_s* L, const float* x, const int32_t* pos, int T, int hist,
     EpiArgs eo = base_epi(L);
     eo.resid = x;
     eo.out_f32 = h;
-    { ProfScope ps(L, stage, 3, st); rc |= launch_gemm_w4(EPI_RESID, attn, T, qd, L->o.d, eo, st); }
+    { ProfScope ps(L, stage, 3, st); rc |= launch_gemm_w4(EPI_RESID, attn, qd, L->o.d, eo, w.o, T, part, cnt, st); }
     { ProfScope ps(L, stage, 4, st); rc |= launch_rmsnorm(h, (const uint16_t*)L->mlp_norm.p, c.rms_eps, T, H, xn2, st); }
     EpiArgs eg = base_epi(L);
     eg.act_out = g;
-    { ProfScope ps(L, stage, 5, st); rc |= launch_gemm_w4(EPI_SWIGLU, xn2, T, H, L->gu.d, eg, st); }
+    { ProfScope ps(L, stage, 5, st); rc |= launch_gemm_w4(EPI_SWIGLU, xn2, H, L->gu.d, eg, w.gu, T, part, cnt, st); }
     EpiArgs ed = base_epi(L);
     ed.resid = h;
     ed.out_f32 = y;
-    { ProfScope ps(L, stage, 6, st); rc |= launch_gemm_w4(EPI_RESID, g, T, L->F_pad, L->down.d, ed, st); }
+    { ProfScope ps(L, stage, 6, st); rc |= launch_gemm_w4(EPI_RESID, g, L->F_pad, L->down.d, ed, w.down, T, part, cnt, st); }
     if (rc) return fail(W4_EHIP, "kernel launch failed: %s", hipGetErrorString(hipGetLastError()));
     return W4_OK;
 }
@@ -604,20 +621,25 @@ int layer_create(const layer_config* cfg, const layer_weights_host* w, layer_t* 
         return rc;
     }
     {
-        // [0]: error flag; from byte 64: stamps (8 + 24 * max blocks words of 8 bytes)
+        // [0]: error flag; from byte 64: stamps (8 + 32 * max blocks words of 8 bytes)
         const size_t bytes = 64 + (size_t)kStampWords * 8;
         std::vector<unsigned char> zero(bytes, 0);
         if ((rc = upload(L->sync, zero.data(), bytes))) { delete L; return rc; }
         L->err = (int*)L->sync.p;
         L->stamps = (unsigned long long*)((char*)L->sync.p + 64);
     }
+    {
+        std::vector<unsigned> zero(kGemmCounters, 0u);
+        if ((rc = upload(L->gemm_cnt, zero.data(), zero.size() * 4))) { delete L; return rc; }
+    }
     // work table of the persistent decode: one block per CU; a product with
     // fewer column tiles than blocks is also cut along k (at most 2 parts)
     {
         int dev = 0, cus = 0;
         if (hipGetDevice(&dev) == hipSuccess &&
-            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && cus > 0 &&
-            cus <= kMaxBlocks) {
+            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && cus > 0)
+            L->num_cus = cus;
+        if (cus > 0 && cus <= kMaxBlocks) {
             auto parts = [&](const DevLinear& W) {
                 const int nt = W.N_dev / 32, kb = W.K_pad / 64;
                 return std::max(1, std::min(std::min(2, kb), cus / nt));

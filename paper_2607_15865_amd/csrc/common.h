@@ -140,14 +140,44 @@ __device__ __forceinline__ bf16x2 as_bf16x2(uint32_t u) {
 
 __device__ __forceinline__ float silu(float z) { return z / (1.0f + __expf(-z)); }
 
-// wave-level reductions (64 lanes)
-__device__ __forceinline__ float wave_sum(float v) {
-    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+// wave-level reductions (64 lanes): DPP within each row of 16 lanes (swap
+// lane pairs, swap pairs of pairs, mirror within 8, mirror within 16), then
+// the four row results are read from lanes 0, 16, 32 and 48.
+template <int CTRL>
+__device__ __forceinline__ float dpp_mov(float x) {
+    return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), CTRL, 0xF, 0xF, false));
+}
+
+// Sum over groups of N (8 or 16) adjacent lanes; every lane of a group ends
+// with the group's sum.
+template <int N>
+__device__ __forceinline__ float row_sum(float v) {
+    v += dpp_mov<0xB1>(v);                  // quad_perm [1,0,3,2]
+    v += dpp_mov<0x4E>(v);                  // quad_perm [2,3,0,1]
+    v += dpp_mov<0x141>(v);                 // row_half_mirror
+    if (N == 16) v += dpp_mov<0x140>(v);    // row_mirror
     return v;
 }
-__device__ __forceinline__ float wave_max(float v) {
-    for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+
+__device__ __forceinline__ float row_max16(float v) {
+    v = fmaxf(v, dpp_mov<0xB1>(v));
+    v = fmaxf(v, dpp_mov<0x4E>(v));
+    v = fmaxf(v, dpp_mov<0x141>(v));
+    v = fmaxf(v, dpp_mov<0x140>(v));
     return v;
+}
+
+__device__ __forceinline__ float lane_val(float v, int l) {
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+    v = row_sum<16>(v);
+    return (lane_val(v, 0) + lane_val(v, 16)) + (lane_val(v, 32) + lane_val(v, 48));
+}
+__device__ __forceinline__ float wave_max(float v) {
+    v = row_max16(v);
+    return fmaxf(fmaxf(lane_val(v, 0), lane_val(v, 16)), fmaxf(lane_val(v, 32), lane_val(v, 48)));
 }
 
 // ---------------------------------------------------------------- layouts

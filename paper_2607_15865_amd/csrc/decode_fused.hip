@@ -34,7 +34,7 @@ namespace {
 constexpr int NWAVE = 16;
 constexpr int NTHR = NWAVE * 64;
 constexpr int SPIN_MAX = 1 << 20;  // polls per thread per launch before the error flag is raised
-constexpr int RING = 8;            // weight tiles in flight per wave (gate/up, down)
+constexpr int RING = 4;            // weight tiles in flight per wave (gate/up, down)
 constexpr int RING_QKV = 4;        // q/k/v: its run is about 4 tiles per wave
 constexpr int RING_O = 4;          // o_proj: its run is 2 to 4 tiles per wave
 constexpr int NIT = 4;             // K/V register rows per lane: chunk <= NIT * NWAVE * (64 / (d / 8))
@@ -282,6 +282,7 @@ __global__ void __launch_bounds__(NTHR) decode_fused_kernel(DecodeFusedArgs a) {
         }
         __syncthreads();
     }
+    stamp_done(23);
 
     // ================= P1: q/k/v partial sums =================
     if (owns(1)) {
@@ -292,6 +293,7 @@ __global__ void __launch_bounds__(NTHR) decode_fused_kernel(DecodeFusedArgs a) {
         clear_red();
         if (run1.ka < run1.kz)
             gemv_run<RING_QKV, false, false>(a.qkv, run1, xs, ldx, B, R1, q1, [&](int, const float (&out)[4]) { to_red(0, out); });
+        prefetch(3);
         stamp_done(7);
         __syncthreads();
         for (int i = tid; i < B * 32; i += NTHR) {
@@ -299,17 +301,19 @@ __global__ void __launch_bounds__(NTHR) decode_fused_kernel(DecodeFusedArgs a) {
             put_tagged(a.qkv_part + ((size_t)s1 * B + b) * Nq + t1 * 32 + cc, __float_as_uint(red_sum(0, b, cc)), ep);
         }
     }
-    prefetch(3);
+    if (!owns(1)) prefetch(3);
     stamp_done(0);
 
     // ================= P2: attention units =================
     {
-        constexpr int LPK = D / 8, KPW = 64 / LPK;
+        constexpr int LPK = D / 8, KPW = 64 / LPK;    // q.k: lanes per key (8 dims each), keys per wave
+        constexpr int DP = D / 2, KPL = 128 / D;      // p.v: lanes per key (2 dims each), keys per load
         const int CH = a.chunk, NCH = a.nchunk;
         const int kl = lane / LPK, dseg = lane % LPK;
+        const int vdp = lane % DP, vks = lane / DP;
         float* sc = reinterpret_cast<float*>(smem);                  // [r][CH]
-        float* ored = sc + MAXR * CH;                                // [NWAVE][D]
-        float* stat = ored + NWAVE * D;                              // [r][2]
+        float* ored = sc + MAXR * CH;                                // [NWAVE][r][D]
+        float* stat = ored + NWAVE * MAXR * D;                       // [r][2]
         float* qkvf = stat + 2 * MAXR;                               // [r + 2][D] device order
         uint16_t* qb = reinterpret_cast<uint16_t*>(qkvf + (MAXR + 2) * D);   // [r][D] bf16
         uint16_t* knb = qb + MAXR * D;                               // [D]
@@ -324,19 +328,25 @@ __global__ void __launch_bounds__(NTHR) decode_fused_kernel(DecodeFusedArgs a) {
             const int nkeys = end - start, hist_end = min(end, ctx);
             const uint16_t* kc = a.k_cache + (size_t)b * a.sb + (size_t)g * a.sh;
             const uint16_t* vc = a.v_cache + (size_t)b * a.sb + (size_t)g * a.sh;
-            // K/V history rows of this lane (keys start + (it*NWAVE + wave)*KPW + kl),
-            // mask values and the RoPE factors of this thread's dim, all requested
-            // before the wait for q/k/v.  Loads are unconditional (rows past the
-            // history read row 0 and are not used).
+            // Pass it of wave w covers keys start + (it*NWAVE + w)*KPW + (0..KPW-1).
+            // K: lane holds 8 dims of key kl; V: lane holds dims 2*vdp, 2*vdp+1 of
+            // keys j*KPL + vks.  Mask values and the RoPE factors of this
+            // thread's dim are requested too, all before the wait for q/k/v;
+            // rows past the history read row 0 and are not used.
             const float* mrow = a.mask ? a.mask + (size_t)b * a.max_seq : nullptr;
-            u32x4 kr[NIT], vr[NIT];
+            u32x4 kr[NIT];
+            uint32_t vr[NIT][KPW / KPL];
             float mk[NIT];
 #pragma unroll
             for (int it = 0; it < NIT; it++) {
-                const int key = start + (it * NWAVE + wave) * KPW + kl;
-                const int kk = key < hist_end ? key : 0;
-                kr[it] = *reinterpret_cast<const u32x4*>(kc + (size_t)kk * D + dseg * 8);
-                vr[it] = *reinterpret_cast<const u32x4*>(vc + (size_t)kk * D + dseg * 8);
+                const int kb0 = start + (it * NWAVE + wave) * KPW;
+                const int key = kb0 + kl;
+                kr[it] = *reinterpret_cast<const u32x4*>(kc + (size_t)(key < hist_end ? key : 0) * D + dseg * 8);
+#pragma unroll
+                for (int j = 0; j < KPW / KPL; j++) {
+                    const int kv = kb0 + j * KPL + vks;
+                    vr[it][j] = *reinterpret_cast<const uint32_t*>(vc + (size_t)(kv < hist_end ? kv : 0) * D + vdp * 2);
+                }
                 mk[it] = mrow ? mrow[key < end ? key : start] : 0.f;
             }
             const int ps = meta[MAXB + b];
@@ -370,7 +380,8 @@ __global__ void __launch_bounds__(NTHR) decode_fused_kernel(DecodeFusedArgs a) {
                 uint16_t* vw = a.v_cache + (size_t)b * a.sb + (size_t)g * a.sh + (size_t)ctx * D;
                 for (int j = tid; j < D; j += NTHR) { kw[j] = knb[j]; vw[j] = vnb[j]; }
             }
-            // scores (log2 domain) of every key of the chunk for the r heads
+            // scores (log2 domain) of every key of the chunk for the r heads: the
+            // LPK lanes of a key meet with DPP row operations
 #pragma unroll
             for (int it = 0; it < NIT; it++) {
                 const int kbase = (it * NWAVE + wave) * KPW;
@@ -390,8 +401,7 @@ __global__ void __launch_bounds__(NTHR) decode_fused_kernel(DecodeFusedArgs a) {
 #pragma unroll
                     for (int pp = 0; pp < 4; pp++)
                         v = __builtin_amdgcn_fdot2_f32_bf16(as_bf16x2(qp[pp]), as_bf16x2(kw[pp]), v, false);
-#pragma unroll
-                    for (int o = 1; o < LPK; o <<= 1) v += __shfl_xor(v, o, 64);
+                    v = row_sum<LPK>(v);
                     if (dseg == 0 && key < end) {
                         float sv = v * a.scale_log2;
                         if (mrow) sv += mk[it] * LOG2E;
@@ -416,58 +426,50 @@ __global__ void __launch_bounds__(NTHR) decode_fused_kernel(DecodeFusedArgs a) {
             }
             __syncthreads();
             stamp_done(18);
-            // chunk output of every head: sum of p * v
-            uint64_t* ap = a.apart + ((size_t)b * nq + g * r) * NCH * (D + 2) + (size_t)chunk * (D + 2);
+            // chunk output of every head, sum of p * v: each lane sums its keys
+            // for its two dims, the waves meet in LDS
             for (int i = 0; i < r; i++) {
-                float ov[8];
-#pragma unroll
-                for (int j = 0; j < 8; j++) ov[j] = 0.f;
+                float o0 = 0.f, o1 = 0.f;
 #pragma unroll
                 for (int it = 0; it < NIT; it++) {
                     const int kbase = (it * NWAVE + wave) * KPW;
                     if (kbase >= nkeys) break;
-                    const int key = start + kbase + kl;
-                    if (key < end) {
-                        uint32_t vw[4];
-                        if (key == ctx) {
-                            const uint32_t* vp = reinterpret_cast<const uint32_t*>(vnb + dseg * 8);
-                            vw[0] = vp[0]; vw[1] = vp[1]; vw[2] = vp[2]; vw[3] = vp[3];
-                        } else {
-                            const u32x4 vv = vr[it];
-                            vw[0] = vv[0]; vw[1] = vv[1]; vw[2] = vv[2]; vw[3] = vv[3];
-                        }
-                        const float pv = sc[i * CH + kbase + kl];
 #pragma unroll
-                        for (int pp = 0; pp < 4; pp++) {
-                            ov[2 * pp] += pv * __uint_as_float(vw[pp] << 16);
-                            ov[2 * pp + 1] += pv * __uint_as_float(vw[pp] & 0xFFFF0000u);
+                    for (int j = 0; j < KPW / KPL; j++) {
+                        const int ko = kbase + j * KPL + vks;          // key - start
+                        if (ko < nkeys) {
+                            const uint32_t vw = (start + ko == ctx)
+                                ? *reinterpret_cast<const uint32_t*>(vnb + 2 * vdp) : vr[it][j];
+                            const float pv = sc[i * CH + ko];
+                            o0 += pv * __uint_as_float(vw << 16);
+                            o1 += pv * __uint_as_float(vw & 0xFFFF0000u);
                         }
                     }
                 }
-#pragma unroll
-                for (int j = 0; j < 8; j++) {
-                    float v = ov[j];
-#pragma unroll
-                    for (int o = LPK; o < 64; o <<= 1) v += __shfl_xor(v, o, 64);
-                    ov[j] = v;
+                if (KPL > 1) {        // the lanes of the other keys of a load hold the same dims
+                    o0 += __shfl_xor(o0, DP, 64);
+                    o1 += __shfl_xor(o1, DP, 64);
                 }
-                if (kl == 0)
-#pragma unroll
-                    for (int j = 0; j < 8; j++) ored[wave * D + dseg * 8 + j] = ov[j];
-                __syncthreads();
-                uint64_t* aph = ap + (size_t)i * NCH * (D + 2);
-                for (int dim = tid; dim < D; dim += NTHR) {
-                    float v = 0.f;
-#pragma unroll
-                    for (int w = 0; w < NWAVE; w++) v += ored[w * D + dim];
-                    put_tagged(aph + dim, __float_as_uint(v), ep);
+                if (vks == 0) {
+                    ored[(wave * MAXR + i) * D + 2 * vdp] = o0;
+                    ored[(wave * MAXR + i) * D + 2 * vdp + 1] = o1;
                 }
-                if (tid == 0) {
-                    put_tagged(aph + D, __float_as_uint(stat[2 * i]), ep);
-                    put_tagged(aph + D + 1, __float_as_uint(stat[2 * i + 1]), ep);
-                }
-                __syncthreads();
             }
+            __syncthreads();
+            uint64_t* ap = a.apart + ((size_t)b * nq + g * r) * NCH * (D + 2) + (size_t)chunk * (D + 2);
+            for (int idx = tid; idx < r * D; idx += NTHR) {
+                const int i = idx / D, dim = idx - i * D;
+                float v = 0.f;
+#pragma unroll
+                for (int w = 0; w < NWAVE; w++) v += ored[(w * MAXR + i) * D + dim];
+                put_tagged(ap + (size_t)i * NCH * (D + 2) + dim, __float_as_uint(v), ep);
+            }
+            if (tid < r) {
+                uint64_t* aph = ap + (size_t)tid * NCH * (D + 2);
+                put_tagged(aph + D, __float_as_uint(stat[2 * tid]), ep);
+                put_tagged(aph + D + 1, __float_as_uint(stat[2 * tid + 1]), ep);
+            }
+            __syncthreads();
         }
         stamp_done(9);
 
@@ -555,6 +557,7 @@ __global__ void __launch_bounds__(NTHR) decode_fused_kernel(DecodeFusedArgs a) {
         stamp_done(19);
         if (run3.ka < run3.kz)
             gemv_run<RING_O, false, false>(a.o, run3, xs - klo, ldx, B, R3, q3, [&](int, const float (&out)[4]) { to_red(0, out); });
+        prefetch(4);
         stamp_done(20);
         __syncthreads();
         stamp_done(21);
@@ -563,7 +566,7 @@ __global__ void __launch_bounds__(NTHR) decode_fused_kernel(DecodeFusedArgs a) {
             put_tagged(a.o_part + ((size_t)s3 * B + b) * H + t3 * 32 + cc, __float_as_uint(red_sum(0, b, cc)), ep);
         }
     }
-    prefetch(4);
+    if (!owns(3)) prefetch(4);
     stamp_done(2);
 
     // ================= P4: h, RMSNorm(h), gate/up, SwiGLU =================
@@ -580,8 +583,10 @@ __global__ void __launch_bounds__(NTHR) decode_fused_kernel(DecodeFusedArgs a) {
         if (run4.ka < run4.kz)
             gemv_run<RING, false, false>(a.gu, run4, xs, ldx, B, R4, q4,
                                          [&](int t, const float (&out)[4]) { to_red(t - ta4, out); });
+        prefetch(5);
         stamp_done(13);
         __syncthreads();
+        stamp_done(24);
         const int np = (tb4 - ta4) / 2;
         for (int i = tid; i < np * B * 16; i += NTHR) {
             const int pp = i / (B * 16), rem = i - pp * B * 16, b = rem >> 4, cc = 2 * (rem & 15);
@@ -591,7 +596,7 @@ __global__ void __launch_bounds__(NTHR) decode_fused_kernel(DecodeFusedArgs a) {
             put_tagged(a.g + ((size_t)b * a.F_pad + (ta4 / 2 + pp) * 32 + cc) / 2, word, ep);
         }
     }
-    prefetch(5);
+    if (!owns(4)) prefetch(5);
     stamp_done(3);
 
     // ================= P5: down, y = h + g Wd =================

@@ -42,8 +42,16 @@ __device__ __forceinline__ void epi_qkv_pair(const EpiArgs& ep, int row, int n_b
     }
 }
 
-int launch_gemm_w4(int epi, const f16* X, int M, int ldx, const DevLinear& W, const EpiArgs& ep,
-                   hipStream_t stream);
+// Prefill GEMM launch plan: row tile (32 * TM rows), k splits S, grid.
+struct GemmPlan {
+    int TM = 4, S = 1, nrb = 0, ncb = 0, tiles = 0;
+    size_t part_bytes = 0;        // fp32 partial sums (S > 1)
+};
+GemmPlan gemm_w4_plan(int M, const DevLinear& W, int num_cus);
+// part: plan.part_bytes of workspace; cnt: plan.tiles counters, zero between
+// calls (the kernel leaves them zero).  Both unused when plan.S == 1.
+int launch_gemm_w4(int epi, const f16* X, int ldx, const DevLinear& W, const EpiArgs& ep, const GemmPlan& plan,
+                   int M, float* part, unsigned* cnt, hipStream_t stream);
 
 struct GemvArgs {
     DevLinear W;
