@@ -62,7 +62,7 @@ struct ColSrc {        // where a device column comes from
 struct Repacked {
     std::vector<uint32_t> qw;
     std::vector<uint16_t> scales;
-    std::vector<float> ratios, slast;
+    std::vector<float> ratios;
     std::vector<uint8_t> zeros;
     std::vector<uint32_t> sz;
 };
@@ -126,7 +126,6 @@ void repack_cols(const std::vector<ColSrc>& cols, int K_pad, int G, bool has_zer
                 R.sz[gi] = (uint32_t)s[g] | ((uint32_t)z[g] << 16);
             }
         }
-        R.slast[nd] = (float)f16_value(s[KG - 1]);
     }
 }
 
@@ -134,7 +133,7 @@ void repack_cols(const std::vector<ColSrc>& cols, int K_pad, int G, bool has_zer
 
 struct DevLinearOwned {
     DevLinear d{};
-    DevBuf qw, scales, ratios, slast, zeros, sz, colmap_a, colmap_b, colmap_c;
+    DevBuf qw, scales, ratios, zeros, sz, colmap_a, colmap_b, colmap_c;
 };
 
 struct Profiler {          // one timed kernel per stage
@@ -186,7 +185,6 @@ int build_linear(DevLinearOwned& out, const std::vector<ColSrc>& cols, int K, in
     R.qw.resize((size_t)N_dev * K_pad / 8);
     R.scales.resize((size_t)N_dev * KG);
     R.ratios.resize((size_t)N_dev * KG);
-    R.slast.resize(N_dev);
     if (has_zeros) {
         R.zeros.resize((size_t)N_dev * KG);
         R.sz.resize((size_t)N_dev * KG);
@@ -204,14 +202,12 @@ int build_linear(DevLinearOwned& out, const std::vector<ColSrc>& cols, int K, in
     if ((rc = upload(out.qw, R.qw.data(), R.qw.size() * 4))) return rc;
     if ((rc = upload(out.scales, R.scales.data(), R.scales.size() * 2))) return rc;
     if ((rc = upload(out.ratios, R.ratios.data(), R.ratios.size() * 4))) return rc;
-    if ((rc = upload(out.slast, R.slast.data(), R.slast.size() * 4))) return rc;
     if (has_zeros && (rc = upload(out.zeros, R.zeros.data(), R.zeros.size()))) return rc;
     if (has_zeros && (rc = upload(out.sz, R.sz.data(), R.sz.size() * 4))) return rc;
     DevLinear& d = out.d;
     d.qw = (const uint32_t*)out.qw.p;
     d.scales = (const uint16_t*)out.scales.p;
     d.ratios = (const float*)out.ratios.p;
-    d.slast = (const float*)out.slast.p;
     d.zeros = has_zeros ? (const uint8_t*)out.zeros.p : nullptr;
     d.sz = has_zeros ? (const uint32_t*)out.sz.p : nullptr;
     d.K = K;
@@ -241,7 +237,7 @@ int validate_config(const layer_config* c) {
     if (qd % 128 || qd % KP) return fail(W4_EUNSUPPORTED, "n_heads*head_dim must be a multiple of 128 and of group_size");
     if (c->ffn % 8) return fail(W4_EUNSUPPORTED, "ffn must be a multiple of 8");
     if (c->max_batch > 64) return fail(W4_EUNSUPPORTED, "max_batch above 64");
-    if (c->hidden > 16384 || round_up(c->ffn, KP) > 65536) return fail(W4_EUNSUPPORTED, "hidden or ffn too large");
+    if (c->hidden > 16384 || round_up(c->ffn, std::max(128, KP)) > 65536) return fail(W4_EUNSUPPORTED, "hidden or ffn too large");
     return 0;
 }
 
@@ -546,9 +542,10 @@ int layer_create(const layer_config* cfg, const layer_weights_host* w, layer_t* 
 
     const layer_config& c = *cfg;
     const int H = c.hidden, d = c.head_dim, nq = c.n_heads, nkv = c.n_kv_heads, F = c.ffn, G = c.group_size;
-    const int KP = std::max(64, G);
     const int qd = nq * d, kvd = nkv * d;
-    const int F_pad = round_up(F, KP);
+    // K of every linear a multiple of 128 (and of G): the prefill GEMM takes
+    // its k range in pairs of 64-k tiles
+    const int F_pad = round_up(F, std::max(128, G));
 
     // scales must be finite
     auto finite_scales = [&](const qlinear_host& q, int K, int N) {

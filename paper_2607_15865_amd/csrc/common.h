@@ -18,17 +18,20 @@
 //   Group parameters are group-major, so the 32 lanes of a tile read one
 //   contiguous run: scales fp16 [K_pad / G][N_dev]; ratios for the prefill
 //   GEMM fp32 [K_pad / G][N_dev] with ratio[g][n] = s[g-1][n] / s[g][n]
-//   (g >= 1), and the last scale as fp32 [N_dev].  Zero points (optional):
-//   uint8 [K_pad / G][N_dev], and the same again packed with the scale bits
-//   as uint32 (scale | zero << 16) for the decode GEMV.
+//   (g >= 1).  Zero points (optional): uint8 [K_pad / G][N_dev], and the same
+//   again packed with the scale bits as uint32 (scale | zero << 16) for the
+//   decode GEMV.
 //
-//   K_pad is K rounded up to max(64, G); padded rows and groups carry the zero
-//   point code (weight 0).  A group whose scale is 0 is stored with all codes
-//   at the zero point and a non-zero stand-in scale, so every scale is
-//   non-zero (the ratios are finite) and the group still contributes 0.
+//   K_pad is a multiple of 128 and of G (the padded FFN width of the down
+//   projection; the other K are multiples already); padded rows and groups
+//   carry the zero point code (weight 0).  A group whose scale is 0 is stored
+//   with all codes at the zero point and a non-zero stand-in scale, so every
+//   scale is non-zero (the ratios are finite) and the group still contributes
+//   0.
 #pragma once
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+#include <mutex>
 
 typedef _Float16 f16;
 typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
@@ -51,6 +54,24 @@ __host__ __device__ inline int rope_block(int p, int head_dim) {
     int nb = head_dim / 32;          // 2 or 4
     int half = nb / 2;
     return (p % 2 == 0) ? (p / 2) : (p / 2 + half);
+}
+
+// Dynamic LDS above 64 KB has to be allowed per kernel with
+// hipFuncSetAttribute; the setting lasts, so it is made once per kernel and
+// device (again only when a larger size is asked for), not on every launch.
+struct LdsLimit {
+    int bytes[64] = {};      // per device: the size allowed so far
+    std::mutex mu;
+};
+inline int ensure_lds_limit(LdsLimit& lim, const void* fn, size_t bytes) {
+    if (bytes <= 64 * 1024) return 0;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return -1;
+    std::lock_guard<std::mutex> g(lim.mu);
+    if (lim.bytes[dev] >= (int)bytes) return 0;
+    if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes) != hipSuccess) return -1;
+    lim.bytes[dev] = (int)bytes;
+    return 0;
 }
 
 // ---------------------------------------------------------------- numerics
@@ -129,6 +150,7 @@ __device__ __forceinline__ f16x8 dequant8(uint32_t w, ZeroOff zo, const DqConst&
     return r;
 }
 
+
 // Reinterpret a 32-bit word as a bf16 pair.  Always pass a scalar: clang
 // miscompiles __builtin_bit_cast applied directly to an ext_vector element
 // with a loop index (it reads element 0).
@@ -186,7 +208,6 @@ struct DevLinear {
     const uint32_t* qw;      // tiles
     const uint16_t* scales;  // fp16 bits [KG][N_dev]
     const float* ratios;     // [KG][N_dev]
-    const float* slast;      // [N_dev]
     const uint8_t* zeros;    // [KG][N_dev] or null
     const uint32_t* sz;      // scale bits | zero << 16, [KG][N_dev]; null without zeros
     int K, N;                // logical

@@ -1,5 +1,5 @@
-// Decode stage in one persistent launch (one block of 8 waves per CU), run as
-// a dataflow graph without grid barriers.
+// Decode stage in one persistent launch (one block of 16 waves per CU), run
+// as a dataflow graph without grid barriers.
 //
 // The decode step is a chain of dependent products (Sec. 4.4):
 //   P1  q/k/v GEMV on RMSNorm(x)
@@ -10,7 +10,7 @@
 //   P5  down GEMV                      -> y = h + g Wd
 //
 // Work split: in every GEMV the block owns whole column tiles (32 columns) or
-// a k-part of one, and its 8 waves split the block's k range; the waves'
+// a k-part of one, and its 16 waves split the block's k range; the waves'
 // partials meet in LDS.  A block's weight tiles for the next product are
 // requested (gemv_core ring) as soon as its current run is done, so the
 // weight stream keeps going while the block waits for its inputs.
@@ -23,7 +23,10 @@
 // grid barriers, and a consumer waits only for the producers of its own
 // inputs.  Sums are formed in a fixed order: results do not depend on
 // timing.  Polls are bounded: on a timeout the kernel raises an error flag
-// and runs to completion.  All blocks are co-resident (cooperative launch).
+// and runs to completion.  The launch is an ordinary one with one block per
+// CU (a block's LDS leaves no room for a second), so all blocks are resident
+// once the CUs are free; were one not, its consumers would time out, flag
+// the error and end rather than hang.
 #include "common.h"
 #include "gemv_core.h"
 #include "launch.h"
@@ -637,10 +640,15 @@ __global__ void __launch_bounds__(NTHR) decode_fused_kernel(DecodeFusedArgs a) {
 }
 
 template <int D, int MAXB>
+LdsLimit& lds_limit() {
+    static LdsLimit lim;
+    return lim;
+}
+
+template <int D, int MAXB>
 int launch_t(const DecodeFusedArgs& a, hipStream_t stream) {
     auto fn = decode_fused_kernel<D, MAXB>;
-    if (hipFuncSetAttribute((const void*)fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)a.lds_bytes) != hipSuccess)
-        return -1;
+    if (ensure_lds_limit(lds_limit<D, MAXB>(), (const void*)fn, a.lds_bytes)) return -1;
     // An ordinary launch: one block per CU (the LDS of a block leaves room for
     // no second one), so every block is resident once the CUs are free.  A
     // cooperative launch would guarantee the same at about 20 us per launch.
@@ -680,9 +688,15 @@ int decode_fused_blocks(int head_dim, int B, size_t lds_bytes) {
     if (hipGetDevice(&dev) != hipSuccess) return 0;
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
     const void* fn = nullptr;
-    if (head_dim == 128) fn = B <= 1 ? (const void*)decode_fused_kernel<128, 1> : (const void*)decode_fused_kernel<128, 4>;
-    else fn = B <= 1 ? (const void*)decode_fused_kernel<64, 1> : (const void*)decode_fused_kernel<64, 4>;
-    if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_bytes) != hipSuccess) return 0;
+    LdsLimit* lim = nullptr;
+    if (head_dim == 128) {
+        fn = B <= 1 ? (const void*)decode_fused_kernel<128, 1> : (const void*)decode_fused_kernel<128, 4>;
+        lim = B <= 1 ? &lds_limit<128, 1>() : &lds_limit<128, 4>();
+    } else {
+        fn = B <= 1 ? (const void*)decode_fused_kernel<64, 1> : (const void*)decode_fused_kernel<64, 4>;
+        lim = B <= 1 ? &lds_limit<64, 1>() : &lds_limit<64, 4>();
+    }
+    if (ensure_lds_limit(*lim, fn, lds_bytes)) return 0;
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, fn, NTHR, lds_bytes) != hipSuccess) return 0;
     return occ >= 1 ? cus : 0;
 }

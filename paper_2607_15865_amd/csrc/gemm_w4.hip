@@ -8,14 +8,32 @@
 // ratio: the accumulator u holds sum_g s_g T_g / s_cur, and at the start of
 // group g it is multiplied by s_{g-1} / s_g, so one VALU multiply per output
 // per group and no second accumulator set are needed; the epilogue multiplies
-// by the scale of the last group of the k range.
+// by the scale of the last group of the k range.  (Rounding the scaled weight
+// to fp16 instead would save those multiplies, but its 2^-12 relative error
+// flips the bf16 rounding of q/k/v and of the SwiGLU output often enough to
+// break the parity bound on full-size layers.)
 //
 // Block: 256 threads = 4 waves side by side along N.  Block tile BM x 256
 // with BM = 32 * TM; wave tile BM x 64 (TM x 2 MFMA tiles), so a wave's two
 // 32-column weight tiles are a RoPE pair or a gate/up pair and every
-// dequantised weight fragment feeds TM MFMAs.  The X tile (BM x 64 per k
-// tile) is staged in LDS (double buffered); each wave streams its own weight
-// tiles (1 KB, one 16-byte load per lane) through a ring PF k-tiles deep.
+// dequantised weight fragment feeds TM MFMAs.
+//
+// Pipeline, per iteration of BK = 128 k (two 64-k weight tiles per column):
+// at its start a block requests everything the next iteration needs, and
+// the barrier at its end (whose workgroup release waits for the block's
+// outstanding loads) makes it visible:
+//   * the X tile (BM x 128 fp16) goes straight from memory to LDS with
+//     direct-to-LDS loads (one 1 KB wave load per 4 rows), so it costs no
+//     registers; rows are 256 bytes without padding, and the 16-byte chunk c
+//     of row r is stored at chunk c ^ (r & 15), so the A-fragment reads of
+//     16 consecutive rows hit 16 different bank groups;
+//   * each wave loads its 4 weight tiles (1 KB each, one 16-byte load per
+//     lane) into the free half of a register ring of 8 tile slots;
+//   * inside the iteration the A fragments (LDS) and B fragments of step
+//     t + 1 are prepared while the MFMAs of step t run.
+// Every load is issued unconditionally with clamped addresses (X rows past M
+// read row M - 1; their outputs are dropped).  K_pad is a multiple of 128, so
+// every k range holds whole iterations.
 //
 // Split K: with S > 1 the k tiles are cut into S ranges, one block each.
 // Every block stores its fp32 partial tile, and the last block of a tile to
@@ -30,9 +48,7 @@
 
 namespace {
 
-constexpr int BN = 256, BK = 64;
-constexpr int LDA = BK + 8;      // fp16 elements per LDS row (16-byte pad)
-constexpr int PF = 4;            // weight k-tiles in flight per wave
+constexpr int BN = 256;
 constexpr int NXCD = 8;
 
 struct GemmShape {
@@ -41,13 +57,43 @@ struct GemmShape {
     unsigned* cnt;               // [nrb * ncb] (S > 1), zero between calls
 };
 
-// GEN: zero points or groups of 32 (a group may start at either k half of a
-// tile); otherwise groups of 64 or more without zero points.
-template <int EPI, int TM, bool GEN>
-__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) gemm_w4_kernel(const f16* __restrict__ X, int ldx, DevLinear W, EpiArgs ep,
-                                                      GemmShape gs) {
+// Instruction order of one k16 step for the scheduler: every MFMA is
+// followed by an LDS read of the next step's A fragments (the first TM of
+// them) and a few VALU operations (dequantisation of the next step).
+template <int TM, int NVALU>
+__device__ __forceinline__ void sched_step() {
+#pragma unroll
+    for (int j = 0; j < 2 * TM; j++) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
+        if (j < TM) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // DS read
+        __builtin_amdgcn_sched_group_barrier(0x002, NVALU, 0);   // VALU
+    }
+}
+
+template <int TM>
+constexpr size_t lds_bytes() { return (size_t)2 * 32 * TM * 256; }
+
+// k range of split sp in 64-k tiles; inner split points are even so that
+// iterations hold whole tile pairs
+__host__ __device__ inline void split_range(int sp, int S, int KB, int& lo, int& hi) {
+    const int pairs = KB / 2;
+    lo = (int)((long long)sp * pairs / S) * 2;
+    hi = sp == S - 1 ? KB : (int)((long long)(sp + 1) * pairs / S) * 2;
+}
+
+// GT: group size class, 0 = groups of 32 (two per 64-k tile), 1 = groups of
+// 64, 2 = groups of 128 or more (starting only at the first tile of an
+// iteration); ZP: the linear has zero points.
+template <int EPI, int TM, int GT, bool ZP>
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2)))
+gemm_w4_kernel(const f16* __restrict__ X, int ldx, DevLinear W, EpiArgs ep, GemmShape gs) {
     constexpr int BM = 32 * TM;
-    __shared__ __attribute__((aligned(16))) f16 As[2][BM * LDA];
+    constexpr int XL = BM / 16;                         // X direct-to-LDS loads per wave and iteration
+    constexpr int NH = GT == 0 ? 2 : 1;                 // group parameters per tile
+    constexpr int RS = 8;                               // weight tile slots: two iterations
+    extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+    unsigned char* const As0 = smem;
+    unsigned char* const As1 = smem + BM * 256;
     __shared__ unsigned last_flag;
 
     const int tid = threadIdx.x;
@@ -76,118 +122,147 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) g
     }
     const int m0 = rb * BM;
     const int nt0 = cb * 8 + wave * 2;                  // first of this wave's two column tiles
-    const bool wave_on = nt0 * 32 < W.N_dev;            // columns past N_dev: idle wave
+    const bool wave_on = nt0 * 32 < W.N_dev;            // columns past N_dev: the wave computes on
+                                                        // tile 0 and stores nothing
     const int KB = gs.KB;
-    const int kb_lo = sp * KB / gs.S, kb_hi = (sp + 1) * KB / gs.S;
+    int kb_lo, kb_hi;
+    split_range(sp, gs.S, KB, kb_lo, kb_hi);
+    const int nit = (kb_hi - kb_lo + 1) / 2;
     const int Gm1 = (1 << W.lgG) - 1;
     const int col0 = (wave_on ? nt0 : 0) * 32 + c, col1 = col0 + 32;
     const DqConst dq = dq_const();
 
-    // ---- X tile: BM rows x 64 halves = BM * 8 segments of 16 bytes
-    constexpr int XSEG = BM * 8 / 256;                  // per thread: 1, 2 or 4
-    auto load_x = [&](int kb, u32x4 (&r)[XSEG]) {
+    // ---- X tile of the iteration that starts at 64-k tile kb, straight to
+    // LDS: load i of wave w fills rows 4 (4 i + w) .. + 3; lane L writes
+    // chunk L & 15 of row 4 (4 i + w) + L / 16, which holds logical chunk
+    // (L & 15) ^ (row & 15).
+    const uint32_t xrow_bytes = (uint32_t)ldx * 2u;
+    const char* const Xb = reinterpret_cast<const char*>(X);
+    // row & 15 = (4 wave + lane / 16) & 15 for every load i, so the logical
+    // chunk of this lane is the same in all its loads
+    const int xlc = (lane & 15) ^ ((4 * wave + (lane >> 4)) & 15);
+    uint32_t xoff[XL];                                  // per load: row offset + chunk (bytes)
 #pragma unroll
-        for (int i = 0; i < XSEG; i++) {
-            const int idx = tid + i * 256, row = idx >> 3, seg = idx & 7;
-            const int m = m0 + row;
-            r[i] = m < M ? *reinterpret_cast<const u32x4*>(X + (size_t)m * ldx + kb * BK + seg * 8)
-                         : u32x4{0, 0, 0, 0};
-        }
-    };
-    auto store_x = [&](int buf, const u32x4 (&r)[XSEG]) {
+    for (int i = 0; i < XL; i++) {
+        const int r = 4 * (4 * i + wave) + (lane >> 4);
+        const int m = m0 + r < M ? m0 + r : M - 1;
+        xoff[i] = (uint32_t)m * xrow_bytes + (uint32_t)xlc * 16u;
+    }
+    auto load_x = [&](int kb, unsigned char* As) __attribute__((always_inline)) {
+        const uint32_t kbytes = (uint32_t)(kb < kb_hi ? kb : kb_lo) * 128u;
 #pragma unroll
-        for (int i = 0; i < XSEG; i++) {
-            const int idx = tid + i * 256, row = idx >> 3, seg = idx & 7;
-            *reinterpret_cast<u32x4*>(&As[buf][row * LDA + seg * 8]) = r[i];
-        }
+        for (int i = 0; i < XL; i++)
+            __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(Xb + (xoff[i] + kbytes)),
+                                             (__attribute__((address_space(3))) void*)(As + (4 * i + wave) * 1024),
+                                             16, 0, 0);
     };
 
-    // ---- weight ring: k-tile kb_lo + j in slot j % PF; the ratios (and zero
-    // points) of the groups that start in the tile's two k halves travel with
-    // it.  Loads past the range re-read the first tile (a cache hit), so every
-    // slot is refilled unconditionally.
-    const u32x4* wt0 = reinterpret_cast<const u32x4*>(W.qw) + (size_t)(wave_on ? nt0 : 0) * (W.K_pad / 64) * 64 + lane;
-    const u32x4* wt1 = wt0 + (size_t)(W.K_pad / 64) * 64;
-    constexpr int NH = GEN ? 2 : 1;                     // k halves with their own group parameters
-    u32x4 rb0[PF], rb1[PF];
-    float rr0[PF][NH], rr1[PF][NH];
-    uint32_t rz[PF][NH];
-    auto load_w = [&](int kb, int u) {
+    // ---- weight ring: slot q holds tile (kb, column q & 1) with the ratios
+    // (and zero points) of its groups.  Loads past the range re-read the
+    // range's first tile (never used).
+    const char* const Wb = reinterpret_cast<const char*>(W.qw);
+    const uint32_t woff0 = ((uint32_t)(wave_on ? nt0 : 0) * (uint32_t)KB * 64u + (uint32_t)lane) * 16u;
+    const uint32_t wcol1 = (uint32_t)KB * 1024u;
+    const char* const Rb = reinterpret_cast<const char*>(W.ratios);
+    u32x4 rw[RS];
+    float rr[RS][NH];
+    uint32_t rz[RS][NH];
+    auto load_w = [&](int q, int kb) __attribute__((always_inline)) {
         const int kk = kb < kb_hi ? kb : kb_lo;
-        rb0[u] = wt0[(size_t)kk * 64];
-        rb1[u] = wt1[(size_t)kk * 64];
+        const int col = (q & 1) ? col1 : col0;
+        rw[q] = *reinterpret_cast<const u32x4*>(Wb + (woff0 + ((q & 1) ? wcol1 : 0u) + (uint32_t)kk * 1024u));
 #pragma unroll
         for (int hh = 0; hh < NH; hh++) {
-            const int g = (kk * 64 + 32 * hh) >> W.lgG;
-            rr0[u][hh] = W.ratios[(size_t)g * W.N_dev + col0];
-            rr1[u][hh] = W.ratios[(size_t)g * W.N_dev + col1];
-            if (GEN && W.zeros)
-                rz[u][hh] = (uint32_t)W.zeros[(size_t)g * W.N_dev + col0] |
-                            ((uint32_t)W.zeros[(size_t)g * W.N_dev + col1] << 8);
-            else
-                rz[u][hh] = 0x0808u;
+            const uint32_t gi = (uint32_t)((kk * 64 + 32 * hh) >> W.lgG) * (uint32_t)W.N_dev + (uint32_t)col;
+            rr[q][hh] = *reinterpret_cast<const float*>(Rb + gi * 4u);
+            if (ZP) rz[q][hh] = (uint32_t)W.zeros[gi];
         }
     };
 
     f32x16 acc[TM][2];
 #pragma unroll
     for (int i = 0; i < TM; i++) { acc[i][0] = f32x16{}; acc[i][1] = f32x16{}; }
+    ZeroOff zo0 = zero_off(8.0f), zo1 = zo0;
+    // A fragment of row tile i, step s, tile half: logical chunk 8 half + 2 s + h
+    // of row 32 i + c, stored at chunk ^ (row & 15) (row & 15 == c & 15)
+    const uint32_t arow = (uint32_t)c * 256u;
 
-    u32x4 xr[XSEG];
-    load_x(kb_lo, xr);
-#pragma unroll
-    for (int u = 0; u < PF; u++) load_w(kb_lo + u, u);
-    store_x(0, xr);
-    ZeroOff zo0 = zero_off((float)(rz[0][0] & 0xFF)), zo1 = zero_off((float)(rz[0][0] >> 8));
-
-    for (int kb0 = kb_lo; kb0 < kb_hi; kb0 += PF) {
-#pragma unroll
-        for (int u = 0; u < PF; u++) {
-            const int kb = kb0 + u;
-            if (kb < kb_hi) {                              // block-uniform
-                __syncthreads();
-                const int buf = (kb - kb_lo) & 1;
-                if (kb + 1 < kb_hi) load_x(kb + 1, xr);
-                const u32x4 b0 = rb0[u], b1 = rb1[u];
-                float r0[NH], r1[NH];
-                uint32_t z[NH];
-#pragma unroll
-                for (int hh = 0; hh < NH; hh++) { r0[hh] = rr0[u][hh]; r1[hh] = rr1[u][hh]; z[hh] = rz[u][hh]; }
-                load_w(kb + PF, u);                        // refill the slot
-                if (wave_on) {
-#pragma unroll
-                    for (int s = 0; s < 4; s++) {
-                        const int k = kb * BK + s * 16;
-                        if ((s == 0 || (GEN && s == 2)) && (k & Gm1) == 0) {
-                            const int hh = GEN ? (s >> 1) : 0;
-                            if (k > kb_lo * BK) {          // a new group inside the range
-                                const float q0 = r0[hh], q1 = r1[hh];
-#pragma unroll
-                                for (int i = 0; i < TM; i++)
-#pragma unroll
-                                    for (int e = 0; e < 16; e++) { acc[i][0][e] *= q0; acc[i][1][e] *= q1; }
-                            }
-                            if (GEN && W.zeros) {
-                                zo0 = zero_off((float)(z[hh] & 0xFF));
-                                zo1 = zero_off((float)(z[hh] >> 8));
-                            }
-                        }
-                        const f16x8 bf0 = dequant8(b0[s], zo0, dq), bf1 = dequant8(b1[s], zo1, dq);
-#pragma unroll
-                        for (int i = 0; i < TM; i++) {
-                            const f16x8 af = *reinterpret_cast<const f16x8*>(&As[buf][(i * 32 + c) * LDA + s * 16 + h * 8]);
-                            acc[i][0] = __builtin_amdgcn_mfma_f32_32x32x16_f16(af, bf0, acc[i][0], 0, 0, 0);
-                            acc[i][1] = __builtin_amdgcn_mfma_f32_32x32x16_f16(af, bf1, acc[i][1], 0, 0, 0);
-                        }
-                    }
+    // iteration it: tiles kb, kb + 1 from As (ring slots qb .. qb + 3), while
+    // the next iteration's X and weights (slots qn ..) are requested.  With
+    // it == nit (the odd partner of the last iteration) only the loads and
+    // the barrier run, so every iteration issues the same loads.
+    auto iteration = [&](int it, const unsigned char* As, unsigned char* As_next, int qb, int qn)
+        __attribute__((always_inline)) {
+        const int kb = kb_lo + 2 * it;
+        load_x(kb + 2, As_next);
+        load_w(qn, kb + 2);
+        load_w(qn + 1, kb + 2);
+        load_w(qn + 2, kb + 3);
+        load_w(qn + 3, kb + 3);
+        if (kb < kb_hi) {
+            f16x8 a[2][TM], b[2][2];
+            auto prep = [&](int t, int p) __attribute__((always_inline)) {
+                const int half = t >> 2, s = t & 3, q = qb + 2 * half, hh = NH == 2 ? (s >> 1) : 0;
+                if (ZP && (s == 0 || (NH == 2 && s == 2))) {
+                    zo0 = zero_off((float)rz[q][hh]);
+                    zo1 = zero_off((float)rz[q + 1][hh]);
                 }
-                if (kb + 1 < kb_hi) store_x(buf ^ 1, xr);
+                const uint32_t chunk = (uint32_t)((8 * half + 2 * s + h) ^ (c & 15)) * 16u;
+#pragma unroll
+                for (int i = 0; i < TM; i++)
+                    a[p][i] = *reinterpret_cast<const f16x8*>(As + (uint32_t)i * 8192u + arow + chunk);
+                b[p][0] = dequant8(rw[q][s], zo0, dq);
+                b[p][1] = dequant8(rw[q + 1][s], zo1, dq);
+            };
+            // step t starts a group (k a multiple of G past the range start):
+            // the accumulators take the ratio s_prev / s_new (1 elsewhere)
+            auto group_step = [](int t) { return t == 0 || (GT <= 1 && t == 4) || (GT == 0 && (t & 1) == 0 && (t & 3) == 2); };
+            prep(0, 0);
+#pragma unroll
+            for (int t = 0; t < 8; t++) {
+                const int p = t & 1;
+                if (t + 1 < 8) prep(t + 1, p ^ 1);
+                if (group_step(t)) {
+                    const int half = t >> 2, q = qb + 2 * half, hh = NH == 2 ? ((t & 3) >> 1) : 0;
+                    const int k = (kb + half) * 64 + (t & 3) * 16;
+                    const bool start = k > kb_lo * 64 && (k & Gm1) == 0;
+                    const float f0 = start ? rr[q][hh] : 1.0f, f1 = start ? rr[q + 1][hh] : 1.0f;
+#pragma unroll
+                    for (int i = 0; i < TM; i++) {
+#pragma unroll
+                        for (int e = 0; e < 16; e++) acc[i][0][e] *= f0;
+                        acc[i][0] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a[p][i], b[p][0], acc[i][0], 0, 0, 0);
+#pragma unroll
+                        for (int e = 0; e < 16; e++) acc[i][1][e] *= f1;
+                        acc[i][1] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a[p][i], b[p][1], acc[i][1], 0, 0, 0);
+                    }
+                    sched_step<TM, TM == 4 ? 16 : 20>();
+                } else {
+#pragma unroll
+                    for (int i = 0; i < TM; i++) {
+                        acc[i][0] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a[p][i], b[p][0], acc[i][0], 0, 0, 0);
+                        acc[i][1] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a[p][i], b[p][1], acc[i][1], 0, 0, 0);
+                    }
+                    sched_step<TM, TM == 4 ? 4 : 6>();
+                }
             }
         }
+        __syncthreads();
+    };
+
+    load_x(kb_lo, As0);
+    load_w(0, kb_lo);
+    load_w(1, kb_lo);
+    load_w(2, kb_lo + 1);
+    load_w(3, kb_lo + 1);
+    __syncthreads();
+    for (int it = 0; it < nit; it += 2) {
+        iteration(it, As0, As1, 0, 4);
+        iteration(it + 1, As1, As0, 4, 0);
     }
 
     // ---- scale of the range's last group
-    const int glast = ((kb_hi * BK) - 1) >> W.lgG;
+    const int glast = ((kb_hi * 64) - 1) >> W.lgG;
     const float sl0 = (float)__builtin_bit_cast(f16, W.scales[(size_t)glast * W.N_dev + col0]);
     const float sl1 = (float)__builtin_bit_cast(f16, W.scales[(size_t)glast * W.N_dev + col1]);
 
@@ -217,8 +292,12 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) g
         return;
     }
 
-    // ---- split K: store the partial tile; the last block of the tile adds
-    // the S partials in range order and runs the epilogue
+    // ---- split K: store the partial tile; the last block of the tile to
+    // arrive adds the S partials in range order and runs the epilogue.  The
+    // partials are written and read with device-coherent (relaxed, agent
+    // scope) accesses, which go past the non-coherent per-XCD L2, so the
+    // count only has to follow their completion: no cache write-back or
+    // invalidation is needed.
     float* part = gs.part + (size_t)sp * M * W.N_dev;
     if (wave_on) {
 #pragma unroll
@@ -227,23 +306,23 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) g
             for (int e = 0; e < 16; e++) {
                 const int m = m0 + i * 32 + 8 * (e / 4) + 4 * h + (e % 4);
                 if (m < M) {
-                    part[(size_t)m * W.N_dev + col0] = acc[i][0][e] * sl0;
-                    part[(size_t)m * W.N_dev + col1] = acc[i][1][e] * sl1;
+                    __hip_atomic_store(part + (size_t)m * W.N_dev + col0, acc[i][0][e] * sl0, __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_AGENT);
+                    __hip_atomic_store(part + (size_t)m * W.N_dev + col1, acc[i][1][e] * sl1, __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_AGENT);
                 }
             }
     }
-    __threadfence();                 // the partial is visible at device scope before the count
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // this thread's partial stores are complete
     __syncthreads();
     if (tid == 0) {
         unsigned* cnt = gs.cnt + rb * gs.ncb + cb;
-        const unsigned old = atomicAdd(cnt, 1u);
+        const unsigned old = __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         last_flag = (old + 1 == (unsigned)gs.S);
-        if (last_flag) atomicExch(cnt, 0u);   // ready for the next call
+        if (last_flag) __hip_atomic_store(cnt, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);   // ready for the next call
     }
     __syncthreads();
-    if (!last_flag) return;
-    __threadfence();                 // acquire the other blocks' partials
-    if (!wave_on) return;
+    if (!last_flag || !wave_on) return;
 #pragma unroll
     for (int i = 0; i < TM; i++)
 #pragma unroll
@@ -253,46 +332,81 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) g
             float v0 = 0.f, v1 = 0.f;
             for (int s = 0; s < gs.S; s++) {
                 const float* ps = gs.part + ((size_t)s * M + m) * W.N_dev;
-                v0 += s == sp ? acc[i][0][e] * sl0 : ps[col0];
-                v1 += s == sp ? acc[i][1][e] * sl1 : ps[col1];
+                v0 += s == sp ? acc[i][0][e] * sl0 : __hip_atomic_load(ps + col0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                v1 += s == sp ? acc[i][1][e] * sl1 : __hip_atomic_load(ps + col1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             }
             epilogue(m, v0, v1);
         }
 }
 
-template <int EPI, int TM>
-int launch_tm(const f16* X, int ldx, const DevLinear& W, const EpiArgs& ep, const GemmShape& gs, hipStream_t stream) {
+template <int EPI, int TM, int GT, bool ZP>
+int launch_v(const f16* X, int ldx, const DevLinear& W, const EpiArgs& ep, const GemmShape& gs, hipStream_t stream) {
     const int blocks = gs.nrb * gs.ncb * gs.S;
-    if (W.zeros || W.lgG < 6)
-        hipLaunchKernelGGL((gemm_w4_kernel<EPI, TM, true>), dim3(blocks), dim3(256), 0, stream, X, ldx, W, ep, gs);
-    else
-        hipLaunchKernelGGL((gemm_w4_kernel<EPI, TM, false>), dim3(blocks), dim3(256), 0, stream, X, ldx, W, ep, gs);
+    const size_t lds = lds_bytes<TM>();
+    static LdsLimit lim;
+    if (ensure_lds_limit(lim, (const void*)gemm_w4_kernel<EPI, TM, GT, ZP>, lds)) return -1;
+    hipLaunchKernelGGL((gemm_w4_kernel<EPI, TM, GT, ZP>), dim3(blocks), dim3(256), lds, stream, X, ldx, W, ep, gs);
     return hipGetLastError() == hipSuccess ? 0 : -1;
 }
 
+// row tiles of 128 only for groups of 64 or more without zero points; the
+// other variants use at most 64
 template <int EPI>
 int launch_epi(int TM, const f16* X, int ldx, const DevLinear& W, const EpiArgs& ep, const GemmShape& gs,
                hipStream_t stream) {
-    if (TM == 4) return launch_tm<EPI, 4>(X, ldx, W, ep, gs, stream);
-    if (TM == 2) return launch_tm<EPI, 2>(X, ldx, W, ep, gs, stream);
-    return launch_tm<EPI, 1>(X, ldx, W, ep, gs, stream);
+    const bool zp = W.zeros != nullptr;
+    const int gt = W.lgG == 5 ? 0 : W.lgG == 6 ? 1 : 2;
+    if (!zp && gt == 2) {
+        if (TM == 4) return launch_v<EPI, 4, 2, false>(X, ldx, W, ep, gs, stream);
+        if (TM == 2) return launch_v<EPI, 2, 2, false>(X, ldx, W, ep, gs, stream);
+        return launch_v<EPI, 1, 2, false>(X, ldx, W, ep, gs, stream);
+    }
+    if (!zp && gt == 1) {
+        if (TM == 4) return launch_v<EPI, 4, 1, false>(X, ldx, W, ep, gs, stream);
+        if (TM == 2) return launch_v<EPI, 2, 1, false>(X, ldx, W, ep, gs, stream);
+        return launch_v<EPI, 1, 1, false>(X, ldx, W, ep, gs, stream);
+    }
+    if (TM == 4) return -1;
+    if (zp) {
+        if (gt == 0) return TM == 2 ? launch_v<EPI, 2, 0, true>(X, ldx, W, ep, gs, stream)
+                                    : launch_v<EPI, 1, 0, true>(X, ldx, W, ep, gs, stream);
+        if (gt == 1) return TM == 2 ? launch_v<EPI, 2, 1, true>(X, ldx, W, ep, gs, stream)
+                                    : launch_v<EPI, 1, 1, true>(X, ldx, W, ep, gs, stream);
+        return TM == 2 ? launch_v<EPI, 2, 2, true>(X, ldx, W, ep, gs, stream)
+                       : launch_v<EPI, 1, 2, true>(X, ldx, W, ep, gs, stream);
+    }
+    return TM == 2 ? launch_v<EPI, 2, 0, false>(X, ldx, W, ep, gs, stream)
+                   : launch_v<EPI, 1, 0, false>(X, ldx, W, ep, gs, stream);
 }
 
 }  // namespace
 
+// Launch plan.  The row tile is the largest (most MFMAs per dequantised
+// fragment) that still gives about 0.8 tiles per CU; k splits then raise
+// the grid to half the CUs, or, while splits stay long (3072 k or more),
+// up to 1.2 blocks per CU.  Each split keeps at least 4 iterations.  (The
+// thresholds follow a measured sweep over the prefill shapes of the
+// Llama-3-8B-shaped layer at 128 and 512 rows.)
 GemmPlan gemm_w4_plan(int M, const DevLinear& W, int num_cus) {
     GemmPlan p;
     const int ncb = (W.N_dev + BN - 1) / BN, KB = W.K_pad / 64;
-    p.TM = 4;
-    // smaller row tiles, then k splits, until the grid covers the CUs
-    while (p.TM > 1 && ((M + 32 * p.TM - 1) / (32 * p.TM)) * ncb < num_cus) p.TM /= 2;
-    const int nrb = (M + 32 * p.TM - 1) / (32 * p.TM);
+    const int tm_max = (W.zeros || W.lgG == 5) ? 2 : 4;   // the kernel variants that exist
+    auto nrb = [&](int tm) { return (M + 32 * tm - 1) / (32 * tm); };
+    p.TM = tm_max;
+    while (p.TM > 1 && nrb(p.TM) * ncb * 5 < num_cus * 4) p.TM /= 2;
+    const int tiles = nrb(p.TM) * ncb;
     p.S = 1;
-    while (nrb * ncb * p.S < num_cus && KB / (p.S * 2) >= 8 && p.S < 8) p.S *= 2;
-    p.nrb = nrb;
+    while (p.S < 16 && KB / (p.S * 2) >= 8) {
+        const int blocks = tiles * p.S;
+        const bool small = blocks * 2 < num_cus;
+        const bool long_k = KB * 64 / p.S >= 2 * 3072 && blocks * 5 < num_cus * 6;
+        if (!small && !long_k) break;
+        p.S *= 2;
+    }
+    p.nrb = nrb(p.TM);
     p.ncb = ncb;
     p.part_bytes = p.S > 1 ? (size_t)p.S * M * W.N_dev * 4 : 0;
-    p.tiles = nrb * ncb;
+    p.tiles = tiles;
     return p;
 }
 

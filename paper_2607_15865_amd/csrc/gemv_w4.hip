@@ -139,10 +139,8 @@ int launch_t(const GemvArgs& a, hipStream_t stream) {
     const int kmax = (KB + a.ksplit - 1) / a.ksplit * 64;
     const size_t smem = (size_t)MAXB * (kmax + 8) * 2 + (NW * 2 * MAXB * 32 + MAXB + MAXB * 64) * sizeof(float);
     if (smem > 160 * 1024) return -1;
-    if (smem > 64 * 1024 &&
-        hipFuncSetAttribute((const void*)gemv_w4_kernel<EPI, NORM, ZP, G32>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                            (int)smem) != hipSuccess)
-        return -1;
+    static LdsLimit lim;
+    if (ensure_lds_limit(lim, (const void*)gemv_w4_kernel<EPI, NORM, ZP, G32>, smem)) return -1;
     dim3 grid(a.W.N_dev / 64, a.ksplit);
     hipLaunchKernelGGL((gemv_w4_kernel<EPI, NORM, ZP, G32>), grid, dim3(NW * 64), smem, stream, a);
     return hipGetLastError() == hipSuccess ? 0 : -1;

@@ -27,9 +27,14 @@ def _check_new_kv(k, v, ok, ov, start, T, seq=0, rows=None):
         gk, gv, ok, ov = gk[rows], gv[rows], ok[rows], ov[rows]
     assert_parity(gk, ok, "new K")
     assert_parity(gv, ov, "new V")
+    # bf16 rounding of K: a wrong rounding mode (truncation) moves about half
+    # of the entries off the oracle's bf16 value.  The prefill GEMM rounds
+    # each dequantised weight to fp16 once, which moves the pre-rounding K
+    # values by about 1e-4 relative and flips the bf16 value of entries near a
+    # rounding boundary: about 9% on the smallest layer.
     flips = np.mean(gk != ok)
     log(f"  new K entries differing from the oracle's bf16 value: {flips:.2e}")
-    assert flips < 0.05
+    assert flips < 0.2
 
 
 PREFILL_CASES = [("tiny", 32, None), ("tiny", 1, None), ("tiny", 77, None), ("qwen05b", 256, None),
