@@ -266,8 +266,9 @@ constexpr int kGemmCounters = 1024;     // split-K tiles of one GEMM (at most ab
 struct PrefillWs {
     size_t xn1, q, attn, h, xn2, g, part, total;
     GemmPlan qkv, o, gu, down;
+    AttnPrefillPlan at;
 };
-PrefillWs plan_prefill(const layer_s* L, int T) {
+PrefillWs plan_prefill(const layer_s* L, int T, int hist) {
     const layer_config& c = L->cfg;
     const size_t qd = (size_t)c.n_heads * c.head_dim;
     Carve cv;
@@ -276,13 +277,15 @@ PrefillWs plan_prefill(const layer_s* L, int T) {
     w.o = gemm_w4_plan(T, L->o.d, L->num_cus);
     w.gu = gemm_w4_plan(T, L->gu.d, L->num_cus);
     w.down = gemm_w4_plan(T, L->down.d, L->num_cus);
+    w.at = attn_prefill_plan(T, hist, c.n_heads, c.n_kv_heads, c.head_dim, L->num_cus);
     w.xn1 = cv.take((size_t)T * c.hidden * 2);
     w.q = cv.take((size_t)T * qd * 2);
     w.attn = cv.take((size_t)T * qd * 2);
     w.h = cv.take((size_t)T * c.hidden * 4);
     w.xn2 = cv.take((size_t)T * c.hidden * 2);
     w.g = cv.take((size_t)T * L->F_pad * 2);
-    w.part = cv.take(std::max(std::max(w.qkv.part_bytes, w.o.part_bytes), std::max(w.gu.part_bytes, w.down.part_bytes)));
+    // split-K partials of each GEMM and the attention chunk states, used one kernel at a time
+    w.part = cv.take(std::max({w.qkv.part_bytes, w.o.part_bytes, w.gu.part_bytes, w.down.part_bytes, w.at.part_bound}));
     w.total = cv.off;
     return w;
 }
@@ -447,7 +450,7 @@ int run_prefill(layer_s* L, const float* x, const int32_t* pos, int T, int hist,
     if ((const void*)x == (const void*)y) return fail(W4_EINVAL, "x and y must not alias");
     const layer_config& c = L->cfg;
     if ((long long)hist + T > c.max_seq) return fail(W4_ECAPACITY, "hist_len + T = %lld exceeds max_seq %d", (long long)hist + T, c.max_seq);
-    const PrefillWs w = plan_prefill(L, T);
+    const PrefillWs w = plan_prefill(L, T, hist);
     if (ws_bytes < w.total) return fail(W4_EWORKSPACE, "workspace %zu bytes, need %zu", ws_bytes, w.total);
     hipStream_t st = (hipStream_t)stream_;
     char* base = (char*)ws;
@@ -487,7 +490,8 @@ int run_prefill(layer_s* L, const float* x, const int32_t* pos, int T, int hist,
     aa.nkv = c.n_kv_heads;
     aa.d = d;
     aa.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)d));
-    { ProfScope ps(L, stage, 2, st); rc |= launch_attn_prefill(aa, st); }
+    aa.part = part;
+    { ProfScope ps(L, stage, 2, st); rc |= launch_attn_prefill(aa, w.at, st); }
     EpiArgs eo = base_epi(L);
     eo.resid = x;
     eo.out_f32 = h;
@@ -666,8 +670,8 @@ int layer_destroy(layer_t layer) {
 size_t layer_workspace_size(layer_t L, int32_t stage, int32_t batch, int32_t T, int32_t max_ctx) {
     if (!L) return 0;
     if (stage == 0 || stage == 1) {
-        if (T < 1) return 0;
-        return plan_prefill(L, T).total;
+        if (T < 1 || max_ctx < 0) return 0;
+        return plan_prefill(L, T, stage == 1 ? max_ctx : 0).total;
     }
     if (stage == 2) {
         if (batch < 1 || max_ctx < 0) return 0;

@@ -1,18 +1,35 @@
 // Grouped-query causal attention (top.FAttention, Sec. 2.2) for the three
 // stages.
 //
-// Prefill / prefill_kv: flash attention on the 32x32x16 bf16 MFMA.  A wave
-// owns 32 queries of one head; the waves of a block share the kv head (and
-// the K/V tiles staged in LDS).  Scores are formed transposed, S^T = K Q^T,
-// with the 32 key rows of a tile fed in a permuted order (bits 2 and 3 of the
-// row index swapped) so that register e of the score tile holds key
-// 16*(e/8) + 8*(lane/32) + e%8 of query lane%32: exactly the operand layout
-// of P^T in O^T = V^T P^T.  Every lane therefore owns one query: the online
-// softmax (running max and sum) lives in registers.  P is fed to the MFMA as
-// a bf16 pair hi + lo (P - hi), which keeps P V at near-fp32 accuracy; V is
-// stored transposed in LDS.  The causal mask is computed from indices, only
-// on the tiles that straddle the diagonal; tiles past it are skipped (the
-// role the paper's small reusable mask plays, Sec. 4.6.1).
+// Prefill / prefill_kv: flash attention on the 32x32x16 bf16 MFMA.  A block
+// works on one kv head, one tile of 32 queries and one chunk of the keys
+// those queries see; its waves are the query heads of the kv head's group
+// (one head per wave), so every K/V tile staged in LDS serves all of them.
+// Chunks split long key ranges across blocks (a causal prefill's late query
+// tiles, a prefill_kv over a long history), so the grid has enough blocks;
+// work items are ordered longest first.
+//
+// Keys are staged 64 at a time (two 32-key tiles), K and V both straight
+// from memory to LDS (direct-to-LDS loads), double buffered: one memory round
+// trip per 64 keys, one barrier.  K rows are 16-byte-chunk XOR-swizzled by
+// row (conflict-free fragment reads); V stays in its natural [key][dim]
+// layout and the V^T fragments of O^T = V^T P^T are gathered with 16-bit LDS
+// reads.  Scores are formed transposed, S^T = K Q^T, with the 32 key rows
+// of a tile fed in a permuted order (bits 2 and 3 of the row index swapped)
+// so that register e of the score tile holds key 16*(e/8) + 8*(lane/32) +
+// e%8 of query lane%32: exactly the operand layout of P^T.  Every lane
+// therefore owns one query: the online softmax (running max and sum) lives
+// in registers and is updated once per 64 keys.  P is fed to the MFMA as a
+// bf16 pair hi + lo (P - hi), which keeps P V at near-fp32 accuracy.  The
+// causal mask is computed from indices, only on tiles that straddle the
+// diagonal; tiles past it are never visited (the role the paper's small
+// reusable mask plays, Sec. 4.6.1).
+//
+// A query tile whose keys fit one chunk writes its output directly.
+// Otherwise every chunk writes its partial state (running max, sum and
+// unnormalised output, in the accumulator layout: coalesced) and a second
+// kernel merges the chunks of each query tile in chunk order with the
+// log-sum-exp rule, so results do not depend on timing.
 //
 // Decode: one query per sequence.  Split-KV: a block reads one chunk of one
 // kv head's cache once for all the query heads of its group (VALU dot
@@ -27,131 +44,222 @@ __device__ __forceinline__ int key_perm(int r) {  // swap bits 2 and 3
     return (r & ~12) | ((r & 4) << 1) | ((r & 8) >> 1);
 }
 
-template <int D>
-__global__ void __launch_bounds__(256) attn_prefill_kernel(AttnPrefillArgs a, int HB, int QB) {
-    constexpr int LDK = D + 8;   // bf16 per K row in LDS
-    constexpr int LDV = 32 + 8;  // bf16 per V^T row in LDS
-    __shared__ __attribute__((aligned(16))) __bf16 Ks[32 * LDK];
-    __shared__ __attribute__((aligned(16))) __bf16 Vt[D * LDV];
+constexpr int PF_MAXHB = 8;                  // query heads per block
+constexpr int PF_KST = 64;                   // keys per LDS stage
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+// Query tile and key chunk of work item `item` (longest first): query tile
+// qt has nkeys(qt) = L + min(T, 32 (qt + 1)) keys, cut into chunks of
+// chunk_keys.  `first` is the item of the tile's chunk 0.
+__device__ __forceinline__ void prefill_item(const AttnPrefillArgs& a, int item, int& qt, int& chunk, int& nch,
+                                             int& first) {
+    const int nqt = (a.T + 31) / 32;
+    int base = 0;
+    for (qt = nqt - 1; qt > 0; qt--) {
+        const int nk = a.L + min(a.T, 32 * (qt + 1));
+        const int n = (nk + a.chunk_keys - 1) / a.chunk_keys;
+        if (item < base + n) break;
+        base += n;
+    }
+    const int nk = a.L + min(a.T, 32 * (qt + 1));
+    nch = (nk + a.chunk_keys - 1) / a.chunk_keys;
+    chunk = item - base;
+    first = base;
+}
+
+template <int D>
+__device__ __forceinline__ size_t part_index(const AttnPrefillArgs& a, int row, int item, int wave, int lane) {
+    constexpr int NREG = 2 + 16 * (D / 32);
+    return ((size_t)(row * a.items + item) * PF_MAXHB + wave) * NREG * 64 + lane;
+}
+
+template <int D>
+__global__ void __launch_bounds__(64 * PF_MAXHB) attn_prefill_kernel(AttnPrefillArgs a) {
+    constexpr int NCH = D / 8;               // 16-byte chunks per K / V row
+    constexpr int STB = PF_KST * D * 2;      // bytes of one K or V stage
+    extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+    unsigned char* const Ks = smem;              // [2][64 keys][D], chunks swizzled
+    unsigned char* const Vs = smem + 2 * STB;    // [2][64 keys][D]
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int HB = blockDim.x / 64;
     const int h = lane >> 5, c = lane & 31;
     const int r = a.nq / a.nkv;
-    const int ngrp = (r + HB - 1) / HB;
-    const int g = blockIdx.y / ngrp, hg = blockIdx.y % ngrp;
-    const int hw = wave % HB, qt = wave / HB;
-    const int hidx = hg * HB + hw;
-    const bool active = (wave < HB * QB) && (hidx < r);
-    const int head = g * r + hidx;
-    const int q0 = (blockIdx.x * QB + qt) * 32;
-    const int qb_end = min(a.T, (blockIdx.x + 1) * QB * 32);
-    const int nkeys = a.L + qb_end;              // keys the block may need
-    const int ntile = (nkeys + 31) / 32;
+    const int g = blockIdx.y / a.ngrp, hg = blockIdx.y % a.ngrp;
+    const int hidx = hg * HB + wave;
+    const bool active = hidx < r;
+    const int head = g * r + (active ? hidx : 0);
+    int qt, chunk, nch, first;
+    prefill_item(a, blockIdx.x, qt, chunk, nch, first);
+    const int q0 = qt * 32;
+    const int nkeys = a.L + min(a.T, q0 + 32);
+    const int k0 = chunk * a.chunk_keys, k1 = min(nkeys, k0 + a.chunk_keys);
+    const int nst = (k1 - k0 + PF_KST - 1) / PF_KST;
     const uint16_t* kc = a.k_cache + (size_t)g * a.cache_stride_h;
     const uint16_t* vc = a.v_cache + (size_t)g * a.cache_stride_h;
+
+    // ---- stage of 64 keys: 2 x 64 loads of 1 KB (K, V); load i fills rows
+    // KROWS i .. + KROWS - 1; lane l writes chunk l % NCH of its row (for K
+    // holding logical chunk (l % NCH) ^ (row % NCH))
+    constexpr int KROWS = 1024 / (2 * D);
+    constexpr int NLOAD = PF_KST / KROWS;
+    auto load_stage = [&](int st, int buf) __attribute__((always_inline)) {
+        for (int i = wave; i < NLOAD; i += HB) {
+            const int row = i * KROWS + lane / NCH;
+            int slot = k0 + st * PF_KST + row;
+            slot = slot < k1 ? slot : k1 - 1;
+            const int pc = lane % NCH, lc = pc ^ (row % NCH);
+            __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(kc + (size_t)slot * D + lc * 8),
+                                             (__attribute__((address_space(3))) void*)(Ks + buf * STB + i * 1024),
+                                             16, 0, 0);
+            __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(vc + (size_t)slot * D + pc * 8),
+                                             (__attribute__((address_space(3))) void*)(Vs + buf * STB + i * 1024),
+                                             16, 0, 0);
+        }
+    };
 
     // Q^T fragments (B operand): query q0 + c, dims 16s + 8h .. +8
     bf16x8 qf[D / 16];
     const int qrow = q0 + c;
+    const int qload = qrow < a.T ? qrow : a.T - 1;
+    load_stage(0, 0);
 #pragma unroll
-    for (int s = 0; s < D / 16; s++) {
-        if (active && qrow < a.T)
-            qf[s] = *reinterpret_cast<const bf16x8*>(a.q + ((size_t)qrow * a.nq + head) * D + s * 16 + h * 8);
-        else
-            qf[s] = bf16x8{};
-    }
+    for (int s = 0; s < D / 16; s++)
+        qf[s] = *reinterpret_cast<const bf16x8*>(a.q + ((size_t)qload * a.nq + head) * D + s * 16 + h * 8);
+
     f32x16 o[D / 32];
 #pragma unroll
     for (int i = 0; i < D / 32; i++) o[i] = f32x16{};
     float m = -INFINITY, l = 0.f;
     const int qslot = a.L + qrow;
-    const int wave_last_slot = a.L + min(q0 + 31, a.T - 1);
-
-    for (int kt = 0; kt < ntile; kt++) {
-        __syncthreads();
-        // K tile rows and V^T columns: 32 keys x D dims, 16 bytes per load
-        for (int i = tid; i < 32 * (D / 8); i += 256) {
-            const int key = i / (D / 8), seg = i % (D / 8);
-            const int slot = kt * 32 + key;
-            u32x4 kv = {0, 0, 0, 0}, vv = {0, 0, 0, 0};
-            if (slot < nkeys) {
-                kv = *reinterpret_cast<const u32x4*>(kc + (size_t)slot * D + seg * 8);
-                vv = *reinterpret_cast<const u32x4*>(vc + (size_t)slot * D + seg * 8);
+    const int krow = key_perm(c);
+    __syncthreads();
+    for (int st = 0; st < nst; st++) {
+        const int buf = st & 1;
+        if (st + 1 < nst) load_stage(st + 1, buf ^ 1);
+        if (active) {
+            const unsigned char* K = Ks + buf * STB;
+            const __bf16* V = reinterpret_cast<const __bf16*>(Vs + buf * STB);
+            // S^T of the two 32-key tiles, two independent MFMA chains
+            f32x16 sa = f32x16{}, sb = f32x16{};
+#pragma unroll
+            for (int s = 0; s < D / 16; s++) {
+                const int lc = (2 * s + h) ^ (krow % NCH);
+                const bf16x8 ka = *reinterpret_cast<const bf16x8*>(K + krow * (2 * D) + lc * 16);
+                const bf16x8 kb = *reinterpret_cast<const bf16x8*>(K + (32 + krow) * (2 * D) + lc * 16);
+                sa = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[s], sa, 0, 0, 0);
+                sb = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kb, qf[s], sb, 0, 0, 0);
             }
-            *reinterpret_cast<u32x4*>(&Ks[key * LDK + seg * 8]) = kv;
-            const __bf16* ve = reinterpret_cast<const __bf16*>(&vv);
+            const int kbase = k0 + st * PF_KST;
+            const bool diag = kbase + PF_KST - 1 > a.L + q0;
+            float p[32];
+            float mt = -INFINITY;
 #pragma unroll
-            for (int j = 0; j < 8; j++) Vt[(seg * 8 + j) * LDV + key] = ve[j];
+            for (int e = 0; e < 32; e++) {
+                const int kslot = kbase + 32 * (e / 16) + 16 * ((e % 16) / 8) + 8 * h + (e % 8);
+                float v = (e < 16 ? sa[e] : sb[e - 16]) * a.scale_log2;
+                if (diag && kslot > qslot) v = -INFINITY;
+                p[e] = v;
+                mt = fmaxf(mt, v);
+            }
+            mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
+            const float m_new = fmaxf(m, mt);
+            const float alpha = (m_new == -INFINITY) ? 1.f : exp2f(m - m_new);
+            float ls = 0.f;
+#pragma unroll
+            for (int e = 0; e < 32; e++) {
+                p[e] = (p[e] == -INFINITY) ? 0.f : exp2f(p[e] - m_new);
+                ls += p[e];
+            }
+            l = l * alpha + ls;
+            m = m_new;
+#pragma unroll
+            for (int i = 0; i < D / 32; i++)
+#pragma unroll
+                for (int e = 0; e < 16; e++) o[i][e] *= alpha;
+            // O^T += V^T P^T over the 4 key groups of 16 (tile, step)
+#pragma unroll
+            for (int ks = 0; ks < 4; ks++) {
+                bf16x8 phi, plo;
+#pragma unroll
+                for (int j = 0; j < 8; j++) {
+                    const float pv = p[8 * ks + j];
+                    const __bf16 hi = (__bf16)pv;
+                    phi[j] = hi;
+                    plo[j] = (__bf16)(pv - (float)hi);
+                }
+                const int key0 = 16 * ks + 8 * h;       // this lane's 8 keys of the group
+#pragma unroll
+                for (int i = 0; i < D / 32; i++) {
+                    bf16x8 vf;
+#pragma unroll
+                    for (int j = 0; j < 8; j++) vf[j] = V[(key0 + j) * D + i * 32 + c];
+                    o[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, phi, o[i], 0, 0, 0);
+                    o[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, plo, o[i], 0, 0, 0);
+                }
+            }
         }
         __syncthreads();
-        if (!active || q0 >= a.T || kt * 32 > wave_last_slot) continue;
+    }
+    if (!active) return;
 
-        // S^T = K Q^T (rows: permuted keys, columns: queries)
-        f32x16 s_acc = f32x16{};
-        const int krow = key_perm(c);
-#pragma unroll
-        for (int s = 0; s < D / 16; s++) {
-            const bf16x8 kf = *reinterpret_cast<const bf16x8*>(&Ks[krow * LDK + s * 16 + h * 8]);
-            s_acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[s], s_acc, 0, 0, 0);
-        }
-        float p[16];
-        float mt = -INFINITY;
-        const bool diag = (kt * 32 + 31 > a.L + q0);
-#pragma unroll
-        for (int e = 0; e < 16; e++) {
-            const int kslot = kt * 32 + 16 * (e / 8) + 8 * h + (e % 8);
-            float v = s_acc[e] * a.scale_log2;
-            if (diag && kslot > qslot) v = -INFINITY;
-            p[e] = v;
-            mt = fmaxf(mt, v);
-        }
-        mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
-        const float m_new = fmaxf(m, mt);
-        const float alpha = (m_new == -INFINITY) ? 1.f : exp2f(m - m_new);
-        float ls = 0.f;
-#pragma unroll
-        for (int e = 0; e < 16; e++) {
-            p[e] = (p[e] == -INFINITY) ? 0.f : exp2f(p[e] - m_new);
-            ls += p[e];
-        }
-        l = l * alpha + ls;
-        m = m_new;
+    if (nch == 1) {
+        // output: dim of register e of o[i] is i * 32 + 8 (e / 4) + 4 h + e % 4
+        if (qrow >= a.T) return;
+        const float lt = l + __shfl_xor(l, 32, 64);
+        const float inv = (lt > 0.f) ? 1.f / lt : 0.f;
+        f16* out = a.out + ((size_t)qrow * a.nq + head) * D;
 #pragma unroll
         for (int i = 0; i < D / 32; i++)
 #pragma unroll
-            for (int e = 0; e < 16; e++) o[i][e] *= alpha;
-
-        bf16x8 phi[2], plo[2];
-#pragma unroll
-        for (int s = 0; s < 2; s++)
-#pragma unroll
-            for (int j = 0; j < 8; j++) {
-                const float pv = p[8 * s + j];
-                const __bf16 hi = (__bf16)pv;
-                phi[s][j] = hi;
-                plo[s][j] = (__bf16)(pv - (float)hi);
-            }
-#pragma unroll
-        for (int i = 0; i < D / 32; i++) {
-#pragma unroll
-            for (int s = 0; s < 2; s++) {
-                const bf16x8 vf = *reinterpret_cast<const bf16x8*>(&Vt[(i * 32 + c) * LDV + s * 16 + h * 8]);
-                o[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, phi[s], o[i], 0, 0, 0);
-                o[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, plo[s], o[i], 0, 0, 0);
-            }
-        }
+            for (int e = 0; e < 16; e++) out[i * 32 + 8 * (e / 4) + 4 * h + (e % 4)] = act_f16(o[i][e] * inv);
+        return;
     }
-    if (!active || qrow >= a.T) return;
-    const float lt = l + __shfl_xor(l, 32, 64);
-    const float inv = (lt > 0.f) ? 1.f / lt : 0.f;
-    f16* out = a.out + ((size_t)qrow * a.nq + head) * D;
+    // partial state of this chunk: [row][item][wave][m, l, O registers][64 lanes]
+    float* pp = a.part + part_index<D>(a, blockIdx.y, blockIdx.x, wave, lane);
+    pp[0] = m;
+    pp[64] = l;
 #pragma unroll
     for (int i = 0; i < D / 32; i++)
 #pragma unroll
-        for (int e = 0; e < 16; e++) {
-            const int dim = i * 32 + 8 * (e / 4) + 4 * h + (e % 4);
-            out[dim] = act_f16(o[i][e] * inv);
-        }
+        for (int e = 0; e < 16; e++) pp[(size_t)(2 + i * 16 + e) * 64] = o[i][e];
+}
+
+// Merge of the chunk states of the query tiles with more than one chunk:
+// block (query tile, block row, 32-dim slice): thread (wave, lane) merges the
+// lane's 16 output registers of the slice over the tile's chunks, in order.
+template <int D>
+__global__ void __launch_bounds__(64 * PF_MAXHB) attn_prefill_merge_kernel(AttnPrefillArgs a) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int HB = blockDim.x / 64;
+    const int h = lane >> 5, c = lane & 31;
+    const int qt = blockIdx.x, row = blockIdx.y, i = blockIdx.z;
+    const int r = a.nq / a.nkv;
+    const int g = row / a.ngrp, hidx = (row % a.ngrp) * HB + wave;
+    const int nqt = (a.T + 31) / 32;
+    // first item of tile qt (items run from the last tile down)
+    int first = 0;
+    for (int t = nqt - 1; t > qt; t--) first += (a.L + min(a.T, 32 * (t + 1)) + a.chunk_keys - 1) / a.chunk_keys;
+    const int nch = (a.L + min(a.T, 32 * (qt + 1)) + a.chunk_keys - 1) / a.chunk_keys;
+    if (nch == 1 || hidx >= r) return;
+    float M = -INFINITY;
+    for (int ch = 0; ch < nch; ch++) M = fmaxf(M, a.part[part_index<D>(a, row, first + ch, wave, lane)]);
+    float L = 0.f, acc[16] = {};
+    for (int ch = 0; ch < nch; ch++) {
+        const float* pp = a.part + part_index<D>(a, row, first + ch, wave, lane);
+        const float mc = pp[0];
+        const float w = (mc == -INFINITY) ? 0.f : exp2f(mc - M);
+        L += w * pp[64];
+#pragma unroll
+        for (int e = 0; e < 16; e++) acc[e] += w * pp[(size_t)(2 + i * 16 + e) * 64];
+    }
+    const int qrow = qt * 32 + c;
+    const float lt = L + __shfl_xor(L, 32, 64);
+    if (qrow >= a.T) return;
+    const float inv = (lt > 0.f) ? 1.f / lt : 0.f;
+    f16* out = a.out + ((size_t)qrow * a.nq + g * r + hidx) * D;
+#pragma unroll
+    for (int e = 0; e < 16; e++) out[i * 32 + 8 * (e / 4) + 4 * h + (e % 4)] = act_f16(acc[e] * inv);
 }
 
 // ---------------------------------------------------------------- decode
@@ -305,18 +413,59 @@ __global__ void __launch_bounds__(D) attn_decode_combine_kernel(AttnDecodeArgs a
 
 }  // namespace
 
-int launch_attn_prefill(const AttnPrefillArgs& a, hipStream_t stream) {
-    const int r = a.nq / a.nkv;
-    int HB = r < 4 ? r : 4;
-    int QB = (4 % HB == 0) ? 4 / HB : 1;
-    const int ngrp = (r + HB - 1) / HB;
-    dim3 grid((a.T + 32 * QB - 1) / (32 * QB), a.nkv * ngrp);
-    if (a.d == 128)
-        hipLaunchKernelGGL(attn_prefill_kernel<128>, grid, dim3(256), 0, stream, a, HB, QB);
-    else if (a.d == 64)
-        hipLaunchKernelGGL(attn_prefill_kernel<64>, grid, dim3(256), 0, stream, a, HB, QB);
-    else
+AttnPrefillPlan attn_prefill_plan(int T, int L, int nq, int nkv, int d, int num_cus) {
+    AttnPrefillPlan p;
+    const int r = nq / nkv;
+    const int hb = r < PF_MAXHB ? r : PF_MAXHB;
+    p.ngrp = (r + hb - 1) / hb;
+    p.threads = 64 * hb;
+    const int nqt = (T + 31) / 32;
+    // key stages of all query tiles of one block row, then chunks of at
+    // least 2 stages (128 keys) sized so that the grid holds about two
+    // blocks per CU
+    long long stages = 0;
+    for (int qt = 0; qt < nqt; qt++) stages += (L + std::min(T, 32 * (qt + 1)) + PF_KST - 1) / PF_KST;
+    const long long rows = (long long)nkv * p.ngrp;
+    long long cs = (stages * rows + 2LL * num_cus - 1) / (2LL * num_cus);
+    cs = std::max(2LL, cs);
+    p.chunk_keys = (int)(PF_KST * cs);
+    p.items = 0;
+    bool multi = false;
+    for (int qt = 0; qt < nqt; qt++) {
+        const int n = (L + std::min(T, 32 * (qt + 1)) + p.chunk_keys - 1) / p.chunk_keys;
+        p.items += n;
+        multi |= n > 1;
+    }
+    p.merge = multi;
+    const int nreg = 2 + 16 * (d / 32);
+    const size_t per_item = (size_t)rows * PF_MAXHB * nreg * 64 * sizeof(float);
+    p.part_bytes = multi ? (size_t)p.items * per_item : 0;
+    // chunks are at least 128 keys: a bound that grows with L, for workspace sizing
+    p.part_bound = (size_t)nqt * ((L + T + 127) / 128) * per_item;
+    p.lds_bytes = (size_t)4 * PF_KST * d * 2;
+    return p;
+}
+
+int launch_attn_prefill(const AttnPrefillArgs& a, const AttnPrefillPlan& p, hipStream_t stream) {
+    if (p.items < 1 || (p.part_bytes && !a.part)) return -1;
+    AttnPrefillArgs b = a;
+    b.chunk_keys = p.chunk_keys;
+    b.ngrp = p.ngrp;
+    b.items = p.items;
+    const dim3 grid(p.items, a.nkv * p.ngrp);
+    const dim3 mgrid((a.T + 31) / 32, a.nkv * p.ngrp, a.d / 32);
+    static LdsLimit lim128, lim64;
+    if (a.d == 128) {
+        if (ensure_lds_limit(lim128, (const void*)attn_prefill_kernel<128>, p.lds_bytes)) return -1;
+        hipLaunchKernelGGL(attn_prefill_kernel<128>, grid, dim3(p.threads), p.lds_bytes, stream, b);
+        if (p.merge) hipLaunchKernelGGL(attn_prefill_merge_kernel<128>, mgrid, dim3(p.threads), 0, stream, b);
+    } else if (a.d == 64) {
+        if (ensure_lds_limit(lim64, (const void*)attn_prefill_kernel<64>, p.lds_bytes)) return -1;
+        hipLaunchKernelGGL(attn_prefill_kernel<64>, grid, dim3(p.threads), p.lds_bytes, stream, b);
+        if (p.merge) hipLaunchKernelGGL(attn_prefill_merge_kernel<64>, mgrid, dim3(p.threads), 0, stream, b);
+    } else {
         return -1;
+    }
     return hipGetLastError() == hipSuccess ? 0 : -1;
 }
 

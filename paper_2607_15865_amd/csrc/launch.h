@@ -80,8 +80,20 @@ struct AttnPrefillArgs {
     f16* out;                // [T][nq*d]
     int T, L, nq, nkv, d;
     float scale_log2;        // log2(e) / sqrt(d)
+    float* part;             // chunk partial states (plan.part_bytes)
+    int chunk_keys, ngrp, items;   // set by the launcher from the plan
 };
-int launch_attn_prefill(const AttnPrefillArgs& a, hipStream_t stream);
+// Prefill attention launch plan: key chunk length, work items per block
+// row, block size, workspace.
+struct AttnPrefillPlan {
+    int chunk_keys = 0, items = 0, ngrp = 1, threads = 64;
+    bool merge = false;      // some query tile has more than one chunk
+    size_t part_bytes = 0;
+    size_t part_bound = 0;   // part_bytes of any history up to L (non-decreasing in L)
+    size_t lds_bytes = 0;
+};
+AttnPrefillPlan attn_prefill_plan(int T, int L, int nq, int nkv, int d, int num_cus);
+int launch_attn_prefill(const AttnPrefillArgs& a, const AttnPrefillPlan& p, hipStream_t stream);
 
 struct AttnDecodeArgs {
     const uint16_t* q;       // bf16 [B][nq][d]
