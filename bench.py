@@ -98,6 +98,72 @@ def cpu_baseline(cfg, w):
 
 # ---------------------------------------------------------------- main
 
+STACK = dict(name="llama8b", prompt=1024, steps=256)
+
+
+def run_stack(args):
+    """The layer stack (one model's decoder layers, each with its own seeded
+    weights and KV cache): prefill the prompt through all layers, then decode
+    token by token with a growing cache.  Each decode step's layer-0 input is
+    a seeded N(0, 1) row standing in for an embedded sampled token.  Prints
+    one JSON line: end-to-end decode tokens/s."""
+    import numpy as np
+    import torch
+    from paper_2607_15865_amd import binding, synth
+
+    cfg = synth.CONFIGS[STACK["name"]]
+    nl, P, S = args.stack_layers, STACK["prompt"], STACK["steps"]
+    log(f"stack: building {nl} {cfg.name} layers")
+    t0 = time.time()
+    layers = [binding.Layer(cfg, synth.make_layer_words(cfg, l)) for l in range(nl)]
+    log(f"stack: layers built in {time.time() - t0:.1f} s")
+    st = binding.Stack(layers)
+    caches = [l.new_cache(1) for l in layers]
+    kcs, vcs = [c[0] for c in caches], [c[1] for c in caches]
+
+    def rows_f32(bits):
+        return torch.from_numpy((bits.astype(np.uint32) << 16).view(np.float32)).cuda()
+
+    xp = rows_f32(synth.activations(cfg, synth.TID_X_PREFILL, P))
+    yp = torch.empty_like(xp)
+    xd = rows_f32(np.concatenate([synth.activations(cfg, synth.TID_X_DECODE + 1000 * s, 1) for s in range(S)]))
+    yd = torch.empty_like(xd)
+    slots = torch.arange(P, P + S, dtype=torch.int32, device="cuda")
+    e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+    torch.cuda.synchronize()
+    e0.record()
+    st.prefill(xp, torch.arange(P, dtype=torch.int32, device="cuda"), 0, kcs, vcs, yp)
+    e1.record()
+    for s in range(S):
+        st.decode(xd[s:s + 1], slots[s:s + 1], slots[s:s + 1], P + s, kcs, vcs, yd[s:s + 1])
+    e2.record()
+    torch.cuda.synchronize()
+    prefill_ms = e0.elapsed_time(e1)
+    decode_ms = e1.elapsed_time(e2)
+    assert torch.isfinite(yd).all() and torch.isfinite(yp).all()
+    tok_s = S / (decode_ms * 1e-3)
+    # bytes a decode step reads: all weights plus the K/V of every layer (ctx P..P+S-1)
+    wbytes = weight_bytes(cfg) * nl
+    kv = 2 * cfg.n_kv_heads * cfg.head_dim * 2 * nl * (P + S / 2)
+    gbps = (wbytes + kv) * tok_s / 1e9
+    pf = stage_flops(cfg, P, P, 0, 1) * nl
+    line = {
+        "metric": "end-to-end decode tokens/s of a 32-layer W4A16 Llama-3-8B-shaped stack",
+        "value": round(tok_s, 1), "unit": "tokens/s", "n_gpus": 1, "steps": S, "warmup": 0,
+        "ms_per_step": round(decode_ms / S, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16 activations, int4 weights, fp32 accumulate",
+        "data": "synthetic: seeded int4 weights per layer, N(0,1) inputs",
+        "config": {"workload": f"{nl}-layer {cfg.name}-shaped stack: prefill {P} tokens, then {S} decode steps "
+                               f"at B=1 (context {P} -> {P + S - 1})"},
+        "decode": {"layer_step_us": round(decode_ms * 1e3 / (S * nl), 2), "gbps": round(gbps, 1),
+                   "frac_hbm": round(gbps / PEAK_HBM_GBS, 4)},
+        "prefill": {"ms": round(prefill_ms, 3), "tflops": round(pf / (prefill_ms * 1e-3) / 1e12, 1),
+                    "frac_mfma": round(pf / (prefill_ms * 1e-3) / 1e12 / PEAK_MFMA_TFLOPS, 4)},
+    }
+    print(json.dumps(line), flush=True)
+    return 0
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -105,11 +171,17 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--copies", type=int, default=8, help="device copies of the layer (rotation)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--stack", action="store_true",
+                    help="instead: the 32-layer stack, 1024-token prefill then 256 decode steps")
+    ap.add_argument("--stack-layers", type=int, default=32)
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU: the layer's single-GPU kernels; --gpus {args.gpus} is not supported "
               "(multi-GPU sharding is described in DESIGN.md, not built)", file=sys.stderr)
         sys.exit(2)
+
+    if args.stack:
+        return run_stack(args)
 
     import numpy as np
     import torch

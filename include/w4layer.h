@@ -185,6 +185,34 @@ int layer_decode(layer_t layer, const float* x, const int32_t* pos, const int32_
                  void* k_cache, void* v_cache, float* y,
                  void* ws, size_t ws_bytes, void* stream);
 
+/* ---- layer stacks (Sec. 4.5, runtime orchestration) ---------------------- */
+
+/* A stack of n_layers layers of one model run back to back on one stream:
+ * the output of layer i is the input of layer i + 1.  layers, k_caches and
+ * v_caches are host arrays of n_layers entries (each layer has its own
+ * caches, in the layouts the single-layer calls take).  x is the input of
+ * layer 0 and y receives the output of the last layer (no aliasing); the
+ * activations between layers live in the workspace.  All layers must have
+ * the same hidden size.  The calls enqueue the layers' kernels and return.
+ *
+ * stack_workspace_size: bytes for stage 0/1 (prefill / prefill_kv: T tokens,
+ * history up to max_ctx) or 2 (decode: batch sequences, context up to
+ * max_ctx); 0 for invalid arguments.
+ * stack_prefill: every layer runs layer_prefill_kv with hist_len (0: prefill).
+ * stack_decode: every layer runs layer_decode with the same pos, ctx_lens,
+ * max_ctx, attn_mask and B.
+ * Errors: those of the single-layer calls, and W4_EINVAL for a null or
+ * mismatched layer list. */
+size_t stack_workspace_size(const layer_t* layers, int32_t n_layers, int32_t stage, int32_t batch,
+                            int32_t T, int32_t max_ctx);
+int stack_prefill(const layer_t* layers, int32_t n_layers, const float* x, const int32_t* pos,
+                  int32_t T, int32_t hist_len, void* const* k_caches, void* const* v_caches,
+                  float* y, void* ws, size_t ws_bytes, void* stream);
+int stack_decode(const layer_t* layers, int32_t n_layers, const float* x, const int32_t* pos,
+                 const int32_t* ctx_lens, int32_t max_ctx, const float* attn_mask, int32_t B,
+                 void* const* k_caches, void* const* v_caches, float* y,
+                 void* ws, size_t ws_bytes, void* stream);
+
 /* ---- KV cache -------------------------------------------------------------- */
 
 /* In-place Concat (Sec. 4.6.3): copy new keys/values k_new, v_new (bf16
@@ -207,9 +235,9 @@ int kv_append(const kv_desc* desc, void* k_cache, void* v_cache,
 int layer_debug_dequant(layer_t layer, int32_t which, float* out, void* stream);
 
 /* Decode implementation (tuning / testing): 0 automatic (default), 1 a
- * sequence of kernels, 2 one persistent cooperative launch with one block per
- * CU (used automatically for B <= 4 when the layer has no zero points and
- * its on-chip working set fits).  Both compute the same result; the
+ * sequence of kernels, 2 one persistent launch with one block per CU (used
+ * automatically for B <= 4 when the layer has no zero points and its
+ * on-chip working set fits).  Both compute the same result; the
  * persistent path is deterministic.  With 2, a decode call the persistent
  * path cannot serve fails with W4_EUNSUPPORTED.  Errors: W4_EINVAL. */
 int layer_set_decode_path(layer_t layer, int32_t path);

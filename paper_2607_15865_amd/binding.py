@@ -82,6 +82,9 @@ _SIG = {
     "layer_profile_kernel": (ctypes.c_int, [_P, _I, _I]),
     "layer_profile_read": (ctypes.c_int, [_P, _I, ctypes.POINTER(ctypes.c_float), ctypes.POINTER(ctypes.c_int32)]),
     "layer_last_error": (ctypes.c_char_p, []),
+    "stack_workspace_size": (ctypes.c_size_t, [_P, _I, _I, _I, _I, _I]),
+    "stack_prefill": (ctypes.c_int, [_P, _I, _P, _P, _I, _I, _P, _P, _P, _P, ctypes.c_size_t, _P]),
+    "stack_decode": (ctypes.c_int, [_P, _I, _P, _P, _P, _I, _P, _I, _P, _P, _P, _P, ctypes.c_size_t, _P]),
 }
 for _name, (_res, _args) in _SIG.items():
     _f = getattr(_lib, _name)
@@ -198,6 +201,28 @@ def layer_decode(handle, x, pos, ctx_lens, max_ctx, attn_mask, B, k_cache, v_cac
                              _ptr(k_cache), _ptr(v_cache), _ptr(y), _ptr(ws), ws_bytes, _stream(stream))
 
 
+def _ptr_array(handles):
+    arr = (ctypes.c_void_p * len(handles))(*[_ptr(h) for h in handles])
+    return arr
+
+
+def stack_workspace_size(handles, stage: int, batch: int, T: int, max_ctx: int) -> int:
+    return _lib.stack_workspace_size(_ptr_array(handles), len(handles), stage, batch, T, max_ctx)
+
+
+def stack_prefill(handles, x, pos, T, hist_len, k_caches, v_caches, y, ws, ws_bytes, stream=None) -> int:
+    return _lib.stack_prefill(_ptr_array(handles), len(handles), _ptr(x), _ptr(pos), T, hist_len,
+                              _ptr_array(k_caches), _ptr_array(v_caches), _ptr(y), _ptr(ws), ws_bytes,
+                              _stream(stream))
+
+
+def stack_decode(handles, x, pos, ctx_lens, max_ctx, attn_mask, B, k_caches, v_caches, y, ws, ws_bytes,
+                 stream=None) -> int:
+    return _lib.stack_decode(_ptr_array(handles), len(handles), _ptr(x), _ptr(pos), _ptr(ctx_lens), max_ctx,
+                             _ptr(attn_mask), B, _ptr_array(k_caches), _ptr_array(v_caches), _ptr(y), _ptr(ws),
+                             ws_bytes, _stream(stream))
+
+
 def kv_append(desc: kv_desc, k_cache, v_cache, k_new, v_new, B, T, slot_start, stream=None) -> int:
     ss = np.ascontiguousarray(np.asarray(slot_start, dtype=np.int32))
     return _lib.kv_append(ctypes.byref(desc), _ptr(k_cache), _ptr(v_cache), _ptr(k_new), _ptr(v_new), B, T,
@@ -308,3 +333,34 @@ class Layer:
         out = torch.empty((K, N), dtype=torch.float32, device="cuda")
         check(layer_debug_dequant(self.handle, which, out))
         return out
+
+
+class Stack:
+    """A list of Layer objects run back to back (stack_prefill / stack_decode),
+    each with its own K and V cache, sharing one workspace."""
+
+    def __init__(self, layers):
+        import torch
+        self.layers = list(layers)
+        self.handles = [l.handle for l in self.layers]
+        self._ws = torch.empty(0, dtype=torch.uint8, device="cuda")
+
+    def workspace(self, stage, batch, T, max_ctx):
+        import torch
+        n = stack_workspace_size(self.handles, stage, batch, T, max_ctx)
+        if n == 0:
+            raise W4Error(W4_EINVAL, "invalid workspace query")
+        if self._ws.numel() < n:
+            self._ws = torch.empty(n, dtype=torch.uint8, device="cuda")
+        return self._ws, self._ws.numel()
+
+    def prefill(self, x, pos, hist_len, k_caches, v_caches, y, stream=None):
+        stage = STAGE_PREFILL_KV if hist_len > 0 else STAGE_PREFILL
+        ws, n = self.workspace(stage, 1, x.shape[0], hist_len)
+        check(stack_prefill(self.handles, x, pos, x.shape[0], hist_len, k_caches, v_caches, y, ws, n, stream))
+
+    def decode(self, x, pos, ctx_lens, max_ctx, k_caches, v_caches, y, attn_mask=None, stream=None):
+        B = x.shape[0]
+        ws, n = self.workspace(STAGE_DECODE, B, 1, max_ctx)
+        check(stack_decode(self.handles, x, pos, ctx_lens, max_ctx, attn_mask, B, k_caches, v_caches, y, ws, n,
+                           stream))

@@ -875,6 +875,77 @@ int layer_debug_dequant(layer_t L, int32_t which, float* out, void* stream) {
     return W4_OK;
 }
 
+// ---------------------------------------------------------------- stacks
+
+// Activations between layers: two fp32 [rows][hidden] buffers after the
+// layers' own workspace (256-byte aligned).
+static size_t stack_act_offset(size_t layer_ws) { return (layer_ws + 255) / 256 * 256; }
+
+static int check_stack(const layer_t* layers, int32_t n) {
+    if (!layers || n < 1) return fail(W4_EINVAL, "null layer list or n_layers < 1");
+    for (int i = 0; i < n; i++) {
+        if (!layers[i]) return fail(W4_EINVAL, "null layer %d", i);
+        if (layers[i]->cfg.hidden != layers[0]->cfg.hidden) return fail(W4_EINVAL, "layer %d: hidden differs", i);
+    }
+    return W4_OK;
+}
+
+size_t stack_workspace_size(const layer_t* layers, int32_t n, int32_t stage, int32_t batch, int32_t T,
+                            int32_t max_ctx) {
+    if (check_stack(layers, n)) return 0;
+    size_t w = 0;
+    for (int i = 0; i < n; i++) {
+        const size_t wi = layer_workspace_size(layers[i], stage, batch, T, max_ctx);
+        if (wi == 0) return 0;
+        w = std::max(w, wi);
+    }
+    const size_t rows = stage == 2 ? (size_t)batch : (size_t)T;
+    return stack_act_offset(w) + 2 * rows * layers[0]->cfg.hidden * sizeof(float);
+}
+
+int stack_prefill(const layer_t* layers, int32_t n, const float* x, const int32_t* pos, int32_t T, int32_t hist_len,
+                  void* const* k_caches, void* const* v_caches, float* y, void* ws, size_t ws_bytes, void* stream) {
+    int rc;
+    if ((rc = check_stack(layers, n))) return rc;
+    if (!x || !y || !ws || !k_caches || !v_caches) return fail(W4_EINVAL, "null pointer argument");
+    if ((const void*)x == (const void*)y) return fail(W4_EINVAL, "x and y must not alias");
+    if (T < 1 || hist_len < 0) return fail(W4_EINVAL, "T must be >= 1 and hist_len >= 0");
+    const size_t need = stack_workspace_size(layers, n, hist_len > 0 ? 1 : 0, 1, T, hist_len);
+    if (need == 0 || ws_bytes < need) return fail(W4_EWORKSPACE, "workspace %zu bytes, need %zu", ws_bytes, need);
+    const size_t act = stack_act_offset(need - 2 * (size_t)T * layers[0]->cfg.hidden * sizeof(float));
+    float* buf[2] = {(float*)((char*)ws + act), (float*)((char*)ws + act) + (size_t)T * layers[0]->cfg.hidden};
+    const float* in = x;
+    for (int i = 0; i < n; i++) {
+        float* out = i == n - 1 ? y : buf[i & 1];
+        if ((rc = run_prefill(layers[i], in, pos, T, hist_len, k_caches[i], v_caches[i], out, ws, act, stream))) return rc;
+        in = out;
+    }
+    return W4_OK;
+}
+
+int stack_decode(const layer_t* layers, int32_t n, const float* x, const int32_t* pos, const int32_t* ctx_lens,
+                 int32_t max_ctx, const float* attn_mask, int32_t B, void* const* k_caches, void* const* v_caches,
+                 float* y, void* ws, size_t ws_bytes, void* stream) {
+    int rc;
+    if ((rc = check_stack(layers, n))) return rc;
+    if (!x || !y || !ws || !k_caches || !v_caches) return fail(W4_EINVAL, "null pointer argument");
+    if ((const void*)x == (const void*)y) return fail(W4_EINVAL, "x and y must not alias");
+    if (B < 1 || max_ctx < 0) return fail(W4_EINVAL, "B must be >= 1 and max_ctx >= 0");
+    const size_t need = stack_workspace_size(layers, n, 2, B, 1, max_ctx);
+    if (need == 0 || ws_bytes < need) return fail(W4_EWORKSPACE, "workspace %zu bytes, need %zu", ws_bytes, need);
+    const size_t act = stack_act_offset(need - 2 * (size_t)B * layers[0]->cfg.hidden * sizeof(float));
+    float* buf[2] = {(float*)((char*)ws + act), (float*)((char*)ws + act) + (size_t)B * layers[0]->cfg.hidden};
+    const float* in = x;
+    for (int i = 0; i < n; i++) {
+        float* out = i == n - 1 ? y : buf[i & 1];
+        if ((rc = layer_decode(layers[i], in, pos, ctx_lens, max_ctx, attn_mask, B, k_caches[i], v_caches[i], out, ws,
+                               act, stream)))
+            return rc;
+        in = out;
+    }
+    return W4_OK;
+}
+
 int layer_decode_phase_times(layer_t L, float* us_out, int32_t* error_flag) {
     if (!L || !us_out) return fail(W4_EINVAL, "null argument");
     std::vector<unsigned long long> ts(kStampWords);

@@ -214,35 +214,38 @@ gemm_w4_kernel(const f16* __restrict__ X, int ldx, DevLinear W, EpiArgs ep, Gemm
                 b[p][0] = dequant8(rw[q][s], zo0, dq);
                 b[p][1] = dequant8(rw[q + 1][s], zo1, dq);
             };
-            // step t starts a group (k a multiple of G past the range start):
-            // the accumulators take the ratio s_prev / s_new (1 elsewhere)
-            auto group_step = [](int t) { return t == 0 || (GT <= 1 && t == 4) || (GT == 0 && (t & 1) == 0 && (t & 3) == 2); };
+            // After step t, if step t + 1 (step 0 of the next iteration for
+            // t = 7) starts a group inside the range, the accumulators take
+            // its ratio s_prev / s_new.  Doing it here, interleaved with the
+            // last MFMAs of the old group, keeps the multiplies off the
+            // boundary between the groups' MFMA streams.
+            auto next_group = [](int t) { return t == 7 || (GT <= 1 && t == 3) || (GT == 0 && (t & 1) == 1); };
             prep(0, 0);
 #pragma unroll
             for (int t = 0; t < 8; t++) {
                 const int p = t & 1;
                 if (t + 1 < 8) prep(t + 1, p ^ 1);
-                if (group_step(t)) {
-                    const int half = t >> 2, q = qb + 2 * half, hh = NH == 2 ? ((t & 3) >> 1) : 0;
-                    const int k = (kb + half) * 64 + (t & 3) * 16;
-                    const bool start = k > kb_lo * 64 && (k & Gm1) == 0;
+#pragma unroll
+                for (int i = 0; i < TM; i++) {
+                    acc[i][0] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a[p][i], b[p][0], acc[i][0], 0, 0, 0);
+                    acc[i][1] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a[p][i], b[p][1], acc[i][1], 0, 0, 0);
+                }
+                if (next_group(t)) {
+                    const int tn = (t + 1) & 7;                       // the next step
+                    const int half = tn >> 2, hh = NH == 2 ? ((tn & 3) >> 1) : 0;
+                    const int q = (t == 7 ? qn : qb) + 2 * half;
+                    const int k = (kb + (t == 7 ? 2 : 0) + half) * 64 + (tn & 3) * 16;
+                    const bool start = k < kb_hi * 64 && (k & Gm1) == 0;
                     const float f0 = start ? rr[q][hh] : 1.0f, f1 = start ? rr[q + 1][hh] : 1.0f;
 #pragma unroll
-                    for (int i = 0; i < TM; i++) {
+                    for (int i = 0; i < TM; i++)
 #pragma unroll
-                        for (int e = 0; e < 16; e++) acc[i][0][e] *= f0;
-                        acc[i][0] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a[p][i], b[p][0], acc[i][0], 0, 0, 0);
-#pragma unroll
-                        for (int e = 0; e < 16; e++) acc[i][1][e] *= f1;
-                        acc[i][1] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a[p][i], b[p][1], acc[i][1], 0, 0, 0);
-                    }
+                        for (int e = 0; e < 16; e++) {
+                            acc[i][0][e] *= f0;
+                            acc[i][1][e] *= f1;
+                        }
                     sched_step<TM, TM == 4 ? 16 : 20>();
                 } else {
-#pragma unroll
-                    for (int i = 0; i < TM; i++) {
-                        acc[i][0] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a[p][i], b[p][0], acc[i][0], 0, 0, 0);
-                        acc[i][1] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a[p][i], b[p][1], acc[i][1], 0, 0, 0);
-                    }
                     sched_step<TM, TM == 4 ? 4 : 6>();
                 }
             }

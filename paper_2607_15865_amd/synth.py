@@ -144,6 +144,23 @@ def make_layer(cfg: LayerConfig, layer: int = 0, with_zeros: bool = False) -> di
     return w
 
 
+def make_layer_words(cfg: LayerConfig, layer: int = 0) -> dict:
+    """All weights of one layer drawn as packed words: each int32 word of a
+    qweight is uniform, so its eight codes are independent and uniform in
+    [0, 15] (the distribution of make_layer, drawn about 8x faster).  Scales
+    and norm weights as make_layer.  For throughput runs over many layers."""
+    w = {}
+    for j, name in enumerate(LINEARS):
+        K, N = cfg.linear_shape(name)
+        ng = -(-K // cfg.group_size)
+        words = rng_for(cfg.cfg_id, layer, TID_QVALS + j).integers(0, 1 << 32, size=(K // 8, N), dtype=np.uint32)
+        s = np.abs(rng_for(cfg.cfg_id, layer, TID_SCALES + j).normal(0.0, 0.02, size=(ng, N))) / 8.0
+        w[name] = dict(K=K, N=N, qweight=words.view(np.int32), scales=s.astype(np.float16), zeros=None)
+    w["attn_norm"] = bf16_bits(rng_for(cfg.cfg_id, layer, TID_GAMMA1).uniform(0.5, 1.5, cfg.hidden))
+    w["mlp_norm"] = bf16_bits(rng_for(cfg.cfg_id, layer, TID_GAMMA2).uniform(0.5, 1.5, cfg.hidden))
+    return w
+
+
 def normal_bf16(cfg_id: int, layer: int, tensor_id: int, shape) -> np.ndarray:
     """bf16 bits of N(0, 1) draws."""
     return bf16_bits(rng_for(cfg_id, layer, tensor_id).standard_normal(size=shape))

@@ -55,6 +55,15 @@ def test_stage_calls_validate_before_any_hip_call():
     assert B.layer_profile_kernel(None, 0, 1) == B.W4_EINVAL
 
 
+def test_stack_calls_validate_before_any_hip_call():
+    assert B.stack_workspace_size([], 2, 1, 1, 8) == 0
+    assert B.stack_workspace_size([None], 0, 1, 16, 0) == 0
+    assert B.stack_prefill([], 1, 1, 4, 0, [], [], 2, 1, 1 << 20, 0) == B.W4_EINVAL
+    assert B.stack_prefill([None, None], 1, 1, 4, 0, [1, 1], [1, 1], 2, 1, 1 << 20, 0) == B.W4_EINVAL
+    assert "null layer" in B.layer_last_error()
+    assert B.stack_decode([], 1, 1, 1, 8, None, 1, [], [], 2, 1, 1 << 20, 0) == B.W4_EINVAL
+
+
 def test_kv_append_validation():
     cfg = synth.CONFIGS["tiny"]
     rc, d = B.kv_layout(cfg, 2)
