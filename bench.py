@@ -30,6 +30,49 @@ sys.path.insert(0, ROOT)
 PEAK_HBM_GBS = 8000.0            # MI355X HBM3E
 PEAK_MFMA_TFLOPS = 2500.0        # dense bf16 / fp16 MFMA
 
+# HBM traffic per launch of the rooflined kernels: FETCH_SIZE and WRITE_SIZE
+# (rocprofv3 --pmc, one pass each, over "bench.py --steps 2 --warmup 1
+# --no-cpu-baseline"), each divided by what the same counter reads per byte
+# for a plain device copy of known size ("bench.py --copy-calibration").
+# Keyed by the SHA-256 of the kernel's source file: once the source changes
+# the figure no longer describes the kernel and is reported as null.
+TRAFFIC = {
+    "prefill_gate_up": {"bytes": 131356219,
+                        "sha256": "02778ffde942a753e736a9e72b8fb5ff072350fba0cc27f744b10b8ac7de7539"},
+    "decode_fused": {"bytes": 134721722,
+                     "sha256": "2a352f22fb5e6e14e0a0691054f1d38a36a84ce1bdb7106e9dd5b5023818221b"},
+}
+CSRC = os.path.join(ROOT, "paper_2607_15865_amd", "csrc")
+
+
+def traffic(key, source):
+    """Measured HBM bytes per launch of a kernel, or None if its source has
+    changed since the counters were taken."""
+    import hashlib
+    t = TRAFFIC.get(key)
+    if not t:
+        return None
+    with open(os.path.join(CSRC, source), "rb") as f:
+        if hashlib.sha256(f.read()).hexdigest() != t["sha256"]:
+            return None
+    return t["bytes"]
+
+
+def copy_calibration():
+    """A plain device-to-device copy of 512 MiB, four times: the reference
+    reading for FETCH_SIZE and WRITE_SIZE (each copy reads and writes
+    exactly 512 MiB)."""
+    import torch
+    n = 512 << 20
+    src = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(4):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes": n, "copies": 4}), flush=True)
+    return 0
+
 WORKLOAD = dict(name="llama8b", prefill_T=512, pkv_T=128, pkv_L=1024, decode_B=1, decode_ctx=2048)
 
 
@@ -87,12 +130,14 @@ def cpu_baseline(cfg, w):
     kc = O.bf16_to_f64(synth.bf16_bits(rng.standard_normal((1, cfg.n_kv_heads, ctx + 1, cfg.head_dim))))
     vc = O.bf16_to_f64(synth.bf16_bits(rng.standard_normal((1, cfg.n_kv_heads, ctx + 1, cfg.head_dim))))
     x = O.bf16_to_f64(synth.activations(cfg, synth.TID_X_DECODE, 1))
-    t0 = time.perf_counter()
-    O.decode(w, cfg, x, [ctx], kc, vc, [ctx])
+    n, t0 = 0, time.perf_counter()
+    while n == 0 or time.perf_counter() - t0 < 10.0:
+        O.decode(w, cfg, x, [ctx], kc, vc, [ctx])
+        n += 1
     dt = time.perf_counter() - t0
-    return {"value": 1.0 / dt, "unit": "layer-steps/s", "cores": threads or os.cpu_count(),
+    return {"value": n / dt, "unit": "layer-steps/s", "cores": threads or os.cpu_count(),
             "kind": "oracle",
-            "sample": f"1 decode layer-step of the {WORKLOAD['name']}-shaped layer at context {ctx}, B=1, "
+            "sample": f"{n} decode layer-steps of the {WORKLOAD['name']}-shaped layer at context {ctx}, B=1, "
                       f"fp64 numpy including the oracle's per-call weight dequantisation ({dt:.1f} s)"}
 
 
@@ -174,12 +219,16 @@ def main():
     ap.add_argument("--stack", action="store_true",
                     help="instead: the 32-layer stack, 1024-token prefill then 256 decode steps")
     ap.add_argument("--stack-layers", type=int, default=32)
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="instead: a plain 512 MiB device copy, the reference kernel for the HBM byte counters")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU: the layer's single-GPU kernels; --gpus {args.gpus} is not supported "
               "(multi-GPU sharding is described in DESIGN.md, not built)", file=sys.stderr)
         sys.exit(2)
 
+    if args.copy_calibration:
+        return copy_calibration()
     if args.stack:
         return run_stack(args)
 
@@ -288,13 +337,16 @@ def main():
                 "bound": "mfma", "achieved": round(gu_flop / (gu_avg * 1e-3) / 1e12, 1),
                 "peak": PEAK_MFMA_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(gu_flop / (gu_avg * 1e-3) / 1e12 / PEAK_MFMA_TFLOPS, 4),
-                "avg_us": round(gu_avg * 1e3, 2), "launches": gu_n, "traffic": None}
+                "avg_us": round(gu_avg * 1e3, 2), "launches": gu_n,
+                "traffic": traffic("prefill_gate_up", "gemm_w4.hip"),
+                "algorithmic_unit": "2 flop per weight per token (512 tokens x 4096 x 28672 weights)"}
     dgu_avg = dgu_ms / max(dgu_n, 1)
     roofline_decode = {"kernel": "persistent decode kernel (whole decode step, B=1, ctx 2048)",
                        "bound": "hbm", "achieved": round(by_d / (dgu_avg * 1e-3) / 1e9, 1),
                        "peak": PEAK_HBM_GBS, "unit": "GB/s",
                        "frac": round(by_d / (dgu_avg * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
-                       "avg_us": round(dgu_avg * 1e3, 2), "launches": dgu_n, "traffic": None}
+                       "avg_us": round(dgu_avg * 1e3, 2), "launches": dgu_n,
+                       "traffic": traffic("decode_fused", "decode_fused.hip")}
     out = {
         "metric": "decode layer-steps/s (+ prefill/prefill_kv TFLOP/s) of a W4A16 Llama-3-8B-shaped layer",
         "value": round(1.0 / dec_s, 1),

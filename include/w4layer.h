@@ -122,9 +122,15 @@ typedef struct kv_desc {
  * upload them and the fp32 cos/sin table (max_seq x head_dim/2, computed in
  * double precision on the host: the table of Sec. 4.6.2) to the current
  * device.  Synchronous.  On success *out owns all device memory of the layer;
- * the handle is immutable afterwards, so stage calls on different streams
- * may share it.  Errors: W4_EINVAL (null), W4_EUNSUPPORTED (shape, or the
- * current device is not gfx950), W4_EHIP (allocation or copy failed). */
+ * no stage call changes it afterwards (scratch state, such as split-K
+ * counters, lives in the caller's workspace), so stage calls on different
+ * streams may share the handle, each with its own workspace.  One exception:
+ * the persistent decode path (layer_set_decode_path) needs every compute
+ * unit of the device at once, so two of its launches must not overlap on one
+ * device; a caller that runs decode on several streams at once selects path
+ * 1.  The diagnostics (profiling, decode stamps) are not for concurrent use.
+ * Errors: W4_EINVAL (null), W4_EUNSUPPORTED (shape, or the current device is
+ * not gfx950), W4_EHIP (allocation or copy failed). */
 int layer_create(const layer_config* cfg, const layer_weights_host* w, layer_t* out);
 
 /* Free the layer's device memory.  The caller must have drained every stream

@@ -5,6 +5,7 @@
 
 #include <algorithm>
 #include <atomic>
+#include <chrono>
 #include <cmath>
 #include <cstdio>
 #include <cstdarg>
@@ -12,6 +13,7 @@
 #include <string>
 #include <thread>
 #include <vector>
+#include <unistd.h>
 
 #include "../../include/w4layer.h"
 #include "common.h"
@@ -161,8 +163,6 @@ struct layer_s {
     DevBuf sync;
     DevBuf fplan;                 // work table of the persistent decode (decode_fused_plan)
     int fplan_blocks = 0, S_qkv = 1, S_o = 1, S_down = 1;
-    // prefill GEMM split-K tile counters (zero between calls) and the CU count
-    DevBuf gemm_cnt;
     int num_cus = 256;
     int* err = nullptr;
     unsigned long long* stamps = nullptr;
@@ -264,7 +264,7 @@ struct Carve {
 constexpr int kGemmCounters = 1024;     // split-K tiles of one GEMM (at most about one per CU)
 
 struct PrefillWs {
-    size_t xn1, q, attn, h, xn2, g, part, total;
+    size_t xn1, q, attn, h, xn2, g, part, cnt, total;
     GemmPlan qkv, o, gu, down;
     AttnPrefillPlan at;
 };
@@ -286,6 +286,7 @@ PrefillWs plan_prefill(const layer_s* L, int T, int hist) {
     w.g = cv.take((size_t)T * L->F_pad * 2);
     // split-K partials of each GEMM and the attention chunk states, used one kernel at a time
     w.part = cv.take(std::max({w.qkv.part_bytes, w.o.part_bytes, w.gu.part_bytes, w.down.part_bytes, w.at.part_bound}));
+    w.cnt = cv.take((size_t)kGemmCounters * 8);   // tagged split-K arrival counters
     w.total = cv.off;
     return w;
 }
@@ -385,10 +386,23 @@ FusedPlan plan_fused(const layer_s* L, int B, int max_ctx, bool query_device) {
     return p;
 }
 
-// Tag of a persistent decode launch: unique for 2^32 - 1 launches in the
-// process, never 0 (a zeroed workspace holds no valid word).
+// Tag of a launch whose blocks hand data to each other through workspace
+// words (the persistent decode, the split-K arrival counters): unique for
+// 2^32 - 1 launches in the process and never 0 (a zeroed workspace holds no
+// valid word).  The sequence starts at a point mixed from the clock and the
+// process id, so a word that another process left in reused device memory
+// matches a current tag only by chance (about 2^-32 per word).
+uint32_t epoch_start() {
+    uint64_t z = (uint64_t)std::chrono::steady_clock::now().time_since_epoch().count() ^
+                 ((uint64_t)getpid() << 32);
+    z += 0x9E3779B97F4A7C15ull;   // splitmix64 finaliser
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+    return (uint32_t)(z ^ (z >> 31));
+}
+
 uint32_t next_epoch() {
-    static std::atomic<uint32_t> ctr{0};
+    static std::atomic<uint32_t> ctr{epoch_start()};
     uint32_t e = ctr.fetch_add(1, std::memory_order_relaxed) + 1;
     if (e == 0) e = ctr.fetch_add(1, std::memory_order_relaxed) + 1;
     return e;
@@ -461,7 +475,7 @@ int run_prefill(layer_s* L, const float* x, const int32_t* pos, int T, int hist,
     f16* xn2 = (f16*)(base + w.xn2);
     f16* g = (f16*)(base + w.g);
     float* part = (float*)(base + w.part);
-    unsigned* cnt = (unsigned*)L->gemm_cnt.p;
+    unsigned long long* cnt = (unsigned long long*)(base + w.cnt);
     const int H = c.hidden, d = c.head_dim, qd = c.n_heads * d;
     for (const GemmPlan* gp : {&w.qkv, &w.o, &w.gu, &w.down})
         if (gp->S > 1 && gp->tiles > kGemmCounters) return fail(W4_EUNSUPPORTED, "split-K tile count above %d", kGemmCounters);
@@ -477,7 +491,7 @@ int run_prefill(layer_s* L, const float* x, const int32_t* pos, int T, int hist,
     e.cache_stride_h = (long long)c.max_seq * d;
     e.pos = pos;
     e.slot_base = hist;
-    { ProfScope ps(L, stage, 1, st); rc |= launch_gemm_w4(EPI_QKV, xn1, H, L->qkv.d, e, w.qkv, T, part, cnt, st); }
+    { ProfScope ps(L, stage, 1, st); rc |= launch_gemm_w4(EPI_QKV, xn1, H, L->qkv.d, e, w.qkv, T, part, cnt, next_epoch(), st); }
     AttnPrefillArgs aa{};
     aa.q = q;
     aa.k_cache = (const uint16_t*)kc;
@@ -495,15 +509,15 @@ int run_prefill(layer_s* L, const float* x, const int32_t* pos, int T, int hist,
     EpiArgs eo = base_epi(L);
     eo.resid = x;
     eo.out_f32 = h;
-    { ProfScope ps(L, stage, 3, st); rc |= launch_gemm_w4(EPI_RESID, attn, qd, L->o.d, eo, w.o, T, part, cnt, st); }
+    { ProfScope ps(L, stage, 3, st); rc |= launch_gemm_w4(EPI_RESID, attn, qd, L->o.d, eo, w.o, T, part, cnt, next_epoch(), st); }
     { ProfScope ps(L, stage, 4, st); rc |= launch_rmsnorm(h, (const uint16_t*)L->mlp_norm.p, c.rms_eps, T, H, xn2, st); }
     EpiArgs eg = base_epi(L);
     eg.act_out = g;
-    { ProfScope ps(L, stage, 5, st); rc |= launch_gemm_w4(EPI_SWIGLU, xn2, H, L->gu.d, eg, w.gu, T, part, cnt, st); }
+    { ProfScope ps(L, stage, 5, st); rc |= launch_gemm_w4(EPI_SWIGLU, xn2, H, L->gu.d, eg, w.gu, T, part, cnt, next_epoch(), st); }
     EpiArgs ed = base_epi(L);
     ed.resid = h;
     ed.out_f32 = y;
-    { ProfScope ps(L, stage, 6, st); rc |= launch_gemm_w4(EPI_RESID, g, L->F_pad, L->down.d, ed, w.down, T, part, cnt, st); }
+    { ProfScope ps(L, stage, 6, st); rc |= launch_gemm_w4(EPI_RESID, g, L->F_pad, L->down.d, ed, w.down, T, part, cnt, next_epoch(), st); }
     if (rc) return fail(W4_EHIP, "kernel launch failed: %s", hipGetErrorString(hipGetLastError()));
     return W4_OK;
 }
@@ -628,10 +642,6 @@ int layer_create(const layer_config* cfg, const layer_weights_host* w, layer_t* 
         if ((rc = upload(L->sync, zero.data(), bytes))) { delete L; return rc; }
         L->err = (int*)L->sync.p;
         L->stamps = (unsigned long long*)((char*)L->sync.p + 64);
-    }
-    {
-        std::vector<unsigned> zero(kGemmCounters, 0u);
-        if ((rc = upload(L->gemm_cnt, zero.data(), zero.size() * 4))) { delete L; return rc; }
     }
     // work table of the persistent decode: one block per CU; a product with
     // fewer column tiles than blocks is also cut along k (at most 2 parts)

@@ -38,7 +38,10 @@
 // Split K: with S > 1 the k tiles are cut into S ranges, one block each.
 // Every block stores its fp32 partial tile, and the last block of a tile to
 // arrive (a per-tile counter) adds the S partials in range order and runs
-// the epilogue, so the result does not depend on the arrival order.
+// the epilogue, so the result does not depend on the arrival order.  The
+// counters live in the caller's workspace and need no clearing: each is a
+// 64-bit word (launch tag << 32 | arrivals), and an arrival that finds
+// another launch's tag starts the count afresh.
 //
 // Block order: the blocks of one column block (its row blocks and k ranges)
 // are placed on the same XCD (consecutive block ids go round robin over the
@@ -54,7 +57,8 @@ constexpr int NXCD = 8;
 struct GemmShape {
     int M, nrb, ncb, S, KB;
     float* part;                 // [S][M][N_dev] (S > 1)
-    unsigned* cnt;               // [nrb * ncb] (S > 1), zero between calls
+    unsigned long long* cnt;     // [nrb * ncb] tagged arrival counters (S > 1)
+    unsigned tag;                // this launch's tag, unique among launches that share cnt
 };
 
 // Instruction order of one k16 step for the scheduler: every MFMA is
@@ -319,10 +323,13 @@ gemm_w4_kernel(const f16* __restrict__ X, int ldx, DevLinear W, EpiArgs ep, Gemm
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // this thread's partial stores are complete
     __syncthreads();
     if (tid == 0) {
-        unsigned* cnt = gs.cnt + rb * gs.ncb + cb;
-        const unsigned old = __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        last_flag = (old + 1 == (unsigned)gs.S);
-        if (last_flag) __hip_atomic_store(cnt, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);   // ready for the next call
+        unsigned long long* cnt = gs.cnt + rb * gs.ncb + cb;
+        unsigned long long v = __hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT), nv;
+        do {
+            nv = (unsigned)(v >> 32) == gs.tag ? v + 1 : ((unsigned long long)gs.tag << 32 | 1u);
+        } while (!__hip_atomic_compare_exchange_weak(cnt, &v, nv, __ATOMIC_RELAXED, __ATOMIC_RELAXED,
+                                                     __HIP_MEMORY_SCOPE_AGENT));
+        last_flag = ((unsigned)nv == (unsigned)gs.S);
     }
     __syncthreads();
     if (!last_flag || !wave_on) return;
@@ -414,9 +421,9 @@ GemmPlan gemm_w4_plan(int M, const DevLinear& W, int num_cus) {
 }
 
 int launch_gemm_w4(int epi, const f16* X, int ldx, const DevLinear& W, const EpiArgs& ep, const GemmPlan& p,
-                   int M, float* part, unsigned* cnt, hipStream_t stream) {
+                   int M, float* part, unsigned long long* cnt, unsigned tag, hipStream_t stream) {
     if (p.S > 1 && (!part || !cnt)) return -1;
-    GemmShape gs{M, p.nrb, p.ncb, p.S, W.K_pad / 64, part, cnt};
+    GemmShape gs{M, p.nrb, p.ncb, p.S, W.K_pad / 64, part, cnt, tag};
     switch (epi) {
         case EPI_QKV: return launch_epi<EPI_QKV>(p.TM, X, ldx, W, ep, gs, stream);
         case EPI_RESID: return launch_epi<EPI_RESID>(p.TM, X, ldx, W, ep, gs, stream);

@@ -48,10 +48,12 @@ struct GemmPlan {
     size_t part_bytes = 0;        // fp32 partial sums (S > 1)
 };
 GemmPlan gemm_w4_plan(int M, const DevLinear& W, int num_cus);
-// part: plan.part_bytes of workspace; cnt: plan.tiles counters, zero between
-// calls (the kernel leaves them zero).  Both unused when plan.S == 1.
+// part: plan.part_bytes of workspace; cnt: plan.tiles 64-bit arrival
+// counters in any state; tag: non-zero, different from the tag of every
+// earlier launch that used the same counters.  part and cnt are unused when
+// plan.S == 1.
 int launch_gemm_w4(int epi, const f16* X, int ldx, const DevLinear& W, const EpiArgs& ep, const GemmPlan& plan,
-                   int M, float* part, unsigned* cnt, hipStream_t stream);
+                   int M, float* part, unsigned long long* cnt, unsigned tag, hipStream_t stream);
 
 struct GemvArgs {
     DevLinear W;
