@@ -319,7 +319,7 @@ DecodeWs plan_decode(const layer_s* L, int B, int max_ctx) {
 struct FusedPlan {
     bool ok = false;
     int nblocks = 0, chunk = 0, nchunk = 0, S_qkv = 1, S_o = 1, S_down = 1, ldx = 0, comb_per = 0, comb_lpv = 1;
-    size_t off_h = 0, off_red = 0, off_gam = 0, lds_bytes = 0;
+    size_t off_h = 0, off_red = 0, off_gam = 0, off_zero = 0, off_c64 = 0, lds_bytes = 0;
     size_t qkv_part, apart, A, o_part, g, down_part, total;
 };
 
@@ -368,7 +368,12 @@ FusedPlan plan_fused(const layer_s* L, int B, int max_ctx, bool query_device) {
     while (p.comb_lpv < p.nchunk && p.comb_lpv < 64) p.comb_lpv *= 2;
     if (p.nchunk > 4 * p.comb_lpv) return p;
     const size_t comb_bytes = (size_t)p.comb_per * 2;
-    p.off_h = align256(std::max(std::max(xs_bytes, attn_bytes), comb_bytes));
+    // activation rows, then the GEMV's zero operand and correction table; the
+    // attention phase reuses this region
+    p.off_zero = align256(xs_bytes);
+    p.off_c64 = p.off_zero + 256;
+    const size_t gemv_bytes = p.off_c64 + (size_t)((p.ldx - 8) / 64) * 8 * 4;
+    p.off_h = align256(std::max(std::max(gemv_bytes, attn_bytes), comb_bytes));
     p.off_red = align256(p.off_h + (size_t)B * H * 4);
     p.off_gam = align256(p.off_red + (size_t)(NWAVE * SLOTS * maxb * 32 + 8 + NWAVE * maxb + maxb * 32 + 2 * maxb) * 4);
     p.lds_bytes = p.off_gam + (size_t)2 * H * 2;
@@ -751,6 +756,8 @@ int layer_decode(layer_t L, const float* x, const int32_t* pos, const int32_t* c
         a.off_h = fp.off_h;
         a.off_red = fp.off_red;
         a.off_gam = fp.off_gam;
+        a.off_zero = fp.off_zero;
+        a.off_c64 = fp.off_c64;
         a.lds_bytes = fp.lds_bytes;
         int rc;
         { ProfScope ps(L, 2, 6, st); rc = launch_decode_fused(a, st); }

@@ -38,6 +38,8 @@ struct DecodeFusedArgs {
     int nblocks;
     int ldx;                   // fp16 elements per activation row in LDS
     size_t off_h, off_red, off_gam;  // LDS offsets (bytes)
+    size_t off_zero, off_c64;  // LDS: 64 zero fp16; GEMV correction table [ldx / 64][8] fp32
+                               // (inside the region the attention phase reuses)
     size_t lds_bytes;          // dynamic LDS per block
 };
 

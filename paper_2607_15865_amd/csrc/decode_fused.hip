@@ -192,6 +192,8 @@ __global__ void __launch_bounds__(NTHR) decode_fused_kernel(DecodeFusedArgs a) {
     float* own = red8 + 8 + NWAVE * MAXB;                         // [MAXB][32]
     int* meta = reinterpret_cast<int*>(own + MAXB * 32);          // ctx_lens[B], pos[B]
     uint16_t* gam = reinterpret_cast<uint16_t*>(smem + a.off_gam);           // RMSNorm weights [2][H]
+    f16* zero64 = reinterpret_cast<f16*>(smem + a.off_zero);                  // 64 zeros (GEMV phases)
+    float* c64 = reinterpret_cast<float*>(smem + a.off_c64);                  // GEMV corrections
 
     if (a.stamps && blk == 0 && tid == 0) {
         a.stamps[0] = wall_clock64();
@@ -203,17 +205,24 @@ __global__ void __launch_bounds__(NTHR) decode_fused_kernel(DecodeFusedArgs a) {
     };
     stamp_done(5);
 
-    // ---- this block's work (host plan): column tiles and k ranges per product,
-    // read (scalar loads) where they are needed
-    const int* pl = a.plan + blk * 16;
+    // ---- this block's work (host plan): column tiles and k ranges per product.
+    // The row is read once, through the scalar cache (the table is read-only):
+    // a vector load here would wait behind the weight prefetches in flight.
+    int pl[16];
+    {
+        const __attribute__((address_space(4))) int* row =
+            (const __attribute__((address_space(4))) int*)(a.plan + blk * 16);
+#pragma unroll
+        for (int i = 0; i < 16; i++) pl[i] = row[i];
+    }
     const int Nq = a.qkv.N_dev;
     // this wave's run of product ph (1 q/k/v, 3 o_proj, 4 gate/up, 5 down)
     auto wave_run = [&](int ph) {
         int t0, tz, ka, kz;
         if (ph == 4) { t0 = pl[8]; tz = pl[9]; ka = 0; kz = a.gu.K_pad / 64; }
         else {
-            const int* e = pl + (ph == 1 ? 0 : ph == 3 ? 4 : 10);
-            t0 = e[0]; tz = t0 + 1; ka = e[1]; kz = e[2];
+            const int e = ph == 1 ? 0 : ph == 3 ? 4 : 10;
+            t0 = pl[e]; tz = t0 + 1; ka = pl[e + 1]; kz = pl[e + 2];
         }
         return Run{t0, tz, ka + wave * (kz - ka) / NWAVE, ka + (wave + 1) * (kz - ka) / NWAVE};
     };
@@ -277,6 +286,7 @@ __global__ void __launch_bounds__(NTHR) decode_fused_kernel(DecodeFusedArgs a) {
             *reinterpret_cast<u32x4*>(gam + H + tid * 8) = g2;
         }
         if (tid < MAXB + B) meta[tid] = m0;
+        if (tid < 8) reinterpret_cast<u32x4*>(zero64)[tid] = u32x4{0u, 0u, 0u, 0u};
         for (int i = i1 + NTHR * 4; i < B * H; i += NTHR * 4)      // rows past 2 * NTHR * 4 floats
             *reinterpret_cast<float4*>(hbuf + i) = *reinterpret_cast<const float4*>(a.x + i);
         for (int i = tid * 8 + NTHR * 8; i < H; i += NTHR * 8) {
@@ -292,10 +302,12 @@ __global__ void __launch_bounds__(NTHR) decode_fused_kernel(DecodeFusedArgs a) {
         const int t1 = pl[0], s1 = pl[3];
         const Run run1 = wave_run(1);
         norm_rows(hbuf, gam, a.eps, B, H, xs, ldx, red8);
+        gemv_prep(xs, ldx, c64, nullptr, B, 0, H, tid, NTHR);
         stamp_done(6);
         clear_red();
+        const GemvAct xa{xs, ldx, c64, nullptr, zero64};
         if (run1.ka < run1.kz)
-            gemv_run<RING_QKV, false, false>(a.qkv, run1, xs, ldx, B, R1, q1, [&](int, const float (&out)[4]) { to_red(0, out); });
+            gemv_run<RING_QKV, false, false>(a.qkv, run1, xa, B, R1, q1, [&](int, const float (&out)[4]) { to_red(0, out); });
         prefetch(3);
         stamp_done(7);
         __syncthreads();
@@ -556,10 +568,13 @@ __global__ void __launch_bounds__(NTHR) decode_fused_kernel(DecodeFusedArgs a) {
         }
         stamp_done(11);
         clear_red();
+        if (tid < 8) reinterpret_cast<u32x4*>(zero64)[tid] = u32x4{0u, 0u, 0u, 0u};   // (attention reused it)
+        gemv_prep(xs - klo, ldx, c64 - ka3 * GEMV_ROWS, nullptr, B, klo, 2 * kh, tid, NTHR);
         __syncthreads();
         stamp_done(19);
+        const GemvAct xa{xs - klo, ldx, c64 - ka3 * GEMV_ROWS, nullptr, zero64};
         if (run3.ka < run3.kz)
-            gemv_run<RING_O, false, false>(a.o, run3, xs - klo, ldx, B, R3, q3, [&](int, const float (&out)[4]) { to_red(0, out); });
+            gemv_run<RING_O, false, false>(a.o, run3, xa, B, R3, q3, [&](int, const float (&out)[4]) { to_red(0, out); });
         prefetch(4);
         stamp_done(20);
         __syncthreads();
@@ -581,10 +596,13 @@ __global__ void __launch_bounds__(NTHR) decode_fused_kernel(DecodeFusedArgs a) {
         const int ta4 = pl[8], tb4 = pl[9];
         const Run run4 = wave_run(4);
         norm_rows(hbuf, gam + H, a.eps, B, H, xs, ldx, red8);
+        if (tid < 8) reinterpret_cast<u32x4*>(zero64)[tid] = u32x4{0u, 0u, 0u, 0u};   // (attention reused it)
+        gemv_prep(xs, ldx, c64, nullptr, B, 0, H, tid, NTHR);
         stamp_done(22);
         clear_red();
+        const GemvAct xa{xs, ldx, c64, nullptr, zero64};
         if (run4.ka < run4.kz)
-            gemv_run<RING, false, false>(a.gu, run4, xs, ldx, B, R4, q4,
+            gemv_run<RING, false, false>(a.gu, run4, xa, B, R4, q4,
                                          [&](int t, const float (&out)[4]) { to_red(t - ta4, out); });
         prefetch(5);
         stamp_done(13);
@@ -615,9 +633,12 @@ __global__ void __launch_bounds__(NTHR) decode_fused_kernel(DecodeFusedArgs a) {
         }
         stamp_done(14);
         clear_red();
+        if (tid < 8) reinterpret_cast<u32x4*>(zero64)[tid] = u32x4{0u, 0u, 0u, 0u};   // (attention reused it)
+        gemv_prep(xs - klo, ldx, c64 - ka5 * GEMV_ROWS, nullptr, B, klo, 2 * kh, tid, NTHR);
         __syncthreads();
+        const GemvAct xa{xs - klo, ldx, c64 - ka5 * GEMV_ROWS, nullptr, zero64};
         if (run5.ka < run5.kz)
-            gemv_run<RING, false, false>(a.down, run5, xs - klo, ldx, B, R5, q5, [&](int, const float (&out)[4]) { to_red(0, out); });
+            gemv_run<RING, false, false>(a.down, run5, xa, B, R5, q5, [&](int, const float (&out)[4]) { to_red(0, out); });
         stamp_done(15);
         __syncthreads();
         if (s5 > 0) {

@@ -4,25 +4,110 @@
 // A run is the set of tiles (t, kb) with column tile t in [t0, t1) and k-tile
 // kb in [ka, kz), walked column by column.  The wave streams the tiles
 // through a ring of D register slots: a slot is refilled as soon as its
-// tile has been dequantised, so D tiles (D KB per wave) stay in flight.  All
+// tile has been consumed, so D tiles (D KB per wave) stay in flight.  All
 // run bookkeeping is wave-uniform (scalar registers) and kept as byte and
 // element offsets that are advanced, not recomputed, per tile.
 //
-// Arithmetic per tile: the four weight words of a lane are turned into exact
-// fp16 (code - zero) values (dequant8) and multiplied on the 32x32x16 fp16
-// MFMA with the activation rows (bf16 values held as fp16, read from LDS):
-// A = activations (row l % 32 of lane l, clamped to the last real row),
-// B = weights (the tile's lane layout is the MFMA B fragment).  Rows 0..7 of
-// the product sit in accumulator registers 0..3 (row 4h + r in lane half h);
-// the other registers carry rows nobody reads.  Each tile's product (each
-// half tile with groups of 32) starts from zero, is multiplied by its group
-// scale in fp32 and added to the output.
+// Arithmetic per tile.  The four weight words of a lane are not brought to
+// (code - zero): each code pair becomes the fp16 pair it makes when OR-ed
+// into 0x6400 (dequant8_raw, five bit operations per word), which is
+// 1024 + q for the codes in bits 0..3 of a byte and 1024 + 16 q for the codes
+// in bits 4..7.  The activations are prepared to match (gemv_prep): the
+// elements at k % 8 in {2, 3, 6, 7} (the bits 4..7 codes) are divided by 16,
+// and per row and 32-k segment the sums E (other elements) and O (divided
+// elements) are kept.  The product over a segment is then
+//     sum x'(raw) = sum x (q - z) + 1024 (E + O) + z (E + 16 O),
+// so one subtraction per output recovers the exact-weight sum.
+//
+// The product runs on the 16x16x32 fp16 MFMA with the 32-column tile as is:
+// lane l of the B operand is the lane's word s (column 32 t + l % 32,
+// k = 16 s + 8 (l / 32) + 0..7), which the MFMA takes as k block l / 16 and
+// column l % 16.  The column's high bit (l / 16) % 2 thus sits in the k
+// block, and the A operand separates it again: MFMA row m stands for batch
+// row b = 4 (m / 8) + m % 4 and column half c = (m / 4) % 2, and lane l
+// supplies x'[b] only where c equals its own column half (zeros elsewhere).
+// Output register r of lane l is then batch row 4 (l / 32) + r, column
+// 32 t + l % 32: the lane's own column, so the lane's own group scale
+// applies.  Four 16-cycle MFMAs per tile instead of four 32-cycle ones.
 //
 // Group parameters: the raw fp16 scale bits (or scale | zero << 16 when the
 // linear has zero points, ZP) of the group of k 0..31 of a tile, and with
 // groups of 32 (G32) also of k 32..63, travel with the tile in the ring.
 #pragma once
 #include "common.h"
+
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+// fp16 pairs (1024 + q) / (1024 + 16 q) of the eight codes of a word, in k
+// order (pairs at bits 4p and 16 + 4p): five bit operations.
+__device__ __forceinline__ f16x8 dequant8_raw(uint32_t w, const DqConst& k) {
+    const uint32_t w8 = w >> 8;
+    u32x4 r;
+    r[0] = (w & k.lo) | k.magic;
+    r[1] = (w & k.hi) | k.magic;
+    r[2] = (w8 & k.lo) | k.magic;
+    r[3] = (w8 & k.hi) | k.magic;
+    return __builtin_bit_cast(f16x8, r);
+}
+
+constexpr int GEMV_ROWS = 8;     // row stride of the correction tables
+
+// Activation rows prepared by gemv_prep, all indexed by the absolute k of the
+// linear (the pointers are offset by the first k of the range held):
+//   xs[b * ldx + k]                       x' (fp16), rows b < B;
+//   c64[(k / 64) * GEMV_ROWS + b]         1024 (E + O) + 8 (E + 16 O) over the
+//                                         64-k tile (the correction for z = 8);
+//   uv32[(k / 32) * GEMV_ROWS + b]        (E + O, E + 16 O) over the 32-k
+//                                         segment (any zero point); may be
+//                                         null when only z = 8 with groups of
+//                                         64 or more is used;
+//   zero                                  64 zero fp16 (the A operand of the
+//                                         lanes whose column half does not
+//                                         match).
+struct GemvAct {
+    const f16* xs;
+    int ldx;
+    const float* c64;
+    const float2* uv32;
+    const f16* zero;
+};
+
+// Prepare rows b < B, absolute k in [k0, k0 + klen) (klen a multiple of 64)
+// in place: x (bf16 values held as fp16) -> x', and write the correction
+// tables (pointers as in GemvAct, non-const).  Called by all nthr threads of
+// the block; the caller synchronises before and after.
+__device__ __forceinline__ void gemv_prep(f16* xs, int ldx, float* c64, float2* uv32, int B, int k0, int klen,
+                                          int tid, int nthr) {
+    const int nt = klen >> 6;
+    const f16x2 sixteenth = f16x2{(f16)0.0625f, (f16)0.0625f};
+    for (int i = tid; i < B * nt; i += nthr) {
+        const int b = i / nt, t = i - b * nt;
+        const int k = k0 + 64 * t;
+        u32x4* p = reinterpret_cast<u32x4*>(xs + b * ldx + k);
+        float E[2] = {0.f, 0.f}, O[2] = {0.f, 0.f};
+#pragma unroll
+        for (int v = 0; v < 8; v++) {          // 8 elements per 16 bytes: k % 8 = 0..7
+            const u32x4 w = p[v];
+            // element pairs (0,1) (2,3) (4,5) (6,7); the words are taken into
+            // scalars first (see as_bf16x2)
+            const uint32_t w0 = w[0], w1 = w[1], w2 = w[2], w3 = w[3];
+            const f16x2 x0 = __builtin_bit_cast(f16x2, w0), x2 = __builtin_bit_cast(f16x2, w2);
+            const f16x2 x1 = __builtin_bit_cast(f16x2, w1) * sixteenth;
+            const f16x2 x3 = __builtin_bit_cast(f16x2, w3) * sixteenth;
+            E[v >> 2] += ((float)x0[0] + (float)x0[1]) + ((float)x2[0] + (float)x2[1]);
+            O[v >> 2] += ((float)x1[0] + (float)x1[1]) + ((float)x3[0] + (float)x3[1]);
+            p[v] = u32x4{w0, __builtin_bit_cast(uint32_t, x1), w2, __builtin_bit_cast(uint32_t, x3)};
+        }
+        const int kb = k >> 6;
+        c64[kb * GEMV_ROWS + b] = 1024.0f * ((E[0] + O[0]) + (E[1] + O[1])) +
+                                  8.0f * ((E[0] + 16.0f * O[0]) + (E[1] + 16.0f * O[1]));
+        if (uv32) {
+#pragma unroll
+            for (int hh = 0; hh < 2; hh++)
+                uv32[(2 * kb + hh) * GEMV_ROWS + b] = float2{E[hh] + O[hh], E[hh] + 16.0f * O[hh]};
+        }
+    }
+}
 
 template <int D, bool G32>
 struct TileRing {
@@ -101,59 +186,85 @@ __device__ __forceinline__ void ring_prefetch(const DevLinear& W, const Run& run
     }
 }
 
-template <bool ZP>
-__device__ __forceinline__ float take_gparam(uint32_t v, ZeroOff& zo) {
-    if (ZP) zo = zero_off((float)((v >> 16) & 0xFFu));
+// Group scale (fp16 bits in the low half) and zero point of a group word.
+__device__ __forceinline__ float gscale(uint32_t v) {
     return (float)__builtin_bit_cast(f16, (uint16_t)(v & 0xFFFFu));
+}
+template <bool ZP>
+__device__ __forceinline__ float gzero(uint32_t v) {
+    return ZP ? (float)((v >> 16) & 0xFFu) : 8.0f;
 }
 
 // Walk a run whose first D tiles are in R (ring_prefetch, which also set the
-// load cursor q).  xs: activation rows in LDS, row b at xs + b * ldx, indexed
-// by the absolute k of the linear.  For every column tile t of the run,
-// emit(t, out) is called once (wave-uniformly) with out[r] = the run's
-// partial sum over its k-tiles for row 4 * (lane / 32) + r and column
-// 32 t + lane % 32.
+// load cursor q), on activation rows prepared by gemv_prep.  For every column
+// tile t of the run, emit(t, out) is called once (wave-uniformly) with
+// out[r] = the run's partial sum over its k-tiles for row 4 * (lane / 32) + r
+// and column 32 t + lane % 32 (rows >= B hold no meaningful value).
 //
 // The walk is rounded up to a multiple of D tiles; the steps past the end do
 // no arithmetic, but every step refills its slot (past the end with the
 // run's first tile) so that no load sits under a branch.
 template <int D, bool ZP, bool G32, typename Emit>
-__device__ __forceinline__ void gemv_run(const DevLinear& W, const Run& run, const f16* xs, int ldx, int B,
+__device__ __forceinline__ void gemv_run(const DevLinear& W, const Run& run, const GemvAct& xa, int B,
                                          TileRing<D, G32>& R, RunCursor& q, Emit&& emit) {
-    const int lane = threadIdx.x & 63, h = lane >> 5, c = lane & 31;
+    const int lane = threadIdx.x & 63, h = lane >> 5;
     const DqConst dq = dq_const();
-    const int row = c < B ? c : B - 1;
-    const f16* xrow = xs + row * ldx + h * 8;
+    // A operand of this lane: MFMA row m = lane % 16 (batch row bm, column
+    // half cm), k block lane / 16 (column half c1, k half h)
+    const int m = lane & 15, cm = (m >> 2) & 1, bm = 4 * (m >> 3) + (m & 3), c1 = (lane >> 4) & 1;
+    const bool valid = cm == c1 && bm < B;
+    const f16* abase = valid ? xa.xs + bm * xa.ldx + 8 * h : xa.zero + 8 * h;
+    const int astride = valid ? 64 : 0;
     const int n = run.size();
     RunCursor first;
     first.start(W, run);
     int pt = run.t0, pkb = run.ka;                        // tile being processed
     float out[4] = {0.f, 0.f, 0.f, 0.f};
-    const f32x16 zero = {};
+    const f32x4_t zero = {0.f, 0.f, 0.f, 0.f};
     for (int base = 0; base < n; base += D) {
 #pragma unroll
         for (int u = 0; u < D; u++) {
             if (base + u < n) {                           // wave-uniform
-                ZeroOff zo = zero_off(8.0f), zo_hi = zo;
-                const float sa = take_gparam<ZP>(R.sa[u], zo);
-                float sb = sa;
-                if (G32) sb = take_gparam<ZP>(R.sb[G32 ? u : 0], zo_hi);
-                else zo_hi = zo;
-                const f16x8 b0 = dequant8(R.w[u][0], zo, dq), b1 = dequant8(R.w[u][1], zo, dq);
-                const f16x8 b2 = dequant8(R.w[u][2], zo_hi, dq), b3 = dequant8(R.w[u][3], zo_hi, dq);
-                const f16* xk = xrow + pkb * 64;
-                f32x16 acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(*reinterpret_cast<const f16x8*>(xk), b0, zero, 0, 0, 0);
-                acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(*reinterpret_cast<const f16x8*>(xk + 16), b1, acc, 0, 0, 0);
+                const f16* xk = abase + pkb * astride;
+                const f16x8 a0 = *reinterpret_cast<const f16x8*>(xk);
+                const f16x8 a1 = *reinterpret_cast<const f16x8*>(xk + 16);
+                const f16x8 a2 = *reinterpret_cast<const f16x8*>(xk + 32);
+                const f16x8 a3 = *reinterpret_cast<const f16x8*>(xk + 48);
+                const float sa = gscale(R.sa[u]);
+                f32x4_t acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a0, dequant8_raw(R.w[u][0], dq), zero, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a1, dequant8_raw(R.w[u][1], dq), acc, 0, 0, 0);
                 if (G32) {
+                    // k 0..31 and k 32..63 are two groups
+                    const float za = gzero<ZP>(R.sa[u]);
+                    const float sb = gscale(R.sb[G32 ? u : 0]), zb = gzero<ZP>(R.sb[G32 ? u : 0]);
+                    const float2* uv = xa.uv32 + (2 * pkb) * GEMV_ROWS + 4 * h;
 #pragma unroll
-                    for (int r = 0; r < 4; r++) out[r] = __builtin_fmaf(sa, acc[r], out[r]);
-                    acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(*reinterpret_cast<const f16x8*>(xk + 32), b2, zero, 0, 0, 0);
+                    for (int r = 0; r < 4; r++)
+                        out[r] = __builtin_fmaf(sa, acc[r] - __builtin_fmaf(za, uv[r].y, 1024.0f * uv[r].x), out[r]);
+                    acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a2, dequant8_raw(R.w[u][2], dq), zero, 0, 0, 0);
+                    acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a3, dequant8_raw(R.w[u][3], dq), acc, 0, 0, 0);
+                    const float2* uw = uv + GEMV_ROWS;
+#pragma unroll
+                    for (int r = 0; r < 4; r++)
+                        out[r] = __builtin_fmaf(sb, acc[r] - __builtin_fmaf(zb, uw[r].y, 1024.0f * uw[r].x), out[r]);
                 } else {
-                    acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(*reinterpret_cast<const f16x8*>(xk + 32), b2, acc, 0, 0, 0);
-                }
-                acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(*reinterpret_cast<const f16x8*>(xk + 48), b3, acc, 0, 0, 0);
+                    acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a2, dequant8_raw(R.w[u][2], dq), acc, 0, 0, 0);
+                    acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a3, dequant8_raw(R.w[u][3], dq), acc, 0, 0, 0);
+                    if (ZP) {
+                        const float za = gzero<ZP>(R.sa[u]);
+                        const float2* uv = xa.uv32 + (2 * pkb) * GEMV_ROWS + 4 * h;
+                        const float2* uw = uv + GEMV_ROWS;
 #pragma unroll
-                for (int r = 0; r < 4; r++) out[r] = __builtin_fmaf(sb, acc[r], out[r]);
+                        for (int r = 0; r < 4; r++) {
+                            const float cr = __builtin_fmaf(za, uv[r].y + uw[r].y, 1024.0f * (uv[r].x + uw[r].x));
+                            out[r] = __builtin_fmaf(sa, acc[r] - cr, out[r]);
+                        }
+                    } else {
+                        const f32x4_t cc = *reinterpret_cast<const f32x4_t*>(xa.c64 + pkb * GEMV_ROWS + 4 * h);
+#pragma unroll
+                        for (int r = 0; r < 4; r++) out[r] = __builtin_fmaf(sa, acc[r] - cc[r], out[r]);
+                    }
+                }
                 if (pkb == run.kz - 1) {
                     emit(pt, out);
 #pragma unroll

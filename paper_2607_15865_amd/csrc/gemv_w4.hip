@@ -35,14 +35,17 @@ __global__ void __launch_bounds__(NW * 64) gemv_w4_kernel(GemvArgs a) {
     const int klo = kb_lo * 64, klen = (kb_hi - kb_lo) * 64;
     const int ldx = klen + 8;
     const int B = a.B;
+    const int nkb = kb_hi - kb_lo;
     f16* xs = reinterpret_cast<f16*>(smem);                                   // [B][ldx]
-    float* red = reinterpret_cast<float*>(smem + (size_t)MAXB * ldx * 2);     // [NW][2][MAXB][32]
+    f16* zero = xs + MAXB * ldx;                                              // [64]
+    float* c64 = reinterpret_cast<float*>(zero + 64);                         // [nkb][GEMV_ROWS]
+    float2* uv32 = reinterpret_cast<float2*>(c64 + nkb * GEMV_ROWS);          // [2 nkb][GEMV_ROWS]
+    float* red = reinterpret_cast<float*>(uv32 + 2 * nkb * GEMV_ROWS);        // [NW][2][MAXB][32]
     float* rinv = red + NW * 2 * MAXB * 32;                                   // [MAXB]
     float* tot = rinv + MAXB;                                                 // [MAXB][64]
 
     // this wave's k-tiles of both column tiles
-    const int nk = kb_hi - kb_lo;
-    const Run run{pair * 2, pair * 2 + 2, kb_lo + wave * nk / NW, kb_lo + (wave + 1) * nk / NW};
+    const Run run{pair * 2, pair * 2 + 2, kb_lo + wave * nkb / NW, kb_lo + (wave + 1) * nkb / NW};
     TileRing<RING, G32> R;
     RunCursor q;
     if (run.ka < run.kz) ring_prefetch<RING, ZP, G32>(W, run, R, q);
@@ -81,12 +84,17 @@ __global__ void __launch_bounds__(NW * 64) gemv_w4_kernel(GemvArgs a) {
                 *reinterpret_cast<const u32x4*>(a.x_f16 + (size_t)b * a.ldx + klo + v * 8);
         }
     }
+    if (tid < 8) reinterpret_cast<u32x4*>(zero)[tid] = u32x4{0u, 0u, 0u, 0u};
+    __syncthreads();
+    gemv_prep(xs - klo, ldx, c64 - kb_lo * GEMV_ROWS, (ZP || G32) ? uv32 - 2 * kb_lo * GEMV_ROWS : nullptr, B, klo,
+              klen, tid, NW * 64);
     __syncthreads();
 
     // ---- main loop: partial sums of this wave into red[wave]
     const int h = lane >> 5, c = lane & 31;
+    const GemvAct xa{xs - klo, ldx, c64 - kb_lo * GEMV_ROWS, uv32 - 2 * kb_lo * GEMV_ROWS, zero};
     if (run.ka < run.kz) {
-        gemv_run<RING, ZP, G32>(W, run, xs - klo, ldx, B, R, q, [&](int t, const float (&out)[4]) {
+        gemv_run<RING, ZP, G32>(W, run, xa, B, R, q, [&](int t, const float (&out)[4]) {
             const int tt = t - pair * 2;
 #pragma unroll
             for (int r = 0; r < 4; r++) {
@@ -137,7 +145,8 @@ template <int EPI, bool NORM, bool ZP, bool G32>
 int launch_t(const GemvArgs& a, hipStream_t stream) {
     const int KB = a.W.K_pad / 64;
     const int kmax = (KB + a.ksplit - 1) / a.ksplit * 64;
-    const size_t smem = (size_t)MAXB * (kmax + 8) * 2 + (NW * 2 * MAXB * 32 + MAXB + MAXB * 64) * sizeof(float);
+    const size_t smem = (size_t)MAXB * (kmax + 8) * 2 + 128 + (size_t)(kmax / 64) * GEMV_ROWS * 20 +
+                        (NW * 2 * MAXB * 32 + MAXB + MAXB * 64) * sizeof(float);
     if (smem > 160 * 1024) return -1;
     static LdsLimit lim;
     if (ensure_lds_limit(lim, (const void*)gemv_w4_kernel<EPI, NORM, ZP, G32>, smem)) return -1;
