@@ -248,11 +248,18 @@ int layer_debug_dequant(layer_t layer, int32_t which, float* out, void* stream);
  * path cannot serve fails with W4_EUNSUPPORTED.  Errors: W4_EINVAL. */
 int layer_set_decode_path(layer_t layer, int32_t path);
 
+/* Time stamps of the persistent decode path (diagnostics): with on != 0 its
+ * launches record per-block wall-clock stamps for layer_decode_phase_times
+ * and layer_debug_decode_stamps; off (the default) they record none (the
+ * stamp stores lengthen the step).  Errors: W4_EINVAL. */
+int layer_set_decode_trace(layer_t layer, int32_t on);
+
 /* Diagnostics of the persistent decode path: durations in microseconds of
  * its five phases in the last completed call (q/k/v, attention with the
  * combine of its chunks, o_proj, gate/up, down), phase p measured from the
  * moment the last block finished phase p-1 (the kernel start for p = 0) to
- * the moment the last block finished phase p, into us_out[5]; and the error
+ * the moment the last block finished phase p (stamps of the last call made
+ * with layer_set_decode_trace on), into us_out[5]; and the error
  * flag raised by a wait that timed out (0 = none, sticky) into *error_flag
  * (nullable).  Waits for the device.  Errors: W4_EINVAL, W4_EHIP. */
 int layer_decode_phase_times(layer_t layer, float* us_out, int32_t* error_flag);

@@ -79,6 +79,7 @@ _SIG = {
     "layer_set_decode_path": (ctypes.c_int, [_P, _I]),
     "layer_decode_phase_times": (ctypes.c_int, [_P, _P, _P]),
     "layer_debug_decode_stamps": (ctypes.c_int, [_P, _P, _I]),
+    "layer_set_decode_trace": (ctypes.c_int, [_P, _I]),
     "layer_profile_kernel": (ctypes.c_int, [_P, _I, _I]),
     "layer_profile_read": (ctypes.c_int, [_P, _I, ctypes.POINTER(ctypes.c_float), ctypes.POINTER(ctypes.c_int32)]),
     "layer_last_error": (ctypes.c_char_p, []),
@@ -246,6 +247,10 @@ def layer_debug_decode_stamps(handle, n: int = 8 + 32 * 1024):
     out = np.zeros(n, dtype=np.uint64)
     rc = _lib.layer_debug_decode_stamps(handle, out.ctypes.data, n)
     return rc, out
+
+
+def layer_set_decode_trace(handle, on: int) -> int:
+    return _lib.layer_set_decode_trace(handle, int(on))
 
 
 def layer_set_decode_path(handle, path: int) -> int:

@@ -167,6 +167,7 @@ struct layer_s {
     int* err = nullptr;
     unsigned long long* stamps = nullptr;
     int decode_path = 0;   // 0 auto, 1 separate kernels, 2 persistent
+    bool decode_trace = false;   // persistent decode records its time stamps
 };
 
 namespace {
@@ -745,7 +746,7 @@ int layer_decode(layer_t L, const float* x, const int32_t* pos, const int32_t* c
         a.down_part = (uint64_t*)(base + fp.down_part);
         a.epoch = next_epoch();
         a.err = L->err;
-        a.stamps = L->stamps;
+        a.stamps = L->decode_trace ? L->stamps : nullptr;
         a.S_qkv = fp.S_qkv; a.S_o = fp.S_o; a.S_down = fp.S_down;
         a.plan = (const int*)L->fplan.p;
         a.comb_per = fp.comb_per; a.comb_lpv = fp.comb_lpv;
@@ -996,6 +997,12 @@ int layer_set_decode_path(layer_t L, int32_t path) {
     if (!L) return fail(W4_EINVAL, "null layer");
     if (path < 0 || path > 2) return fail(W4_EINVAL, "path must be 0, 1 or 2");
     L->decode_path = path;
+    return W4_OK;
+}
+
+int layer_set_decode_trace(layer_t L, int32_t on) {
+    if (!L) return fail(W4_EINVAL, "null layer");
+    L->decode_trace = on != 0;
     return W4_OK;
 }
 

@@ -66,17 +66,27 @@ struct Waiter {
     int left;
 };
 
-// Payload of the word at p, given a first load v: poll until the tag is ep.
-__device__ __forceinline__ uint32_t settle(const uint64_t* p, uint64_t v, uint32_t ep, Waiter& wt) {
-    while ((uint32_t)(v >> 32) != ep) {
+// Payloads of N words at p[i] (skipped where use[i] is false), given first
+// loads v[i]: poll until every tag is ep.  The late words are loaded again
+// together, so a round of polling costs one memory round trip however many
+// words are late.
+template <int N>
+__device__ __forceinline__ void settle_all(const uint64_t* const (&p)[N], uint64_t (&v)[N], const bool (&use)[N],
+                                           uint32_t ep, Waiter& wt) {
+    for (;;) {
+        bool late = false;
+#pragma unroll
+        for (int i = 0; i < N; i++) late |= use[i] && (uint32_t)(v[i] >> 32) != ep;
+        if (!late) return;
         if (--wt.left < 0) {
             if (wt.left == -1) atomicExch(wt.err, 1);
-            break;
+            return;
         }
-        __builtin_amdgcn_s_sleep(2);
-        v = get_tagged(p);
+        __builtin_amdgcn_s_sleep(1);
+#pragma unroll
+        for (int i = 0; i < N; i++)
+            if (use[i] && (uint32_t)(v[i] >> 32) != ep) v[i] = get_tagged(p[i]);
     }
-    return (uint32_t)v;
 }
 
 // Block-wide read of n elements: element i is the float sum over parts
@@ -85,16 +95,23 @@ __device__ __forceinline__ uint32_t settle(const uint64_t* p, uint64_t v, uint32
 // together before any poll.
 template <typename Addr, typename Sink>
 __device__ __forceinline__ void gather_sum(int n, int S, size_t sstride, uint32_t ep, Waiter& wt, Addr addr, Sink sink) {
-    constexpr int BATCH = 4;
+    constexpr int BATCH = 4, NWD = BATCH * MAXS;
     for (int base = threadIdx.x; base < n; base += NTHR * BATCH) {
-        uint64_t v[BATCH][MAXS];
+        const uint64_t* p[NWD];
+        uint64_t v[NWD];
+        bool use[NWD];
 #pragma unroll
         for (int j = 0; j < BATCH; j++) {
             const int i = base + j * NTHR;
 #pragma unroll
-            for (int s = 0; s < MAXS; s++)
-                v[j][s] = (i < n && s < S) ? get_tagged(addr(i) + s * sstride) : 0;
+            for (int s = 0; s < MAXS; s++) {
+                const int w = j * MAXS + s;
+                use[w] = i < n && s < S;
+                p[w] = addr(use[w] ? i : base) + (use[w] ? (size_t)s * sstride : 0);
+                v[w] = use[w] ? get_tagged(p[w]) : 0;
+            }
         }
+        settle_all(p, v, use, ep, wt);
 #pragma unroll
         for (int j = 0; j < BATCH; j++) {
             const int i = base + j * NTHR;
@@ -102,7 +119,7 @@ __device__ __forceinline__ void gather_sum(int n, int S, size_t sstride, uint32_
             float sum = 0.f;
 #pragma unroll
             for (int s = 0; s < MAXS; s++)
-                if (s < S) sum += __uint_as_float(settle(addr(i) + s * sstride, v[j][s], ep, wt));
+                if (s < S) sum += __uint_as_float((uint32_t)v[j * MAXS + s]);
             sink(i, sum);
         }
     }
@@ -114,19 +131,22 @@ template <typename Addr, typename Sink>
 __device__ __forceinline__ void gather_raw(int n, uint32_t ep, Waiter& wt, Addr addr, Sink sink) {
     constexpr int BATCH = 8;
     for (int base = threadIdx.x; base < n; base += NTHR * BATCH) {
+        const uint64_t* p[BATCH];
         uint64_t v[BATCH];
+        bool use[BATCH];
 #pragma unroll
         for (int j = 0; j < BATCH; j++) {
             const int i = base + j * NTHR;
-            const uint64_t* p = i < n ? addr(i) : nullptr;
-            v[j] = p ? get_tagged(p) : 0;
+            p[j] = i < n ? addr(i) : nullptr;
+            use[j] = p[j] != nullptr;
+            v[j] = use[j] ? get_tagged(p[j]) : 0;
         }
+        settle_all(p, v, use, ep, wt);
 #pragma unroll
         for (int j = 0; j < BATCH; j++) {
             const int i = base + j * NTHR;
             if (i >= n) break;
-            const uint64_t* p = addr(i);
-            if (p) sink(i, settle(p, v[j], ep, wt));
+            if (use[j]) sink(i, (uint32_t)v[j]);
         }
     }
 }
@@ -505,25 +525,32 @@ __global__ void __launch_bounds__(NTHR) decode_fused_kernel(DecodeFusedArgs a) {
                 const int b = head / nq;
                 const int nch = (meta[b] + 1 + CH - 1) / CH;
                 const uint64_t* base = a.apart + (size_t)head * NCH * (D + 2);
-                uint64_t t0[4], t1w[4], t2[4];
-                bool use[4];
+                // words of chunk qq: 3 qq (output dim), 3 qq + 1 (max), 3 qq + 2 (sum)
+                const uint64_t* pw[12];
+                uint64_t tw[12];
+                bool uw[12];
 #pragma unroll
                 for (int qq = 0; qq < 4; qq++) {
                     const int ch = cl + qq * LPV;
-                    use[qq] = valid && qq < cpl && ch < nch;
-                    const uint64_t* p = base + (size_t)(use[qq] ? ch : 0) * (D + 2);
-                    t0[qq] = use[qq] ? get_tagged(p + dim) : 0;
-                    t1w[qq] = use[qq] ? get_tagged(p + D) : 0;
-                    t2[qq] = use[qq] ? get_tagged(p + D + 1) : 0;
+                    const bool use = valid && qq < cpl && ch < nch;
+                    const uint64_t* p = base + (size_t)(use ? ch : 0) * (D + 2);
+                    pw[3 * qq] = p + dim;
+                    pw[3 * qq + 1] = p + D;
+                    pw[3 * qq + 2] = p + D + 1;
+#pragma unroll
+                    for (int e = 0; e < 3; e++) {
+                        uw[3 * qq + e] = use;
+                        tw[3 * qq + e] = use ? get_tagged(pw[3 * qq + e]) : 0;
+                    }
                 }
+                settle_all(pw, tw, uw, ep, wt);
                 float m[4], l[4], o[4];
 #pragma unroll
                 for (int qq = 0; qq < 4; qq++) {
-                    const uint64_t* p = base + (size_t)(cl + qq * LPV) * (D + 2);
-                    if (use[qq]) {
-                        o[qq] = __uint_as_float(settle(p + dim, t0[qq], ep, wt));
-                        m[qq] = __uint_as_float(settle(p + D, t1w[qq], ep, wt));
-                        l[qq] = __uint_as_float(settle(p + D + 1, t2[qq], ep, wt));
+                    if (uw[3 * qq]) {
+                        o[qq] = __uint_as_float((uint32_t)tw[3 * qq]);
+                        m[qq] = __uint_as_float((uint32_t)tw[3 * qq + 1]);
+                        l[qq] = __uint_as_float((uint32_t)tw[3 * qq + 2]);
                     } else {
                         o[qq] = 0.f; m[qq] = -INFINITY; l[qq] = 0.f;
                     }
