@@ -151,17 +151,19 @@ __device__ __forceinline__ void gather_raw(int n, uint32_t ep, Waiter& wt, Addr 
     }
 }
 
-// RMSNorm of B rows (fp32, row b at src + b * K, in LDS) into the activation
-// rows of LDS as fp16-held bf16: xs[b * ldx + k].  gamma: bf16 bits in LDS.
-// red8: 8 + NWAVE * B floats of LDS scratch.
-__device__ __forceinline__ void norm_rows(const float* src, const uint16_t* gamma, float eps, int B, int K,
-                                          f16* xs, int ldx, float* red8) {
+// RMSNorm of B rows (fp32, row b at src + b * K, in LDS) into activation
+// rows prepared for the GEMV core (gemv_prep): x' as fp16 at xs[b * ldx + k]
+// and the correction table c64.  gamma: bf16 bits in LDS.  K a multiple of
+// 128.  red8: 8 + NWAVE * B floats of LDS scratch.  Each thread takes 4
+// adjacent elements per pass, so the 16 lanes of a DPP row hold one 64-k tile.
+__device__ __forceinline__ void norm_prep_rows(const float* src, const uint16_t* gamma, float eps, int B, int K,
+                                               f16* xs, int ldx, float* c64, float* red8) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     for (int b = 0; b < B; b++) {
         float ss = 0.f;
-        for (int k = tid; k < K; k += NTHR) {
-            const float v = src[b * K + k];
-            ss += v * v;
+        for (int k = 4 * tid; k < K; k += 4 * NTHR) {
+            const float4 v = *reinterpret_cast<const float4*>(src + b * K + k);
+            ss += (v.x * v.x + v.y * v.y) + (v.z * v.z + v.w * v.w);
         }
         ss = wave_sum(ss);
         if (lane == 0) red8[8 + b * NWAVE + wave] = ss;
@@ -173,10 +175,29 @@ __device__ __forceinline__ void norm_rows(const float* src, const uint16_t* gamm
         red8[tid] = 1.0f / sqrtf(t / (float)K + eps);
     }
     __syncthreads();
+    const f16 sixteenth = (f16)0.0625f;
     for (int b = 0; b < B; b++) {
         const float rb = red8[b];
-        for (int k = tid; k < K; k += NTHR)
-            xs[b * ldx + k] = act_f16(src[b * K + k] * rb * bf16_bits_to_f32(gamma[k]));
+        for (int k0 = 0; k0 < K; k0 += 4 * NTHR) {          // uniform passes
+            const int k = k0 + 4 * tid;
+            float e = 0.f, o = 0.f;
+            if (k < K) {
+                // elements k % 8 = 0, 1 (or 4, 5) as they are, 2, 3 (or 6, 7) divided by 16
+                const float4 v = *reinterpret_cast<const float4*>(src + b * K + k);
+                const uint2 g = *reinterpret_cast<const uint2*>(gamma + k);
+                const f16 y0 = act_f16(v.x * rb * __uint_as_float(g.x << 16));
+                const f16 y1 = act_f16(v.y * rb * __uint_as_float(g.x & 0xFFFF0000u));
+                const f16 y2 = act_f16(v.z * rb * __uint_as_float(g.y << 16)) * sixteenth;
+                const f16 y3 = act_f16(v.w * rb * __uint_as_float(g.y & 0xFFFF0000u)) * sixteenth;
+                e = (float)y0 + (float)y1;
+                o = (float)y2 + (float)y3;
+                f16 q[4] = {y0, y1, y2, y3};
+                *reinterpret_cast<uint2*>(xs + b * ldx + k) = *reinterpret_cast<const uint2*>(q);
+            }
+            e = row_sum<16>(e);
+            o = row_sum<16>(o);
+            if (k < K && (lane & 15) == 0) c64[(k >> 6) * GEMV_ROWS + b] = gemv_c64(e, o);
+        }
     }
     __syncthreads();
 }
@@ -321,14 +342,12 @@ __global__ void __launch_bounds__(NTHR) decode_fused_kernel(DecodeFusedArgs a) {
     if (owns(1)) {
         const int t1 = pl[0], s1 = pl[3];
         const Run run1 = wave_run(1);
-        norm_rows(hbuf, gam, a.eps, B, H, xs, ldx, red8);
-        gemv_prep(xs, ldx, c64, nullptr, B, 0, H, tid, NTHR);
+        norm_prep_rows(hbuf, gam, a.eps, B, H, xs, ldx, c64, red8);
         stamp_done(6);
         clear_red();
         const GemvAct xa{xs, ldx, c64, nullptr, zero64};
         if (run1.ka < run1.kz)
             gemv_run<RING_QKV, false, false>(a.qkv, run1, xa, B, R1, q1, [&](int, const float (&out)[4]) { to_red(0, out); });
-        prefetch(3);
         stamp_done(7);
         __syncthreads();
         for (int i = tid; i < B * 32; i += NTHR) {
@@ -336,7 +355,9 @@ __global__ void __launch_bounds__(NTHR) decode_fused_kernel(DecodeFusedArgs a) {
             put_tagged(a.qkv_part + ((size_t)s1 * B + b) * Nq + t1 * 32 + cc, __float_as_uint(red_sum(0, b, cc)), ep);
         }
     }
-    if (!owns(1)) prefetch(3);
+    // the next product's weights are requested after the results went out
+    // (the memory pipeline serves a wave's requests in order)
+    prefetch(3);
     stamp_done(0);
 
     // ================= P2: attention units =================
@@ -602,7 +623,6 @@ __global__ void __launch_bounds__(NTHR) decode_fused_kernel(DecodeFusedArgs a) {
         const GemvAct xa{xs - klo, ldx, c64 - ka3 * GEMV_ROWS, nullptr, zero64};
         if (run3.ka < run3.kz)
             gemv_run<RING_O, false, false>(a.o, run3, xa, B, R3, q3, [&](int, const float (&out)[4]) { to_red(0, out); });
-        prefetch(4);
         stamp_done(20);
         __syncthreads();
         stamp_done(21);
@@ -611,7 +631,7 @@ __global__ void __launch_bounds__(NTHR) decode_fused_kernel(DecodeFusedArgs a) {
             put_tagged(a.o_part + ((size_t)s3 * B + b) * H + t3 * 32 + cc, __float_as_uint(red_sum(0, b, cc)), ep);
         }
     }
-    if (!owns(3)) prefetch(4);
+    prefetch(4);
     stamp_done(2);
 
     // ================= P4: h, RMSNorm(h), gate/up, SwiGLU =================
@@ -622,16 +642,14 @@ __global__ void __launch_bounds__(NTHR) decode_fused_kernel(DecodeFusedArgs a) {
     if (owns(4)) {
         const int ta4 = pl[8], tb4 = pl[9];
         const Run run4 = wave_run(4);
-        norm_rows(hbuf, gam + H, a.eps, B, H, xs, ldx, red8);
         if (tid < 8) reinterpret_cast<u32x4*>(zero64)[tid] = u32x4{0u, 0u, 0u, 0u};   // (attention reused it)
-        gemv_prep(xs, ldx, c64, nullptr, B, 0, H, tid, NTHR);
+        norm_prep_rows(hbuf, gam + H, a.eps, B, H, xs, ldx, c64, red8);
         stamp_done(22);
         clear_red();
         const GemvAct xa{xs, ldx, c64, nullptr, zero64};
         if (run4.ka < run4.kz)
             gemv_run<RING, false, false>(a.gu, run4, xa, B, R4, q4,
                                          [&](int t, const float (&out)[4]) { to_red(t - ta4, out); });
-        prefetch(5);
         stamp_done(13);
         __syncthreads();
         stamp_done(24);
@@ -644,7 +662,7 @@ __global__ void __launch_bounds__(NTHR) decode_fused_kernel(DecodeFusedArgs a) {
             put_tagged(a.g + ((size_t)b * a.F_pad + (ta4 / 2 + pp) * 32 + cc) / 2, word, ep);
         }
     }
-    if (!owns(4)) prefetch(5);
+    prefetch(5);
     stamp_done(3);
 
     // ================= P5: down, y = h + g Wd =================

@@ -72,40 +72,50 @@ struct GemvAct {
     const f16* zero;
 };
 
+// Correction table entries from the sums e (other elements) and o (divided
+// elements) of x' over a 64-k tile: the correction for the zero point 8.
+__device__ __forceinline__ float gemv_c64(float e, float o) {
+    return 1024.0f * (e + o) + 8.0f * (e + 16.0f * o);
+}
+
 // Prepare rows b < B, absolute k in [k0, k0 + klen) (klen a multiple of 64)
 // in place: x (bf16 values held as fp16) -> x', and write the correction
-// tables (pointers as in GemvAct, non-const).  Called by all nthr threads of
-// the block; the caller synchronises before and after.
+// tables (pointers as in GemvAct, non-const).  One 8-element chunk per thread
+// and pass; the 8 chunks of a 64-k tile sit in 8 adjacent lanes, which meet
+// with DPP row operations.  Called by all nthr threads of the block (nthr a
+// multiple of 64); the caller synchronises before and after.
 __device__ __forceinline__ void gemv_prep(f16* xs, int ldx, float* c64, float2* uv32, int B, int k0, int klen,
                                           int tid, int nthr) {
-    const int nt = klen >> 6;
+    const int nc = klen >> 3, total = B * nc;
     const f16x2 sixteenth = f16x2{(f16)0.0625f, (f16)0.0625f};
-    for (int i = tid; i < B * nt; i += nthr) {
-        const int b = i / nt, t = i - b * nt;
-        const int k = k0 + 64 * t;
-        u32x4* p = reinterpret_cast<u32x4*>(xs + b * ldx + k);
-        float E[2] = {0.f, 0.f}, O[2] = {0.f, 0.f};
-#pragma unroll
-        for (int v = 0; v < 8; v++) {          // 8 elements per 16 bytes: k % 8 = 0..7
-            const u32x4 w = p[v];
+    for (int base = 0; base < total; base += nthr) {       // uniform passes
+        const int i = base + tid;
+        const bool ok = i < total;
+        const int b = ok ? i / nc : 0, c = ok ? i - b * nc : 0;
+        const int k = k0 + 8 * c;
+        float e = 0.f, o = 0.f;
+        if (ok) {
+            u32x4* p = reinterpret_cast<u32x4*>(xs + b * ldx + k);
+            const u32x4 w = *p;
             // element pairs (0,1) (2,3) (4,5) (6,7); the words are taken into
             // scalars first (see as_bf16x2)
             const uint32_t w0 = w[0], w1 = w[1], w2 = w[2], w3 = w[3];
             const f16x2 x0 = __builtin_bit_cast(f16x2, w0), x2 = __builtin_bit_cast(f16x2, w2);
             const f16x2 x1 = __builtin_bit_cast(f16x2, w1) * sixteenth;
             const f16x2 x3 = __builtin_bit_cast(f16x2, w3) * sixteenth;
-            E[v >> 2] += ((float)x0[0] + (float)x0[1]) + ((float)x2[0] + (float)x2[1]);
-            O[v >> 2] += ((float)x1[0] + (float)x1[1]) + ((float)x3[0] + (float)x3[1]);
-            p[v] = u32x4{w0, __builtin_bit_cast(uint32_t, x1), w2, __builtin_bit_cast(uint32_t, x3)};
+            e = ((float)x0[0] + (float)x0[1]) + ((float)x2[0] + (float)x2[1]);
+            o = ((float)x1[0] + (float)x1[1]) + ((float)x3[0] + (float)x3[1]);
+            *p = u32x4{w0, __builtin_bit_cast(uint32_t, x1), w2, __builtin_bit_cast(uint32_t, x3)};
         }
-        const int kb = k >> 6;
-        c64[kb * GEMV_ROWS + b] = 1024.0f * ((E[0] + O[0]) + (E[1] + O[1])) +
-                                  8.0f * ((E[0] + 16.0f * O[0]) + (E[1] + 16.0f * O[1]));
-        if (uv32) {
-#pragma unroll
-            for (int hh = 0; hh < 2; hh++)
-                uv32[(2 * kb + hh) * GEMV_ROWS + b] = float2{E[hh] + O[hh], E[hh] + 16.0f * O[hh]};
-        }
+        // sums over the 4 chunks of a 32-k segment, then the 8 of a 64-k tile
+        e += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(e), 0xB1, 0xF, 0xF, false));
+        o += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(o), 0xB1, 0xF, 0xF, false));
+        e += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(e), 0x4E, 0xF, 0xF, false));
+        o += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(o), 0x4E, 0xF, 0xF, false));
+        if (uv32 && ok && (c & 3) == 0) uv32[(k >> 5) * GEMV_ROWS + b] = float2{e + o, e + 16.0f * o};
+        e += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(e), 0x141, 0xF, 0xF, false));
+        o += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(o), 0x141, 0xF, 0xF, false));
+        if (ok && (c & 7) == 0) c64[(k >> 6) * GEMV_ROWS + b] = gemv_c64(e, o);
     }
 }
 
