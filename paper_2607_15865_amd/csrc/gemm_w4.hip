@@ -152,25 +152,54 @@ gemm_w4_kernel(const f16* __restrict__ X, int ldx, DevLinear W, EpiArgs ep, Gemm
         const int m = m0 + r < M ? m0 + r : M - 1;
         xoff[i] = (uint32_t)m * xrow_bytes + (uint32_t)xlc * 16u;
     }
-    auto load_x = [&](int kb, unsigned char* As) __attribute__((always_inline)) {
-        const uint32_t kbytes = (uint32_t)(kb < kb_hi ? kb : kb_lo) * 128u;
+    // Pipeline depth P: the loads of iteration it + P are requested in
+    // iteration it.  Row tiles of 32 and 64 (short iterations) stage X in
+    // registers, so the barrier of an iteration waits for LDS writes only and
+    // the deeper loads stay in flight; row tiles of 128 load X straight into
+    // LDS one iteration ahead (their registers hold the accumulators).
+    constexpr bool XREG = TM < 4;
+    constexpr int P = TM == 1 ? 4 : (TM == 2 && GT != 0) ? 3 : 2;
+    constexpr int U = P % 2 == 0 ? P : 2 * P;          // unroll: X stage (mod P) and LDS buffer (mod 2) static
+    constexpr int XS = XREG ? P : 1;
+    u32x4 xr[XS][XL];
+    auto xbytes = [&](int kb) __attribute__((always_inline)) {
+        return (uint32_t)(kb < kb_hi ? kb : kb_lo) * 128u;
+    };
+    // DMA variant: the X tile of the iteration that starts at kb into As
+    auto load_x_lds = [&](int kb, unsigned char* As) __attribute__((always_inline)) {
+        const uint32_t kbytes = xbytes(kb);
 #pragma unroll
         for (int i = 0; i < XL; i++)
             __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(Xb + (xoff[i] + kbytes)),
                                              (__attribute__((address_space(3))) void*)(As + (4 * i + wave) * 1024),
                                              16, 0, 0);
     };
+    // register variant: load into stage st, later written to LDS at the place
+    // the direct-to-LDS load would fill (lane L: 16 bytes at L * 16)
+    auto load_x_reg = [&](int st, int kb) __attribute__((always_inline)) {
+        const uint32_t kbytes = xbytes(kb);
+#pragma unroll
+        for (int i = 0; i < XL; i++)
+            xr[XREG ? st : 0][i] = *reinterpret_cast<const u32x4*>(Xb + (xoff[i] + kbytes));
+    };
+    auto store_x = [&](int st, unsigned char* As) __attribute__((always_inline)) {
+#pragma unroll
+        for (int i = 0; i < XL; i++)
+            *reinterpret_cast<u32x4*>(As + (4 * i + wave) * 1024 + lane * 16) = xr[XREG ? st : 0][i];
+    };
 
-    // ---- weight ring: slot q holds tile (kb, column q & 1) with the ratios
-    // (and zero points) of its groups.  Loads past the range re-read the
-    // range's first tile (never used).
+    // ---- weight ring: group g (slots 4 g .. 4 g + 3) holds the tiles of one
+    // iteration, slot 4 g + 2 half + column with the ratios (and zero points)
+    // of their groups.  Loads past the range re-read the range's first tile
+    // (never used).
+    constexpr int NG = XREG ? P : 2;
     const char* const Wb = reinterpret_cast<const char*>(W.qw);
     const uint32_t woff0 = ((uint32_t)(wave_on ? nt0 : 0) * (uint32_t)KB * 64u + (uint32_t)lane) * 16u;
     const uint32_t wcol1 = (uint32_t)KB * 1024u;
     const char* const Rb = reinterpret_cast<const char*>(W.ratios);
-    u32x4 rw[RS];
-    float rr[RS][NH];
-    uint32_t rz[RS][NH];
+    u32x4 rw[4 * NG];
+    float rr[4 * NG][NH];
+    uint32_t rz[4 * NG][NH];
     auto load_w = [&](int q, int kb) __attribute__((always_inline)) {
         const int kk = kb < kb_hi ? kb : kb_lo;
         const int col = (q & 1) ? col1 : col0;
@@ -182,6 +211,12 @@ gemm_w4_kernel(const f16* __restrict__ X, int ldx, DevLinear W, EpiArgs ep, Gemm
             if (ZP) rz[q][hh] = (uint32_t)W.zeros[gi];
         }
     };
+    auto load_group = [&](int g, int kb) __attribute__((always_inline)) {
+        load_w(4 * g, kb);
+        load_w(4 * g + 1, kb);
+        load_w(4 * g + 2, kb + 1);
+        load_w(4 * g + 3, kb + 1);
+    };
 
     f32x16 acc[TM][2];
 #pragma unroll
@@ -191,81 +226,105 @@ gemm_w4_kernel(const f16* __restrict__ X, int ldx, DevLinear W, EpiArgs ep, Gemm
     // of row 32 i + c, stored at chunk ^ (row & 15) (row & 15 == c & 15)
     const uint32_t arow = (uint32_t)c * 256u;
 
-    // iteration it: tiles kb, kb + 1 from As (ring slots qb .. qb + 3), while
-    // the next iteration's X and weights (slots qn ..) are requested.  With
-    // it == nit (the odd partner of the last iteration) only the loads and
-    // the barrier run, so every iteration issues the same loads.
-    auto iteration = [&](int it, const unsigned char* As, unsigned char* As_next, int qb, int qn)
-        __attribute__((always_inline)) {
-        const int kb = kb_lo + 2 * it;
-        load_x(kb + 2, As_next);
-        load_w(qn, kb + 2);
-        load_w(qn + 1, kb + 2);
-        load_w(qn + 2, kb + 3);
-        load_w(qn + 3, kb + 3);
-        if (kb < kb_hi) {
-            f16x8 a[2][TM], b[2][2];
-            auto prep = [&](int t, int p) __attribute__((always_inline)) {
-                const int half = t >> 2, s = t & 3, q = qb + 2 * half, hh = NH == 2 ? (s >> 1) : 0;
-                if (ZP && (s == 0 || (NH == 2 && s == 2))) {
-                    zo0 = zero_off((float)rz[q][hh]);
-                    zo1 = zero_off((float)rz[q + 1][hh]);
-                }
-                const uint32_t chunk = (uint32_t)((8 * half + 2 * s + h) ^ (c & 15)) * 16u;
+    // the MFMAs of the iteration that starts at kb, on the X tile in As and
+    // weight group qb; qn: the group of the next iteration (its first ratio)
+    auto compute = [&](int kb, const unsigned char* As, int qb, int qn) __attribute__((always_inline)) {
+        f16x8 a[2][TM], b[2][2];
+        auto prep = [&](int t, int p) __attribute__((always_inline)) {
+            const int half = t >> 2, s = t & 3, q = qb + 2 * half, hh = NH == 2 ? (s >> 1) : 0;
+            if (ZP && (s == 0 || (NH == 2 && s == 2))) {
+                zo0 = zero_off((float)rz[q][hh]);
+                zo1 = zero_off((float)rz[q + 1][hh]);
+            }
+            const uint32_t chunk = (uint32_t)((8 * half + 2 * s + h) ^ (c & 15)) * 16u;
+#pragma unroll
+            for (int i = 0; i < TM; i++)
+                a[p][i] = *reinterpret_cast<const f16x8*>(As + (uint32_t)i * 8192u + arow + chunk);
+            b[p][0] = dequant8(rw[q][s], zo0, dq);
+            b[p][1] = dequant8(rw[q + 1][s], zo1, dq);
+        };
+        // After step t, if step t + 1 (step 0 of the next iteration for
+        // t = 7) starts a group inside the range, the accumulators take
+        // its ratio s_prev / s_new.  Doing it here, interleaved with the
+        // last MFMAs of the old group, keeps the multiplies off the
+        // boundary between the groups' MFMA streams.
+        auto next_group = [](int t) { return t == 7 || (GT <= 1 && t == 3) || (GT == 0 && (t & 1) == 1); };
+        prep(0, 0);
+#pragma unroll
+        for (int t = 0; t < 8; t++) {
+            const int p = t & 1;
+            if (t + 1 < 8) prep(t + 1, p ^ 1);
+#pragma unroll
+            for (int i = 0; i < TM; i++) {
+                acc[i][0] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a[p][i], b[p][0], acc[i][0], 0, 0, 0);
+                acc[i][1] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a[p][i], b[p][1], acc[i][1], 0, 0, 0);
+            }
+            if (next_group(t)) {
+                const int tn = (t + 1) & 7;                       // the next step
+                const int half = tn >> 2, hh = NH == 2 ? ((tn & 3) >> 1) : 0;
+                const int q = (t == 7 ? qn : qb) + 2 * half;
+                const int k = (kb + (t == 7 ? 2 : 0) + half) * 64 + (tn & 3) * 16;
+                const bool start = k < kb_hi * 64 && (k & Gm1) == 0;
+                const float f0 = start ? rr[q][hh] : 1.0f, f1 = start ? rr[q + 1][hh] : 1.0f;
 #pragma unroll
                 for (int i = 0; i < TM; i++)
-                    a[p][i] = *reinterpret_cast<const f16x8*>(As + (uint32_t)i * 8192u + arow + chunk);
-                b[p][0] = dequant8(rw[q][s], zo0, dq);
-                b[p][1] = dequant8(rw[q + 1][s], zo1, dq);
-            };
-            // After step t, if step t + 1 (step 0 of the next iteration for
-            // t = 7) starts a group inside the range, the accumulators take
-            // its ratio s_prev / s_new.  Doing it here, interleaved with the
-            // last MFMAs of the old group, keeps the multiplies off the
-            // boundary between the groups' MFMA streams.
-            auto next_group = [](int t) { return t == 7 || (GT <= 1 && t == 3) || (GT == 0 && (t & 1) == 1); };
-            prep(0, 0);
 #pragma unroll
-            for (int t = 0; t < 8; t++) {
-                const int p = t & 1;
-                if (t + 1 < 8) prep(t + 1, p ^ 1);
-#pragma unroll
-                for (int i = 0; i < TM; i++) {
-                    acc[i][0] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a[p][i], b[p][0], acc[i][0], 0, 0, 0);
-                    acc[i][1] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a[p][i], b[p][1], acc[i][1], 0, 0, 0);
-                }
-                if (next_group(t)) {
-                    const int tn = (t + 1) & 7;                       // the next step
-                    const int half = tn >> 2, hh = NH == 2 ? ((tn & 3) >> 1) : 0;
-                    const int q = (t == 7 ? qn : qb) + 2 * half;
-                    const int k = (kb + (t == 7 ? 2 : 0) + half) * 64 + (tn & 3) * 16;
-                    const bool start = k < kb_hi * 64 && (k & Gm1) == 0;
-                    const float f0 = start ? rr[q][hh] : 1.0f, f1 = start ? rr[q + 1][hh] : 1.0f;
-#pragma unroll
-                    for (int i = 0; i < TM; i++)
-#pragma unroll
-                        for (int e = 0; e < 16; e++) {
-                            acc[i][0][e] *= f0;
-                            acc[i][1][e] *= f1;
-                        }
-                    sched_step<TM, TM == 4 ? 16 : 20>();
-                } else {
-                    sched_step<TM, TM == 4 ? 4 : 6>();
-                }
+                    for (int e = 0; e < 16; e++) {
+                        acc[i][0][e] *= f0;
+                        acc[i][1][e] *= f1;
+                    }
+                sched_step<TM, TM == 4 ? 16 : 20>();
+            } else {
+                sched_step<TM, TM == 4 ? 4 : 6>();
             }
         }
-        __syncthreads();
     };
 
-    load_x(kb_lo, As0);
-    load_w(0, kb_lo);
-    load_w(1, kb_lo);
-    load_w(2, kb_lo + 1);
-    load_w(3, kb_lo + 1);
-    __syncthreads();
-    for (int it = 0; it < nit; it += 2) {
-        iteration(it, As0, As1, 0, 4);
-        iteration(it + 1, As1, As0, 4, 0);
+    if constexpr (XREG) {
+        // iteration it (u = it mod U): X of it + P into stage u mod P (X of it
+        // is in LDS already), the MFMAs of it on LDS buffer u mod 2 and weight
+        // group u mod P, then the weights of it + P into that group, X of
+        // it + 1 into the other LDS buffer, and the barrier.  Iterations past
+        // the range (the loop runs a multiple of U) only load, store and wait.
+#pragma unroll
+        for (int j = 0; j < P; j++) {
+            load_x_reg(j, kb_lo + 2 * j);
+            load_group(j, kb_lo + 2 * j);
+        }
+        store_x(0, As0);
+        __syncthreads();
+        for (int it0 = 0; it0 < nit; it0 += U) {
+#pragma unroll
+            for (int u = 0; u < U; u++) {
+                const int kb = kb_lo + 2 * (it0 + u);
+                const int st = u % P;
+                load_x_reg(st, kb + 2 * P);
+                if (kb < kb_hi) compute(kb, (u & 1) ? As1 : As0, 4 * st, 4 * ((u + 1) % P));
+                load_group(st, kb + 2 * P);
+                store_x((u + 1) % P, (u & 1) ? As0 : As1);
+                __syncthreads();
+            }
+        }
+    } else {
+        // iteration it: X and weights of it + 1 requested (X straight to LDS),
+        // the MFMAs of it, then the barrier, whose workgroup release waits for
+        // the block's outstanding loads.  With it == nit (the odd partner of
+        // the last iteration) only the loads and the barrier run.
+        auto iteration = [&](int it, const unsigned char* As, unsigned char* As_next, int qb, int qn)
+            __attribute__((always_inline)) {
+            const int kb = kb_lo + 2 * it;
+            load_x_lds(kb + 2, As_next);
+            load_group(qn / 4, kb + 2);
+            if (kb < kb_hi) compute(kb, As, qb, qn);
+            __syncthreads();
+        };
+        load_x_lds(kb_lo, As0);
+        load_group(0, kb_lo);
+        __syncthreads();
+        for (int it = 0; it < nit; it += 2) {
+            iteration(it, As0, As1, 0, 4);
+            iteration(it + 1, As1, As0, 4, 0);
+        }
     }
 
     // ---- scale of the range's last group
@@ -273,29 +332,95 @@ gemm_w4_kernel(const f16* __restrict__ X, int ldx, DevLinear W, EpiArgs ep, Gemm
     const float sl0 = (float)__builtin_bit_cast(f16, W.scales[(size_t)glast * W.N_dev + col0]);
     const float sl1 = (float)__builtin_bit_cast(f16, W.scales[(size_t)glast * W.N_dev + col1]);
 
-    auto epilogue = [&](int m, float v0, float v1) {
+    // Epilogue of row tile i: v0[e], v1[e] are the sums of columns col0 and
+    // col1 for row m0 + 32 i + 8 (e / 4) + 4 h + e % 4.  Every value the
+    // epilogue reads (residual, positions, RoPE factors) is requested for
+    // all 16 rows before the first store: a store could alias a later read,
+    // so interleaved they would cost a memory round trip per row.
+    auto tile_epilogue = [&](int i, const float (&v0)[16], const float (&v1)[16]) __attribute__((always_inline)) {
+        int mr[16];
+#pragma unroll
+        for (int e = 0; e < 16; e++) {
+            const int m = m0 + i * 32 + 8 * (e / 4) + 4 * h + (e % 4);
+            mr[e] = m < M ? m : -1;
+        }
+        auto row = [&](int e) { return mr[e] < 0 ? M - 1 : mr[e]; };
         if (EPI == EPI_RESID) {
-            const size_t o = (size_t)m * W.N;
-            ep.out_f32[o + col0] = ep.resid[o + col0] + v0;
-            ep.out_f32[o + col1] = ep.resid[o + col1] + v1;
+            float r0[16], r1[16];
+#pragma unroll
+            for (int e = 0; e < 16; e++) {
+                const size_t o = (size_t)row(e) * W.N;
+                r0[e] = ep.resid[o + col0];
+                r1[e] = ep.resid[o + col1];
+            }
+#pragma unroll
+            for (int e = 0; e < 16; e++) {
+                if (mr[e] < 0) continue;
+                const size_t o = (size_t)mr[e] * W.N;
+                ep.out_f32[o + col0] = r0[e] + v0[e];
+                ep.out_f32[o + col1] = r1[e] + v1[e];
+            }
         } else if (EPI == EPI_SWIGLU) {
             const int f = (nt0 / 2) * 32 + c;          // tile pair (2j, 2j+1) = gate block j, up block j
-            ep.act_out[(size_t)m * ep.F_pad + f] = act_f16(silu(v0) * v1);
+#pragma unroll
+            for (int e = 0; e < 16; e++)
+                if (mr[e] >= 0) ep.act_out[(size_t)mr[e] * ep.F_pad + f] = act_f16(silu(v0[e]) * v1[e]);
         } else {
-            epi_qkv_pair(ep, m, nt0 * 32, c, v0, v1, ep.slot_base + m, 0);
+            // q/k/v: the column pair (nt0 * 32 + c, + 32) holds dims dim0 and
+            // dim1 of one head (see epi_qkv_pair); RoPE on q and k
+            const int d = ep.head_dim, qd = ep.nq * d, kd = ep.nkv * d;
+            int n = nt0 * 32, kind, head;
+            if (n < qd) { kind = 0; head = n / d; n -= head * d; }
+            else if (n < qd + kd) { kind = 1; n -= qd; head = n / d; n -= head * d; }
+            else { kind = 2; n -= qd + kd; head = n / d; n -= head * d; }
+            const int p0 = n / 32;
+            const int dim0 = 32 * rope_block(p0, d) + c;
+            const int dim1 = 32 * rope_block(p0 + 1, d) + c;
+            float cs[16], sn[16];
+            if (kind < 2) {
+                int ps[16];
+#pragma unroll
+                for (int e = 0; e < 16; e++) ps[e] = ep.pos[row(e)];
+#pragma unroll
+                for (int e = 0; e < 16; e++) {
+                    cs[e] = ep.rope_cos[(size_t)ps[e] * (d / 2) + dim0];
+                    sn[e] = ep.rope_sin[(size_t)ps[e] * (d / 2) + dim0];
+                }
+            }
+#pragma unroll
+            for (int e = 0; e < 16; e++) {
+                if (mr[e] < 0) continue;
+                float o0 = v0[e], o1 = v1[e];
+                if (kind < 2) {
+                    o0 = v0[e] * cs[e] - v1[e] * sn[e];
+                    o1 = v1[e] * cs[e] + v0[e] * sn[e];
+                }
+                const uint16_t b0 = bf16_bits_rne(o0), b1 = bf16_bits_rne(o1);
+                uint16_t* dst;
+                if (kind == 0) {
+                    dst = ep.q_out + ((size_t)mr[e] * ep.nq + head) * d;
+                } else {
+                    uint16_t* cache = (kind == 1) ? ep.k_cache : ep.v_cache;
+                    dst = cache + (size_t)head * ep.cache_stride_h + (size_t)(ep.slot_base + mr[e]) * d;
+                }
+                dst[dim0] = b0;
+                dst[dim1] = b1;
+            }
         }
     };
 
     if (gs.S == 1) {
         if (!wave_on) return;
-        // rows of register e: 8*(e/4) + 4*h + (e%4)
 #pragma unroll
-        for (int i = 0; i < TM; i++)
+        for (int i = 0; i < TM; i++) {
+            float v0[16], v1[16];
 #pragma unroll
             for (int e = 0; e < 16; e++) {
-                const int m = m0 + i * 32 + 8 * (e / 4) + 4 * h + (e % 4);
-                if (m < M) epilogue(m, acc[i][0][e] * sl0, acc[i][1][e] * sl1);
+                v0[e] = acc[i][0][e] * sl0;
+                v1[e] = acc[i][1][e] * sl1;
             }
+            tile_epilogue(i, v0, v1);
+        }
         return;
     }
 
@@ -333,20 +458,40 @@ gemm_w4_kernel(const f16* __restrict__ X, int ldx, DevLinear W, EpiArgs ep, Gemm
     }
     __syncthreads();
     if (!last_flag || !wave_on) return;
+    // The sum, row tile by row tile: the 32 values of a range are requested
+    // together (one memory round trip per range), rows past M read row M - 1
+    // and are dropped.
 #pragma unroll
-    for (int i = 0; i < TM; i++)
+    for (int i = 0; i < TM; i++) {
+        float t0[16], t1[16];
 #pragma unroll
-        for (int e = 0; e < 16; e++) {
-            const int m = m0 + i * 32 + 8 * (e / 4) + 4 * h + (e % 4);
-            if (m >= M) continue;
-            float v0 = 0.f, v1 = 0.f;
-            for (int s = 0; s < gs.S; s++) {
-                const float* ps = gs.part + ((size_t)s * M + m) * W.N_dev;
-                v0 += s == sp ? acc[i][0][e] * sl0 : __hip_atomic_load(ps + col0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                v1 += s == sp ? acc[i][1][e] * sl1 : __hip_atomic_load(ps + col1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        for (int e = 0; e < 16; e++) { t0[e] = 0.f; t1[e] = 0.f; }
+        for (int s = 0; s < gs.S; s++) {
+            if (s == sp) {
+#pragma unroll
+                for (int e = 0; e < 16; e++) {
+                    t0[e] += acc[i][0][e] * sl0;
+                    t1[e] += acc[i][1][e] * sl1;
+                }
+            } else {
+                const float* ps = gs.part + (size_t)s * M * W.N_dev;
+                float v0[16], v1[16];
+#pragma unroll
+                for (int e = 0; e < 16; e++) {
+                    const int m = m0 + i * 32 + 8 * (e / 4) + 4 * h + (e % 4);
+                    const size_t ro = (size_t)(m < M ? m : M - 1) * W.N_dev;
+                    v0[e] = __hip_atomic_load(ps + ro + col0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    v1[e] = __hip_atomic_load(ps + ro + col1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                }
+#pragma unroll
+                for (int e = 0; e < 16; e++) {
+                    t0[e] += v0[e];
+                    t1[e] += v1[e];
+                }
             }
-            epilogue(m, v0, v1);
         }
+        tile_epilogue(i, t0, t1);
+    }
 }
 
 template <int EPI, int TM, int GT, bool ZP>
