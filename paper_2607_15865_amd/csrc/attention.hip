@@ -242,16 +242,39 @@ __global__ void __launch_bounds__(64 * PF_MAXHB) attn_prefill_merge_kernel(AttnP
     for (int t = nqt - 1; t > qt; t--) first += (a.L + min(a.T, 32 * (t + 1)) + a.chunk_keys - 1) / a.chunk_keys;
     const int nch = (a.L + min(a.T, 32 * (qt + 1)) + a.chunk_keys - 1) / a.chunk_keys;
     if (nch == 1 || hidx >= r) return;
-    float M = -INFINITY;
-    for (int ch = 0; ch < nch; ch++) M = fmaxf(M, a.part[part_index<D>(a, row, first + ch, wave, lane)]);
-    float L = 0.f, acc[16] = {};
-    for (int ch = 0; ch < nch; ch++) {
-        const float* pp = a.part + part_index<D>(a, row, first + ch, wave, lane);
-        const float mc = pp[0];
-        const float w = (mc == -INFINITY) ? 0.f : exp2f(mc - M);
-        L += w * pp[64];
+    // chunks in groups of CB: the states of a group are requested together,
+    // then merged into the running maximum M, sum L and output acc
+    constexpr int CB = 4;
+    float M = -INFINITY, L = 0.f, acc[16] = {};
+    for (int ch0 = 0; ch0 < nch; ch0 += CB) {
+        float mc[CB], lc[CB], v[CB][16];
 #pragma unroll
-        for (int e = 0; e < 16; e++) acc[e] += w * pp[(size_t)(2 + i * 16 + e) * 64];
+        for (int j = 0; j < CB; j++) {
+            const int ch = ch0 + j < nch ? ch0 + j : nch - 1;
+            const float* pp = a.part + part_index<D>(a, row, first + ch, wave, lane);
+            mc[j] = pp[0];
+            lc[j] = pp[64];
+#pragma unroll
+            for (int e = 0; e < 16; e++) v[j][e] = pp[(size_t)(2 + i * 16 + e) * 64];
+        }
+        float Mn = M;
+#pragma unroll
+        for (int j = 0; j < CB; j++)
+            if (ch0 + j < nch) Mn = fmaxf(Mn, mc[j]);
+        if (Mn == -INFINITY) continue;
+        const float sc = (M == -INFINITY) ? 0.f : exp2f(M - Mn);
+        L *= sc;
+#pragma unroll
+        for (int e = 0; e < 16; e++) acc[e] *= sc;
+#pragma unroll
+        for (int j = 0; j < CB; j++) {
+            if (ch0 + j >= nch || mc[j] == -INFINITY) continue;
+            const float w = exp2f(mc[j] - Mn);
+            L += w * lc[j];
+#pragma unroll
+            for (int e = 0; e < 16; e++) acc[e] += w * v[j][e];
+        }
+        M = Mn;
     }
     const int qrow = qt * 32 + c;
     const float lt = L + __shfl_xor(L, 32, 64);

@@ -537,9 +537,9 @@ int launch_epi(int TM, const f16* X, int ldx, const DevLinear& W, const EpiArgs&
 }  // namespace
 
 // Launch plan.  The row tile is the largest (most MFMAs per dequantised
-// fragment) that still gives about 0.8 tiles per CU; k splits then raise
-// the grid to half the CUs, or, while splits stay long (3072 k or more),
-// up to 1.2 blocks per CU.  Each split keeps at least 4 iterations.  (The
+// fragment) that still gives 0.75 tiles per CU; k splits then raise the grid
+// to 0.75 blocks per CU, or, while splits stay long (6144 k or more), up to
+// 1.2 blocks per CU.  Each split keeps at least 4 iterations.  (The
 // thresholds follow a measured sweep over the prefill shapes of the
 // Llama-3-8B-shaped layer at 128 and 512 rows.)
 GemmPlan gemm_w4_plan(int M, const DevLinear& W, int num_cus) {
@@ -548,12 +548,12 @@ GemmPlan gemm_w4_plan(int M, const DevLinear& W, int num_cus) {
     const int tm_max = (W.zeros || W.lgG == 5) ? 2 : 4;   // the kernel variants that exist
     auto nrb = [&](int tm) { return (M + 32 * tm - 1) / (32 * tm); };
     p.TM = tm_max;
-    while (p.TM > 1 && nrb(p.TM) * ncb * 5 < num_cus * 4) p.TM /= 2;
+    while (p.TM > 1 && nrb(p.TM) * ncb * 4 < num_cus * 3) p.TM /= 2;
     const int tiles = nrb(p.TM) * ncb;
     p.S = 1;
     while (p.S < 16 && KB / (p.S * 2) >= 8) {
         const int blocks = tiles * p.S;
-        const bool small = blocks * 2 < num_cus;
+        const bool small = blocks * 4 < num_cus * 3;
         const bool long_k = KB * 64 / p.S >= 2 * 3072 && blocks * 5 < num_cus * 6;
         if (!small && !long_k) break;
         p.S *= 2;

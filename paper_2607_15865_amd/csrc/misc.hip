@@ -6,23 +6,43 @@ namespace {
 
 // top.RMSNorm (Sec. 2.2): y = x / sqrt(mean(x^2) + eps) * gamma over a row,
 // rounded to bf16 and held as fp16 (the matmul operand).  One block per row.
+// RMSNorm of one row per block (256 threads), rounded to bf16 and held as
+// fp16.  NV: 16-byte chunks of the row per thread (H <= NV * 1024), kept in
+// registers between the sum of squares and the output.
+template <int NV>
 __global__ void __launch_bounds__(256) rmsnorm_kernel(const float* __restrict__ x, const uint16_t* __restrict__ gamma,
                                                       float eps, int H, f16* __restrict__ out) {
     __shared__ float part[4];
     const int row = blockIdx.x, tid = threadIdx.x;
     const float* xr = x + (size_t)row * H;
-    float ss = 0.f;
-    for (int k = tid * 4; k < H; k += 1024) {
-        const float4 v = *reinterpret_cast<const float4*>(xr + k);
-        ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+    float4 v[NV];
+    uint2 g[NV];
+#pragma unroll
+    for (int j = 0; j < NV; j++) {
+        const int k = (tid + 256 * j) * 4;
+        v[j] = k < H ? *reinterpret_cast<const float4*>(xr + k) : float4{0.f, 0.f, 0.f, 0.f};
+        g[j] = k < H ? *reinterpret_cast<const uint2*>(gamma + k) : uint2{0u, 0u};
     }
+    float ss = 0.f;
+#pragma unroll
+    for (int j = 0; j < NV; j++) ss += (v[j].x * v[j].x + v[j].y * v[j].y) + (v[j].z * v[j].z + v[j].w * v[j].w);
     ss = wave_sum(ss);
     if ((tid & 63) == 0) part[tid >> 6] = ss;
     __syncthreads();
     const float tot = part[0] + part[1] + part[2] + part[3];
     const float rinv = 1.0f / sqrtf(tot / (float)H + eps);
     f16* orow = out + (size_t)row * H;
-    for (int k = tid; k < H; k += 256) orow[k] = act_f16(xr[k] * rinv * bf16_bits_to_f32(gamma[k]));
+#pragma unroll
+    for (int j = 0; j < NV; j++) {
+        const int k = (tid + 256 * j) * 4;
+        if (k >= H) break;
+        f16 o[4];
+        o[0] = act_f16(v[j].x * rinv * __uint_as_float(g[j].x << 16));
+        o[1] = act_f16(v[j].y * rinv * __uint_as_float(g[j].x & 0xFFFF0000u));
+        o[2] = act_f16(v[j].z * rinv * __uint_as_float(g[j].y << 16));
+        o[3] = act_f16(v[j].w * rinv * __uint_as_float(g[j].y & 0xFFFF0000u));
+        *reinterpret_cast<uint2*>(orow + k) = *reinterpret_cast<const uint2*>(o);
+    }
 }
 
 struct SlotStarts { int32_t v[64]; };
@@ -77,7 +97,13 @@ __global__ void debug_dequant_kernel(DevLinear W, const int32_t* __restrict__ co
 }  // namespace
 
 int launch_rmsnorm(const float* x, const uint16_t* gamma, float eps, int M, int H, f16* out, hipStream_t stream) {
-    hipLaunchKernelGGL(rmsnorm_kernel, dim3(M), dim3(256), 0, stream, x, gamma, eps, H, out);
+    if (H % 4 || H > 16 * 1024) return -1;
+    const int nv = (H + 1023) / 1024;
+    if (nv <= 1) hipLaunchKernelGGL(rmsnorm_kernel<1>, dim3(M), dim3(256), 0, stream, x, gamma, eps, H, out);
+    else if (nv <= 2) hipLaunchKernelGGL(rmsnorm_kernel<2>, dim3(M), dim3(256), 0, stream, x, gamma, eps, H, out);
+    else if (nv <= 4) hipLaunchKernelGGL(rmsnorm_kernel<4>, dim3(M), dim3(256), 0, stream, x, gamma, eps, H, out);
+    else if (nv <= 8) hipLaunchKernelGGL(rmsnorm_kernel<8>, dim3(M), dim3(256), 0, stream, x, gamma, eps, H, out);
+    else hipLaunchKernelGGL(rmsnorm_kernel<16>, dim3(M), dim3(256), 0, stream, x, gamma, eps, H, out);
     return hipGetLastError() == hipSuccess ? 0 : -1;
 }
 
