@@ -34,27 +34,38 @@ PEAK_MFMA_TFLOPS = 2500.0        # dense bf16 / fp16 MFMA
 # (rocprofv3 --pmc, one pass each, over "bench.py --steps 2 --warmup 1
 # --no-cpu-baseline"), each divided by what the same counter reads per byte
 # for a plain device copy of known size ("bench.py --copy-calibration").
-# Keyed by the SHA-256 of the kernel's source file: once the source changes
+# Keyed by the SHA-256 of the kernel's source files: once one of them changes
 # the figure no longer describes the kernel and is reported as null.
 TRAFFIC = {
-    "prefill_gate_up": {"bytes": 131356219,
-                        "sha256": "02778ffde942a753e736a9e72b8fb5ff072350fba0cc27f744b10b8ac7de7539"},
-    "decode_fused": {"bytes": 134721722,
-                     "sha256": "2a352f22fb5e6e14e0a0691054f1d38a36a84ce1bdb7106e9dd5b5023818221b"},
+    "prefill_gate_up": {"bytes": 133036923,
+                       "sha256": "da4d33024a46a4ed2e1b33ecc24e8dcc099937cdec0cabe744acd9c774515614"},
+    "decode_fused": {"bytes": 133850047,
+                    "sha256": "a0d617f529e40bea725bd1cf691a68ebef83a62a53ee0537916492624c4f0c61"},
 }
 CSRC = os.path.join(ROOT, "paper_2607_15865_amd", "csrc")
 
 
-def traffic(key, source):
-    """Measured HBM bytes per launch of a kernel, or None if its source has
-    changed since the counters were taken."""
+TRAFFIC_SOURCES = {
+    "prefill_gate_up": ("gemm_w4.hip", "common.h", "launch.h"),
+    "decode_fused": ("decode_fused.hip", "decode_fused.h", "gemv_core.h", "common.h", "launch.h"),
+}
+
+
+def source_hash(key):
     import hashlib
+    h = hashlib.sha256()
+    for name in TRAFFIC_SOURCES[key]:
+        with open(os.path.join(CSRC, name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def traffic(key):
+    """Measured HBM bytes per launch of a kernel, or None if one of its
+    sources has changed since the counters were taken."""
     t = TRAFFIC.get(key)
-    if not t:
+    if not t or source_hash(key) != t["sha256"]:
         return None
-    with open(os.path.join(CSRC, source), "rb") as f:
-        if hashlib.sha256(f.read()).hexdigest() != t["sha256"]:
-            return None
     return t["bytes"]
 
 
@@ -338,7 +349,7 @@ def main():
                 "peak": PEAK_MFMA_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(gu_flop / (gu_avg * 1e-3) / 1e12 / PEAK_MFMA_TFLOPS, 4),
                 "avg_us": round(gu_avg * 1e3, 2), "launches": gu_n,
-                "traffic": traffic("prefill_gate_up", "gemm_w4.hip"),
+                "traffic": traffic("prefill_gate_up"),
                 "algorithmic_unit": "2 flop per weight per token (512 tokens x 4096 x 28672 weights)"}
     dgu_avg = dgu_ms / max(dgu_n, 1)
     roofline_decode = {"kernel": "persistent decode kernel (whole decode step, B=1, ctx 2048)",
@@ -346,7 +357,7 @@ def main():
                        "peak": PEAK_HBM_GBS, "unit": "GB/s",
                        "frac": round(by_d / (dgu_avg * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
                        "avg_us": round(dgu_avg * 1e3, 2), "launches": dgu_n,
-                       "traffic": traffic("decode_fused", "decode_fused.hip")}
+                       "traffic": traffic("decode_fused")}
     out = {
         "metric": "decode layer-steps/s (+ prefill/prefill_kv TFLOP/s) of a W4A16 Llama-3-8B-shaped layer",
         "value": round(1.0 / dec_s, 1),
