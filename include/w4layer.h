@@ -286,10 +286,11 @@ int layer_debug_decode_stamps(layer_t layer, uint64_t* out, int32_t n);
  * 6 the whole persistent decode launch);
  * kernel < 0 switches timing of that stage off.  While selected, each stage
  * call records a HIP event pair around that launch on the call's stream (at
- * most 4096 pairs per stage until the next read).  layer_profile_read waits
- * for the recorded events of a stage, returns the summed duration in
- * *total_ms and the number of timed launches in *launches, and clears the
- * record.  A layer_prefill_kv call with hist_len 0 counts as stage 0.
+ * most 4096 pairs per stage until the next read).  Switching timing off and
+ * on again with the same kernel keeps the record; selecting another kernel
+ * clears it.  layer_profile_read waits for the recorded events of a stage,
+ * returns the summed duration in *total_ms and the number of timed launches
+ * in *launches, and clears the record.  A layer_prefill_kv call with hist_len 0 counts as stage 0.
  * Errors: W4_EINVAL, W4_EHIP. */
 int layer_profile_kernel(layer_t layer, int32_t stage, int32_t kernel);
 int layer_profile_read(layer_t layer, int32_t stage, float* total_ms, int32_t* launches);

@@ -141,6 +141,7 @@ struct DevLinearOwned {
 struct Profiler {          // one timed kernel per stage
     static constexpr int kMax = 4096;
     int kernel[3] = {-1, -1, -1};
+    int recorded[3] = {-1, -1, -1};  // the kernel whose launches the record holds
     std::vector<hipEvent_t> ev[3];   // 2 per recorded launch
     int used[3] = {0, 0, 0};
     ~Profiler() {
@@ -1010,7 +1011,10 @@ int layer_profile_kernel(layer_t L, int32_t stage, int32_t kernel) {
     if (!L) return fail(W4_EINVAL, "null layer");
     if (stage < 0 || stage > 2) return fail(W4_EINVAL, "stage must be 0..2");
     L->prof.kernel[stage] = kernel < 0 ? -1 : kernel;
-    L->prof.used[stage] = 0;
+    if (kernel >= 0 && kernel != L->prof.recorded[stage]) {
+        L->prof.used[stage] = 0;
+        L->prof.recorded[stage] = kernel;
+    }
     return W4_OK;
 }
 
