@@ -151,7 +151,8 @@ struct RunCursor {
         const int KBf = W.K_pad >> 6;
         kb++;
         woff += 1024u;
-        if (((kb * 64) & ((1 << W.lgG) - 1)) == 0) grow += (uint32_t)W.N_dev;
+        if (W.lgG < 6) grow += (uint32_t)W.N_dev << (6 - W.lgG);   // groups of 32: two per tile
+        else if (((kb * 64) & ((1 << W.lgG) - 1)) == 0) grow += (uint32_t)W.N_dev;
         if (kb == run.kz) {
             kb = run.ka;
             woff += (uint32_t)(KBf - (run.kz - run.ka)) << 10;
