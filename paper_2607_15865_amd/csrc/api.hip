@@ -351,35 +351,38 @@ FusedPlan plan_fused(const layer_s* L, int B, int max_ctx, bool query_device) {
     p.S_qkv = L->S_qkv;
     p.S_o = L->S_o;
     p.S_down = L->S_down;
-    // attention units: B * n_kv_heads * nchunk, about one per block
+    // attention units: B * n_kv_heads * nchunk, about one per block; the
+    // chunk shrinks (in steps of 32 keys) until the block's LDS fits
     const int per_group = std::max(1, P / (B * c.n_kv_heads));
     int ch = (max_ctx + 1 + per_group - 1) / per_group;
     ch = std::max(16, (ch + 15) / 16 * 16);
     ch = std::min(ch, decode_fused_max_chunk(d));
-    p.chunk = ch;
-    p.nchunk = (max_ctx + 1 + ch - 1) / ch;
     const int kr_o = (L->o.d.K_pad / 64 + p.S_o - 1) / p.S_o * 64;
     const int kr_d = (L->down.d.K_pad / 64 + p.S_down - 1) / p.S_down * 64;
     p.ldx = std::max(std::max(H, kr_o), kr_d) + 8;
     const int maxb = B <= 1 ? 1 : 4;
     const size_t xs_bytes = (size_t)B * p.ldx * 2;
-    const size_t attn_bytes = (size_t)(MAXR * ch + NWAVE * MAXR * d + 2 * MAXR + (MAXR + 2) * d) * 4 + (size_t)(MAXR * d + 2 * d) * 2;
-    const int V = B * qd;
-    p.comb_per = (((V + P - 1) / P) + 1) & ~1;
-    p.comb_lpv = 1;
-    while (p.comb_lpv < p.nchunk && p.comb_lpv < 64) p.comb_lpv *= 2;
-    if (p.nchunk > 4 * p.comb_lpv) return p;
-    const size_t comb_bytes = (size_t)p.comb_per * 2;
     // activation rows, then the GEMV's zero operand and correction table; the
     // attention phase reuses this region
     p.off_zero = align256(xs_bytes);
     p.off_c64 = p.off_zero + 256;
     const size_t gemv_bytes = p.off_c64 + (size_t)((p.ldx - 8) / 64) * 8 * 4;
-    p.off_h = align256(std::max(std::max(gemv_bytes, attn_bytes), comb_bytes));
-    p.off_red = align256(p.off_h + (size_t)B * H * 4);
-    p.off_gam = align256(p.off_red + (size_t)(NWAVE * SLOTS * maxb * 32 + 8 + NWAVE * maxb + maxb * 32 + 2 * maxb) * 4);
-    p.lds_bytes = p.off_gam + (size_t)2 * H * 2;
+    const int V = B * qd;
+    p.comb_per = (((V + P - 1) / P) + 1) & ~1;
+    const size_t comb_bytes = (size_t)p.comb_per * 2;
+    for (;; ch = ch > 32 ? (ch - 1) / 32 * 32 : 16) {
+        p.chunk = ch;
+        p.nchunk = (max_ctx + 1 + ch - 1) / ch;
+        p.off_h = align256(std::max(std::max(gemv_bytes, decode_fused_attn_bytes(ch, d)), comb_bytes));
+        p.off_red = align256(p.off_h + (size_t)B * H * 4);
+        p.off_gam = align256(p.off_red + (size_t)(NWAVE * SLOTS * maxb * 32 + 8 + NWAVE * maxb + maxb * 32 + 2 * maxb) * 4);
+        p.lds_bytes = p.off_gam + (size_t)2 * H * 2;
+        if (p.lds_bytes <= 160 * 1024 || ch == 16) break;
+    }
     if (p.lds_bytes > 160 * 1024) return p;
+    p.comb_lpv = 1;
+    while (p.comb_lpv < p.nchunk && p.comb_lpv < 64) p.comb_lpv *= 2;
+    if (p.nchunk > 4 * p.comb_lpv) return p;
     if (query_device && decode_fused_blocks(d, B, p.lds_bytes) != p.nblocks) return p;
     Carve cv;
     p.qkv_part = cv.take((size_t)p.S_qkv * B * L->qkv.d.N_dev * 8);

@@ -56,3 +56,12 @@ void decode_fused_plan(int nblocks, const DevLinear& qkv, const DevLinear& o, co
 int decode_fused_blocks(int head_dim, int B, size_t lds_bytes);
 // Largest attention chunk (keys per unit) the kernel supports for head_dim.
 int decode_fused_max_chunk(int head_dim);
+// LDS bytes of the attention phase for chunks of ch keys, head size d: the K
+// and V stages ([ch rounded up to 32][d] bf16 each), the per-group outputs
+// and statistics ([ch / 32][8 heads][d + 2] fp32), q/k/v in fp32
+// ([10][d]), the rotated q, k and v in bf16 ([10][d]) and the mask values
+// (ch rounded up to 64, fp32).
+inline size_t decode_fused_attn_bytes(int ch, int d) {
+    const size_t chp = (size_t)(ch + 31) / 32 * 32, ng = chp / 32;
+    return 4 * chp * d + (ng * 8 * d + ng * 16 + 10 * (size_t)d) * 4 + 10 * (size_t)d * 2 + (chp + 63) / 64 * 64 * 4;
+}

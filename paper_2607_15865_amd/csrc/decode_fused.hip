@@ -40,7 +40,6 @@ constexpr int SPIN_MAX = 1 << 20;  // polls per thread per launch before the err
 constexpr int RING = 4;            // weight tiles in flight per wave (gate/up, down)
 constexpr int RING_QKV = 4;        // q/k/v: its run is about 4 tiles per wave
 constexpr int RING_O = 4;          // o_proj: its run is 2 to 4 tiles per wave
-constexpr int NIT = 4;             // K/V register rows per lane: chunk <= NIT * NWAVE * (64 / (d / 8))
 constexpr int MAXS = 2;            // k-parts of a column tile
 constexpr int MAXR = 8;            // query heads per kv head
 constexpr int SLOTS = 4;           // column tiles per block in one product
@@ -212,6 +211,30 @@ __device__ __forceinline__ int devpos(int j) {
     return p * 32 + (j & 31);
 }
 
+// Chunk partial of head i, dim `dim` from the ng key groups' (max, sum,
+// output) in LDS (gst [group][MAXR][2], ored [group][MAXR][D]), rescaled to
+// their common max M.  NGR >= ng bounds the unrolled loop; the slots past
+// ng read group 0 and weigh 0, so the loads need no branches.
+template <int NGR, int D>
+__device__ __forceinline__ void group_merge(const float* gst, const float* ored, int ng, int i, int dim, float& M,
+                                            float& v, float& l) {
+    float mw[NGR];
+#pragma unroll
+    for (int w = 0; w < NGR; w++) mw[w] = gst[((w < ng ? w : 0) * MAXR + i) * 2];
+    M = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < NGR; w++) M = w < ng ? fmaxf(M, mw[w]) : M;
+    v = 0.f;
+    l = 0.f;
+#pragma unroll
+    for (int w = 0; w < NGR; w++) {
+        const int ww = w < ng ? w : 0;
+        const float sc = (w < ng && mw[w] != -INFINITY) ? exp2f(mw[w] - M) : 0.f;
+        v += sc * ored[(ww * MAXR + i) * D + dim];
+        l += sc * gst[(ww * MAXR + i) * 2 + 1];
+    }
+}
+
 // ---------------------------------------------------------------- kernel
 
 template <int D, int MAXB>
@@ -355,56 +378,84 @@ __global__ void __launch_bounds__(NTHR) decode_fused_kernel(DecodeFusedArgs a) {
             put_tagged(a.qkv_part + ((size_t)s1 * B + b) * Nq + t1 * 32 + cc, __float_as_uint(red_sum(0, b, cc)), ep);
         }
     }
-    // the next product's weights are requested after the results went out
-    // (the memory pipeline serves a wave's requests in order)
-    prefetch(3);
-    stamp_done(0);
-
     // ================= P2: attention units =================
+    // A unit is one chunk of keys of one (row, kv head).  Its K and V rows go
+    // straight from memory to LDS; the r query heads of the group are the
+    // columns of the 16x16x32 bf16 MFMA.  Key group k (keys 32k .. 32k + 31)
+    // goes to two waves: each forms the group's scores S^T = K Q^T as two
+    // 16-key tiles whose rows are fed in the order that leaves the
+    // probabilities in the operand layout of P^T, the softmax over the
+    // group's keys in registers, then half of the dims of O^T = V^T P^T with
+    // P as a bf16 pair hi + lo.  The groups' (max, sum, output) meet in LDS
+    // and leave as one chunk partial (up to 8 groups: 256 keys).
     {
-        constexpr int LPK = D / 8, KPW = 64 / LPK;    // q.k: lanes per key (8 dims each), keys per wave
-        constexpr int DP = D / 2, KPL = 128 / D;      // p.v: lanes per key (2 dims each), keys per load
+        constexpr int NCK = D / 8;                   // 16-byte chunks per K / V row
+        constexpr int KROWS = 1024 / (2 * D);         // rows per 1 KB stage load
         const int CH = a.chunk, NCH = a.nchunk;
-        const int kl = lane / LPK, dseg = lane % LPK;
-        const int vdp = lane % DP, vks = lane / DP;
-        float* sc = reinterpret_cast<float*>(smem);                  // [r][CH]
-        float* ored = sc + MAXR * CH;                                // [NWAVE][r][D]
-        float* stat = ored + NWAVE * MAXR * D;                       // [r][2]
-        float* qkvf = stat + 2 * MAXR;                               // [r + 2][D] device order
-        uint16_t* qb = reinterpret_cast<uint16_t*>(qkvf + (MAXR + 2) * D);   // [r][D] bf16
-        uint16_t* knb = qb + MAXR * D;                               // [D]
-        uint16_t* vnb = knb + D;                                     // [D]
+        const int CHP = (CH + 31) & ~31, NG = CHP / 32;
+        unsigned char* Kst = smem;                                           // [CHP][D] bf16
+        unsigned char* Vst = smem + (size_t)CHP * D * 2;                     // [CHP][D] bf16
+        float* ored = reinterpret_cast<float*>(Vst + (size_t)CHP * D * 2);   // [NG][MAXR][D]
+        float* gst = ored + NG * MAXR * D;                                   // [NG][MAXR][2]
+        float* qkvf = gst + NG * MAXR * 2;                                   // [r + 2][D] device order
+        uint16_t* qb = reinterpret_cast<uint16_t*>(qkvf + (MAXR + 2) * D);    // [r][D] bf16
+        uint16_t* knb = qb + MAXR * D;                                       // [D]
+        uint16_t* vnb = knb + D;                                             // [D]
+        float* mst = reinterpret_cast<float*>(vnb + D);                      // [CHP] mask values
+        // 16-byte chunk c of stage row k sits at c ^ kswz(k) (K) or c ^ vswz(k)
+        // (V): the fragment reads below then hit distinct banks
+        auto kswz = [](int k) { return ((k & 3) | ((k >> 1) & 12)) & (NCK - 1); };
+        auto vswz = [](int k) { return 2 * ((k >> 3) & 3); };
         const float LOG2E = 1.4426950408889634f;
+        const int n16 = lane & 15, q4 = lane >> 4;
         const int units = B * nkv * NCH;
+        // K and V rows start .. start + 32 ng - 1 of unit u into the stages;
+        // rows past the history (the new key, the padding) read row 0 and
+        // are rewritten before use
+        auto load_stage = [&](int u) {
+            const int b = u / (nkv * NCH), g = (u / NCH) % nkv, chunk = u % NCH;
+            const int ctx = meta[b];
+            const int start = chunk * CH, end = min(start + CH, ctx + 1);
+            const int hist_end = min(end, ctx), ng = (end - start + 31) / 32;
+            if (a.mask && wave < ng / 2 + (ng & 1)) {     // mask values of keys start + 64 wave + lane
+                const int kk = 64 * wave + lane;
+                __builtin_amdgcn_global_load_lds(
+                    reinterpret_cast<const void*>(a.mask + (size_t)b * a.max_seq + (start + kk < end ? start + kk : start)),
+                    (__attribute__((address_space(3))) void*)(mst + 64 * wave), 4, 0, 0);
+            }
+            const uint16_t* kc = a.k_cache + (size_t)b * a.sb + (size_t)g * a.sh;
+            const uint16_t* vc = a.v_cache + (size_t)b * a.sb + (size_t)g * a.sh;
+            for (int i = wave; i < ng * 32 / KROWS; i += NWAVE) {
+                const int row = i * KROWS + lane / NCK, pc = lane % NCK;
+                const int key = start + row;
+                const size_t src = (size_t)(key < hist_end ? key : 0) * D;
+                __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(kc + src + (pc ^ kswz(row)) * 8),
+                                                 (__attribute__((address_space(3))) void*)(Kst + i * 1024), 16, 0, 0);
+                __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(vc + src + (pc ^ vswz(row)) * 8),
+                                                 (__attribute__((address_space(3))) void*)(Vst + i * 1024), 16, 0, 0);
+            }
+        };
+        // The o_proj weights are requested once the q/k/v results went out
+        // (the memory pipeline serves a wave's requests in order), then the
+        // first unit's K and V; P1 has finished with the activation rows that
+        // the stages overwrite.
+        prefetch(3);
+        if (blk < units) load_stage(blk);
+        stamp_done(0);
         for (int u = blk; u < units; u += P) {
             const int b = u / (nkv * NCH), g = (u / NCH) % nkv, chunk = u % NCH;
             const int ctx = meta[b];
             const int start = chunk * CH, end = min(start + CH, ctx + 1);
             if (start >= end) continue;
-            const int nkeys = end - start, hist_end = min(end, ctx);
-            const uint16_t* kc = a.k_cache + (size_t)b * a.sb + (size_t)g * a.sh;
-            const uint16_t* vc = a.v_cache + (size_t)b * a.sb + (size_t)g * a.sh;
-            // Pass it of wave w covers keys start + (it*NWAVE + w)*KPW + (0..KPW-1).
-            // K: lane holds 8 dims of key kl; V: lane holds dims 2*vdp, 2*vdp+1 of
-            // keys j*KPL + vks.  Mask values and the RoPE factors of this
-            // thread's dim are requested too, all before the wait for q/k/v;
-            // rows past the history read row 0 and are not used.
-            const float* mrow = a.mask ? a.mask + (size_t)b * a.max_seq : nullptr;
-            u32x4 kr[NIT];
-            uint32_t vr[NIT][KPW / KPL];
-            float mk[NIT];
-#pragma unroll
-            for (int it = 0; it < NIT; it++) {
-                const int kb0 = start + (it * NWAVE + wave) * KPW;
-                const int key = kb0 + kl;
-                kr[it] = *reinterpret_cast<const u32x4*>(kc + (size_t)(key < hist_end ? key : 0) * D + dseg * 8);
-#pragma unroll
-                for (int j = 0; j < KPW / KPL; j++) {
-                    const int kv = kb0 + j * KPL + vks;
-                    vr[it][j] = *reinterpret_cast<const uint32_t*>(vc + (size_t)(kv < hist_end ? kv : 0) * D + vdp * 2);
-                }
-                mk[it] = mrow ? mrow[key < end ? key : start] : 0.f;
-            }
+            const int nkeys = end - start;
+            const int ng = (nkeys + 31) / 32;
+            // two waves per key group: each repeats the group's scores and
+            // softmax and takes half of its 16-dim blocks of P V
+            constexpr int ns = 2;
+            const int gw = wave / ns, part = wave % ns;
+            if (u != blk) load_stage(u);
+            // the RoPE factors of this thread's dim, requested before the wait
+            // for q/k/v
             const int ps = meta[MAXB + b];
             const int jr = tid % (D / 2);            // the RoPE dim of every item of this thread
             const float rc = a.rope_cos[(size_t)ps * (D / 2) + jr], rs = a.rope_sin[(size_t)ps * (D / 2) + jr];
@@ -418,17 +469,39 @@ __global__ void __launch_bounds__(NTHR) decode_fused_kernel(DecodeFusedArgs a) {
                            return qrow + col;
                        },
                        [&](int i, float v) { qkvf[i] = v; });
-            __syncthreads();
+            __syncthreads();           // also: the stage loads have landed
             stamp_done(8);
-            // RoPE of q and k (Sec. 3.1, table of Sec. 4.6.2), bf16
+            // RoPE of q and k (Sec. 3.1, table of Sec. 4.6.2), bf16; the new
+            // key and value also replace stage row ctx - start when the chunk
+            // holds it, and the padding rows of V become zeros (their
+            // probabilities are 0, and 0 times a stale NaN would not be)
+            const int nrow = ctx - start;
+            const bool has_new = ctx < end;
             for (int i = tid; i < (r + 1) * (D / 2); i += NTHR) {
                 const int hh = i / (D / 2), j = jr;
                 const float v0 = qkvf[hh * D + devpos<D>(j)], v1 = qkvf[hh * D + devpos<D>(j + D / 2)];
-                uint16_t* dst = hh < r ? qb + hh * D : knb;
-                dst[j] = bf16_bits_rne(v0 * rc - v1 * rs);
-                dst[j + D / 2] = bf16_bits_rne(v1 * rc + v0 * rs);
+                const uint16_t e0 = bf16_bits_rne(v0 * rc - v1 * rs), e1 = bf16_bits_rne(v1 * rc + v0 * rs);
+                if (hh < r) {
+                    qb[hh * D + j] = e0;
+                    qb[hh * D + j + D / 2] = e1;
+                } else {
+                    knb[j] = e0;
+                    knb[j + D / 2] = e1;
+                    if (has_new) {
+                        uint16_t* kr = reinterpret_cast<uint16_t*>(Kst + (size_t)nrow * D * 2);
+                        kr[(((j >> 3) ^ kswz(nrow)) << 3) | (j & 7)] = e0;
+                        kr[((((j + D / 2) >> 3) ^ kswz(nrow)) << 3) | (j & 7)] = e1;
+                    }
+                }
             }
-            for (int j = tid; j < D; j += NTHR) vnb[j] = bf16_bits_rne(qkvf[(r + 1) * D + devpos<D>(j)]);
+            for (int j = tid; j < D; j += NTHR) {
+                const uint16_t e = bf16_bits_rne(qkvf[(r + 1) * D + devpos<D>(j)]);
+                vnb[j] = e;
+                if (has_new)
+                    reinterpret_cast<uint16_t*>(Vst + (size_t)nrow * D * 2)[(((j >> 3) ^ vswz(nrow)) << 3) | (j & 7)] = e;
+            }
+            for (int i = tid; i < (ng * 32 - nkeys) * NCK; i += NTHR)
+                reinterpret_cast<u32x4*>(Vst + (size_t)nkeys * D * 2)[i] = u32x4{0u, 0u, 0u, 0u};
             __syncthreads();
             stamp_done(16);
             if (chunk == 0) {     // the new row goes to cache slot ctx (read by later launches only)
@@ -436,97 +509,99 @@ __global__ void __launch_bounds__(NTHR) decode_fused_kernel(DecodeFusedArgs a) {
                 uint16_t* vw = a.v_cache + (size_t)b * a.sb + (size_t)g * a.sh + (size_t)ctx * D;
                 for (int j = tid; j < D; j += NTHR) { kw[j] = knb[j]; vw[j] = vnb[j]; }
             }
-            // scores (log2 domain) of every key of the chunk for the r heads: the
-            // LPK lanes of a key meet with DPP row operations
+            if (gw < ng) {
+                // S^T of the tiles t = 0, 1: A row n16 of tile t is key
+                // 32 gw + 8 (n16 / 4) + 4 t + n16 % 4, so output register j of
+                // lane (n16, q4) is key 8 q4 + 4 t + j of the group's 32, head n16.
+                // Q^T (B operand): head n16 (zero past r), dims 32 s + 8 q4 .. + 7
+                f32x4 sacc[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+                const int row0 = 32 * gw + 8 * (n16 >> 2) + (n16 & 3), row1 = row0 + 4;
+                const unsigned char* K0 = Kst + (size_t)row0 * D * 2;
+                const unsigned char* K1 = Kst + (size_t)row1 * D * 2;
+                const uint16_t* qsrc = qb + (n16 < r ? n16 : 0) * D + 8 * q4;
 #pragma unroll
-            for (int it = 0; it < NIT; it++) {
-                const int kbase = (it * NWAVE + wave) * KPW;
-                if (kbase >= nkeys) break;
-                const int key = start + kbase + kl;
-                uint32_t kw[4];
-                if (key == ctx) {
-                    const uint32_t* kp = reinterpret_cast<const uint32_t*>(knb + dseg * 8);
-                    kw[0] = kp[0]; kw[1] = kp[1]; kw[2] = kp[2]; kw[3] = kp[3];
-                } else {
-                    const u32x4 kk = kr[it];
-                    kw[0] = kk[0]; kw[1] = kk[1]; kw[2] = kk[2]; kw[3] = kk[3];
+                for (int s = 0; s < D / 32; s++) {
+                    const u32x4 w = *reinterpret_cast<const u32x4*>(qsrc + 32 * s);
+                    const bf16x8 qf = __builtin_bit_cast(bf16x8, n16 < r ? w : u32x4{0u, 0u, 0u, 0u});
+                    const bf16x8 k0 = *reinterpret_cast<const bf16x8*>(K0 + (((4 * s + q4) ^ kswz(row0)) << 4));
+                    const bf16x8 k1 = *reinterpret_cast<const bf16x8*>(K1 + (((4 * s + q4) ^ kswz(row1)) << 4));
+                    sacc[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k0, qf, sacc[0], 0, 0, 0);
+                    sacc[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k1, qf, sacc[1], 0, 0, 0);
                 }
-                for (int i = 0; i < r; i++) {
-                    const uint32_t* qp = reinterpret_cast<const uint32_t*>(qb + i * D + dseg * 8);
-                    float v = 0.f;
+                // scores in the log2 domain, masked past the chunk; max and sum
+                // over the group's keys (registers, then lanes n16 + 16 q4)
+                float sv[8];
+                float mx = -INFINITY;
 #pragma unroll
-                    for (int pp = 0; pp < 4; pp++)
-                        v = __builtin_amdgcn_fdot2_f32_bf16(as_bf16x2(qp[pp]), as_bf16x2(kw[pp]), v, false);
-                    v = row_sum<LPK>(v);
-                    if (dseg == 0 && key < end) {
-                        float sv = v * a.scale_log2;
-                        if (mrow) sv += mk[it] * LOG2E;
-                        sc[i * CH + kbase + kl] = sv;
-                    }
+                for (int e = 0; e < 8; e++) {
+                    const int kk = 32 * gw + 8 * q4 + e;
+                    float v = sacc[e / 4][e % 4] * a.scale_log2;
+                    if (a.mask) v += mst[kk] * LOG2E;
+                    v = kk < nkeys ? v : -INFINITY;
+                    sv[e] = v;
+                    mx = fmaxf(mx, v);
+                }
+                mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+                mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+                bf16x8 phi, plo;
+                float ls = 0.f;
+#pragma unroll
+                for (int e = 0; e < 8; e++) {
+                    const float pv = (mx == -INFINITY) ? 0.f : exp2f(sv[e] - mx);
+                    ls += pv;
+                    const __bf16 hi = (__bf16)pv;
+                    phi[e] = hi;
+                    plo[e] = (__bf16)(pv - (float)hi);
+                }
+                ls += __shfl_xor(ls, 16, 64);
+                ls += __shfl_xor(ls, 32, 64);
+                // O^T += V^T P^T per 16-dim block: lane (n16, q4) holds V of keys
+                // 8 q4 .. + 7, dim 16 db + n16 (16-bit reads of the V stage)
+                const uint16_t* Vw = reinterpret_cast<const uint16_t*>(Vst + (size_t)(32 * gw + 8 * q4) * D * 2);
+                const int nb = D / 16 / ns;
+#pragma unroll
+                for (int d0 = 0; d0 < D / 16; d0++) {
+                    if (d0 >= nb) break;
+                    const int db = part * nb + d0;
+                    const int pos = ((((2 * db + (n16 >> 3)) ^ (2 * q4)) << 3) | (n16 & 7));
+                    u32x4 vw;
+#pragma unroll
+                    for (int j = 0; j < 4; j++)
+                        vw[j] = (uint32_t)Vw[2 * j * D + pos] | ((uint32_t)Vw[(2 * j + 1) * D + pos] << 16);
+                    const bf16x8 vf = __builtin_bit_cast(bf16x8, vw);
+                    f32x4 o = f32x4{0.f, 0.f, 0.f, 0.f};
+                    o = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, phi, o, 0, 0, 0);
+                    o = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, plo, o, 0, 0, 0);
+                    // register j: dim 16 db + 4 q4 + j of head n16
+                    if (n16 < r)
+                        *reinterpret_cast<f32x4*>(ored + (gw * MAXR + n16) * D + 16 * db + 4 * q4) = o;
+                }
+                if (n16 < r && q4 == 0 && part == 0) {
+                    gst[(gw * MAXR + n16) * 2] = mx;
+                    gst[(gw * MAXR + n16) * 2 + 1] = ls;
                 }
             }
             __syncthreads();
             stamp_done(17);
-            for (int i = wave; i < r; i += NWAVE) {
-                float mx = -INFINITY;
-                for (int j = lane; j < nkeys; j += 64) mx = fmaxf(mx, sc[i * CH + j]);
-                mx = wave_max(mx);
-                float sum = 0.f;
-                for (int j = lane; j < nkeys; j += 64) {
-                    const float pv = (mx == -INFINITY) ? 0.f : exp2f(sc[i * CH + j] - mx);
-                    sc[i * CH + j] = pv;
-                    sum += pv;
-                }
-                sum = wave_sum(sum);
-                if (lane == 0) { stat[2 * i] = mx; stat[2 * i + 1] = sum; }
-            }
-            __syncthreads();
-            stamp_done(18);
-            // chunk output of every head, sum of p * v: each lane sums its keys
-            // for its two dims, the waves meet in LDS
-            for (int i = 0; i < r; i++) {
-                float o0 = 0.f, o1 = 0.f;
-#pragma unroll
-                for (int it = 0; it < NIT; it++) {
-                    const int kbase = (it * NWAVE + wave) * KPW;
-                    if (kbase >= nkeys) break;
-#pragma unroll
-                    for (int j = 0; j < KPW / KPL; j++) {
-                        const int ko = kbase + j * KPL + vks;          // key - start
-                        if (ko < nkeys) {
-                            const uint32_t vw = (start + ko == ctx)
-                                ? *reinterpret_cast<const uint32_t*>(vnb + 2 * vdp) : vr[it][j];
-                            const float pv = sc[i * CH + ko];
-                            o0 += pv * __uint_as_float(vw << 16);
-                            o1 += pv * __uint_as_float(vw & 0xFFFF0000u);
-                        }
-                    }
-                }
-                if (KPL > 1) {        // the lanes of the other keys of a load hold the same dims
-                    o0 += __shfl_xor(o0, DP, 64);
-                    o1 += __shfl_xor(o1, DP, 64);
-                }
-                if (vks == 0) {
-                    ored[(wave * MAXR + i) * D + 2 * vdp] = o0;
-                    ored[(wave * MAXR + i) * D + 2 * vdp + 1] = o1;
-                }
-            }
-            __syncthreads();
+            // the chunk partial: the groups' outputs rescaled to the common max
             uint64_t* ap = a.apart + ((size_t)b * nq + g * r) * NCH * (D + 2) + (size_t)chunk * (D + 2);
             for (int idx = tid; idx < r * D; idx += NTHR) {
                 const int i = idx / D, dim = idx - i * D;
-                float v = 0.f;
-#pragma unroll
-                for (int w = 0; w < NWAVE; w++) v += ored[(w * MAXR + i) * D + dim];
-                put_tagged(ap + (size_t)i * NCH * (D + 2) + dim, __float_as_uint(v), ep);
+                float M, v, l;
+                if (ng <= 4) group_merge<4, D>(gst, ored, ng, i, dim, M, v, l);
+                else group_merge<8, D>(gst, ored, ng, i, dim, M, v, l);
+                uint64_t* aph = ap + (size_t)i * NCH * (D + 2);
+                put_tagged(aph + dim, __float_as_uint(v), ep);
+                if (dim == 0) {
+                    put_tagged(aph + D, __float_as_uint(M), ep);
+                    put_tagged(aph + D + 1, __float_as_uint(l), ep);
+                }
             }
-            if (tid < r) {
-                uint64_t* aph = ap + (size_t)tid * NCH * (D + 2);
-                put_tagged(aph + D, __float_as_uint(stat[2 * tid]), ep);
-                put_tagged(aph + D + 1, __float_as_uint(stat[2 * tid + 1]), ep);
-            }
-            __syncthreads();
+            // the next unit writes the stages and q/k/v only after its own
+            // first barrier, and the group outputs after its second: every
+            // thread has finished this unit's reads by then
         }
+        __syncthreads();
         stamp_done(9);
 
         // ---- combine: this block's slice [v0, v1) of A (an even count).  LPV
@@ -747,7 +822,7 @@ void decode_fused_plan(int P, const DevLinear& qkv, const DevLinear& o, const De
     }
 }
 
-int decode_fused_max_chunk(int head_dim) { return NIT * NWAVE * (64 / (head_dim / 8)); }
+int decode_fused_max_chunk(int) { return 256; }   // 8 key groups
 
 int decode_fused_blocks(int head_dim, int B, size_t lds_bytes) {
     int dev = 0, cus = 0, occ = 0;
@@ -769,6 +844,9 @@ int decode_fused_blocks(int head_dim, int B, size_t lds_bytes) {
 
 int launch_decode_fused(const DecodeFusedArgs& a, hipStream_t stream) {
     if (a.B > 4 || a.S_qkv > MAXS || a.S_o > MAXS || a.S_down > MAXS) return -1;
+    if (a.chunk < 1 || a.chunk > decode_fused_max_chunk(a.d) || a.nkv < 1 || a.nq % a.nkv || a.nq / a.nkv > MAXR)
+        return -1;
+    if (a.off_h < decode_fused_attn_bytes(a.chunk, a.d)) return -1;
     if (a.d == 128) return a.B <= 1 ? launch_t<128, 1>(a, stream) : launch_t<128, 4>(a, stream);
     if (a.d == 64) return a.B <= 1 ? launch_t<64, 1>(a, stream) : launch_t<64, 4>(a, stream);
     return -1;
