@@ -125,6 +125,76 @@ def stage_bytes(cfg, M, T, L, B):
             + 8 * M * cfg.hidden)
 
 
+# ---------------------------------------------------------------- extras
+
+def extras(cfg, layers, caches, binding, synth, stream, reps=30):
+    """Timed after the bench steps, outside them: speculative-decode
+    verification (prefill_kv of T = 2, 4, 8 draft tokens over a 2048-token
+    history) and a 4096-token prompt as one prefill against 4 segments of 1024
+    (one prefill, three prefill_kv).  Median of `reps` calls rotating over the
+    device copies, HIP events on the library's stream."""
+    import numpy as np
+    import torch
+    h0 = layers[0].handle
+    sp = stream.cuda_stream
+    L, Tp, chunk = 2048, cfg.max_seq, 1024
+    ws_bytes = max([binding.layer_workspace_size(h0, 1, 1, T, L) for T in (2, 4, 8)]
+                   + [binding.layer_workspace_size(h0, 0, 1, Tp, 0),
+                      binding.layer_prefill_chunked_workspace_size(h0, Tp, chunk)])
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
+
+    def f32(bits):
+        u = bits.astype(np.uint32) << 16
+        return torch.from_numpy(u.view(np.float32).copy()).cuda()
+
+    def median_us(call):
+        ts = []
+        for i in range(reps + 2):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            call(i)
+            e1.record(stream)
+            e1.synchronize()
+            if i >= 2:
+                ts.append(e0.elapsed_time(e1) * 1e3)
+        return float(np.median(ts))
+
+    res = {"verify": {}}
+    for T in (2, 4, 8):
+        x = f32(synth.activations(cfg, synth.TID_X_PREFILL_KV, T))
+        y = torch.empty_like(x)
+        pos = torch.arange(L, L + T, dtype=torch.int32, device="cuda")
+
+        def call(i, x=x, y=y, pos=pos, T=T):
+            k, v = caches[i % len(layers)]
+            binding.check(binding.layer_prefill_kv(layers[i % len(layers)].handle, x, pos, T, L, k, v, y, ws,
+                                                   ws_bytes, sp))
+        us = median_us(call)
+        by = stage_bytes(cfg, T, T, L, 1)
+        res["verify"][f"T{T}"] = {"hist": L, "us": round(us, 2), "mbytes": round(by / 1e6, 2),
+                                  "gbps": round(by / (us * 1e-6) / 1e9, 1),
+                                  "frac_hbm": round(by / (us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)}
+    x = f32(synth.activations(cfg, synth.TID_X_PREFILL, Tp))
+    y = torch.empty_like(x)
+    pos = torch.arange(Tp, dtype=torch.int32, device="cuda")
+    fl = stage_flops(cfg, Tp, Tp, 0, 1)
+
+    def one(i):
+        k, v = caches[i % len(layers)]
+        binding.check(binding.layer_prefill(layers[i % len(layers)].handle, x, pos, Tp, k, v, y, ws, ws_bytes, sp))
+
+    def seg(i):
+        k, v = caches[i % len(layers)]
+        binding.check(binding.layer_prefill_chunked(layers[i % len(layers)].handle, x, pos, Tp, chunk, k, v, y, ws,
+                                                    ws_bytes, sp))
+    for name, call in (("prefill_4096", one), ("prefill_4096_in_4x1024", seg)):
+        us = median_us(call)
+        res[name] = {"ms": round(us / 1e3, 4), "gflop": round(fl / 1e9, 1),
+                     "tflops": round(fl / (us * 1e-6) / 1e12, 1),
+                     "frac_mfma": round(fl / (us * 1e-6) / 1e12 / PEAK_MFMA_TFLOPS, 4)}
+    return res
+
+
 # ---------------------------------------------------------------- CPU baseline
 
 def cpu_baseline(cfg, w):
@@ -388,6 +458,7 @@ def main():
         "roofline": roofline,
         "roofline_decode": roofline_decode,
     }
+    out["extras"] = extras(cfg, layers, caches, binding, synth, stream)
     if not args.no_cpu_baseline:
         log("bench: timing the CPU oracle (one decode layer-step)")
         out["cpu_baseline"] = cpu_baseline(cfg, w)

@@ -171,6 +171,24 @@ int layer_prefill_kv(layer_t layer, const float* x, const int32_t* pos, int32_t 
                      void* k_cache, void* v_cache, float* y,
                      void* ws, size_t ws_bytes, void* stream);
 
+/* Long prompts in segments (the third scenario of Sec. 4.1): tokens
+ * 0..chunk-1 by layer_prefill, then every following run of chunk tokens
+ * (the last one ragged) by layer_prefill_kv over the tokens before it, all
+ * on `stream` in order.  The result equals layer_prefill over the T tokens
+ * up to rounding order (each segment's attention sees the cache slots the
+ * earlier segments wrote).
+ *   x, y     fp32 [T][hidden]; pos int32 [T]; caches as for layer_prefill
+ *            (slots 0..T-1 are written);
+ *   chunk    tokens per segment, >= 1;
+ *   ws       at least layer_prefill_chunked_workspace_size(layer, T, chunk)
+ *            bytes, reused by every segment.
+ * Errors: as layer_prefill; arguments are validated before the first
+ * segment is enqueued. */
+size_t layer_prefill_chunked_workspace_size(layer_t layer, int32_t T, int32_t chunk);
+int layer_prefill_chunked(layer_t layer, const float* x, const int32_t* pos, int32_t T, int32_t chunk,
+                          void* k_cache, void* v_cache, float* y,
+                          void* ws, size_t ws_bytes, void* stream);
+
 /* Decode (Sec. 4.4): one new token for each of B sequences.
  *   x         fp32 [B][hidden];
  *   pos       int32 [B] position ids;

@@ -73,6 +73,8 @@ _SIG = {
     "layer_workspace_size": (ctypes.c_size_t, [_P, _I, _I, _I, _I]),
     "layer_prefill": (ctypes.c_int, [_P, _P, _P, _I, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "layer_prefill_kv": (ctypes.c_int, [_P, _P, _P, _I, _I, _P, _P, _P, _P, ctypes.c_size_t, _P]),
+    "layer_prefill_chunked_workspace_size": (ctypes.c_size_t, [_P, _I, _I]),
+    "layer_prefill_chunked": (ctypes.c_int, [_P, _P, _P, _I, _I, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "layer_decode": (ctypes.c_int, [_P, _P, _P, _P, _I, _P, _I, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "kv_append": (ctypes.c_int, [ctypes.POINTER(kv_desc), _P, _P, _P, _P, _I, _I, _P, _P]),
     "layer_debug_dequant": (ctypes.c_int, [_P, _I, _P, _P]),
@@ -194,6 +196,15 @@ def layer_prefill(handle, x, pos, T, k_cache, v_cache, y, ws, ws_bytes, stream=N
 def layer_prefill_kv(handle, x, pos, T, hist_len, k_cache, v_cache, y, ws, ws_bytes, stream=None) -> int:
     return _lib.layer_prefill_kv(handle, _ptr(x), _ptr(pos), T, hist_len, _ptr(k_cache), _ptr(v_cache), _ptr(y),
                                  _ptr(ws), ws_bytes, _stream(stream))
+
+
+def layer_prefill_chunked_workspace_size(handle, T, chunk) -> int:
+    return _lib.layer_prefill_chunked_workspace_size(handle, T, chunk)
+
+
+def layer_prefill_chunked(handle, x, pos, T, chunk, k_cache, v_cache, y, ws, ws_bytes, stream=None) -> int:
+    return _lib.layer_prefill_chunked(handle, _ptr(x), _ptr(pos), T, chunk, _ptr(k_cache), _ptr(v_cache), _ptr(y),
+                                      _ptr(ws), ws_bytes, _stream(stream))
 
 
 def layer_decode(handle, x, pos, ctx_lens, max_ctx, attn_mask, B, k_cache, v_cache, y, ws, ws_bytes,
@@ -322,6 +333,17 @@ class Layer:
     def prefill_kv(self, x, pos, hist_len, k_cache, v_cache, y, stream=None):
         ws, n = self.workspace(STAGE_PREFILL_KV, 1, x.shape[0], hist_len)
         check(layer_prefill_kv(self.handle, x, pos, x.shape[0], hist_len, k_cache, v_cache, y, ws, n, stream))
+
+    def prefill_chunked(self, x, pos, chunk, k_cache, v_cache, y, stream=None):
+        import torch
+        T = x.shape[0]
+        n = layer_prefill_chunked_workspace_size(self.handle, T, chunk)
+        if n == 0:
+            raise W4Error(W4_EINVAL, "invalid workspace query")
+        if self._ws.numel() < n:
+            self._ws = torch.empty(n, dtype=torch.uint8, device="cuda")
+        check(layer_prefill_chunked(self.handle, x, pos, T, chunk, k_cache, v_cache, y, self._ws, self._ws.numel(),
+                                    stream))
 
     def decode(self, x, pos, ctx_lens, max_ctx, k_cache, v_cache, y, attn_mask=None, stream=None):
         B = x.shape[0]

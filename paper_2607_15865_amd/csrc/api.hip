@@ -713,6 +713,30 @@ int layer_prefill_kv(layer_t L, const float* x, const int32_t* pos, int32_t T, i
     return run_prefill(L, x, pos, T, hist_len, kc, vc, y, ws, ws_bytes, stream);
 }
 
+size_t layer_prefill_chunked_workspace_size(layer_t L, int32_t T, int32_t chunk) {
+    if (!L || T < 1 || chunk < 1) return 0;
+    size_t n = 0;
+    for (int s = 0; s < T; s += chunk) n = std::max(n, plan_prefill(L, std::min(chunk, T - s), s).total);
+    return n;
+}
+
+int layer_prefill_chunked(layer_t L, const float* x, const int32_t* pos, int32_t T, int32_t chunk, void* kc,
+                          void* vc, float* y, void* ws, size_t ws_bytes, void* stream) {
+    if (!L) return fail(W4_EINVAL, "null layer");
+    if (!x || !pos || !kc || !vc || !y || !ws) return fail(W4_EINVAL, "null pointer argument");
+    if (T < 1 || chunk < 1) return fail(W4_EINVAL, "T and chunk must be >= 1");
+    if (T > L->cfg.max_seq) return fail(W4_ECAPACITY, "T = %d exceeds max_seq %d", T, L->cfg.max_seq);
+    const size_t need = layer_prefill_chunked_workspace_size(L, T, chunk);
+    if (ws_bytes < need) return fail(W4_EWORKSPACE, "workspace %zu bytes, need %zu", ws_bytes, need);
+    const size_t H = (size_t)L->cfg.hidden;
+    for (int s = 0; s < T; s += chunk) {
+        const int n = std::min(chunk, T - s);
+        const int rc = run_prefill(L, x + (size_t)s * H, pos + s, n, s, kc, vc, y + (size_t)s * H, ws, ws_bytes, stream);
+        if (rc) return rc;
+    }
+    return W4_OK;
+}
+
 int layer_decode(layer_t L, const float* x, const int32_t* pos, const int32_t* ctx_lens, int32_t max_ctx,
                  const float* attn_mask, int32_t B, void* kc, void* vc, float* y, void* ws, size_t ws_bytes,
                  void* stream) {

@@ -89,6 +89,63 @@ def test_prefill_kv(name, T, L):
     _check_new_kv(k, v, ko, vo, L, T)
 
 
+VERIFY_CASES = [("tiny", 2, 120), ("tiny", 8, 100), ("qwen05b", 3, 1000), ("llama8b", 4, 4000),
+                ("llama8b", 8, 2048), ("qwen7b", 5, 8000)]
+
+
+@pytest.mark.parametrize("name,T,L", VERIFY_CASES)
+def test_prefill_kv_verify(name, T, L):
+    """Speculative-decode verification (the extension named as future work in
+    Sec. 6): prefill_kv of T = 2..8 draft tokens over a long history, with
+    the N(0,1) bf16 cache of the decode workloads as the history."""
+    cfg, w = host_layer(name)
+    W = oracle_weights(name)
+    lay = device_layer(name)
+    log(f"prefill_kv verify {name} T={T} L={L}")
+    kb, vb = synth.kv_fill(cfg, 1)
+    kc, vc = O.bf16_to_f64(kb)[0], O.bf16_to_f64(vb)[0]
+    k = torch.from_numpy(kb.view(np.int16).copy()).cuda()
+    v = torch.from_numpy(vb.view(np.int16).copy()).cuda()
+    xb, xv = _x(cfg, synth.TID_X_PREFILL_KV, T)
+    pos = np.arange(L, L + T)
+    x = bits_to_torch_f32(xb)
+    y = torch.empty_like(x)
+    lay.prefill_kv(x, torch.from_numpy(pos.astype(np.int32)).cuda(), L, k, v, y)
+    torch.cuda.synchronize()
+    yo, ko, vo = O.prefill_kv(w, cfg, xv, pos, kc, vc, L, W=W)
+    assert_parity(y.cpu().numpy(), yo, "y")
+    _check_new_kv(k, v, ko, vo, L, T)
+    # the history is untouched
+    assert np.array_equal(k.cpu().numpy()[0][:, :L, :], kb.view(np.int16)[0][:, :L, :])
+
+
+CHUNKED_CASES = [("tiny", 100, 32), ("qwen05b", 1000, 256), ("llama8b", 2048, 512)]
+
+
+@pytest.mark.parametrize("name,T,chunk", CHUNKED_CASES)
+def test_prefill_chunked(name, T, chunk):
+    """A long prompt in segments (the third scenario of Sec. 4.1): one prefill
+    of `chunk` tokens, then prefill_kv chunks over the tokens before them (the
+    last one ragged), against the oracle's one-shot prefill of all T tokens."""
+    cfg, w = host_layer(name)
+    W = oracle_weights(name)
+    lay = device_layer(name)
+    log(f"prefill_chunked {name} T={T} chunk={chunk}")
+    rows = None
+    if T > 256:
+        rows = sorted({0, 1, chunk - 1, chunk, chunk + 1, 2 * chunk - 1, 2 * chunk, T // 2, T - chunk, T - 2, T - 1})
+    xb, xv = _x(cfg, synth.TID_X_PREFILL, T)
+    k, v = lay.new_cache(1, 0)
+    x = bits_to_torch_f32(xb)
+    y = torch.empty_like(x)
+    lay.prefill_chunked(x, torch.arange(T, dtype=torch.int32, device="cuda"), chunk, k, v, y)
+    torch.cuda.synchronize()
+    yo, ko, vo = O.prefill(w, cfg, xv, np.arange(T), rows=rows, W=W)
+    gy = y.cpu().numpy().astype(np.float64)
+    assert_parity(gy if rows is None else gy[rows], yo, "y")
+    _check_new_kv(k, v, ko, vo, 0, T)
+
+
 DECODE_CASES = [("tiny", 1, [48], 0), ("tiny", 1, [48], 1), ("tiny", 4, [0, 9, 64, 126], 0),
                 ("tiny", 4, [0, 9, 64, 126], 1), ("tiny", 3, [127, 2, 40], 2), ("qwen05b", 1, [512], 0),
                 ("qwen05b", 2, [512, 100], 2), ("qwen05b", 2, [512, 100], 1), ("llama8b", 1, [2048], 0), ("llama8b", 1, [2048], 1),
