@@ -30,7 +30,10 @@
 //   * each wave loads its 4 weight tiles (1 KB each, one 16-byte load per
 //     lane) into the free half of a register ring of 8 tile slots;
 //   * inside the iteration the A fragments (LDS) and B fragments of step
-//     t + 1 are prepared while the MFMAs of step t run.
+//     t + 1 are prepared while the MFMAs of step t run;
+//   * the scale ratio that the accumulators take at the end of an iteration
+//     (the next iteration's first group) was requested an iteration earlier,
+//     so no instruction of an iteration waits for that iteration's loads.
 // Every load is issued unconditionally with clamped addresses (X rows past M
 // read row M - 1; their outputs are dropped).  K_pad is a multiple of 128, so
 // every k range holds whole iterations.
@@ -211,6 +214,18 @@ gemm_w4_kernel(const f16* __restrict__ X, int ldx, DevLinear W, EpiArgs ep, Gemm
             if (ZP) rz[q][hh] = (uint32_t)W.zeros[gi];
         }
     };
+    // DMA variant: the scale ratio of the first tile of the iteration that
+    // starts at kb (both columns), two iterations ahead in a ring of two
+    // slots, so the group boundary at the end of an iteration never waits
+    // for loads of the same iteration (slot it % 2 holds the ratio of
+    // iteration it + 2 from the start of iteration it on).
+    float rn[2][2];
+    auto load_rn = [&](int slot, int kb) __attribute__((always_inline)) {
+        const int kk = kb < kb_hi ? kb : kb_lo;
+        const uint32_t g0 = (uint32_t)((kk * 64) >> W.lgG) * (uint32_t)W.N_dev;
+        rn[slot][0] = *reinterpret_cast<const float*>(Rb + (g0 + (uint32_t)col0) * 4u);
+        rn[slot][1] = *reinterpret_cast<const float*>(Rb + (g0 + (uint32_t)col1) * 4u);
+    };
     auto load_group = [&](int g, int kb) __attribute__((always_inline)) {
         load_w(4 * g, kb);
         load_w(4 * g + 1, kb);
@@ -265,7 +280,12 @@ gemm_w4_kernel(const f16* __restrict__ X, int ldx, DevLinear W, EpiArgs ep, Gemm
                 const int q = (t == 7 ? qn : qb) + 2 * half;
                 const int k = (kb + (t == 7 ? 2 : 0) + half) * 64 + (tn & 3) * 16;
                 const bool start = k < kb_hi * 64 && (k & Gm1) == 0;
-                const float f0 = start ? rr[q][hh] : 1.0f, f1 = start ? rr[q + 1][hh] : 1.0f;
+                float r0 = rr[q][hh], r1 = rr[q + 1][hh];
+                if (!XREG && t == 7) {          // the next iteration's first tile (NH == 1)
+                    r0 = rn[(qb >> 2) ^ 1][0];
+                    r1 = rn[(qb >> 2) ^ 1][1];
+                }
+                const float f0 = start ? r0 : 1.0f, f1 = start ? r1 : 1.0f;
 #pragma unroll
                 for (int i = 0; i < TM; i++)
 #pragma unroll
@@ -313,6 +333,7 @@ gemm_w4_kernel(const f16* __restrict__ X, int ldx, DevLinear W, EpiArgs ep, Gemm
         auto iteration = [&](int it, const unsigned char* As, unsigned char* As_next, int qb, int qn)
             __attribute__((always_inline)) {
             const int kb = kb_lo + 2 * it;
+            load_rn(qb >> 2, kb + 4);
             load_x_lds(kb + 2, As_next);
             load_group(qn / 4, kb + 2);
             if (kb < kb_hi) compute(kb, As, qb, qn);
@@ -320,6 +341,7 @@ gemm_w4_kernel(const f16* __restrict__ X, int ldx, DevLinear W, EpiArgs ep, Gemm
         };
         load_x_lds(kb_lo, As0);
         load_group(0, kb_lo);
+        load_rn(1, kb_lo + 2);
         __syncthreads();
         for (int it = 0; it < nit; it += 2) {
             iteration(it, As0, As1, 0, 4);
