@@ -125,10 +125,11 @@ typedef struct kv_desc {
  * no stage call changes it afterwards (scratch state, such as split-K
  * counters, lives in the caller's workspace), so stage calls on different
  * streams may share the handle, each with its own workspace.  One exception:
- * the persistent decode path (layer_set_decode_path) needs every compute
- * unit of the device at once, so two of its launches must not overlap on one
- * device; a caller that runs decode on several streams at once selects path
- * 1.  The diagnostics (profiling, decode stamps) are not for concurrent use.
+ * the persistent decode path (layer_set_decode_path; it also serves
+ * prefill / prefill_kv calls of at most 4 tokens) needs every compute unit
+ * of the device at once, so two of its launches must not overlap on one
+ * device; a caller that runs such calls on several streams at once selects
+ * path 1.  The diagnostics (profiling, decode stamps) are not for concurrent use.
  * Errors: W4_EINVAL (null), W4_EUNSUPPORTED (shape, or the current device is
  * not gfx950), W4_EHIP (allocation or copy failed). */
 int layer_create(const layer_config* cfg, const layer_weights_host* w, layer_t* out);
@@ -263,7 +264,11 @@ int layer_debug_dequant(layer_t layer, int32_t which, float* out, void* stream);
  * automatically for B <= 4 when the layer has no zero points and its
  * on-chip working set fits).  Both compute the same result; the
  * persistent path is deterministic.  With 2, a decode call the persistent
- * path cannot serve fails with W4_EUNSUPPORTED.  Errors: W4_EINVAL. */
+ * path cannot serve fails with W4_EUNSUPPORTED.  The same launch also
+ * serves layer_prefill / layer_prefill_kv calls of T <= 4 tokens (its rows
+ * are then the tokens of one sequence, and row t also attends to the new
+ * keys of rows before it) unless the path is 1, which keeps them on the
+ * prefill kernels.  Errors: W4_EINVAL. */
 int layer_set_decode_path(layer_t layer, int32_t path);
 
 /* Time stamps of the persistent decode path (diagnostics): with on != 0 its

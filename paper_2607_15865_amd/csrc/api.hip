@@ -322,7 +322,7 @@ struct FusedPlan {
     bool ok = false;
     int nblocks = 0, chunk = 0, nchunk = 0, S_qkv = 1, S_o = 1, S_down = 1, ldx = 0, comb_per = 0, comb_lpv = 1;
     size_t off_h = 0, off_red = 0, off_gam = 0, off_zero = 0, off_c64 = 0, lds_bytes = 0;
-    size_t qkv_part, apart, A, o_part, g, down_part, total;
+    size_t qkv_part = 0, apart = 0, A = 0, o_part = 0, g = 0, down_part = 0, total = 0;
 };
 
 size_t align256(size_t v) { return (v + 255) / 256 * 256; }
@@ -466,6 +466,67 @@ EpiArgs base_epi(const layer_s* L) {
     return e;
 }
 
+// The persistent decode launch for plan fp.  shared: the B rows are
+// consecutive tokens of one sequence (prefill_kv with at most 4 tokens) with
+// one cache, row b at context ctx_base + b; otherwise row b of a batch at
+// context ctx_lens[b] in cache b.
+int launch_fused(layer_s* L, const FusedPlan& fp, const float* x, const int32_t* pos, const int32_t* ctx_lens,
+                 int ctx_base, bool shared, const float* attn_mask, int B, void* kc, void* vc, float* y, void* ws,
+                 hipStream_t st) {
+    const layer_config& c = L->cfg;
+    char* base = (char*)ws;
+    DecodeFusedArgs a{};
+    a.qkv = L->qkv.d; a.o = L->o.d; a.gu = L->gu.d; a.down = L->down.d;
+    a.attn_norm = (const uint16_t*)L->attn_norm.p;
+    a.mlp_norm = (const uint16_t*)L->mlp_norm.p;
+    a.eps = c.rms_eps;
+    a.rope_cos = (const float*)L->rope_cos.p;
+    a.rope_sin = (const float*)L->rope_sin.p;
+    a.H = c.hidden; a.nq = c.n_heads; a.nkv = c.n_kv_heads; a.d = c.head_dim; a.F_pad = L->F_pad; a.B = B;
+    a.x = x; a.pos = pos; a.ctx_lens = shared ? nullptr : ctx_lens; a.mask = attn_mask; a.max_seq = c.max_seq;
+    a.ctx_base = ctx_base; a.shared = shared ? 1 : 0;
+    a.k_cache = (uint16_t*)kc; a.v_cache = (uint16_t*)vc;
+    a.sh = (long long)c.max_seq * c.head_dim; a.sb = shared ? 0 : a.sh * c.n_kv_heads;
+    a.y = y;
+    a.qkv_part = (uint64_t*)(base + fp.qkv_part);
+    a.apart = (uint64_t*)(base + fp.apart);
+    a.A = (uint64_t*)(base + fp.A);
+    a.o_part = (uint64_t*)(base + fp.o_part);
+    a.g = (uint64_t*)(base + fp.g);
+    a.down_part = (uint64_t*)(base + fp.down_part);
+    a.epoch = next_epoch();
+    a.err = L->err;
+    a.stamps = L->decode_trace ? L->stamps : nullptr;
+    a.S_qkv = fp.S_qkv; a.S_o = fp.S_o; a.S_down = fp.S_down;
+    a.plan = (const int*)L->fplan.p;
+    a.comb_per = fp.comb_per; a.comb_lpv = fp.comb_lpv;
+    a.chunk = fp.chunk; a.nchunk = fp.nchunk;
+    a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)c.head_dim));
+    a.nblocks = fp.nblocks;
+    a.ldx = fp.ldx;
+    a.off_h = fp.off_h;
+    a.off_red = fp.off_red;
+    a.off_gam = fp.off_gam;
+    a.off_zero = fp.off_zero;
+    a.off_c64 = fp.off_c64;
+    a.lds_bytes = fp.lds_bytes;
+    return launch_decode_fused(a, st);
+}
+
+// prefill / prefill_kv of T <= 4 tokens run as one persistent launch (the
+// rows are the tokens) unless the layer is held to separate kernels
+FusedPlan small_prefill_plan(layer_s* L, int T, int hist) {
+    if (T > 4 || L->decode_path == 1) return FusedPlan{};
+    return plan_fused(L, T, hist + T - 1, true);
+}
+
+size_t prefill_ws_bytes(layer_s* L, int T, int hist) {
+    size_t n = plan_prefill(L, T, hist).total;
+    const FusedPlan fp = small_prefill_plan(L, T, hist);
+    if (fp.ok) n = std::max(n, fp.total);
+    return n;
+}
+
 int run_prefill(layer_s* L, const float* x, const int32_t* pos, int T, int hist, void* kc, void* vc, float* y,
                 void* ws, size_t ws_bytes, void* stream_) {
     if (!L) return fail(W4_EINVAL, "null layer");
@@ -474,9 +535,18 @@ int run_prefill(layer_s* L, const float* x, const int32_t* pos, int T, int hist,
     if ((const void*)x == (const void*)y) return fail(W4_EINVAL, "x and y must not alias");
     const layer_config& c = L->cfg;
     if ((long long)hist + T > c.max_seq) return fail(W4_ECAPACITY, "hist_len + T = %lld exceeds max_seq %d", (long long)hist + T, c.max_seq);
+    hipStream_t st = (hipStream_t)stream_;
+    const int stage = hist > 0 ? 1 : 0;
+    const FusedPlan fp = small_prefill_plan(L, T, hist);
+    if (fp.ok) {
+        if (ws_bytes < fp.total) return fail(W4_EWORKSPACE, "workspace %zu bytes, need %zu", ws_bytes, fp.total);
+        int rc;
+        { ProfScope ps(L, stage, 7, st); rc = launch_fused(L, fp, x, pos, nullptr, hist, true, nullptr, T, kc, vc, y, ws, st); }
+        if (rc) return fail(W4_EHIP, "persistent launch failed: %s", hipGetErrorString(hipGetLastError()));
+        return W4_OK;
+    }
     const PrefillWs w = plan_prefill(L, T, hist);
     if (ws_bytes < w.total) return fail(W4_EWORKSPACE, "workspace %zu bytes, need %zu", ws_bytes, w.total);
-    hipStream_t st = (hipStream_t)stream_;
     char* base = (char*)ws;
     f16* xn1 = (f16*)(base + w.xn1);
     uint16_t* q = (uint16_t*)(base + w.q);
@@ -491,7 +561,6 @@ int run_prefill(layer_s* L, const float* x, const int32_t* pos, int T, int hist,
         if (gp->S > 1 && gp->tiles > kGemmCounters) return fail(W4_EUNSUPPORTED, "split-K tile count above %d", kGemmCounters);
 
     int rc = 0;
-    const int stage = hist > 0 ? 1 : 0;
     { ProfScope ps(L, stage, 0, st); rc |= launch_rmsnorm(x, (const uint16_t*)L->attn_norm.p, c.rms_eps, T, H, xn1, st); }
     EpiArgs e = base_epi(L);
     e.q_out = q;
@@ -691,7 +760,7 @@ size_t layer_workspace_size(layer_t L, int32_t stage, int32_t batch, int32_t T, 
     if (!L) return 0;
     if (stage == 0 || stage == 1) {
         if (T < 1 || max_ctx < 0) return 0;
-        return plan_prefill(L, T, stage == 1 ? max_ctx : 0).total;
+        return prefill_ws_bytes(L, T, stage == 1 ? max_ctx : 0);
     }
     if (stage == 2) {
         if (batch < 1 || max_ctx < 0) return 0;
@@ -716,7 +785,7 @@ int layer_prefill_kv(layer_t L, const float* x, const int32_t* pos, int32_t T, i
 size_t layer_prefill_chunked_workspace_size(layer_t L, int32_t T, int32_t chunk) {
     if (!L || T < 1 || chunk < 1) return 0;
     size_t n = 0;
-    for (int s = 0; s < T; s += chunk) n = std::max(n, plan_prefill(L, std::min(chunk, T - s), s).total);
+    for (int s = 0; s < T; s += chunk) n = std::max(n, prefill_ws_bytes(L, std::min(chunk, T - s), s));
     return n;
 }
 
@@ -753,43 +822,8 @@ int layer_decode(layer_t L, const float* x, const int32_t* pos, const int32_t* c
     if (L->decode_path == 2 && !fp.ok) return fail(W4_EUNSUPPORTED, "persistent decode not possible for this shape/batch");
     if (fp.ok) {
         if (ws_bytes < fp.total) return fail(W4_EWORKSPACE, "workspace %zu bytes, need %zu", ws_bytes, fp.total);
-        char* base = (char*)ws;
-        DecodeFusedArgs a{};
-        a.qkv = L->qkv.d; a.o = L->o.d; a.gu = L->gu.d; a.down = L->down.d;
-        a.attn_norm = (const uint16_t*)L->attn_norm.p;
-        a.mlp_norm = (const uint16_t*)L->mlp_norm.p;
-        a.eps = c.rms_eps;
-        a.rope_cos = (const float*)L->rope_cos.p;
-        a.rope_sin = (const float*)L->rope_sin.p;
-        a.H = c.hidden; a.nq = c.n_heads; a.nkv = c.n_kv_heads; a.d = c.head_dim; a.F_pad = L->F_pad; a.B = B;
-        a.x = x; a.pos = pos; a.ctx_lens = ctx_lens; a.mask = attn_mask; a.max_seq = c.max_seq;
-        a.k_cache = (uint16_t*)kc; a.v_cache = (uint16_t*)vc;
-        a.sh = (long long)c.max_seq * c.head_dim; a.sb = a.sh * c.n_kv_heads;
-        a.y = y;
-        a.qkv_part = (uint64_t*)(base + fp.qkv_part);
-        a.apart = (uint64_t*)(base + fp.apart);
-        a.A = (uint64_t*)(base + fp.A);
-        a.o_part = (uint64_t*)(base + fp.o_part);
-        a.g = (uint64_t*)(base + fp.g);
-        a.down_part = (uint64_t*)(base + fp.down_part);
-        a.epoch = next_epoch();
-        a.err = L->err;
-        a.stamps = L->decode_trace ? L->stamps : nullptr;
-        a.S_qkv = fp.S_qkv; a.S_o = fp.S_o; a.S_down = fp.S_down;
-        a.plan = (const int*)L->fplan.p;
-        a.comb_per = fp.comb_per; a.comb_lpv = fp.comb_lpv;
-        a.chunk = fp.chunk; a.nchunk = fp.nchunk;
-        a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)c.head_dim));
-        a.nblocks = fp.nblocks;
-        a.ldx = fp.ldx;
-        a.off_h = fp.off_h;
-        a.off_red = fp.off_red;
-        a.off_gam = fp.off_gam;
-        a.off_zero = fp.off_zero;
-        a.off_c64 = fp.off_c64;
-        a.lds_bytes = fp.lds_bytes;
         int rc;
-        { ProfScope ps(L, 2, 6, st); rc = launch_decode_fused(a, st); }
+        { ProfScope ps(L, 2, 6, st); rc = launch_fused(L, fp, x, pos, ctx_lens, 0, false, attn_mask, B, kc, vc, y, ws, st); }
         if (rc) return fail(W4_EHIP, "persistent decode launch failed: %s", hipGetErrorString(hipGetLastError()));
         return W4_OK;
     }

@@ -12,7 +12,10 @@ struct DecodeFusedArgs {
     int H, nq, nkv, d, F_pad, B;
     const float* x;            // [B][H]
     const int32_t* pos;        // [B]
-    const int32_t* ctx_lens;   // [B]
+    const int32_t* ctx_lens;   // [B], or null: row b's context is ctx_base + b
+    int ctx_base;
+    int shared;                // rows are consecutive tokens of one sequence: one cache
+                               // (sb = 0), row b also attends to rows 0 .. b-1 (B <= 4)
     const float* mask;         // [B][max_seq] or null
     int max_seq;
     uint16_t* k_cache;
@@ -59,9 +62,10 @@ int decode_fused_max_chunk(int head_dim);
 // LDS bytes of the attention phase for chunks of ch keys, head size d: the K
 // and V stages ([ch rounded up to 32][d] bf16 each), the per-group outputs
 // and statistics ([ch / 32][8 heads][d + 2] fp32), q/k/v in fp32
-// ([10][d]), the rotated q, k and v in bf16 ([10][d]) and the mask values
-// (ch rounded up to 64, fp32).
+// ([16][d]: 8 query heads, k, v and the k, v of up to 3 earlier rows), the
+// rotated q, k and v in bf16 ([10][d]) and the mask values (ch rounded up to
+// 64, fp32).
 inline size_t decode_fused_attn_bytes(int ch, int d) {
     const size_t chp = (size_t)(ch + 31) / 32 * 32, ng = chp / 32;
-    return 4 * chp * d + (ng * 8 * d + ng * 16 + 10 * (size_t)d) * 4 + 10 * (size_t)d * 2 + (chp + 63) / 64 * 64 * 4;
+    return 4 * chp * d + (ng * 8 * d + ng * 16 + 16 * (size_t)d) * 4 + 10 * (size_t)d * 2 + (chp + 63) / 64 * 64 * 4;
 }

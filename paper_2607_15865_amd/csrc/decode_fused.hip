@@ -340,7 +340,7 @@ __global__ void __launch_bounds__(NTHR) decode_fused_kernel(DecodeFusedArgs a) {
         g1 = *reinterpret_cast<const u32x4*>(a.attn_norm + gi);
         g2 = *reinterpret_cast<const u32x4*>(a.mlp_norm + gi);
         int m0 = 0;
-        if (tid < B) m0 = a.ctx_lens[tid];
+        if (tid < B) m0 = a.ctx_lens ? a.ctx_lens[tid] : a.ctx_base + tid;
         else if (tid >= MAXB && tid < MAXB + B) m0 = a.pos[tid - MAXB];
         prefetch(1);
         if (i0 < B * H) *reinterpret_cast<float4*>(hbuf + i0) = xv[0];
@@ -397,8 +397,10 @@ __global__ void __launch_bounds__(NTHR) decode_fused_kernel(DecodeFusedArgs a) {
         unsigned char* Vst = smem + (size_t)CHP * D * 2;                     // [CHP][D] bf16
         float* ored = reinterpret_cast<float*>(Vst + (size_t)CHP * D * 2);   // [NG][MAXR][D]
         float* gst = ored + NG * MAXR * D;                                   // [NG][MAXR][2]
-        float* qkvf = gst + NG * MAXR * 2;                                   // [r + 2][D] device order
-        uint16_t* qb = reinterpret_cast<uint16_t*>(qkvf + (MAXR + 2) * D);    // [r][D] bf16
+        // q/k/v of the unit's row (r + 2 rows), then k/v of up to 3 earlier
+        // rows (shared-cache mode)
+        float* qkvf = gst + NG * MAXR * 2;                                   // [r + 2 + 6][D] device order
+        uint16_t* qb = reinterpret_cast<uint16_t*>(qkvf + (MAXR + 8) * D);    // [r][D] bf16
         uint16_t* knb = qb + MAXR * D;                                       // [D]
         uint16_t* vnb = knb + D;                                             // [D]
         float* mst = reinterpret_cast<float*>(vnb + D);                      // [CHP] mask values
@@ -416,7 +418,7 @@ __global__ void __launch_bounds__(NTHR) decode_fused_kernel(DecodeFusedArgs a) {
             const int b = u / (nkv * NCH), g = (u / NCH) % nkv, chunk = u % NCH;
             const int ctx = meta[b];
             const int start = chunk * CH, end = min(start + CH, ctx + 1);
-            const int hist_end = min(end, ctx), ng = (end - start + 31) / 32;
+            const int hist_end = min(end, a.shared ? a.ctx_base : ctx), ng = (end - start + 31) / 32;
             if (a.mask && wave < ng / 2 + (ng & 1)) {     // mask values of keys start + 64 wave + lane
                 const int kk = 64 * wave + lane;
                 __builtin_amdgcn_global_load_lds(
@@ -459,10 +461,29 @@ __global__ void __launch_bounds__(NTHR) decode_fused_kernel(DecodeFusedArgs a) {
             const int ps = meta[MAXB + b];
             const int jr = tid % (D / 2);            // the RoPE dim of every item of this thread
             const float rc = a.rope_cos[(size_t)ps * (D / 2) + jr], rs = a.rope_sin[(size_t)ps * (D / 2) + jr];
-            // q (r heads), k_new, v_new of row b: sums of the q/k/v parts
+            // Shared-cache mode (rows are consecutive tokens of one sequence):
+            // the earlier rows o_lo .. o_lo + np - 1 hold slots of this chunk
+            // that no launch has written yet; their keys and values come from
+            // their q/k/v parts, rotated with their own positions.
+            const int o_lo = a.shared ? max(0, start - a.ctx_base) : 0;
+            const int np = a.shared ? max(0, min(b, end - a.ctx_base) - o_lo) : 0;
+            float rco[3], rso[3];
+#pragma unroll
+            for (int j = 0; j < 3; j++) {
+                const int pj = j < np ? meta[MAXB + o_lo + j] : 0;
+                rco[j] = j < np ? a.rope_cos[(size_t)pj * (D / 2) + jr] : 0.f;
+                rso[j] = j < np ? a.rope_sin[(size_t)pj * (D / 2) + jr] : 0.f;
+            }
+            // q (r heads), k_new, v_new of row b, then k and v of the earlier
+            // rows: sums of the q/k/v parts
             const uint64_t* qrow = a.qkv_part + (size_t)b * Nq;
-            gather_sum((r + 2) * D, a.S_qkv, (size_t)B * Nq, ep, wt,
-                       [&](int i) {
+            gather_sum((r + 2 + 2 * np) * D, a.S_qkv, (size_t)B * Nq, ep, wt,
+                       [&](int i) -> const uint64_t* {
+                           if (i >= (r + 2) * D) {
+                               const int jo = (i - (r + 2) * D) / (2 * D), rem = i - (r + 2) * D - jo * 2 * D;
+                               const int col = rem < D ? qd + g * D + rem : qd + kd + g * D + (rem - D);
+                               return a.qkv_part + (size_t)(o_lo + jo) * Nq + col;
+                           }
                            const int col = i < r * D ? g * r * D + i
                                          : i < (r + 1) * D ? qd + g * D + (i - r * D)
                                                            : qd + kd + g * D + (i - (r + 1) * D);
@@ -477,28 +498,38 @@ __global__ void __launch_bounds__(NTHR) decode_fused_kernel(DecodeFusedArgs a) {
             // probabilities are 0, and 0 times a stale NaN would not be)
             const int nrow = ctx - start;
             const bool has_new = ctx < end;
-            for (int i = tid; i < (r + 1) * (D / 2); i += NTHR) {
+            for (int i = tid; i < (r + 1 + np) * (D / 2); i += NTHR) {
                 const int hh = i / (D / 2), j = jr;
-                const float v0 = qkvf[hh * D + devpos<D>(j)], v1 = qkvf[hh * D + devpos<D>(j + D / 2)];
-                const uint16_t e0 = bf16_bits_rne(v0 * rc - v1 * rs), e1 = bf16_bits_rne(v1 * rc + v0 * rs);
+                const int jo = hh - r - 1;                    // earlier row (hh > r)
+                const float* src = hh <= r ? qkvf + hh * D : qkvf + (r + 2) * D + jo * 2 * D;
+                const float cs = jo < 0 ? rc : jo == 0 ? rco[0] : jo == 1 ? rco[1] : rco[2];
+                const float sn = jo < 0 ? rs : jo == 0 ? rso[0] : jo == 1 ? rso[1] : rso[2];
+                const float v0 = src[devpos<D>(j)], v1 = src[devpos<D>(j + D / 2)];
+                const uint16_t e0 = bf16_bits_rne(v0 * cs - v1 * sn), e1 = bf16_bits_rne(v1 * cs + v0 * sn);
                 if (hh < r) {
                     qb[hh * D + j] = e0;
                     qb[hh * D + j + D / 2] = e1;
                 } else {
-                    knb[j] = e0;
-                    knb[j + D / 2] = e1;
-                    if (has_new) {
-                        uint16_t* kr = reinterpret_cast<uint16_t*>(Kst + (size_t)nrow * D * 2);
-                        kr[(((j >> 3) ^ kswz(nrow)) << 3) | (j & 7)] = e0;
-                        kr[((((j + D / 2) >> 3) ^ kswz(nrow)) << 3) | (j & 7)] = e1;
+                    if (hh == r) {
+                        knb[j] = e0;
+                        knb[j + D / 2] = e1;
+                    }
+                    const int row = hh == r ? nrow : a.ctx_base + o_lo + jo - start;
+                    if (hh > r || has_new) {
+                        uint16_t* kr = reinterpret_cast<uint16_t*>(Kst + (size_t)row * D * 2);
+                        kr[(((j >> 3) ^ kswz(row)) << 3) | (j & 7)] = e0;
+                        kr[((((j + D / 2) >> 3) ^ kswz(row)) << 3) | (j & 7)] = e1;
                     }
                 }
             }
-            for (int j = tid; j < D; j += NTHR) {
-                const uint16_t e = bf16_bits_rne(qkvf[(r + 1) * D + devpos<D>(j)]);
-                vnb[j] = e;
-                if (has_new)
-                    reinterpret_cast<uint16_t*>(Vst + (size_t)nrow * D * 2)[(((j >> 3) ^ vswz(nrow)) << 3) | (j & 7)] = e;
+            for (int j = tid; j < D * (1 + np); j += NTHR) {
+                const int ro = j / D, dm = j - ro * D;         // ro 0: this row's value, ro > 0: earlier row ro - 1
+                const float* src = ro == 0 ? qkvf + (r + 1) * D : qkvf + (r + 2) * D + (ro - 1) * 2 * D + D;
+                const uint16_t e = bf16_bits_rne(src[devpos<D>(dm)]);
+                if (ro == 0) vnb[dm] = e;
+                const int row = ro == 0 ? nrow : a.ctx_base + o_lo + ro - 1 - start;
+                if (ro > 0 || has_new)
+                    reinterpret_cast<uint16_t*>(Vst + (size_t)row * D * 2)[(((dm >> 3) ^ vswz(row)) << 3) | (dm & 7)] = e;
             }
             for (int i = tid; i < (ng * 32 - nkeys) * NCK; i += NTHR)
                 reinterpret_cast<u32x4*>(Vst + (size_t)nkeys * D * 2)[i] = u32x4{0u, 0u, 0u, 0u};
@@ -844,6 +875,7 @@ int decode_fused_blocks(int head_dim, int B, size_t lds_bytes) {
 
 int launch_decode_fused(const DecodeFusedArgs& a, hipStream_t stream) {
     if (a.B > 4 || a.S_qkv > MAXS || a.S_o > MAXS || a.S_down > MAXS) return -1;
+    if (a.shared ? (a.ctx_lens != nullptr || a.sb != 0 || a.ctx_base < 0) : a.ctx_lens == nullptr) return -1;
     if (a.chunk < 1 || a.chunk > decode_fused_max_chunk(a.d) || a.nkv < 1 || a.nq % a.nkv || a.nq / a.nkv > MAXR)
         return -1;
     if (a.off_h < decode_fused_attn_bytes(a.chunk, a.d)) return -1;

@@ -89,8 +89,11 @@ def test_prefill_kv(name, T, L):
     _check_new_kv(k, v, ko, vo, L, T)
 
 
-VERIFY_CASES = [("tiny", 2, 120), ("tiny", 8, 100), ("qwen05b", 3, 1000), ("llama8b", 4, 4000),
-                ("llama8b", 8, 2048), ("qwen7b", 5, 8000)]
+# T <= 4 runs as one persistent launch whose rows share the cache (rows that
+# straddle a key-chunk boundary: tiny 4 over 94), T > 4 on the prefill kernels
+VERIFY_CASES = [("tiny", 2, 120), ("tiny", 4, 94), ("tiny", 3, 0), ("tiny", 8, 100), ("qwen05b", 3, 1000),
+                ("qwen05b", 4, 1019), ("llama8b", 2, 3000), ("llama8b", 4, 4000), ("llama8b", 8, 2048),
+                ("qwen7b", 2, 8190), ("qwen7b", 5, 8000)]
 
 
 @pytest.mark.parametrize("name,T,L", VERIFY_CASES)
@@ -110,11 +113,14 @@ def test_prefill_kv_verify(name, T, L):
     pos = np.arange(L, L + T)
     x = bits_to_torch_f32(xb)
     y = torch.empty_like(x)
-    lay.prefill_kv(x, torch.from_numpy(pos.astype(np.int32)).cuda(), L, k, v, y)
-    torch.cuda.synchronize()
     yo, ko, vo = O.prefill_kv(w, cfg, xv, pos, kc, vc, L, W=W)
-    assert_parity(y.cpu().numpy(), yo, "y")
-    _check_new_kv(k, v, ko, vo, L, T)
+    for path in ((0, 1) if T <= 4 else (0,)):
+        lay.set_decode_path(path)
+        lay.prefill_kv(x, torch.from_numpy(pos.astype(np.int32)).cuda(), L, k, v, y)
+        torch.cuda.synchronize()
+        assert_parity(y.cpu().numpy(), yo, f"y (path {path})")
+        _check_new_kv(k, v, ko, vo, L, T)
+    lay.set_decode_path(0)
     # the history is untouched
     assert np.array_equal(k.cpu().numpy()[0][:, :L, :], kb.view(np.int16)[0][:, :L, :])
 
