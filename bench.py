@@ -195,6 +195,106 @@ def extras(cfg, layers, caches, binding, synth, stream, reps=30):
     return res
 
 
+# ---------------------------------------------------------------- other workloads
+
+def reports(binding, synth, stream, reps=20):
+    """The other workloads' stages, timed after the bench steps (outside
+    them): the Qwen-7B-shaped layer's prefill of 2048 tokens and its decode at
+    context 8192 with 1 and 8 rows (3 rotating copies of weights and 8-row
+    caches, 258 MB each), and the Qwen-0.5B-shaped layer's prefill of 256,
+    prefill_kv of 64 over 256 and decode at context 512 (68 copies of 7.7 MB,
+    so the rotation exceeds the 256 MB last-level cache; these calls are
+    launch-bound).  Median of `reps` calls, HIP events on the library's
+    stream; synthetic seeded weights, N(0,1) caches."""
+    import numpy as np
+    import torch
+    sp = stream.cuda_stream
+
+    def f32(bits):
+        u = bits.astype(np.uint32) << 16
+        return torch.from_numpy(u.view(np.float32).copy()).cuda()
+
+    def median_us(call):
+        ts = []
+        for i in range(reps + 2):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            call(i)
+            e1.record(stream)
+            e1.synchronize()
+            if i >= 2:
+                ts.append(e0.elapsed_time(e1) * 1e3)
+        return float(np.median(ts))
+
+    def flops_entry(cfg, us, M, T, L):
+        fl = stage_flops(cfg, M, T, L, 1)
+        return {"us": round(us, 2), "gflop": round(fl / 1e9, 2), "tflops": round(fl / (us * 1e-6) / 1e12, 1),
+                "frac_mfma": round(fl / (us * 1e-6) / 1e12 / PEAK_MFMA_TFLOPS, 4)}
+
+    def bytes_entry(cfg, us, B, ctx, M=None, T=1):
+        by = stage_bytes(cfg, M or B, T, ctx, B)
+        return {"us": round(us, 2), "mbytes": round(by / 1e6, 2), "gbps": round(by / (us * 1e-6) / 1e9, 1),
+                "frac_hbm": round(by / (us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)}
+
+    out = {}
+    for name, ncp, Bmax in (("qwen7b", 3, 8), ("qwen05b", 68, 1)):
+        cfg = synth.CONFIGS[name]
+        run = synth.RUNS[name]
+        log(f"bench: {name} report ({ncp} copies)")
+        w = synth.make_layer(cfg)
+        layers = [binding.Layer(cfg, w) for _ in range(ncp)]
+        kb, vb = synth.kv_fill(cfg, Bmax)
+        caches = [(torch.from_numpy(kb.view(np.int16)).cuda(), torch.from_numpy(vb.view(np.int16)).cuda())
+                  for _ in range(ncp)]
+        h0 = layers[0].handle
+        Tp, ctx = run["prefill_T"], run["decode_ctx"]
+        need = [binding.layer_workspace_size(h0, 0, 1, Tp, 0)]
+        need += [binding.layer_workspace_size(h0, 2, B, 1, ctx) for B in run["decode_B"]]
+        if run["pkv_T"]:
+            need.append(binding.layer_workspace_size(h0, 1, 1, run["pkv_T"], run["pkv_hist"]))
+        ws_bytes = max(need)
+        ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
+        res = {}
+        xp = f32(synth.activations(cfg, synth.TID_X_PREFILL, Tp))
+        yp = torch.empty_like(xp)
+        pp = torch.arange(Tp, dtype=torch.int32, device="cuda")
+
+        def pre(i):
+            k, v = caches[i % ncp]
+            binding.check(binding.layer_prefill(layers[i % ncp].handle, xp, pp, Tp, k, v, yp, ws, ws_bytes, sp))
+        res[f"prefill_T{Tp}"] = flops_entry(cfg, median_us(pre), Tp, Tp, 0)
+        if run["pkv_T"]:
+            Tk, Lk = run["pkv_T"], run["pkv_hist"]
+            xk = f32(synth.activations(cfg, synth.TID_X_PREFILL_KV, Tk))
+            yk = torch.empty_like(xk)
+            pk = torch.arange(Lk, Lk + Tk, dtype=torch.int32, device="cuda")
+
+            def pkv(i):
+                k, v = caches[i % ncp]
+                binding.check(binding.layer_prefill_kv(layers[i % ncp].handle, xk, pk, Tk, Lk, k, v, yk, ws, ws_bytes,
+                                                       sp))
+            us = median_us(pkv)
+            res[f"prefill_kv_T{Tk}_over_{Lk}"] = dict(flops_entry(cfg, us, Tk, Tk, Lk),
+                                                     **{k2: v2 for k2, v2 in bytes_entry(cfg, us, 1, Lk, Tk, Tk).items()
+                                                        if k2 != "us"})
+        for B in run["decode_B"]:
+            xd = f32(synth.activations(cfg, synth.TID_X_DECODE, B))
+            yd = torch.empty_like(xd)
+            cd = torch.full((B,), ctx, dtype=torch.int32, device="cuda")
+
+            def dec(i, xd=xd, yd=yd, cd=cd, B=B):
+                k, v = caches[i % ncp]
+                binding.check(binding.layer_decode(layers[i % ncp].handle, xd, cd, cd, ctx, None, B, k, v, yd, ws,
+                                                   ws_bytes, sp))
+            res[f"decode_B{B}_ctx{ctx}"] = bytes_entry(cfg, median_us(dec), B, ctx)
+        out[name] = res
+        torch.cuda.synchronize()
+        for lay in layers:
+            lay.close()
+        del caches, ws
+    return out
+
+
 # ---------------------------------------------------------------- CPU baseline
 
 def cpu_baseline(cfg, w):
@@ -300,6 +400,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--copies", type=int, default=8, help="device copies of the layer (rotation)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-reports", action="store_true",
+                    help="skip the other workloads (Qwen-7B- and Qwen-0.5B-shaped layers) timed after the steps")
     ap.add_argument("--stack", action="store_true",
                     help="instead: the 32-layer stack, 1024-token prefill then 256 decode steps")
     ap.add_argument("--stack-layers", type=int, default=32)
@@ -459,6 +561,8 @@ def main():
         "roofline_decode": roofline_decode,
     }
     out["extras"] = extras(cfg, layers, caches, binding, synth, stream)
+    if not args.no_reports:
+        out["reports"] = reports(binding, synth, stream)
     if not args.no_cpu_baseline:
         log("bench: timing the CPU oracle (one decode layer-step)")
         out["cpu_baseline"] = cpu_baseline(cfg, w)

@@ -321,6 +321,7 @@ DecodeWs plan_decode(const layer_s* L, int B, int max_ctx) {
 struct FusedPlan {
     bool ok = false;
     int nblocks = 0, chunk = 0, nchunk = 0, S_qkv = 1, S_o = 1, S_down = 1, ldx = 0, comb_per = 0, comb_lpv = 1;
+    int slots = 0;                // gate/up column tiles of the busiest block
     size_t off_h = 0, off_red = 0, off_gam = 0, off_zero = 0, off_c64 = 0, lds_bytes = 0;
     size_t qkv_part = 0, apart = 0, A = 0, o_part = 0, g = 0, down_part = 0, total = 0;
 };
@@ -336,7 +337,7 @@ FusedPlan plan_fused(const layer_s* L, int B, int max_ctx, bool query_device) {
     if (L->qkv.d.sz || L->o.d.sz || L->gu.d.sz || L->down.d.sz) return p;   // zero points: separate kernels
     if (c.group_size < 64) return p;                                         // groups of 32: separate kernels
     const int d = c.head_dim, qd = c.n_heads * d, H = c.hidden, r = c.n_heads / c.n_kv_heads;
-    constexpr int MAXR = 8, NWAVE = 16, SLOTS = 4;
+    constexpr int MAXR = 8, NWAVE = 16;
     p.nblocks = 256;
     if (query_device) {
         int dev = 0, cus = 0;
@@ -347,7 +348,9 @@ FusedPlan plan_fused(const layer_s* L, int B, int max_ctx, bool query_device) {
     }
     const int P = p.nblocks;
     if (P > kMaxBlocks || r > MAXR || P != L->fplan_blocks) return p;
-    if (L->gu.d.N_dev / 64 > 2 * P) return p;                                // at most 2 gate/up pairs per block
+    const int gu_pairs = L->gu.d.N_dev / 64;                                 // whole gate/up pairs per block
+    p.slots = 2 * std::max(1, (gu_pairs + P - 1) / P);
+    if (p.slots > 8) return p;
     p.S_qkv = L->S_qkv;
     p.S_o = L->S_o;
     p.S_down = L->S_down;
@@ -375,7 +378,7 @@ FusedPlan plan_fused(const layer_s* L, int B, int max_ctx, bool query_device) {
         p.nchunk = (max_ctx + 1 + ch - 1) / ch;
         p.off_h = align256(std::max(std::max(gemv_bytes, decode_fused_attn_bytes(ch, d)), comb_bytes));
         p.off_red = align256(p.off_h + (size_t)B * H * 4);
-        p.off_gam = align256(p.off_red + (size_t)(NWAVE * SLOTS * maxb * 32 + 8 + NWAVE * maxb + maxb * 32 + 2 * maxb) * 4);
+        p.off_gam = align256(p.off_red + (size_t)(NWAVE * p.slots * maxb * 32 + 8 + NWAVE * maxb + maxb * 32 + 2 * maxb) * 4);
         p.lds_bytes = p.off_gam + (size_t)2 * H * 2;
         if (p.lds_bytes <= 160 * 1024 || ch == 16) break;
     }
@@ -500,6 +503,7 @@ int launch_fused(layer_s* L, const FusedPlan& fp, const float* x, const int32_t*
     a.S_qkv = fp.S_qkv; a.S_o = fp.S_o; a.S_down = fp.S_down;
     a.plan = (const int*)L->fplan.p;
     a.comb_per = fp.comb_per; a.comb_lpv = fp.comb_lpv;
+    a.slots = fp.slots;
     a.chunk = fp.chunk; a.nchunk = fp.nchunk;
     a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)c.head_dim));
     a.nblocks = fp.nblocks;

@@ -36,6 +36,7 @@ struct DecodeFusedArgs {
     const int* plan;           // per block: 16 ints (decode_fused_plan)
     int S_qkv, S_o, S_down;    // k-parts per column tile
     int comb_per, comb_lpv;    // attention outputs combined per block, lanes per output
+    int slots;                 // column tiles per block in one product (LDS partial slots)
     int chunk, nchunk;         // attention keys per unit, units per (row, kv head)
     float scale_log2;
     int nblocks;

@@ -42,7 +42,6 @@ constexpr int RING_QKV = 4;        // q/k/v: its run is about 4 tiles per wave
 constexpr int RING_O = 4;          // o_proj: its run is 2 to 4 tiles per wave
 constexpr int MAXS = 2;            // k-parts of a column tile
 constexpr int MAXR = 8;            // query heads per kv head
-constexpr int SLOTS = 4;           // column tiles per block in one product
 
 #define GLOBAL_AS __attribute__((address_space(1)))
 template <typename T>
@@ -251,6 +250,7 @@ __global__ void __launch_bounds__(NTHR) decode_fused_kernel(DecodeFusedArgs a) {
     const int h = lane >> 5, c = lane & 31;
     f16* xs = reinterpret_cast<f16*>(smem);
     float* hbuf = reinterpret_cast<float*>(smem + a.off_h);       // [B][H]
+    const int SLOTS = a.slots;                                    // column tiles per block in one product
     float* red = reinterpret_cast<float*>(smem + a.off_red);      // [NWAVE][SLOTS][B][32]
     float* red8 = red + NWAVE * SLOTS * MAXB * 32;                // 8 + NWAVE * MAXB
     float* own = red8 + 8 + NWAVE * MAXB;                         // [MAXB][32]
@@ -876,6 +876,7 @@ int decode_fused_blocks(int head_dim, int B, size_t lds_bytes) {
 int launch_decode_fused(const DecodeFusedArgs& a, hipStream_t stream) {
     if (a.B > 4 || a.S_qkv > MAXS || a.S_o > MAXS || a.S_down > MAXS) return -1;
     if (a.shared ? (a.ctx_lens != nullptr || a.sb != 0 || a.ctx_base < 0) : a.ctx_lens == nullptr) return -1;
+    if (a.slots < 1) return -1;
     if (a.chunk < 1 || a.chunk > decode_fused_max_chunk(a.d) || a.nkv < 1 || a.nq % a.nkv || a.nq / a.nkv > MAXR)
         return -1;
     if (a.off_h < decode_fused_attn_bytes(a.chunk, a.d)) return -1;

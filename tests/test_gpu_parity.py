@@ -155,7 +155,8 @@ def test_prefill_chunked(name, T, chunk):
 DECODE_CASES = [("tiny", 1, [48], 0), ("tiny", 1, [48], 1), ("tiny", 4, [0, 9, 64, 126], 0),
                 ("tiny", 4, [0, 9, 64, 126], 1), ("tiny", 3, [127, 2, 40], 2), ("qwen05b", 1, [512], 0),
                 ("qwen05b", 2, [512, 100], 2), ("qwen05b", 2, [512, 100], 1), ("llama8b", 1, [2048], 0), ("llama8b", 1, [2048], 1),
-                ("llama8b", 2, [2048, 1500], 2), ("qwen7b", 1, [8192], 0),
+                ("llama8b", 2, [2048, 1500], 2), ("qwen7b", 1, [8192], 0), ("qwen7b", 1, [8192], 2),
+                ("qwen7b", 2, [8192, 3000], 2),
                 ("qwen7b", 8, [8192, 17, 4000, 8191, 1, 2048, 6000, 8100], 0)]
 
 
