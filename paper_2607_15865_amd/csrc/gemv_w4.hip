@@ -59,22 +59,35 @@ __global__ void __launch_bounds__(NW * 64) gemv_w4_kernel(GemvArgs a) {
 
     // ---- prologue: activation slice into LDS
     if (NORM) {
+        // wave b reduces row b; 16-byte loads, unrolled so that 8 are in
+        // flight at once (a loop that waits for each load pays one L2 round
+        // trip per step)
         const int K = W.K;
         for (int b = wave; b < B; b += NW) {
             const float* xr = a.x_f32 + (size_t)b * K;
             float ss = 0.f;
+#pragma unroll 8
             for (int k = lane * 4; k < K; k += 256) {
-                float4 v = *reinterpret_cast<const float4*>(xr + k);
-                ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+                const float4 v = *reinterpret_cast<const float4*>(xr + k);
+                ss += (v.x * v.x + v.y * v.y) + (v.z * v.z + v.w * v.w);
             }
             ss = wave_sum(ss);
             if (lane == 0) rinv[b] = 1.0f / sqrtf(ss / (float)K + a.eps);
         }
         __syncthreads();
-        for (int i = tid; i < B * klen; i += NW * 64) {
-            const int b = i / klen, k = i - b * klen;
-            const float g = bf16_bits_to_f32(a.gamma[klo + k]);
-            xs[b * ldx + k] = act_f16(a.x_f32[(size_t)b * K + klo + k] * rinv[b] * g);
+        // the block's k slice, 4 elements per thread and pass
+        const int k4n = klen / 4;
+#pragma unroll 4
+        for (int i = tid; i < B * k4n; i += NW * 64) {
+            const int b = i / k4n, k = 4 * (i - b * k4n);
+            const float4 v = *reinterpret_cast<const float4*>(a.x_f32 + (size_t)b * K + klo + k);
+            const uint2 g = *reinterpret_cast<const uint2*>(a.gamma + klo + k);
+            const float rb = rinv[b];
+            f16 o[4] = {act_f16(v.x * rb * __uint_as_float(g.x << 16)),
+                        act_f16(v.y * rb * __uint_as_float(g.x & 0xFFFF0000u)),
+                        act_f16(v.z * rb * __uint_as_float(g.y << 16)),
+                        act_f16(v.w * rb * __uint_as_float(g.y & 0xFFFF0000u))};
+            *reinterpret_cast<uint2*>(xs + b * ldx + k) = *reinterpret_cast<const uint2*>(o);
         }
     } else {
         const int nv = klen / 8;
