@@ -293,12 +293,9 @@ PrefillWs plan_prefill(const layer_s* L, int T, int hist) {
     return w;
 }
 
-constexpr int DEC_MAX_CHUNKS = 32;
-int decode_chunk(int max_ctx) {
-    const int keys = max_ctx + 1;
-    int ch = 64 * ((keys + 64 * DEC_MAX_CHUNKS - 1) / (64 * DEC_MAX_CHUNKS));
-    return std::min(512, std::max(64, ch));
-}
+// keys per chunk of the separate-kernel decode attention (its split kernel
+// stages one chunk of K and V in LDS)
+int decode_chunk(int) { return 64; }
 
 struct DecodeWs { size_t q, part, attn, h, g, total; int chunk, nchunks; };
 DecodeWs plan_decode(const layer_s* L, int B, int max_ctx) {

@@ -31,10 +31,11 @@
 // kernel merges the chunks of each query tile in chunk order with the
 // log-sum-exp rule, so results do not depend on timing.
 //
-// Decode: one query per sequence.  Split-KV: a block reads one chunk of one
-// kv head's cache once for all the query heads of its group (VALU dot
-// products, v_dot2 on bf16 pairs), writes a partial (max, sum, unnormalised
-// output), and a combine kernel merges the chunks with the log-sum-exp rule.
+// Decode: one query per sequence.  Split-KV: a block stages one 64-key chunk
+// of one kv head's cache in LDS once for all the query heads of its group,
+// forms scores and P V on the 16x16x32 bf16 MFMA, writes a partial (max,
+// sum, unnormalised output), and a combine kernel merges the chunks with the
+// log-sum-exp rule.
 #include "common.h"
 #include "launch.h"
 
@@ -288,149 +289,210 @@ __global__ void __launch_bounds__(64 * PF_MAXHB) attn_prefill_merge_kernel(AttnP
 // ---------------------------------------------------------------- decode
 
 constexpr int MAXR = 8;      // query heads per kv head
-constexpr int DEC_MAXCH = 512;
+constexpr int DEC_CH = 64;       // keys per chunk of the decode split kernel
 
+// One chunk of DEC_CH keys of one (row, kv head) for all r query heads of
+// the group, on the 16x16x32 bf16 MFMA (the design of the persistent decode's
+// attention units): the chunk's K and V rows go straight from memory to LDS
+// (16-byte chunks XOR-swizzled by row), the heads are the MFMA columns
+// (padded to 16), and each of the two 32-key groups goes to two waves that
+// both form its scores S^T = K Q^T and softmax in registers and each take
+// half of the dims of O^T = V^T P^T (P as a bf16 pair hi + lo).  Rows past
+// the chunk's keys read the chunk's first row (a written cache slot, so V
+// stays finite) and get probability 0.  The two groups' states are merged
+// in LDS into the chunk partial (max, sum, unnormalised output).
 template <int D>
 __global__ void __launch_bounds__(256) attn_decode_split_kernel(AttnDecodeArgs a) {
-    constexpr int LPK = D / 8;        // lanes per key
-    constexpr int KPW = 64 / LPK;     // keys per wave load
-    __shared__ float sc[MAXR][DEC_MAXCH];
-    __shared__ float ored[4][MAXR][D];
-    __shared__ float stat[MAXR][2];
+    constexpr int NCK = D / 8, KROWS = 1024 / (2 * D), CH = DEC_CH;
+    extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+    unsigned char* Kst = smem;                                         // [CH][D] bf16
+    unsigned char* Vst = smem + CH * D * 2;                            // [CH][D] bf16
+    float* ored = reinterpret_cast<float*>(Vst + CH * D * 2);          // [2][MAXR][D]
+    float* gst = ored + 2 * MAXR * D;                                  // [2][MAXR][2]
+    float* mst = gst + 2 * MAXR * 2;                                   // [CH]
+    uint16_t* qb = reinterpret_cast<uint16_t*>(mst + CH);              // [MAXR][D]
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int b = blockIdx.x / a.nkv, g = blockIdx.x % a.nkv;
     const int chunk = blockIdx.y;
     const int ctx = a.ctx_lens[b];
-    const int start = chunk * a.chunk;
-    const int end = min(start + a.chunk, ctx + 1);
+    const int start = chunk * CH, end = min(start + CH, ctx + 1);
     if (start >= end) return;
+    const int nkeys = end - start, ng = (nkeys + 31) / 32;
     const int r = a.nq / a.nkv;
-    const int kl = lane / LPK, dseg = lane % LPK;
     const uint16_t* kc = a.k_cache + (size_t)b * a.stride_b + (size_t)g * a.stride_h;
     const uint16_t* vc = a.v_cache + (size_t)b * a.stride_b + (size_t)g * a.stride_h;
+    auto kswz = [](int k) { return ((k & 3) | ((k >> 1) & 12)) & (NCK - 1); };
+    auto vswz = [](int k) { return 2 * ((k >> 3) & 3); };
 
-    // q of the group's heads: dims 8*dseg .. +8, as bf16 pairs
-    uint32_t qv[MAXR][4];
-#pragma unroll
-    for (int i = 0; i < MAXR; i++) {
-        u32x4 t = {0, 0, 0, 0};
-        if (i < r) t = *reinterpret_cast<const u32x4*>(a.q + ((size_t)b * a.nq + g * r + i) * D + dseg * 8);
-        qv[i][0] = t[0]; qv[i][1] = t[1]; qv[i][2] = t[2]; qv[i][3] = t[3];
+    // K, V rows (and the mask values) straight to LDS, q of the group's heads
+    for (int i = wave; i < CH / KROWS; i += 4) {
+        const int row = i * KROWS + lane / NCK, pc = lane % NCK;
+        const size_t src = (size_t)(start + (row < nkeys ? row : 0)) * D;
+        __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(kc + src + (pc ^ kswz(row)) * 8),
+                                         (__attribute__((address_space(3))) void*)(Kst + i * 1024), 16, 0, 0);
+        __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(vc + src + (pc ^ vswz(row)) * 8),
+                                         (__attribute__((address_space(3))) void*)(Vst + i * 1024), 16, 0, 0);
     }
-    const float* mrow = a.mask ? a.mask + (size_t)b * a.max_seq : nullptr;
+    if (a.mask && wave == 0)
+        __builtin_amdgcn_global_load_lds(
+            reinterpret_cast<const void*>(a.mask + (size_t)b * a.max_seq + start + (lane < nkeys ? lane : 0)),
+            (__attribute__((address_space(3))) void*)mst, 4, 0, 0);
+    for (int i = tid; i < r * D / 8; i += 256)
+        reinterpret_cast<u32x4*>(qb)[i] =
+            *reinterpret_cast<const u32x4*>(a.q + ((size_t)b * a.nq + g * r) * D + i * 8);
+    __syncthreads();           // also: the stage loads have landed
+
+    const int n16 = lane & 15, q4 = lane >> 4;
+    const int gw = wave >> 1, part = wave & 1;
     const float LOG2E = 1.4426950408889634f;
-
-    // scores
-    for (int k0 = start + wave * KPW; k0 < end; k0 += 4 * KPW) {
-        const int key = k0 + kl;
-        const bool valid = key < end;
-        u32x4 kk = {0, 0, 0, 0};
-        if (valid) kk = *reinterpret_cast<const u32x4*>(kc + (size_t)key * D + dseg * 8);
-        const uint32_t kw[4] = {kk[0], kk[1], kk[2], kk[3]};
+    if (gw < ng) {
+        // S^T of tiles t = 0, 1: A row n16 of tile t is key 32 gw + 8 (n16 / 4)
+        // + 4 t + n16 % 4, so register j of lane (n16, q4) is key 8 q4 + 4 t + j
+        // of the group, head n16
+        f32x4 sacc[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+        const int row0 = 32 * gw + 8 * (n16 >> 2) + (n16 & 3), row1 = row0 + 4;
+        const unsigned char* K0 = Kst + (size_t)row0 * D * 2;
+        const unsigned char* K1 = Kst + (size_t)row1 * D * 2;
+        const uint16_t* qsrc = qb + (n16 < r ? n16 : 0) * D + 8 * q4;
 #pragma unroll
-        for (int i = 0; i < MAXR; i++) {
-            if (i >= r) break;
-            float v = 0.f;
-#pragma unroll
-            for (int p = 0; p < 4; p++)
-                v = __builtin_amdgcn_fdot2_f32_bf16(as_bf16x2(qv[i][p]), as_bf16x2(kw[p]), v, false);
-#pragma unroll
-            for (int o = 1; o < LPK; o <<= 1) v += __shfl_xor(v, o, 64);
-            if (dseg == 0 && valid) {
-                float s = v * a.scale_log2;
-                if (mrow) s += mrow[key] * LOG2E;
-                sc[i][key - start] = s;
-            }
+        for (int s = 0; s < D / 32; s++) {
+            const u32x4 w = *reinterpret_cast<const u32x4*>(qsrc + 32 * s);
+            const bf16x8 qf = __builtin_bit_cast(bf16x8, n16 < r ? w : u32x4{0u, 0u, 0u, 0u});
+            const bf16x8 k0 = *reinterpret_cast<const bf16x8*>(K0 + (((4 * s + q4) ^ kswz(row0)) << 4));
+            const bf16x8 k1 = *reinterpret_cast<const bf16x8*>(K1 + (((4 * s + q4) ^ kswz(row1)) << 4));
+            sacc[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k0, qf, sacc[0], 0, 0, 0);
+            sacc[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k1, qf, sacc[1], 0, 0, 0);
         }
-    }
-    __syncthreads();
-    // softmax statistics of the chunk (one wave per head)
-    const int n = end - start;
-    for (int i = wave; i < r; i += 4) {
+        float sv[8];
         float mx = -INFINITY;
-        for (int j = lane; j < n; j += 64) mx = fmaxf(mx, sc[i][j]);
-        mx = wave_max(mx);
-        float sum = 0.f;
-        for (int j = lane; j < n; j += 64) {
-            const float pv = (mx == -INFINITY) ? 0.f : exp2f(sc[i][j] - mx);
-            sc[i][j] = pv;
-            sum += pv;
+#pragma unroll
+        for (int e = 0; e < 8; e++) {
+            const int kk = 32 * gw + 8 * q4 + e;
+            float v = sacc[e / 4][e % 4] * a.scale_log2;
+            if (a.mask) v += mst[kk] * LOG2E;
+            v = kk < nkeys ? v : -INFINITY;
+            sv[e] = v;
+            mx = fmaxf(mx, v);
         }
-        sum = wave_sum(sum);
-        if (lane == 0) { stat[i][0] = mx; stat[i][1] = sum; }
+        mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+        bf16x8 phi, plo;
+        float ls = 0.f;
+#pragma unroll
+        for (int e = 0; e < 8; e++) {
+            const float pv = (mx == -INFINITY) ? 0.f : exp2f(sv[e] - mx);
+            ls += pv;
+            const __bf16 hi = (__bf16)pv;
+            phi[e] = hi;
+            plo[e] = (__bf16)(pv - (float)hi);
+        }
+        ls += __shfl_xor(ls, 16, 64);
+        ls += __shfl_xor(ls, 32, 64);
+        // O^T += V^T P^T over this wave's half of the 16-dim blocks: lane
+        // (n16, q4) holds V of keys 8 q4 .. + 7, dim 16 db + n16
+        const uint16_t* Vw = reinterpret_cast<const uint16_t*>(Vst + (size_t)(32 * gw + 8 * q4) * D * 2);
+#pragma unroll
+        for (int d0 = 0; d0 < D / 32; d0++) {
+            const int db = part * (D / 32) + d0;
+            const int pos = ((((2 * db + (n16 >> 3)) ^ (2 * q4)) << 3) | (n16 & 7));
+            u32x4 vw;
+#pragma unroll
+            for (int j = 0; j < 4; j++)
+                vw[j] = (uint32_t)Vw[2 * j * D + pos] | ((uint32_t)Vw[(2 * j + 1) * D + pos] << 16);
+            const bf16x8 vf = __builtin_bit_cast(bf16x8, vw);
+            f32x4 o = f32x4{0.f, 0.f, 0.f, 0.f};
+            o = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, phi, o, 0, 0, 0);
+            o = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, plo, o, 0, 0, 0);
+            if (n16 < r) *reinterpret_cast<f32x4*>(ored + (gw * MAXR + n16) * D + 16 * db + 4 * q4) = o;
+        }
+        if (n16 < r && q4 == 0 && part == 0) {
+            gst[(gw * MAXR + n16) * 2] = mx;
+            gst[(gw * MAXR + n16) * 2 + 1] = ls;
+        }
     }
     __syncthreads();
-    // P V
-    float ov[MAXR][8];
-#pragma unroll
-    for (int i = 0; i < MAXR; i++)
-#pragma unroll
-        for (int j = 0; j < 8; j++) ov[i][j] = 0.f;
-    for (int k0 = start + wave * KPW; k0 < end; k0 += 4 * KPW) {
-        const int key = k0 + kl;
-        if (key >= end) continue;
-        const u32x4 vv = *reinterpret_cast<const u32x4*>(vc + (size_t)key * D + dseg * 8);
-        const uint32_t vw[4] = {vv[0], vv[1], vv[2], vv[3]};
-        float vf[8];
-#pragma unroll
-        for (int p = 0; p < 4; p++) {
-            vf[2 * p] = __uint_as_float(vw[p] << 16);
-            vf[2 * p + 1] = __uint_as_float(vw[p] & 0xFFFF0000u);
-        }
-#pragma unroll
-        for (int i = 0; i < MAXR; i++) {
-            if (i >= r) break;
-            const float pv = sc[i][key - start];
-#pragma unroll
-            for (int j = 0; j < 8; j++) ov[i][j] += pv * vf[j];
-        }
-    }
-    // reduce over the keys of the wave (lanes with equal dseg), then waves
-#pragma unroll
-    for (int i = 0; i < MAXR; i++) {
-        if (i >= r) break;
-#pragma unroll
-        for (int j = 0; j < 8; j++) {
-            float v = ov[i][j];
-#pragma unroll
-            for (int o = LPK; o < 64; o <<= 1) v += __shfl_xor(v, o, 64);
-            ov[i][j] = v;
-        }
-        if (kl == 0)
-#pragma unroll
-            for (int j = 0; j < 8; j++) ored[wave][i][dseg * 8 + j] = ov[i][j];
-    }
-    __syncthreads();
+    // the chunk partial of every head: the groups rescaled to their common max
     for (int idx = tid; idx < r * D; idx += 256) {
-        const int i = idx / D, dim = idx % D;
-        const float v = ored[0][i][dim] + ored[1][i][dim] + ored[2][i][dim] + ored[3][i][dim];
+        const int i = idx / D, dim = idx - i * D;
+        const float m0 = gst[i * 2], m1 = ng > 1 ? gst[(MAXR + i) * 2] : -INFINITY;
+        const float M = fmaxf(m0, m1);
+        float v = 0.f, l = 0.f;
+        if (M != -INFINITY) {
+            const float s0 = m0 == -INFINITY ? 0.f : exp2f(m0 - M);
+            const float s1 = m1 == -INFINITY ? 0.f : exp2f(m1 - M);
+            v = s0 * ored[i * D + dim] + (ng > 1 ? s1 * ored[(MAXR + i) * D + dim] : 0.f);
+            l = s0 * gst[i * 2 + 1] + (ng > 1 ? s1 * gst[(MAXR + i) * 2 + 1] : 0.f);
+        }
         float* pp = a.part + (((size_t)b * a.nq + g * r + i) * a.nchunks + chunk) * (D + 2);
         pp[dim] = v;
-        if (dim == 0) { pp[D] = stat[i][0]; pp[D + 1] = stat[i][1]; }
+        if (dim == 0) { pp[D] = M; pp[D + 1] = l; }
     }
 }
 
+// Merge of the chunk partials of one (row, head): thread group gq (of
+// DEC_CG groups of D threads, one thread per dim) merges the chunks
+// gq, gq + DEC_CG, ... in order, in batches of CB whose states are requested
+// together; the groups' states then meet in LDS and group 0 merges them in
+// group order.
+constexpr int DEC_CG = 4;
+
 template <int D>
-__global__ void __launch_bounds__(D) attn_decode_combine_kernel(AttnDecodeArgs a) {
+__global__ void __launch_bounds__(D * DEC_CG) attn_decode_combine_kernel(AttnDecodeArgs a) {
+    __shared__ float gm[DEC_CG], gl[DEC_CG], go[DEC_CG][D];
     const int b = blockIdx.x / a.nq, head = blockIdx.x % a.nq;
-    const int dim = threadIdx.x;
+    const int dim = threadIdx.x % D, gq = threadIdx.x / D;
     const int ctx = a.ctx_lens[b];
     const int nch = (ctx + 1 + a.chunk - 1) / a.chunk;
     const float* pp = a.part + ((size_t)b * a.nq + head) * a.nchunks * (D + 2);
-    float M = -INFINITY;
-    for (int ch = 0; ch < nch; ch++) M = fmaxf(M, pp[ch * (D + 2) + D]);
-    float L = 0.f, O = 0.f;
-    if (M != -INFINITY) {
-        for (int ch = 0; ch < nch; ch++) {
-            const float mc = pp[ch * (D + 2) + D];
-            if (mc == -INFINITY) continue;
-            const float w = exp2f(mc - M);
-            L += w * pp[ch * (D + 2) + D + 1];
-            O += w * pp[ch * (D + 2) + dim];
+    constexpr int CB = 8;
+    float M = -INFINITY, L = 0.f, O = 0.f;
+    for (int c0 = gq; c0 < nch; c0 += CB * DEC_CG) {
+        float mc[CB], lc[CB], oc[CB];
+#pragma unroll
+        for (int j = 0; j < CB; j++) {
+            const int ch0 = c0 + j * DEC_CG;
+            const int ch = ch0 < nch ? ch0 : gq;
+            mc[j] = pp[ch * (D + 2) + D];
+            lc[j] = pp[ch * (D + 2) + D + 1];
+            oc[j] = pp[ch * (D + 2) + dim];
+        }
+        float Mn = M;
+#pragma unroll
+        for (int j = 0; j < CB; j++)
+            if (c0 + j * DEC_CG < nch) Mn = fmaxf(Mn, mc[j]);
+        if (Mn == -INFINITY) continue;
+        const float sc = (M == -INFINITY) ? 0.f : exp2f(M - Mn);
+        L *= sc;
+        O *= sc;
+#pragma unroll
+        for (int j = 0; j < CB; j++) {
+            if (c0 + j * DEC_CG >= nch || mc[j] == -INFINITY) continue;
+            const float w = exp2f(mc[j] - Mn);
+            L += w * lc[j];
+            O += w * oc[j];
+        }
+        M = Mn;
+    }
+    if (dim == 0) { gm[gq] = M; gl[gq] = L; }
+    go[gq][dim] = O;
+    __syncthreads();
+    if (gq != 0) return;
+    float Mt = -INFINITY;
+#pragma unroll
+    for (int q = 0; q < DEC_CG; q++) Mt = fmaxf(Mt, gm[q]);
+    float Lt = 0.f, Ot = 0.f;
+    if (Mt != -INFINITY) {
+#pragma unroll
+        for (int q = 0; q < DEC_CG; q++) {
+            if (gm[q] == -INFINITY) continue;
+            const float w = exp2f(gm[q] - Mt);
+            Lt += w * gl[q];
+            Ot += w * go[q][dim];
         }
     }
-    const float v = (L > 0.f) ? O / L : 0.f;
+    const float v = (Lt > 0.f) ? Ot / Lt : 0.f;
     a.out[((size_t)b * a.nq + head) * D + dim] = act_f16(v);
 }
 
@@ -493,14 +555,16 @@ int launch_attn_prefill(const AttnPrefillArgs& a, const AttnPrefillPlan& p, hipS
 }
 
 int launch_attn_decode(const AttnDecodeArgs& a, hipStream_t stream) {
-    if (a.chunk > DEC_MAXCH || a.nq / a.nkv > MAXR) return -1;
+    if (a.chunk != DEC_CH || a.nq / a.nkv > MAXR) return -1;
     dim3 g1(a.B * a.nkv, a.nchunks), g2(a.B * a.nq);
+    // K and V stages, the two groups' outputs and statistics, mask values, q
+    const size_t lds = (size_t)2 * DEC_CH * a.d * 2 + (2 * MAXR * a.d + 4 * MAXR + DEC_CH) * 4 + (size_t)MAXR * a.d * 2;
     if (a.d == 128) {
-        hipLaunchKernelGGL(attn_decode_split_kernel<128>, g1, dim3(256), 0, stream, a);
-        hipLaunchKernelGGL(attn_decode_combine_kernel<128>, g2, dim3(128), 0, stream, a);
+        hipLaunchKernelGGL(attn_decode_split_kernel<128>, g1, dim3(256), lds, stream, a);
+        hipLaunchKernelGGL(attn_decode_combine_kernel<128>, g2, dim3(128 * DEC_CG), 0, stream, a);
     } else if (a.d == 64) {
-        hipLaunchKernelGGL(attn_decode_split_kernel<64>, g1, dim3(256), 0, stream, a);
-        hipLaunchKernelGGL(attn_decode_combine_kernel<64>, g2, dim3(64), 0, stream, a);
+        hipLaunchKernelGGL(attn_decode_split_kernel<64>, g1, dim3(256), lds, stream, a);
+        hipLaunchKernelGGL(attn_decode_combine_kernel<64>, g2, dim3(64 * DEC_CG), 0, stream, a);
     } else {
         return -1;
     }

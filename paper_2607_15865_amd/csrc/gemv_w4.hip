@@ -91,6 +91,7 @@ __global__ void __launch_bounds__(NW * 64) gemv_w4_kernel(GemvArgs a) {
         }
     } else {
         const int nv = klen / 8;
+#pragma unroll 4
         for (int i = tid; i < B * nv; i += NW * 64) {
             const int b = i / nv, v = i - b * nv;
             *reinterpret_cast<u32x4*>(xs + b * ldx + v * 8) =
