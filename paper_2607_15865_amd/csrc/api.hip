@@ -297,7 +297,7 @@ PrefillWs plan_prefill(const layer_s* L, int T, int hist) {
 // stages one chunk of K and V in LDS)
 int decode_chunk(int) { return 64; }
 
-struct DecodeWs { size_t q, part, attn, h, g, total; int chunk, nchunks; };
+struct DecodeWs { size_t q, part, attn, h, g, xn, total; int chunk, nchunks; };
 DecodeWs plan_decode(const layer_s* L, int B, int max_ctx) {
     const layer_config& c = L->cfg;
     const size_t qd = (size_t)c.n_heads * c.head_dim;
@@ -310,6 +310,7 @@ DecodeWs plan_decode(const layer_s* L, int B, int max_ctx) {
     w.attn = cv.take((size_t)B * qd * 2);
     w.h = cv.take((size_t)B * c.hidden * 4);
     w.g = cv.take((size_t)B * L->F_pad * 2);
+    w.xn = cv.take((size_t)B * c.hidden * 2);
     w.total = cv.off;
     return w;
 }
@@ -858,7 +859,15 @@ int layer_decode(layer_t L, const float* x, const int32_t* pos, const int32_t* c
     a1.copy_src = x;
     a1.copy_dst = h;
     a1.copy_n = B * H;
-    { ProfScope ps(L, 2, 0, st); rc |= launch_gemv_w4(EPI_QKV, true, a1, st); }
+    // with 4 rows or more the rows are normalised once, not in every block
+    const bool prenorm = B >= 4;
+    f16* xn = (f16*)(base + w.xn);
+    if (prenorm) {
+        rc |= launch_rmsnorm(x, (const uint16_t*)L->attn_norm.p, c.rms_eps, B, H, xn, st);
+        a1.x_f16 = xn;
+        a1.ldx = H;
+    }
+    { ProfScope ps(L, 2, 0, st); rc |= launch_gemv_w4(EPI_QKV, !prenorm, a1, st); }
 
     AttnDecodeArgs ad{};
     ad.q = q;
@@ -902,7 +911,12 @@ int layer_decode(layer_t L, const float* x, const int32_t* pos, const int32_t* c
     a3.copy_src = h;
     a3.copy_dst = y;
     a3.copy_n = B * H;
-    { ProfScope ps(L, 2, 4, st); rc |= launch_gemv_w4(EPI_SWIGLU, true, a3, st); }
+    if (prenorm) {
+        rc |= launch_rmsnorm(h, (const uint16_t*)L->mlp_norm.p, c.rms_eps, B, H, xn, st);
+        a3.x_f16 = xn;
+        a3.ldx = H;
+    }
+    { ProfScope ps(L, 2, 4, st); rc |= launch_gemv_w4(EPI_SWIGLU, !prenorm, a3, st); }
 
     GemvArgs a4{};
     a4.W = L->down.d;

@@ -11,7 +11,9 @@
 //
 // Optional prologue: RMSNorm of the fp32 rows (every block reduces the whole
 // row; the rows are small and L2-resident), rounded to bf16.  The first
-// weight tiles are requested before the prologue runs.
+// weight tiles are requested before the prologue runs.  (For 4 rows or more
+// the caller normalises the rows once beforehand instead and passes them as
+// fp16: the per-block reduction then costs more than the extra launch.)
 #include "common.h"
 #include "gemv_core.h"
 #include "launch.h"
@@ -171,8 +173,9 @@ int launch_t(const GemvArgs& a, hipStream_t stream) {
 
 template <bool ZP, bool G32>
 int launch_zp(int epi, bool norm, const GemvArgs& a, hipStream_t stream) {
-    if (epi == EPI_QKV && norm) return launch_t<EPI_QKV, true, ZP, G32>(a, stream);
-    if (epi == EPI_SWIGLU && norm) return launch_t<EPI_SWIGLU, true, ZP, G32>(a, stream);
+    if (epi == EPI_QKV) return norm ? launch_t<EPI_QKV, true, ZP, G32>(a, stream) : launch_t<EPI_QKV, false, ZP, G32>(a, stream);
+    if (epi == EPI_SWIGLU)
+        return norm ? launch_t<EPI_SWIGLU, true, ZP, G32>(a, stream) : launch_t<EPI_SWIGLU, false, ZP, G32>(a, stream);
     if (epi == EPI_RESID && !norm) return launch_t<EPI_RESID, false, ZP, G32>(a, stream);
     return -1;
 }
