@@ -49,6 +49,8 @@ def test_stage_calls_validate_before_any_hip_call():
     assert B.layer_prefill(None, 1, 1, 4, 1, 1, 2, 1, 1 << 20, 0) == B.W4_EINVAL
     assert B.layer_prefill_kv(None, 1, 1, 4, 0, 1, 1, 2, 1, 1 << 20, 0) == B.W4_EINVAL
     assert B.layer_decode(None, 1, 1, 1, 8, None, 1, 1, 1, 2, 1, 1 << 20, 0) == B.W4_EINVAL
+    assert B.layer_prefill_chunked(None, 1, 1, 4, 2, 1, 1, 2, 1, 1 << 20, 0) == B.W4_EINVAL
+    assert B.layer_prefill_chunked_workspace_size(None, 4, 2) == 0
     assert "null layer" in B.layer_last_error()
     assert B.layer_workspace_size(None, 0, 1, 16, 0) == 0
     assert B.layer_debug_dequant(None, 0, 1, stream=0) == B.W4_EINVAL

@@ -8,7 +8,7 @@ import pytest
 import torch
 
 from oracle import layer as O
-from paper_2607_15865_amd import synth
+from paper_2607_15865_amd import binding, synth
 from gpu_helpers import (assert_parity, bits_to_torch_f32, cache_values, device_layer, host_layer, log,
                          oracle_weights, to_cache_bits)
 
@@ -150,6 +150,28 @@ def test_prefill_chunked(name, T, chunk):
     gy = y.cpu().numpy().astype(np.float64)
     assert_parity(gy if rows is None else gy[rows], yo, "y")
     _check_new_kv(k, v, ko, vo, 0, T)
+
+
+def test_prefill_chunked_validation():
+    """Argument errors of the segmentation driver are reported before any
+    segment is enqueued: the output keeps its contents."""
+    cfg, _ = host_layer("tiny")
+    lay = device_layer("tiny")
+    h = lay.handle
+    T, chunk = 40, 16
+    n = binding.layer_prefill_chunked_workspace_size(h, T, chunk)
+    assert n > 0 and binding.layer_prefill_chunked_workspace_size(h, T, 0) == 0
+    x = torch.zeros(T, cfg.hidden, device="cuda")
+    y = torch.full_like(x, 7.0)
+    pos = torch.arange(T, dtype=torch.int32, device="cuda")
+    k, v = lay.new_cache(1, 0)
+    ws = torch.empty(n, dtype=torch.uint8, device="cuda")
+    assert binding.layer_prefill_chunked(h, x, pos, T, 0, k, v, y, ws, n) == binding.W4_EINVAL
+    assert binding.layer_prefill_chunked(h, x, pos, T, chunk, k, v, y, ws, n - 1) == binding.W4_EWORKSPACE
+    assert binding.layer_prefill_chunked(h, x, pos, cfg.max_seq + 1, chunk, k, v, y, ws, n) == binding.W4_ECAPACITY
+    assert binding.layer_prefill_chunked(h, x, pos, T, chunk, k, v, x, ws, n) == binding.W4_EINVAL
+    torch.cuda.synchronize()
+    assert bool((y == 7.0).all())
 
 
 DECODE_CASES = [("tiny", 1, [48], 0), ("tiny", 1, [48], 1), ("tiny", 4, [0, 9, 64, 126], 0),
