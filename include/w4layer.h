@@ -126,7 +126,7 @@ typedef struct kv_desc {
  * counters, lives in the caller's workspace), so stage calls on different
  * streams may share the handle, each with its own workspace.  One exception:
  * the persistent decode path (layer_set_decode_path; it also serves
- * prefill / prefill_kv calls of at most 4 tokens) needs every compute unit
+ * prefill / prefill_kv calls of a few tokens) needs every compute unit
  * of the device at once, so two of its launches must not overlap on one
  * device; a caller that runs such calls on several streams at once selects
  * path 1.  The diagnostics (profiling, decode stamps) are not for concurrent use.
@@ -260,15 +260,18 @@ int kv_append(const kv_desc* desc, void* k_cache, void* v_cache,
 int layer_debug_dequant(layer_t layer, int32_t which, float* out, void* stream);
 
 /* Decode implementation (tuning / testing): 0 automatic (default), 1 a
- * sequence of kernels, 2 one persistent launch with one block per CU (used
- * automatically for B <= 4 when the layer has no zero points and its
- * on-chip working set fits).  Both compute the same result; the
- * persistent path is deterministic.  With 2, a decode call the persistent
- * path cannot serve fails with W4_EUNSUPPORTED.  The same launch also
- * serves layer_prefill / layer_prefill_kv calls of T <= 4 tokens (its rows
- * are then the tokens of one sequence, and row t also attends to the new
- * keys of rows before it) unless the path is 1, which keeps them on the
- * prefill kernels.  Errors: W4_EINVAL. */
+ * sequence of kernels, 2 one persistent launch with one block per CU (B <=
+ * 4, no zero points, groups of 64 or more, and the on-chip working set must
+ * fit; chosen automatically for B <= 2).  Both compute the same result up to
+ * rounding order; the persistent path is deterministic, the kernel sequence
+ * adds k-split partials with atomics.  With 2, a decode call the persistent
+ * path cannot serve fails with W4_EUNSUPPORTED.  The decode kernels also
+ * serve layer_prefill / layer_prefill_kv calls of a few tokens, the tokens
+ * as rows of one sequence sharing its cache (row t also attends to the new
+ * keys of rows before it): with path 0 up to 2 tokens as the persistent
+ * launch and up to 8 as the kernel sequence, with path 2 up to 4 as the
+ * persistent launch; path 1 keeps every prefill call on the prefill
+ * kernels.  Errors: W4_EINVAL. */
 int layer_set_decode_path(layer_t layer, int32_t path);
 
 /* Time stamps of the persistent decode path (diagnostics): with on != 0 its

@@ -320,6 +320,7 @@ struct FusedPlan {
     bool ok = false;
     int nblocks = 0, chunk = 0, nchunk = 0, S_qkv = 1, S_o = 1, S_down = 1, ldx = 0, comb_per = 0, comb_lpv = 1;
     int slots = 0;                // gate/up column tiles of the busiest block
+    int gam_lds = 1;              // RMSNorm weights in LDS
     size_t off_h = 0, off_red = 0, off_gam = 0, off_zero = 0, off_c64 = 0, lds_bytes = 0;
     size_t qkv_part = 0, apart = 0, A = 0, o_part = 0, g = 0, down_part = 0, total = 0;
 };
@@ -371,14 +372,20 @@ FusedPlan plan_fused(const layer_s* L, int B, int max_ctx, bool query_device) {
     const int V = B * qd;
     p.comb_per = (((V + P - 1) / P) + 1) & ~1;
     const size_t comb_bytes = (size_t)p.comb_per * 2;
-    for (;; ch = ch > 32 ? (ch - 1) / 32 * 32 : 16) {
-        p.chunk = ch;
-        p.nchunk = (max_ctx + 1 + ch - 1) / ch;
-        p.off_h = align256(std::max(std::max(gemv_bytes, decode_fused_attn_bytes(ch, d)), comb_bytes));
-        p.off_red = align256(p.off_h + (size_t)B * H * 4);
-        p.off_gam = align256(p.off_red + (size_t)(NWAVE * p.slots * maxb * 32 + 8 + NWAVE * maxb + maxb * 32 + 2 * maxb) * 4);
-        p.lds_bytes = p.off_gam + (size_t)2 * H * 2;
-        if (p.lds_bytes <= 160 * 1024 || ch == 16) break;
+    // first with the RMSNorm weights in LDS, then (if no chunk fits) without
+    const int ch0 = ch;
+    for (int gl = 1; gl >= (B == 1 ? 1 : 0); gl--) {
+        p.gam_lds = gl;
+        for (ch = ch0;; ch = ch > 32 ? (ch - 1) / 32 * 32 : 16) {
+            p.chunk = ch;
+            p.nchunk = (max_ctx + 1 + ch - 1) / ch;
+            p.off_h = align256(std::max(std::max(gemv_bytes, decode_fused_attn_bytes(ch, d)), comb_bytes));
+            p.off_red = align256(p.off_h + (size_t)B * H * 4);
+            p.off_gam = align256(p.off_red + (size_t)(NWAVE * p.slots * maxb * 32 + 8 + NWAVE * maxb + maxb * 32 + 2 * maxb) * 4);
+            p.lds_bytes = p.off_gam + (gl ? (size_t)2 * H * 2 : 0);
+            if (p.lds_bytes <= 160 * 1024 || ch == 16) break;
+        }
+        if (p.lds_bytes <= 160 * 1024) break;
     }
     if (p.lds_bytes > 160 * 1024) return p;
     p.comb_lpv = 1;
@@ -502,6 +509,7 @@ int launch_fused(layer_s* L, const FusedPlan& fp, const float* x, const int32_t*
     a.plan = (const int*)L->fplan.p;
     a.comb_per = fp.comb_per; a.comb_lpv = fp.comb_lpv;
     a.slots = fp.slots;
+    a.gam_lds = fp.gam_lds;
     a.chunk = fp.chunk; a.nchunk = fp.nchunk;
     a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)c.head_dim));
     a.nblocks = fp.nblocks;
@@ -515,17 +523,135 @@ int launch_fused(layer_s* L, const FusedPlan& fp, const float* x, const int32_t*
     return launch_decode_fused(a, st);
 }
 
-// prefill / prefill_kv of T <= 4 tokens run as one persistent launch (the
-// rows are the tokens) unless the layer is held to separate kernels
+// The decode as a sequence of kernels (GEMVs on up to 8 rows, split-KV
+// attention, chunk merge).  shared: the B rows are consecutive tokens of one
+// sequence with one cache (prefill / prefill_kv of at most 8 tokens), row b
+// at context ctx_base + b: the q/k/v GEMV writes every row's new key and
+// value before the attention kernel reads the cache.  ps_stage: the profiling
+// stage the launches count for (2 decode, 0/1 prefill).
+int run_decode_seq(layer_s* L, const float* x, const int32_t* pos, const int32_t* ctx_lens, int ctx_base, bool shared,
+                   const float* attn_mask, int B, int max_ctx, void* kc, void* vc, float* y, void* ws,
+                   size_t ws_bytes, hipStream_t st, int ps_stage) {
+    const layer_config& c = L->cfg;
+    const DecodeWs w = plan_decode(L, B, max_ctx);
+    if (ws_bytes < w.total) return fail(W4_EWORKSPACE, "workspace %zu bytes, need %zu", ws_bytes, w.total);
+    char* base = (char*)ws;
+    uint16_t* q = (uint16_t*)(base + w.q);
+    float* part = (float*)(base + w.part);
+    f16* attn = (f16*)(base + w.attn);
+    float* h = (float*)(base + w.h);
+    f16* g = (f16*)(base + w.g);
+    const int H = c.hidden, d = c.head_dim, qd = c.n_heads * d;
+    const long long sh = (long long)c.max_seq * d, sb = shared ? 0 : sh * c.n_kv_heads;
+    int rc = 0;
+
+    GemvArgs a1{};
+    a1.W = L->qkv.d;
+    a1.x_f32 = x;
+    a1.gamma = (const uint16_t*)L->attn_norm.p;
+    a1.eps = c.rms_eps;
+    a1.B = B;
+    a1.ksplit = 1;
+    a1.ep = base_epi(L);
+    a1.ep.q_out = q;
+    a1.ep.k_cache = (uint16_t*)kc;
+    a1.ep.v_cache = (uint16_t*)vc;
+    a1.ep.cache_stride_b = sb;
+    a1.ep.cache_stride_h = sh;
+    a1.ep.pos = pos;
+    a1.ep.slot_dev = shared ? nullptr : ctx_lens;
+    a1.ep.slot_base = ctx_base;
+    a1.copy_src = x;
+    a1.copy_dst = h;
+    a1.copy_n = B * H;
+    // with 4 rows or more the rows are normalised once, not in every block
+    const bool prenorm = B >= 4;
+    f16* xn = (f16*)(base + w.xn);
+    if (prenorm) {
+        rc |= launch_rmsnorm(x, (const uint16_t*)L->attn_norm.p, c.rms_eps, B, H, xn, st);
+        a1.x_f16 = xn;
+        a1.ldx = H;
+    }
+    { ProfScope ps(L, ps_stage, ps_stage == 2 ? 0 : 1, st); rc |= launch_gemv_w4(EPI_QKV, !prenorm, a1, st); }
+
+    AttnDecodeArgs ad{};
+    ad.q = q;
+    ad.k_cache = (const uint16_t*)kc;
+    ad.v_cache = (const uint16_t*)vc;
+    ad.stride_b = sb;
+    ad.stride_h = sh;
+    ad.ctx_lens = shared ? nullptr : ctx_lens;
+    ad.ctx_base = ctx_base;
+    ad.mask = attn_mask;
+    ad.max_seq = c.max_seq;
+    ad.part = part;
+    ad.out = attn;
+    ad.B = B;
+    ad.nq = c.n_heads;
+    ad.nkv = c.n_kv_heads;
+    ad.d = d;
+    ad.chunk = w.chunk;
+    ad.nchunks = w.nchunks;
+    ad.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)d));
+    { ProfScope ps(L, ps_stage, ps_stage == 2 ? 1 : 2, st); rc |= launch_attn_decode(ad, st); }
+
+    GemvArgs a2{};
+    a2.W = L->o.d;
+    a2.x_f16 = attn;
+    a2.ldx = qd;
+    a2.B = B;
+    a2.ksplit = gemv_ksplit(L->o.d, 512, B);
+    a2.ep = base_epi(L);
+    a2.ep.out_f32 = h;
+    { ProfScope ps(L, ps_stage, 3, st); rc |= launch_gemv_w4(EPI_RESID, false, a2, st); }
+
+    GemvArgs a3{};
+    a3.W = L->gu.d;
+    a3.x_f32 = h;
+    a3.gamma = (const uint16_t*)L->mlp_norm.p;
+    a3.eps = c.rms_eps;
+    a3.B = B;
+    a3.ksplit = 1;
+    a3.ep = base_epi(L);
+    a3.ep.act_out = g;
+    a3.copy_src = h;
+    a3.copy_dst = y;
+    a3.copy_n = B * H;
+    if (prenorm) {
+        rc |= launch_rmsnorm(h, (const uint16_t*)L->mlp_norm.p, c.rms_eps, B, H, xn, st);
+        a3.x_f16 = xn;
+        a3.ldx = H;
+    }
+    { ProfScope ps(L, ps_stage, ps_stage == 2 ? 4 : 5, st); rc |= launch_gemv_w4(EPI_SWIGLU, !prenorm, a3, st); }
+
+    GemvArgs a4{};
+    a4.W = L->down.d;
+    a4.x_f16 = g;
+    a4.ldx = L->F_pad;
+    a4.B = B;
+    a4.ksplit = gemv_ksplit(L->down.d, 512, B);
+    a4.ep = base_epi(L);
+    a4.ep.out_f32 = y;
+    { ProfScope ps(L, ps_stage, ps_stage == 2 ? 5 : 6, st); rc |= launch_gemv_w4(EPI_RESID, false, a4, st); }
+    if (rc) return fail(W4_EHIP, "kernel launch failed: %s", hipGetErrorString(hipGetLastError()));
+    return W4_OK;
+}
+
+// Prefill / prefill_kv of a few tokens runs on the decode kernels, the tokens
+// as rows sharing one cache: up to 2 tokens (4 with decode path 2) as one
+// persistent launch, up to 8 (decode path 0) as the decode kernel sequence;
+// decode path 1 keeps every call on the prefill kernels.
 FusedPlan small_prefill_plan(layer_s* L, int T, int hist) {
-    if (T > 4 || L->decode_path == 1) return FusedPlan{};
+    if (!((L->decode_path == 0 && T <= 2) || (L->decode_path == 2 && T <= 4))) return FusedPlan{};
     return plan_fused(L, T, hist + T - 1, true);
 }
+bool small_prefill_seq(const layer_s* L, int T) { return L->decode_path == 0 && T <= 8; }
 
 size_t prefill_ws_bytes(layer_s* L, int T, int hist) {
     size_t n = plan_prefill(L, T, hist).total;
     const FusedPlan fp = small_prefill_plan(L, T, hist);
     if (fp.ok) n = std::max(n, fp.total);
+    else if (small_prefill_seq(L, T)) n = std::max(n, plan_decode(L, T, hist + T - 1).total);
     return n;
 }
 
@@ -547,6 +673,8 @@ int run_prefill(layer_s* L, const float* x, const int32_t* pos, int T, int hist,
         if (rc) return fail(W4_EHIP, "persistent launch failed: %s", hipGetErrorString(hipGetLastError()));
         return W4_OK;
     }
+    if (small_prefill_seq(L, T))
+        return run_decode_seq(L, x, pos, nullptr, hist, true, nullptr, T, hist + T - 1, kc, vc, y, ws, ws_bytes, st, stage);
     const PrefillWs w = plan_prefill(L, T, hist);
     if (ws_bytes < w.total) return fail(W4_EWORKSPACE, "workspace %zu bytes, need %zu", ws_bytes, w.total);
     char* base = (char*)ws;
@@ -820,7 +948,9 @@ int layer_decode(layer_t L, const float* x, const int32_t* pos, const int32_t* c
     if (B > 8) return fail(W4_EUNSUPPORTED, "decode batch above 8");
     if ((long long)max_ctx + 1 > c.max_seq) return fail(W4_ECAPACITY, "max_ctx + 1 = %lld exceeds max_seq %d", (long long)max_ctx + 1, c.max_seq);
     hipStream_t st = (hipStream_t)stream;
-    const FusedPlan fp = plan_fused(L, B, max_ctx, true);
+    // the persistent launch: forced by path 2, automatic for at most 2 rows
+    // (from 3 rows on the kernel sequence is the faster one)
+    const FusedPlan fp = L->decode_path == 1 || (L->decode_path == 0 && B > 2) ? FusedPlan{} : plan_fused(L, B, max_ctx, true);
     if (L->decode_path == 2 && !fp.ok) return fail(W4_EUNSUPPORTED, "persistent decode not possible for this shape/batch");
     if (fp.ok) {
         if (ws_bytes < fp.total) return fail(W4_EWORKSPACE, "workspace %zu bytes, need %zu", ws_bytes, fp.total);
@@ -829,106 +959,9 @@ int layer_decode(layer_t L, const float* x, const int32_t* pos, const int32_t* c
         if (rc) return fail(W4_EHIP, "persistent decode launch failed: %s", hipGetErrorString(hipGetLastError()));
         return W4_OK;
     }
-    const DecodeWs w = plan_decode(L, B, max_ctx);
-    if (ws_bytes < w.total) return fail(W4_EWORKSPACE, "workspace %zu bytes, need %zu", ws_bytes, w.total);
-    char* base = (char*)ws;
-    uint16_t* q = (uint16_t*)(base + w.q);
-    float* part = (float*)(base + w.part);
-    f16* attn = (f16*)(base + w.attn);
-    float* h = (float*)(base + w.h);
-    f16* g = (f16*)(base + w.g);
-    const int H = c.hidden, d = c.head_dim, qd = c.n_heads * d;
-    const long long sh = (long long)c.max_seq * d, sb = sh * c.n_kv_heads;
-    int rc = 0;
-
-    GemvArgs a1{};
-    a1.W = L->qkv.d;
-    a1.x_f32 = x;
-    a1.gamma = (const uint16_t*)L->attn_norm.p;
-    a1.eps = c.rms_eps;
-    a1.B = B;
-    a1.ksplit = 1;
-    a1.ep = base_epi(L);
-    a1.ep.q_out = q;
-    a1.ep.k_cache = (uint16_t*)kc;
-    a1.ep.v_cache = (uint16_t*)vc;
-    a1.ep.cache_stride_b = sb;
-    a1.ep.cache_stride_h = sh;
-    a1.ep.pos = pos;
-    a1.ep.slot_dev = ctx_lens;
-    a1.copy_src = x;
-    a1.copy_dst = h;
-    a1.copy_n = B * H;
-    // with 4 rows or more the rows are normalised once, not in every block
-    const bool prenorm = B >= 4;
-    f16* xn = (f16*)(base + w.xn);
-    if (prenorm) {
-        rc |= launch_rmsnorm(x, (const uint16_t*)L->attn_norm.p, c.rms_eps, B, H, xn, st);
-        a1.x_f16 = xn;
-        a1.ldx = H;
-    }
-    { ProfScope ps(L, 2, 0, st); rc |= launch_gemv_w4(EPI_QKV, !prenorm, a1, st); }
-
-    AttnDecodeArgs ad{};
-    ad.q = q;
-    ad.k_cache = (const uint16_t*)kc;
-    ad.v_cache = (const uint16_t*)vc;
-    ad.stride_b = sb;
-    ad.stride_h = sh;
-    ad.ctx_lens = ctx_lens;
-    ad.mask = attn_mask;
-    ad.max_seq = c.max_seq;
-    ad.part = part;
-    ad.out = attn;
-    ad.B = B;
-    ad.nq = c.n_heads;
-    ad.nkv = c.n_kv_heads;
-    ad.d = d;
-    ad.chunk = w.chunk;
-    ad.nchunks = w.nchunks;
-    ad.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)d));
-    { ProfScope ps(L, 2, 1, st); rc |= launch_attn_decode(ad, st); }
-
-    GemvArgs a2{};
-    a2.W = L->o.d;
-    a2.x_f16 = attn;
-    a2.ldx = qd;
-    a2.B = B;
-    a2.ksplit = gemv_ksplit(L->o.d, 512, B);
-    a2.ep = base_epi(L);
-    a2.ep.out_f32 = h;
-    { ProfScope ps(L, 2, 3, st); rc |= launch_gemv_w4(EPI_RESID, false, a2, st); }
-
-    GemvArgs a3{};
-    a3.W = L->gu.d;
-    a3.x_f32 = h;
-    a3.gamma = (const uint16_t*)L->mlp_norm.p;
-    a3.eps = c.rms_eps;
-    a3.B = B;
-    a3.ksplit = 1;
-    a3.ep = base_epi(L);
-    a3.ep.act_out = g;
-    a3.copy_src = h;
-    a3.copy_dst = y;
-    a3.copy_n = B * H;
-    if (prenorm) {
-        rc |= launch_rmsnorm(h, (const uint16_t*)L->mlp_norm.p, c.rms_eps, B, H, xn, st);
-        a3.x_f16 = xn;
-        a3.ldx = H;
-    }
-    { ProfScope ps(L, 2, 4, st); rc |= launch_gemv_w4(EPI_SWIGLU, !prenorm, a3, st); }
-
-    GemvArgs a4{};
-    a4.W = L->down.d;
-    a4.x_f16 = g;
-    a4.ldx = L->F_pad;
-    a4.B = B;
-    a4.ksplit = gemv_ksplit(L->down.d, 512, B);
-    a4.ep = base_epi(L);
-    a4.ep.out_f32 = y;
-    { ProfScope ps(L, 2, 5, st); rc |= launch_gemv_w4(EPI_RESID, false, a4, st); }
-    if (rc) return fail(W4_EHIP, "kernel launch failed: %s", hipGetErrorString(hipGetLastError()));
-    return W4_OK;
+    int rc;
+    { rc = run_decode_seq(L, x, pos, ctx_lens, 0, false, attn_mask, B, max_ctx, kc, vc, y, ws, ws_bytes, st, 2); }
+    return rc;
 }
 
 int kv_append(const kv_desc* desc, void* kc, void* vc, const void* k_new, const void* v_new, int32_t B, int32_t T,

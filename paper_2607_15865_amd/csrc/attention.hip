@@ -316,7 +316,7 @@ __global__ void __launch_bounds__(256) attn_decode_split_kernel(AttnDecodeArgs a
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int b = blockIdx.x / a.nkv, g = blockIdx.x % a.nkv;
     const int chunk = blockIdx.y;
-    const int ctx = a.ctx_lens[b];
+    const int ctx = a.ctx_lens ? a.ctx_lens[b] : a.ctx_base + b;
     const int start = chunk * CH, end = min(start + CH, ctx + 1);
     if (start >= end) return;
     const int nkeys = end - start, ng = (nkeys + 31) / 32;
@@ -443,7 +443,7 @@ __global__ void __launch_bounds__(D * DEC_CG) attn_decode_combine_kernel(AttnDec
     __shared__ float gm[DEC_CG], gl[DEC_CG], go[DEC_CG][D];
     const int b = blockIdx.x / a.nq, head = blockIdx.x % a.nq;
     const int dim = threadIdx.x % D, gq = threadIdx.x / D;
-    const int ctx = a.ctx_lens[b];
+    const int ctx = a.ctx_lens ? a.ctx_lens[b] : a.ctx_base + b;
     const int nch = (ctx + 1 + a.chunk - 1) / a.chunk;
     const float* pp = a.part + ((size_t)b * a.nq + head) * a.nchunks * (D + 2);
     constexpr int CB = 8;

@@ -227,8 +227,8 @@ struct EpiArgs {
     long long cache_stride_b; // elements between sequences (decode)
     long long cache_stride_h; // elements between kv heads
     const int32_t* pos;       // [M] position ids
-    const int32_t* slot_dev;  // decode: [B] device slots (ctx_lens); null in prefill
-    int slot_base;            // prefill: slot of row 0 (hist_len)
+    const int32_t* slot_dev;  // decode: [B] device slots (ctx_lens), or null
+    int slot_base;            // with slot_dev null: slot of row 0 (rows are consecutive slots)
     const float* rope_cos;    // [max_seq][d/2]
     const float* rope_sin;
     int nq, nkv, head_dim;

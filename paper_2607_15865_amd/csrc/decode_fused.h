@@ -37,6 +37,7 @@ struct DecodeFusedArgs {
     int S_qkv, S_o, S_down;    // k-parts per column tile
     int comb_per, comb_lpv;    // attention outputs combined per block, lanes per output
     int slots;                 // column tiles per block in one product (LDS partial slots)
+    int gam_lds;               // RMSNorm weights held in LDS (at off_gam) or read from memory
     int chunk, nchunk;         // attention keys per unit, units per (row, kv head)
     float scale_log2;
     int nblocks;

@@ -256,6 +256,7 @@ __global__ void __launch_bounds__(NTHR) decode_fused_kernel(DecodeFusedArgs a) {
     float* own = red8 + 8 + NWAVE * MAXB;                         // [MAXB][32]
     int* meta = reinterpret_cast<int*>(own + MAXB * 32);          // ctx_lens[B], pos[B]
     uint16_t* gam = reinterpret_cast<uint16_t*>(smem + a.off_gam);           // RMSNorm weights [2][H]
+    const bool gam_lds = MAXB == 1 || a.gam_lds;                             // (one row always has room)
     f16* zero64 = reinterpret_cast<f16*>(smem + a.off_zero);                  // 64 zeros (GEMV phases)
     float* c64 = reinterpret_cast<float*>(smem + a.off_c64);                  // GEMV corrections
 
@@ -345,7 +346,7 @@ __global__ void __launch_bounds__(NTHR) decode_fused_kernel(DecodeFusedArgs a) {
         prefetch(1);
         if (i0 < B * H) *reinterpret_cast<float4*>(hbuf + i0) = xv[0];
         if (i1 < B * H) *reinterpret_cast<float4*>(hbuf + i1) = xv[1];
-        if (tid * 8 < H) {
+        if (gam_lds && tid * 8 < H) {
             *reinterpret_cast<u32x4*>(gam + tid * 8) = g1;
             *reinterpret_cast<u32x4*>(gam + H + tid * 8) = g2;
         }
@@ -353,7 +354,7 @@ __global__ void __launch_bounds__(NTHR) decode_fused_kernel(DecodeFusedArgs a) {
         if (tid < 8) reinterpret_cast<u32x4*>(zero64)[tid] = u32x4{0u, 0u, 0u, 0u};
         for (int i = i1 + NTHR * 4; i < B * H; i += NTHR * 4)      // rows past 2 * NTHR * 4 floats
             *reinterpret_cast<float4*>(hbuf + i) = *reinterpret_cast<const float4*>(a.x + i);
-        for (int i = tid * 8 + NTHR * 8; i < H; i += NTHR * 8) {
+        for (int i = tid * 8 + NTHR * 8; gam_lds && i < H; i += NTHR * 8) {
             *reinterpret_cast<u32x4*>(gam + i) = *reinterpret_cast<const u32x4*>(a.attn_norm + i);
             *reinterpret_cast<u32x4*>(gam + H + i) = *reinterpret_cast<const u32x4*>(a.mlp_norm + i);
         }
@@ -365,7 +366,8 @@ __global__ void __launch_bounds__(NTHR) decode_fused_kernel(DecodeFusedArgs a) {
     if (owns(1)) {
         const int t1 = pl[0], s1 = pl[3];
         const Run run1 = wave_run(1);
-        norm_prep_rows(hbuf, gam, a.eps, B, H, xs, ldx, c64, red8);
+        // (the RMSNorm weights are in LDS unless the block's LDS has no room)
+        norm_prep_rows(hbuf, gam_lds ? gam : a.attn_norm, a.eps, B, H, xs, ldx, c64, red8);
         stamp_done(6);
         clear_red();
         const GemvAct xa{xs, ldx, c64, nullptr, zero64};
@@ -749,7 +751,7 @@ __global__ void __launch_bounds__(NTHR) decode_fused_kernel(DecodeFusedArgs a) {
         const int ta4 = pl[8], tb4 = pl[9];
         const Run run4 = wave_run(4);
         if (tid < 8) reinterpret_cast<u32x4*>(zero64)[tid] = u32x4{0u, 0u, 0u, 0u};   // (attention reused it)
-        norm_prep_rows(hbuf, gam + H, a.eps, B, H, xs, ldx, c64, red8);
+        norm_prep_rows(hbuf, gam_lds ? gam + H : a.mlp_norm, a.eps, B, H, xs, ldx, c64, red8);
         stamp_done(22);
         clear_red();
         const GemvAct xa{xs, ldx, c64, nullptr, zero64};
@@ -876,7 +878,7 @@ int decode_fused_blocks(int head_dim, int B, size_t lds_bytes) {
 int launch_decode_fused(const DecodeFusedArgs& a, hipStream_t stream) {
     if (a.B > 4 || a.S_qkv > MAXS || a.S_o > MAXS || a.S_down > MAXS) return -1;
     if (a.shared ? (a.ctx_lens != nullptr || a.sb != 0 || a.ctx_base < 0) : a.ctx_lens == nullptr) return -1;
-    if (a.slots < 1) return -1;
+    if (a.slots < 1 || (a.B == 1 && !a.gam_lds)) return -1;
     if (a.chunk < 1 || a.chunk > decode_fused_max_chunk(a.d) || a.nkv < 1 || a.nq % a.nkv || a.nq / a.nkv > MAXR)
         return -1;
     if (a.off_h < decode_fused_attn_bytes(a.chunk, a.d)) return -1;

@@ -151,7 +151,7 @@ __global__ void __launch_bounds__(NW * 64) gemv_w4_kernel(GemvArgs a) {
     } else {
         for (int i = tid; i < B * 32; i += NW * 64) {
             const int b = i / 32, cc = i % 32;
-            const int slot = a.ep.slot_dev[b];
+            const int slot = a.ep.slot_dev ? a.ep.slot_dev[b] : a.ep.slot_base + b;
             epi_qkv_pair(a.ep, b, pair * 64, cc, tot[b * 64 + cc], tot[b * 64 + 32 + cc], slot, b);
         }
     }

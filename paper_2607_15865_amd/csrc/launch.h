@@ -102,7 +102,8 @@ struct AttnDecodeArgs {
     const uint16_t* k_cache; // bf16 [B][nkv][max_seq][d]
     const uint16_t* v_cache;
     long long stride_b, stride_h;
-    const int32_t* ctx_lens; // [B] device
+    const int32_t* ctx_lens; // [B] device, or null: row b's context is ctx_base + b
+    int ctx_base;
     const float* mask;       // [B][max_seq] or null
     int max_seq;
     float* part;             // [B][nq][nchunks][d + 2]

@@ -89,8 +89,10 @@ def test_prefill_kv(name, T, L):
     _check_new_kv(k, v, ko, vo, L, T)
 
 
-# T <= 4 runs as one persistent launch whose rows share the cache (rows that
-# straddle a key-chunk boundary: tiny 4 over 94), T > 4 on the prefill kernels
+# Decode path 0 runs T <= 2 as one persistent launch and T <= 8 on the decode
+# kernel sequence, the tokens as rows sharing one cache (rows that straddle a
+# key-chunk boundary: tiny 4 over 94); path 2 runs T <= 4 as the persistent
+# launch; path 1 keeps the prefill kernels.
 VERIFY_CASES = [("tiny", 2, 120), ("tiny", 4, 94), ("tiny", 3, 0), ("tiny", 8, 100), ("qwen05b", 3, 1000),
                 ("qwen05b", 4, 1019), ("llama8b", 2, 3000), ("llama8b", 4, 4000), ("llama8b", 8, 2048),
                 ("qwen7b", 2, 8190), ("qwen7b", 5, 8000)]
@@ -114,7 +116,7 @@ def test_prefill_kv_verify(name, T, L):
     x = bits_to_torch_f32(xb)
     y = torch.empty_like(x)
     yo, ko, vo = O.prefill_kv(w, cfg, xv, pos, kc, vc, L, W=W)
-    for path in ((0, 1) if T <= 4 else (0,)):
+    for path in ((0, 1, 2) if T <= 4 else (0, 1)):
         lay.set_decode_path(path)
         lay.prefill_kv(x, torch.from_numpy(pos.astype(np.int32)).cuda(), L, k, v, y)
         torch.cuda.synchronize()
@@ -177,7 +179,8 @@ def test_prefill_chunked_validation():
 DECODE_CASES = [("tiny", 1, [48], 0), ("tiny", 1, [48], 1), ("tiny", 4, [0, 9, 64, 126], 0),
                 ("tiny", 4, [0, 9, 64, 126], 1), ("tiny", 3, [127, 2, 40], 2), ("qwen05b", 1, [512], 0),
                 ("qwen05b", 2, [512, 100], 2), ("qwen05b", 2, [512, 100], 1), ("llama8b", 1, [2048], 0), ("llama8b", 1, [2048], 1),
-                ("llama8b", 2, [2048, 1500], 2), ("qwen7b", 1, [8192], 0), ("qwen7b", 1, [8192], 2),
+                ("llama8b", 2, [2048, 1500], 2), ("llama8b", 3, [3000, 17, 2048], 2),
+                ("llama8b", 4, [2048, 1, 4095, 700], 2), ("qwen7b", 1, [8192], 0), ("qwen7b", 1, [8192], 2),
                 ("qwen7b", 2, [8192, 3000], 2),
                 ("qwen7b", 8, [8192, 17, 4000, 8191, 1, 2048, 6000, 8100], 0)]
 
@@ -231,20 +234,26 @@ def test_decode_mask():
     mask[0, rng.choice(300, 40, replace=False)] = -np.inf
     mask[1, :] = rng.normal(0, 2, cfg.max_seq).astype(np.float32)
     mask[2, :65] = -np.inf
-    outs = []
-    for m in (None, np.zeros_like(mask), mask):
-        k = torch.from_numpy(kb.view(np.int16)).cuda()
-        v = torch.from_numpy(vb.view(np.int16)).cuda()
-        x = bits_to_torch_f32(xb)
-        y = torch.empty_like(x)
-        md = None if m is None else torch.from_numpy(m).cuda()
-        lay.decode(x, torch.from_numpy(ctx).cuda(), torch.from_numpy(ctx).cuda(), int(ctx.max()), k, v, y, md)
-        torch.cuda.synchronize()
-        outs.append(y.cpu().numpy())
-    # the persistent decode path (B <= 4) is deterministic: a zero mask is bit-identical to none
-    assert np.array_equal(outs[0], outs[1])
     yo, _, _ = O.decode(w, cfg, xv, ctx, kc, vc, ctx, mask.astype(np.float64), W=W)
-    assert_parity(outs[2], yo, "y masked")
+    yz, _, _ = O.decode(w, cfg, xv, ctx, kc, vc, ctx, W=W)
+    for path in (2, 0):            # the persistent launch, then the automatic choice (kernels for 3 rows)
+        lay.set_decode_path(path)
+        outs = []
+        for m in (None, np.zeros_like(mask), mask):
+            k = torch.from_numpy(kb.view(np.int16)).cuda()
+            v = torch.from_numpy(vb.view(np.int16)).cuda()
+            x = bits_to_torch_f32(xb)
+            y = torch.empty_like(x)
+            md = None if m is None else torch.from_numpy(m).cuda()
+            lay.decode(x, torch.from_numpy(ctx).cuda(), torch.from_numpy(ctx).cuda(), int(ctx.max()), k, v, y, md)
+            torch.cuda.synchronize()
+            outs.append(y.cpu().numpy())
+        if path == 2:
+            # the persistent launch is deterministic: a zero mask is bit-identical to none
+            assert np.array_equal(outs[0], outs[1])
+        assert_parity(outs[1], yz, f"y zero mask (path {path})")
+        assert_parity(outs[2], yo, f"y masked (path {path})")
+    lay.set_decode_path(0)
 
 
 @pytest.mark.parametrize("path,B", [(1, 8), (2, 4)])
