@@ -37,7 +37,6 @@ struct DecodeFusedArgs {
     int S_qkv, S_o, S_down;    // k-parts per column tile
     int comb_per, comb_lpv;    // attention outputs combined per block, lanes per output
     int slots;                 // column tiles per block in one product (LDS partial slots)
-    int gam_lds;               // RMSNorm weights held in LDS (at off_gam) or read from memory
     int chunk, nchunk;         // attention keys per unit, units per (row, kv head)
     float scale_log2;
     int nblocks;
@@ -46,6 +45,7 @@ struct DecodeFusedArgs {
     size_t off_zero, off_c64;  // LDS: 64 zero fp16; GEMV correction table [ldx / 64][8] fp32
                                // (inside the region the attention phase reuses)
     size_t lds_bytes;          // dynamic LDS per block
+    int gam_lds;               // RMSNorm weights held in LDS (at off_gam) or read from memory
 };
 
 int launch_decode_fused(const DecodeFusedArgs& a, hipStream_t stream);
