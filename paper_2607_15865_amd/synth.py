@@ -38,6 +38,12 @@ TID_GAMMA2 = 11
 TID_QVALS = 20            # + linear index
 TID_SCALES = 30           # + linear index
 TID_ZEROS = 40            # + linear index
+TID_EMBED = 60            # model ends: embedding table, final norm, LM head
+TID_FINAL_NORM = 61
+TID_HEAD_QVALS = 62
+TID_HEAD_SCALES = 63
+TID_HEAD_ZEROS = 64
+TID_TOKENS = 65
 
 
 @dataclasses.dataclass(frozen=True)
@@ -192,3 +198,34 @@ def zero_linear(lin: dict) -> dict:
 
 def as_optional(a: Optional[np.ndarray]):
     return None if a is None else np.ascontiguousarray(a)
+
+
+def make_lm(cfg: LayerConfig, vocab: int, with_zeros: bool = False, words: bool = False) -> dict:
+    """The two ends of a model with cfg's hidden size: a bf16 embedding
+    table [vocab][hidden] of N(0, 1) draws, a final RMSNorm weight (bf16,
+    uniform in [0.5, 1.5]) and a 4-bit LM head [hidden][vocab] drawn like
+    the layer's linears (codes uniform in [0, 15], fp16 scales
+    |N(0, 0.02)| / 8, zero point 8 unless zero points are drawn).  With
+    words=True the head's packed words are drawn directly, as in
+    make_layer_words (no "q" array)."""
+    H, G = cfg.hidden, cfg.group_size
+    ng = -(-H // G)
+    s = np.abs(rng_for(cfg.cfg_id, 0, TID_HEAD_SCALES).normal(0.0, 0.02, size=(ng, vocab))) / 8.0
+    zeros = None
+    if with_zeros:
+        zeros = rng_for(cfg.cfg_id, 0, TID_HEAD_ZEROS).integers(0, 16, size=(ng, vocab), dtype=np.uint8)
+    if words:
+        w = rng_for(cfg.cfg_id, 0, TID_HEAD_QVALS).integers(0, 1 << 32, size=(H // 8, vocab), dtype=np.uint32)
+        head = dict(K=H, N=vocab, qweight=w.view(np.int32), scales=s.astype(np.float16), zeros=zeros)
+    else:
+        q = rng_for(cfg.cfg_id, 0, TID_HEAD_QVALS).integers(0, 16, size=(H, vocab), dtype=np.uint8)
+        head = dict(K=H, N=vocab, q=q, qweight=pack_int4(q), scales=s.astype(np.float16), zeros=zeros)
+    return dict(vocab=vocab,
+                embed=normal_bf16(cfg.cfg_id, 0, TID_EMBED, (vocab, H)),
+                final_norm=bf16_bits(rng_for(cfg.cfg_id, 0, TID_FINAL_NORM).uniform(0.5, 1.5, H)),
+                head=head)
+
+
+def tokens(cfg: LayerConfig, vocab: int, n: int, seed: int = 0) -> np.ndarray:
+    """n token ids uniform in [0, vocab) (int32)."""
+    return rng_for(cfg.cfg_id, seed, TID_TOKENS).integers(0, vocab, size=n).astype(np.int32)
