@@ -389,8 +389,71 @@ def run_stack(args):
         "prefill": {"ms": round(prefill_ms, 3), "tflops": round(pf / (prefill_ms * 1e-3) / 1e12, 1),
                     "frac_mfma": round(pf / (prefill_ms * 1e-3) / 1e12 / PEAK_MFMA_TFLOPS, 4)},
     }
+    line["model"] = run_model_loop(cfg, st, kcs, vcs, P, S, decode_ms, binding, synth)
     print(json.dumps(line), flush=True)
     return 0
+
+
+def run_model_loop(cfg, st, kcs, vcs, P, S, layers_ms, binding, synth, vocab=128256, reps=30):
+    """The whole-model greedy loop on the stack: embed the prompt, prefill it
+    through every layer, LM head + greedy pick on its last row, then S steps
+    of embed(picked token) -> every layer's decode -> LM head + pick, with no
+    host round trip inside the timed region.  The ends use a Llama-3-8B
+    vocabulary of 128256 tokens (seeded int4 head, bf16 embedding rows).
+    Also the LM head + pick alone at B=1 (median of reps, HIP events)."""
+    import numpy as np
+    import torch
+    lw = synth.make_lm(cfg, vocab, words=True)
+    lm = binding.LM(cfg, lw, max_batch=1)
+    del lw
+    H = cfg.hidden
+    prompt = torch.from_numpy(synth.tokens(cfg, vocab, P)).cuda()
+    xp = torch.empty(P, H, device="cuda")
+    yp = torch.empty_like(xp)
+    x1 = torch.empty(1, H, device="cuda")
+    y1 = torch.empty_like(x1)
+    logits = torch.empty(1, vocab, device="cuda")
+    picks = torch.empty(S + 1, dtype=torch.int32, device="cuda")
+    slots = torch.arange(P, P + S, dtype=torch.int32, device="cuda")
+    lm.head(y1, logits, picks[:1])               # workspace allocation outside the timed region
+    e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+    torch.cuda.synchronize()
+    e0.record()
+    lm.embed(prompt, xp)
+    st.prefill(xp, torch.arange(P, dtype=torch.int32, device="cuda"), 0, kcs, vcs, yp)
+    lm.head(yp[P - 1:P], logits, picks[0:1])
+    e1.record()
+    for s in range(S):
+        lm.embed(picks[s:s + 1], x1)
+        st.decode(x1, slots[s:s + 1], slots[s:s + 1], P + s, kcs, vcs, y1)
+        lm.head(y1, logits, picks[s + 1:s + 2])
+    e2.record()
+    torch.cuda.synchronize()
+    assert lm.error() == 0
+    toks = picks.cpu().numpy()
+    assert ((toks >= 0) & (toks < vocab)).all()
+    loop_ms = e1.elapsed_time(e2)
+    ts = []
+    for i in range(reps + 2):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        lm.head(y1, logits, picks[:1])
+        b.record()
+        b.synchronize()
+        if i >= 2:
+            ts.append(a.elapsed_time(b) * 1e3)
+    head_us = float(np.median(ts))
+    G = cfg.group_size
+    hbytes = H * vocab // 2 + (H // G) * vocab * 2 + 4 * vocab + 4 * H
+    lm.close()
+    return {"workload": f"embed -> {len(kcs)} layers -> LM head (vocab {vocab}) -> greedy pick, "
+                        f"prompt {P}, {S} generated tokens at B=1",
+            "tokens_per_s": round(S / (loop_ms * 1e-3), 1), "ms_per_token": round(loop_ms / S, 4),
+            "ends_ms_per_token": round((loop_ms - layers_ms) / S, 4),
+            "prefill_to_first_token_ms": round(e0.elapsed_time(e1), 3),
+            "lm_head_pick_us": round(head_us, 2),
+            "lm_head_gbps": round(hbytes / (head_us * 1e-6) / 1e9, 1),
+            "lm_head_frac_hbm": round(hbytes / (head_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)}
 
 
 def main():

@@ -238,6 +238,73 @@ int stack_decode(const layer_t* layers, int32_t n_layers, const float* x, const 
                  void* const* k_caches, void* const* v_caches, float* y,
                  void* ws, size_t ws_bytes, void* stream);
 
+/* ---- model ends (Sec. 2 inference loop, Sec. 4.5 runtime orchestration) -- */
+
+/* The steps either side of the decoder layers in the runtime loop: the
+ * word embedding turns token ids into the first layer's input, the LM head
+ * (final RMSNorm + a 4-bit linear hidden x vocab) turns the last layer's
+ * output into logits, and greedy sampling picks the next token on the
+ * device, so a decode loop needs no host round trip per token.
+ * Supported: vocab a positive multiple of 64; hidden a multiple of 128 and
+ * of group_size, at most 7680 (the head's GEMV keeps up to 8 whole input
+ * rows on chip); group_size in {32, 64, 128, 256}; 1 <= max_batch <= 64. */
+typedef struct lm_config {
+    int32_t vocab;
+    int32_t hidden;
+    int32_t group_size;
+    float   rms_eps;     /* of the final RMSNorm, inside the square root */
+    int32_t max_batch;
+} lm_config;
+
+/* Host weights, read only during lm_create:
+ *   embed       bf16 bit patterns [vocab][hidden]; row t embeds token t;
+ *   final_norm  bf16 bit patterns [hidden], the final RMSNorm weight;
+ *   head        the LM head, K = hidden, N = vocab, in the qlinear_host
+ *               format (codes, fp16 scales, optional zero points). */
+typedef struct lm_weights_host {
+    const uint16_t* embed;
+    const uint16_t* final_norm;
+    qlinear_host    head;
+} lm_weights_host;
+
+typedef struct lm_s* lm_t;
+
+/* Copies the weights to the current device (the head repacked into the
+ * tiled layout of the layer's linears) and returns a handle in *out.
+ * Errors: W4_EINVAL (null pointer, non-finite scale), W4_EUNSUPPORTED
+ * (shape), W4_EHIP. */
+int lm_create(const lm_config* cfg, const lm_weights_host* w, lm_t* out);
+int lm_destroy(lm_t lm);
+
+/* Word embedding: x[b][:] = embed[tokens[b]][:] as fp32 (exact), for any
+ * number of rows B >= 1 (a whole prompt, or one token per sequence).
+ *   tokens  int32 [B] device;  x  fp32 [B][hidden] device out.
+ * A token id outside [0, vocab) gives a zero row and sets the handle's
+ * error flag (lm_error).  Errors: W4_EINVAL, W4_EHIP. */
+int lm_embed(lm_t lm, const int32_t* tokens, int32_t B, float* x, void* stream);
+
+/* Bytes of workspace lm_head needs for B rows; 0 for invalid arguments. */
+size_t lm_head_workspace_size(lm_t lm, int32_t B);
+
+/* LM head and greedy sampling:
+ *   logits[b][v] = sum_k bf16(RMSNorm(x[b]))[k] * W[k][v]  (fp32 sums, the
+ *   normalised row rounded once to bf16 as in the layer), and, when
+ *   next_tokens is not NULL, next_tokens[b] = the index of the largest
+ *   logit of row b, the lowest index among equal maxima (a NaN logit never
+ *   wins; a row of NaNs gives 0).
+ *   x            fp32 [B][hidden] device (e.g. the last layer's y);
+ *   logits       fp32 [B][vocab] device out;
+ *   next_tokens  int32 [B] device out, or NULL;
+ *   ws           at least lm_head_workspace_size(lm, B).
+ * Deterministic.  Errors: W4_EINVAL, W4_ECAPACITY, W4_EWORKSPACE, W4_EHIP. */
+int lm_head(lm_t lm, const float* x, int32_t B, float* logits, int32_t* next_tokens,
+            void* ws, size_t ws_bytes, void* stream);
+
+/* Reads and clears the error flag lm_embed sets: *flag = 1 if an
+ * out-of-range token id was seen since the last call, else 0.  Waits for
+ * the device.  Errors: W4_EINVAL, W4_EHIP. */
+int lm_error(lm_t lm, int32_t* flag);
+
 /* ---- KV cache -------------------------------------------------------------- */
 
 /* In-place Concat (Sec. 4.6.3): copy new keys/values k_new, v_new (bf16

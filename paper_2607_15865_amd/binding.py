@@ -58,6 +58,15 @@ class layer_weights_host(ctypes.Structure):
                [(n, qlinear_host) for n in ("q", "k", "v", "o", "gate", "up", "down")]
 
 
+class lm_config(ctypes.Structure):
+    _fields_ = [("vocab", ctypes.c_int32), ("hidden", ctypes.c_int32), ("group_size", ctypes.c_int32),
+                ("rms_eps", ctypes.c_float), ("max_batch", ctypes.c_int32)]
+
+
+class lm_weights_host(ctypes.Structure):
+    _fields_ = [("embed", ctypes.c_void_p), ("final_norm", ctypes.c_void_p), ("head", qlinear_host)]
+
+
 class kv_desc(ctypes.Structure):
     _fields_ = [("batch", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32), ("max_seq", ctypes.c_int32),
                 ("head_dim", ctypes.c_int32), ("stride_b", ctypes.c_int64), ("stride_h", ctypes.c_int64),
@@ -88,6 +97,12 @@ _SIG = {
     "stack_workspace_size": (ctypes.c_size_t, [_P, _I, _I, _I, _I, _I]),
     "stack_prefill": (ctypes.c_int, [_P, _I, _P, _P, _I, _I, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "stack_decode": (ctypes.c_int, [_P, _I, _P, _P, _P, _I, _P, _I, _P, _P, _P, _P, ctypes.c_size_t, _P]),
+    "lm_create": (ctypes.c_int, [ctypes.POINTER(lm_config), ctypes.POINTER(lm_weights_host), ctypes.POINTER(_P)]),
+    "lm_destroy": (ctypes.c_int, [_P]),
+    "lm_embed": (ctypes.c_int, [_P, _P, _I, _P, _P]),
+    "lm_head_workspace_size": (ctypes.c_size_t, [_P, _I]),
+    "lm_head": (ctypes.c_int, [_P, _P, _I, _P, _P, _P, ctypes.c_size_t, _P]),
+    "lm_error": (ctypes.c_int, [_P, ctypes.POINTER(ctypes.c_int32)]),
 }
 for _name, (_res, _args) in _SIG.items():
     _f = getattr(_lib, _name)
@@ -280,6 +295,92 @@ def layer_profile_read(handle, stage: int):
 
 
 # ------------------------------------------------------------ convenience
+
+def lm_create(vocab: int, hidden: int, group_size: int, rms_eps: float, max_batch: int, lm: dict):
+    """lm: the host format of synth.make_lm (embed bf16 bits [vocab][hidden],
+    final_norm bf16 bits [hidden], head a linear dict hidden x vocab)."""
+    keep = []
+
+    def arr(a, dtype):
+        a = np.ascontiguousarray(a)
+        if a.dtype != dtype:
+            a = a.view(dtype) if a.dtype.itemsize == np.dtype(dtype).itemsize else a.astype(dtype)
+        keep.append(a)
+        return a.ctypes.data
+
+    head = lm["head"]
+    z = head.get("zeros")
+    wh = lm_weights_host(arr(lm["embed"], np.uint16), arr(lm["final_norm"], np.uint16),
+                         qlinear_host(arr(head["qweight"], np.int32), arr(head["scales"], np.uint16),
+                                      None if z is None else arr(z, np.uint8)))
+    c = lm_config(vocab, hidden, group_size, rms_eps, max_batch)
+    h = _P()
+    rc = _lib.lm_create(ctypes.byref(c), ctypes.byref(wh), ctypes.byref(h))
+    return rc, h.value
+
+
+def lm_destroy(handle) -> int:
+    return _lib.lm_destroy(handle)
+
+
+def lm_embed(handle, tokens, B, x, stream=None) -> int:
+    return _lib.lm_embed(handle, _ptr(tokens), B, _ptr(x), _stream(stream))
+
+
+def lm_head_workspace_size(handle, B) -> int:
+    return _lib.lm_head_workspace_size(handle, B)
+
+
+def lm_head(handle, x, B, logits, next_tokens, ws, ws_bytes, stream=None) -> int:
+    return _lib.lm_head(handle, _ptr(x), B, _ptr(logits), _ptr(next_tokens), _ptr(ws), ws_bytes, _stream(stream))
+
+
+def lm_error(handle):
+    f = ctypes.c_int32(0)
+    rc = _lib.lm_error(handle, ctypes.byref(f))
+    return rc, f.value
+
+
+class LM:
+    """Owns a model-ends handle (embedding, LM head, greedy sampling) plus
+    reusable workspace; methods raise W4Error."""
+
+    def __init__(self, cfg, lm: dict, max_batch: int = 8):
+        import torch
+        self.cfg, self.vocab = cfg, lm["vocab"]
+        rc, self.handle = lm_create(self.vocab, cfg.hidden, cfg.group_size, cfg.rms_eps, max_batch, lm)
+        check(rc)
+        self._ws = torch.empty(0, dtype=torch.uint8, device="cuda")
+
+    def close(self):
+        if self.handle:
+            lm_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def embed(self, tokens, x, stream=None):
+        check(lm_embed(self.handle, tokens, tokens.shape[0], x, stream))
+
+    def head(self, x, logits, next_tokens=None, stream=None):
+        import torch
+        B = x.shape[0]
+        n = lm_head_workspace_size(self.handle, B)
+        if n == 0:
+            raise W4Error(W4_EINVAL, "invalid workspace query")
+        if self._ws.numel() < n:
+            self._ws = torch.empty(n, dtype=torch.uint8, device="cuda")
+        check(lm_head(self.handle, x, B, logits, next_tokens, self._ws, self._ws.numel(), stream))
+
+    def error(self) -> int:
+        rc, f = lm_error(self.handle)
+        check(rc)
+        return f
+
 
 class Layer:
     """Owns a layer handle plus reusable workspace; methods raise W4Error."""

@@ -1145,3 +1145,137 @@ int layer_profile_read(layer_t L, int32_t stage, float* total_ms, int32_t* launc
 }
 
 }  // extern "C"
+
+// ---------------------------------------------------------------- model ends
+
+struct lm_s {
+    lm_config cfg{};
+    DevLinearOwned head;
+    DevBuf embed, final_norm, zeros, err;
+    int device = 0;
+};
+
+namespace {
+
+constexpr int kLmRows = 8;   // rows per launch of the head's GEMV
+
+size_t lm_ws_layout(const lm_s* M, int B, size_t* off_pv, size_t* off_pi) {
+    const size_t a = 256;
+    const size_t xn = ((size_t)B * M->cfg.hidden * 2 + a - 1) / a * a;
+    const size_t pairs = (size_t)B * argmax_blocks(M->cfg.vocab);
+    const size_t pv = (pairs * 4 + a - 1) / a * a;
+    if (off_pv) *off_pv = xn;
+    if (off_pi) *off_pi = xn + pv;
+    return xn + pv + (pairs * 4 + a - 1) / a * a;
+}
+
+}  // namespace
+
+extern "C" {
+
+int lm_create(const lm_config* cfg, const lm_weights_host* w, lm_t* out) {
+    if (!cfg || !w || !out) return fail(W4_EINVAL, "null argument");
+    *out = nullptr;
+    const lm_config c = *cfg;
+    const int G = c.group_size;
+    if (c.vocab <= 0 || c.hidden <= 0 || c.max_batch <= 0 || !(c.rms_eps >= 0.f))
+        return fail(W4_EINVAL, "non-positive dimension or bad rms_eps in config");
+    if (c.vocab % 64) return fail(W4_EUNSUPPORTED, "vocab must be a multiple of 64");
+    if (G != 32 && G != 64 && G != 128 && G != 256) return fail(W4_EUNSUPPORTED, "group_size must be 32, 64, 128 or 256");
+    if (c.hidden % 128 || c.hidden % G || c.hidden > 7680)
+        return fail(W4_EUNSUPPORTED, "hidden must be a multiple of 128 and of group_size, at most 7680");
+    if (c.max_batch > 64) return fail(W4_EUNSUPPORTED, "max_batch must be at most 64");
+    if (!w->embed || !w->final_norm || !w->head.qweight || !w->head.scales) return fail(W4_EINVAL, "null weight");
+    const int H = c.hidden, V = c.vocab, KG = H / G;
+    for (size_t i = 0; i < (size_t)KG * V; i++)
+        if ((w->head.scales[i] & 0x7C00u) == 0x7C00u) return fail(W4_EINVAL, "non-finite scale in the LM head");
+    if (w->head.zeros)
+        for (size_t i = 0; i < (size_t)KG * V; i++)
+            if (w->head.zeros[i] > 15) return fail(W4_EINVAL, "zero point above 15 in the LM head");
+
+    lm_s* M = new lm_s();
+    M->cfg = c;
+    (void)hipGetDevice(&M->device);
+    const HostLin hl{w->head.qweight, w->head.scales, w->head.zeros, H, V};
+    std::vector<ColSrc> cols(V);
+    for (int n = 0; n < V; n++) cols[n] = ColSrc{&hl, n};
+    int rc = build_linear(M->head, cols, H, H, G, w->head.zeros != nullptr);
+    if (!rc) rc = upload(M->embed, w->embed, (size_t)V * H * 2);
+    if (!rc) rc = upload(M->final_norm, w->final_norm, (size_t)H * 2);
+    if (!rc) {
+        // all-zero residual rows: the head's GEMV stores 0 + sum
+        const size_t zb = (size_t)kLmRows * V * 4;
+        if (hipMalloc(&M->zeros.p, zb) != hipSuccess || hipMemset(M->zeros.p, 0, zb) != hipSuccess ||
+            hipMalloc(&M->err.p, 4) != hipSuccess || hipMemset(M->err.p, 0, 4) != hipSuccess ||
+            hipDeviceSynchronize() != hipSuccess)
+            rc = fail(W4_EHIP, "device allocation failed");
+    }
+    if (rc) {
+        delete M;
+        return rc;
+    }
+    *out = M;
+    return W4_OK;
+}
+
+int lm_destroy(lm_t lm) {
+    if (!lm) return fail(W4_EINVAL, "null handle");
+    delete lm;
+    return W4_OK;
+}
+
+int lm_embed(lm_t M, const int32_t* tokens, int32_t B, float* x, void* stream) {
+    if (!M || !tokens || !x) return fail(W4_EINVAL, "null argument");
+    if (B < 1) return fail(W4_EINVAL, "B must be positive");
+    if (launch_embed((const uint16_t*)M->embed.p, tokens, M->cfg.vocab, M->cfg.hidden, B, x, (int*)M->err.p,
+                     (hipStream_t)stream))
+        return fail(W4_EHIP, "kernel launch failed: %s", hipGetErrorString(hipGetLastError()));
+    return W4_OK;
+}
+
+size_t lm_head_workspace_size(lm_t M, int32_t B) {
+    if (!M || B < 1 || B > M->cfg.max_batch) return 0;
+    return lm_ws_layout(M, B, nullptr, nullptr);
+}
+
+int lm_head(lm_t M, const float* x, int32_t B, float* logits, int32_t* next_tokens, void* ws, size_t ws_bytes,
+            void* stream) {
+    if (!M || !x || !logits) return fail(W4_EINVAL, "null argument");
+    if (B < 1) return fail(W4_EINVAL, "B must be positive");
+    if (B > M->cfg.max_batch) return fail(W4_ECAPACITY, "B %d > max_batch %d", B, M->cfg.max_batch);
+    size_t off_pv = 0, off_pi = 0;
+    const size_t need = lm_ws_layout(M, B, &off_pv, &off_pi);
+    if (!ws || ws_bytes < need) return fail(W4_EWORKSPACE, "workspace of %zu bytes, %zu needed", ws_bytes, need);
+    hipStream_t st = (hipStream_t)stream;
+    const lm_config& c = M->cfg;
+    const int H = c.hidden, V = c.vocab;
+    f16* xn = (f16*)ws;
+    int rc = launch_rmsnorm(x, (const uint16_t*)M->final_norm.p, c.rms_eps, B, H, xn, st);
+    for (int r0 = 0; r0 < B && !rc; r0 += kLmRows) {
+        GemvArgs a{};
+        a.W = M->head.d;
+        a.x_f16 = xn + (size_t)r0 * H;
+        a.ldx = H;
+        a.B = std::min(kLmRows, B - r0);
+        a.ksplit = 1;
+        a.ep.resid = (const float*)M->zeros.p;
+        a.ep.out_f32 = logits + (size_t)r0 * V;
+        rc = launch_gemv_w4(EPI_RESID, false, a, st);
+    }
+    if (!rc && next_tokens)
+        rc = launch_argmax(logits, B, V, (float*)((char*)ws + off_pv), (int*)((char*)ws + off_pi), next_tokens, st);
+    if (rc) return fail(W4_EHIP, "kernel launch failed: %s", hipGetErrorString(hipGetLastError()));
+    return W4_OK;
+}
+
+int lm_error(lm_t M, int32_t* flag) {
+    if (!M || !flag) return fail(W4_EINVAL, "null argument");
+    int v = 0;
+    HIP_TRY(hipMemcpy(&v, M->err.p, 4, hipMemcpyDeviceToHost));
+    HIP_TRY(hipMemset(M->err.p, 0, 4));
+    HIP_TRY(hipDeviceSynchronize());
+    *flag = v;
+    return W4_OK;
+}
+
+}  // extern "C"

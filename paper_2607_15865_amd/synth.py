@@ -207,7 +207,8 @@ def make_lm(cfg: LayerConfig, vocab: int, with_zeros: bool = False, words: bool 
     the layer's linears (codes uniform in [0, 15], fp16 scales
     |N(0, 0.02)| / 8, zero point 8 unless zero points are drawn).  With
     words=True the head's packed words are drawn directly, as in
-    make_layer_words (no "q" array)."""
+    make_layer_words (no "q" array), and the embedding table repeats 8192
+    drawn rows."""
     H, G = cfg.hidden, cfg.group_size
     ng = -(-H // G)
     s = np.abs(rng_for(cfg.cfg_id, 0, TID_HEAD_SCALES).normal(0.0, 0.02, size=(ng, vocab))) / 8.0
@@ -220,8 +221,12 @@ def make_lm(cfg: LayerConfig, vocab: int, with_zeros: bool = False, words: bool 
     else:
         q = rng_for(cfg.cfg_id, 0, TID_HEAD_QVALS).integers(0, 16, size=(H, vocab), dtype=np.uint8)
         head = dict(K=H, N=vocab, q=q, qweight=pack_int4(q), scales=s.astype(np.float16), zeros=zeros)
-    return dict(vocab=vocab,
-                embed=normal_bf16(cfg.cfg_id, 0, TID_EMBED, (vocab, H)),
+    if words:   # throughput runs: 8192 distinct embedding rows, repeated
+        base = normal_bf16(cfg.cfg_id, 0, TID_EMBED, (min(vocab, 8192), H))
+        embed = np.tile(base, (-(-vocab // base.shape[0]), 1))[:vocab]
+    else:
+        embed = normal_bf16(cfg.cfg_id, 0, TID_EMBED, (vocab, H))
+    return dict(vocab=vocab, embed=embed,
                 final_norm=bf16_bits(rng_for(cfg.cfg_id, 0, TID_FINAL_NORM).uniform(0.5, 1.5, H)),
                 head=head)
 

@@ -95,3 +95,23 @@ def test_bandwidth_utilisation_definition():
         size, tps, printed = float(row[1]), float(row[2]), float(row[3])
         util = 100.0 * tps * size / 64.0
         assert abs(util - printed) < 0.5, row
+
+
+def test_lm_validation_before_any_hip_call():
+    cfg = synth.CONFIGS["tiny"]
+    lm = synth.make_lm(cfg, 128)
+    H, G = cfg.hidden, cfg.group_size
+    assert B.lm_create(96, H, G, 1e-6, 8, lm)[0] == B.W4_EUNSUPPORTED          # vocab % 64
+    assert B.lm_create(128, H, 48, 1e-6, 8, lm)[0] == B.W4_EUNSUPPORTED        # group size
+    assert B.lm_create(128, 7808, G, 1e-6, 8, lm)[0] == B.W4_EUNSUPPORTED      # hidden too large
+    assert B.lm_create(128, H, G, 1e-6, 65, lm)[0] == B.W4_EUNSUPPORTED        # max_batch
+    assert B.lm_create(128, H, G, -1.0, 8, lm)[0] == B.W4_EINVAL               # eps
+    bad = dict(lm, head=dict(lm["head"], scales=lm["head"]["scales"].copy()))
+    bad["head"]["scales"][1, 5] = np.float16(np.inf)
+    assert B.lm_create(128, H, G, 1e-6, 8, bad)[0] == B.W4_EINVAL
+    assert "scale" in B.layer_last_error()
+    assert B.lm_embed(None, 0, 1, 0, 0) == B.W4_EINVAL
+    assert B.lm_head(None, 0, 1, 0, None, 0, 0, 0) == B.W4_EINVAL
+    assert B.lm_head_workspace_size(None, 1) == 0
+    assert B.lm_error(None)[0] == B.W4_EINVAL
+    assert B.lm_destroy(None) == B.W4_EINVAL

@@ -1,0 +1,198 @@
+"""The model ends on the GPU (embedding, LM head, greedy sampling; the
+runtime loop of Sec. 2 / Sec. 4.5) against the oracle: the embedding
+bit-exact, the logits to the parity bound, the greedy pick exactly the
+argmax of the GPU's own logits and, against the oracle's logits, within the
+parity bound of the largest one (near-ties may pick either).  A greedy loop
+over a small two-layer model closes the cycle embed -> layers -> head ->
+pick -> embed on the device, checked step by step against the oracle fed
+the same tokens."""
+import functools
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import layer as O
+from oracle import lm as M
+from paper_2607_15865_amd import binding, synth
+from gpu_helpers import MAX_ABS, assert_parity, host_layer, log, oracle_weights
+
+pytestmark = pytest.mark.gpu
+
+
+@functools.lru_cache(maxsize=2)
+def host_lm(name, vocab, group=None, with_zeros=False, words=False):
+    cfg = synth.CONFIGS[name]
+    if group:
+        cfg = synth.replace(cfg, group_size=group)
+    return cfg, synth.make_lm(cfg, vocab, with_zeros=with_zeros, words=words)
+
+
+def sub_head(head, cols):
+    z = head.get("zeros")
+    return dict(K=head["K"], N=len(cols), qweight=np.ascontiguousarray(head["qweight"][:, cols]),
+                scales=np.ascontiguousarray(head["scales"][:, cols]),
+                zeros=None if z is None else np.ascontiguousarray(z[:, cols]))
+
+
+def check_pick(gl, ol, tok, what):
+    """gl: GPU logits [V] (fp32), ol: oracle logits at the same columns."""
+    assert tok == int(np.argmax(gl)), f"{what}: pick {tok} is not the argmax of the GPU logits"
+    assert ol[tok] >= ol.max() - 2 * MAX_ABS, f"{what}: oracle logit {ol[tok]} vs max {ol.max()}"
+
+
+def test_embed_bitexact_and_out_of_range():
+    cfg, lw = host_lm("tiny", 1024)
+    lmh = binding.LM(cfg, lw, max_batch=16)
+    tok = np.array([0, 1023, 5, 5, 777, 300, 2, 1000, 64, 17, 512], dtype=np.int32)
+    t = torch.from_numpy(tok).cuda()
+    x = torch.full((len(tok), cfg.hidden), 7.0, device="cuda")
+    lmh.embed(t, x)
+    assert np.array_equal(x.cpu().numpy().astype(np.float64), M.embed(lw["embed"], tok))
+    assert lmh.error() == 0
+    bad = torch.tensor([3, -1, 1024], dtype=torch.int32, device="cuda")
+    xb = torch.full((3, cfg.hidden), 7.0, device="cuda")
+    lmh.embed(bad, xb)
+    xbh = xb.cpu().numpy()
+    assert np.array_equal(xbh[0], M.embed(lw["embed"], [3])[0]) and not xbh[1:].any()
+    assert lmh.error() == 1 and lmh.error() == 0
+    lmh.close()
+
+
+HEAD_CASES = [
+    # name, vocab, group, zeros, B: one argmax block, two with a ragged tail,
+    # groups of 32, zero points, more rows than one GEMV launch takes
+    ("tiny", 1024, None, False, 1),
+    ("tiny", 8384, None, False, 3),
+    ("tiny", 2048, 32, False, 2),
+    ("tiny", 2048, None, True, 2),
+    ("tiny", 1024, None, False, 11),
+]
+
+
+@pytest.mark.parametrize("name,vocab,group,zeros,B", HEAD_CASES)
+def test_head_parity(name, vocab, group, zeros, B):
+    log(f"lm head {name} vocab {vocab} group {group} zeros {zeros} B {B}")
+    cfg, lw = host_lm(name, vocab, group, zeros)
+    lmh = binding.LM(cfg, lw, max_batch=16)
+    rng = np.random.default_rng(vocab + B)
+    x = (rng.standard_normal((B, cfg.hidden)) * 1.5).astype(np.float32)
+    logits = torch.empty(B, vocab, device="cuda")
+    nxt = torch.full((B,), -1, dtype=torch.int32, device="cuda")
+    lmh.head(torch.from_numpy(x).cuda(), logits, nxt)
+    gl = logits.cpu().numpy()
+    ol = M.lm_logits(x, lw["final_norm"], lw["head"], cfg.group_size, cfg.rms_eps)
+    assert_parity(gl, ol, "logits")
+    picks = nxt.cpu().numpy()
+    for b in range(B):
+        check_pick(gl[b], ol[b], int(picks[b]), f"row {b}")
+    # logits only
+    logits2 = torch.empty_like(logits)
+    lmh.head(torch.from_numpy(x).cuda(), logits2, None)
+    assert torch.equal(logits, logits2)
+    lmh.close()
+
+
+def test_head_ties_pick_lowest_index():
+    """Exact ties (every weight 0.5 or 1.0 times a normalised row of ones,
+    so every logit is an exact sum): all columns equal pick token 0; equal
+    maxima inside one argmax block, then in two blocks, pick the lowest."""
+    cfg = synth.CONFIGS["tiny"]
+    V, H, G = 16384, cfg.hidden, cfg.group_size
+    x = torch.ones(1, H, device="cuda")
+    logits = torch.empty(1, V, device="cuda")
+    nxt = torch.empty(1, dtype=torch.int32, device="cuda")
+
+    def pick(big):
+        q = np.full((H, V), 9, dtype=np.uint8)            # weight 0.5
+        q[:, big] = 10                                    # weight 1.0
+        head = dict(K=H, N=V, qweight=synth.pack_int4(q),
+                    scales=np.full((H // G, V), 0.5, dtype=np.float16), zeros=None)
+        lw = dict(vocab=V, embed=np.zeros((V, H), dtype=np.uint16),
+                  final_norm=np.full(H, 0x3F80, dtype=np.uint16), head=head)
+        lmh = binding.LM(cfg, lw)
+        lmh.head(x, logits, nxt)
+        lmh.close()
+        return int(nxt.item())
+
+    assert pick([]) == 0
+    assert pick([12000, 9000]) == 9000
+    assert pick([12000, 9000, 5000]) == 5000
+    assert pick([V - 1]) == V - 1
+
+
+def test_head_full_size_sampled():
+    """Llama-3-8B ends (hidden 4096, vocab 128256) at B=2: logits of 512
+    sampled columns plus the GPU's 16 best against the oracle on those
+    columns; the pick exactly the argmax of the GPU logits."""
+    V = 128256
+    cfg, lw = host_lm("llama8b", V, words=True)
+    log(f"lm head llama8b vocab {V} B 2")
+    lmh = binding.LM(cfg, lw)
+    B = 2
+    rng = np.random.default_rng(3)
+    x = (rng.standard_normal((B, cfg.hidden)) * 2.0).astype(np.float32)
+    logits = torch.empty(B, V, device="cuda")
+    nxt = torch.empty(B, dtype=torch.int32, device="cuda")
+    lmh.head(torch.from_numpy(x).cuda(), logits, nxt)
+    gl = logits.cpu().numpy()
+    picks = nxt.cpu().numpy()
+    for b in range(B):
+        cols = np.unique(np.concatenate([rng.choice(V, 512, replace=False), np.argsort(-gl[b])[:16],
+                                         [0, V - 1]]))
+        ol = M.lm_logits(x[b:b + 1], lw["final_norm"], sub_head(lw["head"], cols), cfg.group_size,
+                         cfg.rms_eps)[0]
+        assert_parity(gl[b, cols], ol, f"row {b} sampled logits")
+        assert int(picks[b]) == int(np.argmax(gl[b]))
+        j = int(np.searchsorted(cols, picks[b]))
+        assert ol[j] >= ol.max() - 2 * MAX_ABS
+    lmh.close()
+
+
+def test_greedy_loop_two_layers():
+    """embed -> 2-layer stack -> head -> pick -> embed, 8 prompt tokens and 6
+    generated ones, all on the device; the oracle runs the same token
+    sequence through its layers (decode == prefill over the whole sequence
+    by causality) and its head."""
+    name, nl, V, T, D = "tiny", 2, 1024, 8, 6
+    cfg = synth.CONFIGS[name]
+    _, lw = host_lm(name, V)
+    hw = [host_layer(name, layer=l)[1] for l in range(nl)]
+    W = [oracle_weights(name, layer=l) for l in range(nl)]
+    layers = [binding.Layer(cfg, hw[l]) for l in range(nl)]
+    st = binding.Stack(layers)
+    caches = [l.new_cache(1, 0) for l in layers]
+    kcs, vcs = [c[0] for c in caches], [c[1] for c in caches]
+    lmh = binding.LM(cfg, lw)
+    H = cfg.hidden
+    prompt = synth.tokens(cfg, V, T)
+    x = torch.empty(T, H, device="cuda")
+    lmh.embed(torch.from_numpy(prompt).cuda(), x)
+    y = torch.empty_like(x)
+    st.prefill(x, torch.arange(T, dtype=torch.int32, device="cuda"), 0, kcs, vcs, y)
+    logits = torch.empty(1, V, device="cuda")
+    nxt = torch.empty(1, dtype=torch.int32, device="cuda")
+    lmh.head(y[T - 1:T], logits, nxt)
+    g_logits, g_tok = [logits.cpu().numpy()[0]], [int(nxt.item())]
+    x1 = torch.empty(1, H, device="cuda")
+    y1 = torch.empty_like(x1)
+    for s in range(D):
+        t = T + s
+        lmh.embed(nxt, x1)
+        td = torch.tensor([t], dtype=torch.int32, device="cuda")
+        st.decode(x1, td, td, t, kcs, vcs, y1)
+        lmh.head(y1, logits, nxt)
+        g_logits.append(logits.cpu().numpy()[0])
+        g_tok.append(int(nxt.item()))
+    log(f"  generated {g_tok}")
+    seq = np.concatenate([prompt, np.array(g_tok[:D], dtype=np.int32)])
+    xv = M.embed(lw["embed"], seq)
+    for l in range(nl):
+        xv = O.prefill(hw[l], cfg, xv, np.arange(len(seq)), W=W[l])[0]
+    ol = M.lm_logits(xv[T - 1:], lw["final_norm"], lw["head"], cfg.group_size, cfg.rms_eps)
+    for i in range(D + 1):
+        assert_parity(g_logits[i], ol[i], f"step {i} logits")
+        check_pick(g_logits[i], ol[i], g_tok[i], f"step {i}")
+    lmh.close()
+    for l in layers:
+        l.close()
