@@ -13,7 +13,8 @@
  *   layer_decode      one token per sequence against a cache  (Sec. 4.4)
  *
  * plus the KV-cache calls kv_layout / kv_append (the in-place Concat of
- * Sec. 4.6.3).
+ * Sec. 4.6.3), layer stacks (stack_*), and the model ends around the layers
+ * (lm_*: embedding, LM head and greedy sampling of the runtime loop, Sec. 2).
  *
  * Conventions shared by every call
  *   - Return value 0 on success, a negative W4_E* code on failure; the
