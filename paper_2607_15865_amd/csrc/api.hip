@@ -19,6 +19,7 @@
 #include "common.h"
 #include "decode_fused.h"
 #include "launch.h"
+#include "lm.h"
 
 namespace {
 

@@ -11,7 +11,7 @@
 #include <climits>
 
 #include "common.h"
-#include "launch.h"
+#include "lm.h"
 
 namespace {
 
