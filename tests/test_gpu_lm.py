@@ -121,15 +121,15 @@ def test_head_ties_pick_lowest_index():
     assert pick([V - 1]) == V - 1
 
 
-def test_head_full_size_sampled():
-    """Llama-3-8B ends (hidden 4096, vocab 128256) at B=2: logits of 512
-    sampled columns plus the GPU's 16 best against the oracle on those
-    columns; the pick exactly the argmax of the GPU logits."""
-    V = 128256
-    cfg, lw = host_lm("llama8b", V, words=True)
-    log(f"lm head llama8b vocab {V} B 2")
+@pytest.mark.parametrize("name,V,B", [("llama8b", 128256, 2), ("qwen7b", 152064, 3)])
+def test_head_full_size_sampled(name, V, B):
+    """Full-size ends (Llama-3-8B: hidden 4096, vocab 128256; Qwen2.5-7B:
+    hidden 3584, vocab 152064): logits of 512 sampled columns plus the
+    GPU's 16 best and both ends of the vocabulary against the oracle on
+    those columns; the pick exactly the argmax of the GPU logits."""
+    cfg, lw = host_lm(name, V, words=True)
+    log(f"lm head {name} vocab {V} B {B}")
     lmh = binding.LM(cfg, lw)
-    B = 2
     rng = np.random.default_rng(3)
     x = (rng.standard_normal((B, cfg.hidden)) * 2.0).astype(np.float32)
     logits = torch.empty(B, V, device="cuda")
@@ -193,6 +193,62 @@ def test_greedy_loop_two_layers():
     for i in range(D + 1):
         assert_parity(g_logits[i], ol[i], f"step {i} logits")
         check_pick(g_logits[i], ol[i], g_tok[i], f"step {i}")
+    lmh.close()
+    for l in layers:
+        l.close()
+
+
+def test_greedy_loop_batch_of_two():
+    """Two sequences decoded together: one prefill per prompt into its own
+    cache row, then 4 steps of embed -> 2-layer stack decode at B = 2 ->
+    head + pick for both rows at once; each sequence against the oracle fed
+    its own tokens."""
+    name, nl, V, T, D, B = "tiny", 2, 1024, 6, 4, 2
+    cfg = synth.CONFIGS[name]
+    _, lw = host_lm(name, V)
+    hw = [host_layer(name, layer=l)[1] for l in range(nl)]
+    W = [oracle_weights(name, layer=l) for l in range(nl)]
+    layers = [binding.Layer(cfg, hw[l]) for l in range(nl)]
+    st = binding.Stack(layers)
+    caches = [l.new_cache(B, 0) for l in layers]
+    lmh = binding.LM(cfg, lw)
+    H = cfg.hidden
+    prompts = [synth.tokens(cfg, V, T, seed=10 + b) for b in range(B)]
+    nxt = torch.empty(B, dtype=torch.int32, device="cuda")
+    logits = torch.empty(B, V, device="cuda")
+    y_last = torch.empty(B, H, device="cuda")
+    for b in range(B):   # each prompt into cache row b (a one-sequence view of that row)
+        kcs = [c[0][b:b + 1] for c in caches]
+        vcs = [c[1][b:b + 1] for c in caches]
+        x = torch.empty(T, H, device="cuda")
+        lmh.embed(torch.from_numpy(prompts[b]).cuda(), x)
+        y = torch.empty_like(x)
+        st.prefill(x, torch.arange(T, dtype=torch.int32, device="cuda"), 0, kcs, vcs, y)
+        y_last[b] = y[T - 1]
+    lmh.head(y_last, logits, nxt)
+    g_logits, g_tok = [logits.cpu().numpy()], [nxt.cpu().numpy().copy()]
+    kcs, vcs = [c[0] for c in caches], [c[1] for c in caches]
+    x1 = torch.empty(B, H, device="cuda")
+    y1 = torch.empty_like(x1)
+    for s in range(D):
+        t = T + s
+        lmh.embed(nxt, x1)
+        td = torch.full((B,), t, dtype=torch.int32, device="cuda")
+        st.decode(x1, td, td, t, kcs, vcs, y1)
+        lmh.head(y1, logits, nxt)
+        g_logits.append(logits.cpu().numpy())
+        g_tok.append(nxt.cpu().numpy().copy())
+    for b in range(B):
+        toks = [int(g[b]) for g in g_tok]
+        log(f"  sequence {b}: generated {toks}")
+        seq = np.concatenate([prompts[b], np.array(toks[:D], dtype=np.int32)])
+        xv = M.embed(lw["embed"], seq)
+        for l in range(nl):
+            xv = O.prefill(hw[l], cfg, xv, np.arange(len(seq)), W=W[l])[0]
+        ol = M.lm_logits(xv[T - 1:], lw["final_norm"], lw["head"], cfg.group_size, cfg.rms_eps)
+        for i in range(D + 1):
+            assert_parity(g_logits[i][b], ol[i], f"seq {b} step {i} logits")
+            check_pick(g_logits[i][b], ol[i], toks[i], f"seq {b} step {i}")
     lmh.close()
     for l in layers:
         l.close()
