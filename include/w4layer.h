@@ -248,7 +248,10 @@ int stack_decode(const layer_t* layers, int32_t n_layers, const float* x, const 
  * device, so a decode loop needs no host round trip per token.
  * Supported: vocab a positive multiple of 64; hidden a multiple of 128 and
  * of group_size, at most 7680 (the head's GEMV keeps up to 8 whole input
- * rows on chip); group_size in {32, 64, 128, 256}; 1 <= max_batch <= 64. */
+ * rows on chip); group_size in {32, 64, 128, 256}; 1 <= max_batch <= 64.
+ * The handle holds only weights, a read-only zero buffer and the embedding
+ * error flag: calls on different streams may share it, each lm_head call
+ * with its own workspace. */
 typedef struct lm_config {
     int32_t vocab;
     int32_t hidden;

@@ -5,10 +5,9 @@
 namespace {
 
 // top.RMSNorm (Sec. 2.2): y = x / sqrt(mean(x^2) + eps) * gamma over a row,
-// rounded to bf16 and held as fp16 (the matmul operand).  One block per row.
-// RMSNorm of one row per block (256 threads), rounded to bf16 and held as
-// fp16.  NV: 16-byte chunks of the row per thread (H <= NV * 1024), kept in
-// registers between the sum of squares and the output.
+// rounded to bf16 and held as fp16 (the matmul operand).  One block of 256
+// threads per row.  NV: 16-byte chunks of the row per thread (H <= NV * 1024),
+// kept in registers between the sum of squares and the output.
 template <int NV>
 __global__ void __launch_bounds__(256) rmsnorm_kernel(const float* __restrict__ x, const uint16_t* __restrict__ gamma,
                                                       float eps, int H, f16* __restrict__ out) {
