@@ -252,3 +252,30 @@ def test_greedy_loop_batch_of_two():
     lmh.close()
     for l in layers:
         l.close()
+
+
+def test_lm_argument_errors_launch_nothing():
+    """Capacity, workspace and null-pointer errors are reported before any
+    launch: the output buffers keep their contents."""
+    cfg, lw = host_lm("tiny", 1024)
+    lmh = binding.LM(cfg, lw, max_batch=2)
+    h = lmh.handle
+    x = torch.ones(3, cfg.hidden, device="cuda")
+    logits = torch.full((3, 1024), 5.0, device="cuda")
+    nxt = torch.full((3,), -7, dtype=torch.int32, device="cuda")
+    need = binding.lm_head_workspace_size(h, 2)
+    assert need > 0 and binding.lm_head_workspace_size(h, 3) == 0 and binding.lm_head_workspace_size(h, 0) == 0
+    ws = torch.empty(need, dtype=torch.uint8, device="cuda")
+    assert binding.lm_head(h, x, 3, logits, nxt, ws, need) == binding.W4_ECAPACITY
+    assert binding.lm_head(h, x, 2, logits, nxt, ws, need - 1) == binding.W4_EWORKSPACE
+    assert binding.lm_head(h, x, 2, logits, nxt, None, 0) == binding.W4_EWORKSPACE
+    assert binding.lm_head(h, x, 0, logits, nxt, ws, need) == binding.W4_EINVAL
+    assert binding.lm_head(h, None, 2, logits, nxt, ws, need) == binding.W4_EINVAL
+    assert binding.lm_embed(h, nxt, 0, x) == binding.W4_EINVAL
+    assert binding.lm_embed(h, None, 1, x) == binding.W4_EINVAL
+    torch.cuda.synchronize()
+    assert bool((logits == 5.0).all()) and bool((nxt == -7).all())
+    assert binding.lm_head(h, x, 2, logits, nxt, ws, need) == binding.W4_OK
+    torch.cuda.synchronize()
+    assert bool((nxt[:2] >= 0).all()) and int(nxt[2]) == -7
+    lmh.close()
