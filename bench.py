@@ -390,6 +390,9 @@ def run_stack(args):
                     "frac_mfma": round(pf / (prefill_ms * 1e-3) / 1e12 / PEAK_MFMA_TFLOPS, 4)},
     }
     line["model"] = run_model_loop(cfg, st, kcs, vcs, P, S, decode_ms, binding, synth)
+    if args.stack_batch > 1:
+        del caches, kcs, vcs
+        line["model_batch"] = run_model_loop_batch(cfg, layers, st, args.stack_batch, binding, synth)
     print(json.dumps(line), flush=True)
     return 0
 
@@ -456,6 +459,56 @@ def run_model_loop(cfg, st, kcs, vcs, P, S, layers_ms, binding, synth, vocab=128
             "lm_head_frac_hbm": round(hbytes / (head_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)}
 
 
+def run_model_loop_batch(cfg, layers, st, B, binding, synth, vocab=128256, P=256, S=64):
+    """The whole-model greedy loop for B sequences decoded together: each
+    prompt of P tokens prefilled into its own cache row, then S steps of
+    embed(B picked tokens) -> every layer's decode at B -> LM head + pick
+    for the B rows, no host round trip inside the timed region.  Reports
+    the aggregate generated tokens/s."""
+    import torch
+    lw = synth.make_lm(cfg, vocab, words=True)
+    lm = binding.LM(cfg, lw, max_batch=B)
+    del lw
+    H = cfg.hidden
+    caches = [l.new_cache(B) for l in layers]
+    kcs, vcs = [c[0] for c in caches], [c[1] for c in caches]
+    x1 = torch.empty(B, H, device="cuda")
+    y1 = torch.empty_like(x1)
+    logits = torch.empty(B, vocab, device="cuda")
+    picks = torch.empty(S + 1, B, dtype=torch.int32, device="cuda")
+    lm.head(y1, logits, picks[0])                # workspace allocation outside the timed region
+    xp = torch.empty(P, H, device="cuda")
+    yp = torch.empty_like(xp)
+    ylast = torch.empty(B, H, device="cuda")
+    pos = torch.arange(P, dtype=torch.int32, device="cuda")
+    ctxs = (torch.arange(S, dtype=torch.int32, device="cuda")[:, None] + P).repeat(1, B).contiguous()
+    e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+    torch.cuda.synchronize()
+    e0.record()
+    for b in range(B):
+        prompt = torch.from_numpy(synth.tokens(cfg, vocab, P, seed=100 + b)).cuda()
+        lm.embed(prompt, xp)
+        st.prefill(xp, pos, 0, [k[b:b + 1] for k in kcs], [v[b:b + 1] for v in vcs], yp)
+        ylast[b] = yp[P - 1]
+    lm.head(ylast, logits, picks[0])
+    e1.record()
+    for s in range(S):
+        lm.embed(picks[s], x1)
+        st.decode(x1, ctxs[s], ctxs[s], P + s, kcs, vcs, y1)
+        lm.head(y1, logits, picks[s + 1])
+    e2.record()
+    torch.cuda.synchronize()
+    assert lm.error() == 0
+    toks = picks.cpu().numpy()
+    assert ((toks >= 0) & (toks < vocab)).all()
+    loop_ms = e1.elapsed_time(e2)
+    lm.close()
+    return {"workload": f"{B} sequences: prompts of {P} prefilled, then {S} greedy steps at B={B} through "
+                        f"embed -> {len(layers)} layers -> LM head (vocab {vocab}) -> pick",
+            "tokens_per_s": round(B * S / (loop_ms * 1e-3), 1), "ms_per_step": round(loop_ms / S, 4),
+            "prefill_ms": round(e0.elapsed_time(e1), 3)}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -470,6 +523,8 @@ def main():
     ap.add_argument("--stack", action="store_true",
                     help="instead: the 32-layer stack, 1024-token prefill then 256 decode steps")
     ap.add_argument("--stack-layers", type=int, default=32)
+    ap.add_argument("--stack-batch", type=int, default=1,
+                    help="with --stack: also run the whole-model greedy loop for this many sequences at once")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="instead: a plain 512 MiB device copy, the reference kernel for the HBM byte counters")
     args = ap.parse_args()
