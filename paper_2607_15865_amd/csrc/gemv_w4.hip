@@ -41,8 +41,9 @@ __global__ void __launch_bounds__(NW * 64) gemv_w4_kernel(GemvArgs a) {
     f16* xs = reinterpret_cast<f16*>(smem);                                   // [B][ldx]
     f16* zero = xs + B * ldx;                                                 // [64]
     float* c64 = reinterpret_cast<float*>(zero + 64);                         // [nkb][GEMV_ROWS]
-    float2* uv32 = reinterpret_cast<float2*>(c64 + nkb * GEMV_ROWS);          // [2 nkb][GEMV_ROWS]
-    float* red = reinterpret_cast<float*>(uv32 + 2 * nkb * GEMV_ROWS);        // [NW][2][MAXB][32]
+    // [2 nkb][GEMV_ROWS], present only with zero points or groups of 32
+    float2* uv32 = reinterpret_cast<float2*>(c64 + nkb * GEMV_ROWS);
+    float* red = reinterpret_cast<float*>(uv32 + ((ZP || G32) ? 2 * nkb * GEMV_ROWS : 0));  // [NW][2][MAXB][32]
     float* rinv = red + NW * 2 * MAXB * 32;                                   // [MAXB]
     float* tot = rinv + MAXB;                                                 // [MAXB][64]
 
@@ -161,7 +162,7 @@ template <int EPI, bool NORM, bool ZP, bool G32>
 int launch_t(const GemvArgs& a, hipStream_t stream) {
     const int KB = a.W.K_pad / 64;
     const int kmax = (KB + a.ksplit - 1) / a.ksplit * 64;
-    const size_t smem = (size_t)a.B * (kmax + 8) * 2 + 128 + (size_t)(kmax / 64) * GEMV_ROWS * 20 +
+    const size_t smem = (size_t)a.B * (kmax + 8) * 2 + 128 + (size_t)(kmax / 64) * GEMV_ROWS * ((ZP || G32) ? 20 : 4) +
                         (NW * 2 * MAXB * 32 + MAXB + MAXB * 64) * sizeof(float);
     if (smem > 160 * 1024) return -1;
     static LdsLimit lim;
