@@ -38,13 +38,15 @@ __global__ void __launch_bounds__(NW * 64) gemv_w4_kernel(GemvArgs a) {
     const int ldx = klen + 8;
     const int B = a.B;
     const int nkb = kb_hi - kb_lo;
+    // the activation rows, and after the main loop the wave partials over them
+    const int reg0 = max(B * ldx * 2, NW * 2 * B * 32 * 4);
     f16* xs = reinterpret_cast<f16*>(smem);                                   // [B][ldx]
-    f16* zero = xs + B * ldx;                                                 // [64]
+    float* red = reinterpret_cast<float*>(smem);                              // [NW][2][B][32]
+    f16* zero = reinterpret_cast<f16*>(smem + reg0);                          // [64]
     float* c64 = reinterpret_cast<float*>(zero + 64);                         // [nkb][GEMV_ROWS]
     // [2 nkb][GEMV_ROWS], present only with zero points or groups of 32
     float2* uv32 = reinterpret_cast<float2*>(c64 + nkb * GEMV_ROWS);
-    float* red = reinterpret_cast<float*>(uv32 + ((ZP || G32) ? 2 * nkb * GEMV_ROWS : 0));  // [NW][2][MAXB][32]
-    float* rinv = red + NW * 2 * MAXB * 32;                                   // [MAXB]
+    float* rinv = reinterpret_cast<float*>(uv32 + ((ZP || G32) ? 2 * nkb * GEMV_ROWS : 0));  // [MAXB]
     float* tot = rinv + MAXB;                                                 // [MAXB][64]
 
     // this wave's k-tiles of both column tiles
@@ -107,27 +109,36 @@ __global__ void __launch_bounds__(NW * 64) gemv_w4_kernel(GemvArgs a) {
               klen, tid, NW * 64);
     __syncthreads();
 
-    // ---- main loop: partial sums of this wave into red[wave]
+    // ---- main loop: partial sums of this wave's two tiles, kept in registers
     const int h = lane >> 5, c = lane & 31;
     const GemvAct xa{xs - klo, ldx, c64 - kb_lo * GEMV_ROWS, uv32 - 2 * kb_lo * GEMV_ROWS, zero};
+    float p0[4] = {0.f, 0.f, 0.f, 0.f}, p1[4] = {0.f, 0.f, 0.f, 0.f};
     if (run.ka < run.kz) {
         gemv_run<RING, ZP, G32>(W, run, xa, B, R, q, [&](int t, const float (&out)[4]) {
-            const int tt = t - pair * 2;
+            if (t == pair * 2) {
 #pragma unroll
-            for (int r = 0; r < 4; r++) {
-                const int b = 4 * h + r;
-                if (b < B) red[((wave * 2 + tt) * MAXB + b) * 32 + c] = out[r];
+                for (int r = 0; r < 4; r++) p0[r] = out[r];
+            } else {
+#pragma unroll
+                for (int r = 0; r < 4; r++) p1[r] = out[r];
             }
         });
-    } else {
-        for (int i = lane; i < 2 * MAXB * 32; i += 64) red[wave * 2 * MAXB * 32 + i] = 0.f;
+    }
+    __syncthreads();   // every wave is done with the activation rows
+#pragma unroll
+    for (int r = 0; r < 4; r++) {
+        const int b = 4 * h + r;
+        if (b < B) {
+            red[((wave * 2 + 0) * B + b) * 32 + c] = p0[r];
+            red[((wave * 2 + 1) * B + b) * 32 + c] = p1[r];
+        }
     }
     __syncthreads();
     for (int i = tid; i < B * 64; i += NW * 64) {
         const int b = i / 64, cc = i % 64;
         const int tt = cc / 32, c2 = cc % 32;
         float v = 0.f;
-        for (int w = 0; w < NW; w++) v += red[((w * 2 + tt) * MAXB + b) * 32 + c2];
+        for (int w = 0; w < NW; w++) v += red[((w * 2 + tt) * B + b) * 32 + c2];
         tot[b * 64 + cc] = v;
     }
     __syncthreads();
@@ -162,8 +173,8 @@ template <int EPI, bool NORM, bool ZP, bool G32>
 int launch_t(const GemvArgs& a, hipStream_t stream) {
     const int KB = a.W.K_pad / 64;
     const int kmax = (KB + a.ksplit - 1) / a.ksplit * 64;
-    const size_t smem = (size_t)a.B * (kmax + 8) * 2 + 128 + (size_t)(kmax / 64) * GEMV_ROWS * ((ZP || G32) ? 20 : 4) +
-                        (NW * 2 * MAXB * 32 + MAXB + MAXB * 64) * sizeof(float);
+    const size_t smem = std::max((size_t)a.B * (kmax + 8) * 2, (size_t)NW * 2 * a.B * 32 * 4) + 128 +
+                        (size_t)(kmax / 64) * GEMV_ROWS * ((ZP || G32) ? 20 : 4) + (MAXB + MAXB * 64) * sizeof(float);
     if (smem > 160 * 1024) return -1;
     static LdsLimit lim;
     if (ensure_lds_limit(lim, (const void*)gemv_w4_kernel<EPI, NORM, ZP, G32>, smem)) return -1;
