@@ -309,6 +309,23 @@ int lm_head(lm_t lm, const float* x, int32_t B, float* logits, int32_t* next_tok
  * the device.  Errors: W4_EINVAL, W4_EHIP. */
 int lm_error(lm_t lm, int32_t* flag);
 
+/* One step of the runtime loop's greedy decode (Sec. 2, Sec. 4.5): embed
+ * tokens[b] (lm_embed), run every layer's decode on one stream
+ * (stack_decode, no attention mask), then the LM head and the greedy pick
+ * (lm_head) into logits and next_tokens.  tokens and next_tokens (int32 [B],
+ * device) may be the same buffer: the embedding reads it before the pick
+ * writes it, in stream order, so a loop feeds each step's picks to the next
+ * step without the host.  pos, ctx_lens, max_ctx, caches as for
+ * stack_decode; logits fp32 [B][vocab] device out.  ws: at least
+ * model_decode_workspace_size(layers, n_layers, lm, B, max_ctx) bytes (0 for
+ * invalid arguments).  Arguments are checked before the first launch.
+ * Errors: W4_EINVAL, W4_ECAPACITY, W4_EWORKSPACE, W4_EHIP. */
+size_t model_decode_workspace_size(const layer_t* layers, int32_t n_layers, lm_t lm, int32_t B, int32_t max_ctx);
+int model_decode_greedy(const layer_t* layers, int32_t n_layers, lm_t lm, const int32_t* tokens,
+                        const int32_t* pos, const int32_t* ctx_lens, int32_t max_ctx, int32_t B,
+                        void* const* k_caches, void* const* v_caches, float* logits, int32_t* next_tokens,
+                        void* ws, size_t ws_bytes, void* stream);
+
 /* ---- KV cache -------------------------------------------------------------- */
 
 /* In-place Concat (Sec. 4.6.3): copy new keys/values k_new, v_new (bf16

@@ -103,6 +103,8 @@ _SIG = {
     "lm_head_workspace_size": (ctypes.c_size_t, [_P, _I]),
     "lm_head": (ctypes.c_int, [_P, _P, _I, _P, _P, _P, ctypes.c_size_t, _P]),
     "lm_error": (ctypes.c_int, [_P, ctypes.POINTER(ctypes.c_int32)]),
+    "model_decode_workspace_size": (ctypes.c_size_t, [_P, _I, _P, _I, _I]),
+    "model_decode_greedy": (ctypes.c_int, [_P, _I, _P, _P, _P, _P, _I, _I, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
 }
 for _name, (_res, _args) in _SIG.items():
     _f = getattr(_lib, _name)
@@ -339,6 +341,17 @@ def lm_error(handle):
     f = ctypes.c_int32(0)
     rc = _lib.lm_error(handle, ctypes.byref(f))
     return rc, f.value
+
+
+def model_decode_workspace_size(handles, lm_handle, B, max_ctx) -> int:
+    return _lib.model_decode_workspace_size(_ptr_array(handles), len(handles), lm_handle, B, max_ctx)
+
+
+def model_decode_greedy(handles, lm_handle, tokens, pos, ctx_lens, max_ctx, B, k_caches, v_caches, logits,
+                        next_tokens, ws, ws_bytes, stream=None) -> int:
+    return _lib.model_decode_greedy(_ptr_array(handles), len(handles), lm_handle, _ptr(tokens), _ptr(pos),
+                                    _ptr(ctx_lens), max_ctx, B, _ptr_array(k_caches), _ptr_array(v_caches),
+                                    _ptr(logits), _ptr(next_tokens), _ptr(ws), ws_bytes, _stream(stream))
 
 
 class LM:

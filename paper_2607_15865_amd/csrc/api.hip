@@ -1279,4 +1279,55 @@ int lm_error(lm_t M, int32_t* flag) {
     return W4_OK;
 }
 
+// ---------------------------------------------------------------- runtime loop step
+
+namespace {
+size_t model_act_bytes(int B, int H) { return ((size_t)B * H * 4 + 255) / 256 * 256; }
+// every layer holds B sequences and a context of max_ctx + 1
+bool model_fits(const layer_t* layers, int n, int B, int max_ctx) {
+    for (int i = 0; i < n; i++)
+        if (!layers[i] || B > layers[i]->cfg.max_batch || max_ctx + 1 > layers[i]->cfg.max_seq) return false;
+    return true;
+}
+}
+
+size_t model_decode_workspace_size(const layer_t* layers, int32_t n_layers, lm_t lm, int32_t B, int32_t max_ctx) {
+    if (!layers || n_layers < 1 || !lm || !layers[0] || layers[0]->cfg.hidden != lm->cfg.hidden) return 0;
+    if (B < 1 || max_ctx < 0 || !model_fits(layers, n_layers, B, max_ctx)) return 0;
+    const size_t st = stack_workspace_size(layers, n_layers, 2, B, 1, max_ctx);
+    const size_t hd = lm_head_workspace_size(lm, B);
+    if (!st || !hd) return 0;
+    return 2 * model_act_bytes(B, lm->cfg.hidden) + std::max(st, hd);
+}
+
+int model_decode_greedy(const layer_t* layers, int32_t n_layers, lm_t lm, const int32_t* tokens, const int32_t* pos,
+                        const int32_t* ctx_lens, int32_t max_ctx, int32_t B, void* const* k_caches,
+                        void* const* v_caches, float* logits, int32_t* next_tokens, void* ws, size_t ws_bytes,
+                        void* stream) {
+    if (!layers || n_layers < 1 || !lm || !tokens || !pos || !ctx_lens || !k_caches || !v_caches || !logits ||
+        !next_tokens)
+        return fail(W4_EINVAL, "null pointer argument");
+    for (int i = 0; i < n_layers; i++)
+        if (!layers[i] || !k_caches[i] || !v_caches[i]) return fail(W4_EINVAL, "null layer or cache %d", i);
+    if (layers[0]->cfg.hidden != lm->cfg.hidden) return fail(W4_EINVAL, "layers and LM ends differ in hidden size");
+    if (B < 1 || max_ctx < 0) return fail(W4_EINVAL, "B must be >= 1 and max_ctx >= 0");
+    if (B > lm->cfg.max_batch) return fail(W4_ECAPACITY, "B %d > the LM ends' max_batch %d", B, lm->cfg.max_batch);
+    if (!model_fits(layers, n_layers, B, max_ctx))
+        return fail(W4_ECAPACITY, "B %d or max_ctx %d + 1 beyond a layer's max_batch / max_seq", B, max_ctx);
+    const size_t need = model_decode_workspace_size(layers, n_layers, lm, B, max_ctx);
+    if (need == 0) return fail(W4_ECAPACITY, "B or max_ctx outside what the layers hold");
+    if (!ws || ws_bytes < need) return fail(W4_EWORKSPACE, "workspace %zu bytes, need %zu", ws_bytes, need);
+    const size_t act = model_act_bytes(B, lm->cfg.hidden);
+    float* x = (float*)ws;
+    float* y = (float*)((char*)ws + act);
+    void* scratch = (char*)ws + 2 * act;
+    const size_t sbytes = ws_bytes - 2 * act;
+    int rc;
+    if ((rc = lm_embed(lm, tokens, B, x, stream))) return rc;
+    if ((rc = stack_decode(layers, n_layers, x, pos, ctx_lens, max_ctx, nullptr, B, k_caches, v_caches, y, scratch,
+                           sbytes, stream)))
+        return rc;
+    return lm_head(lm, y, B, logits, next_tokens, scratch, sbytes, stream);
+}
+
 }  // extern "C"

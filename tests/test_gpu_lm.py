@@ -279,3 +279,61 @@ def test_lm_argument_errors_launch_nothing():
     torch.cuda.synchronize()
     assert bool((nxt[:2] >= 0).all()) and int(nxt[2]) == -7
     lmh.close()
+
+
+def test_model_decode_greedy_matches_composed_calls():
+    """The native loop step (embed -> stack decode -> head + pick in one
+    call, the picks fed back in place) gives bit for bit the logits and
+    tokens of the same calls made one by one, which the two-layer loop test
+    holds against the oracle."""
+    name, nl, V, T, D = "tiny", 2, 1024, 8, 5
+    cfg = synth.CONFIGS[name]
+    _, lw = host_lm(name, V)
+    hw = [host_layer(name, layer=l)[1] for l in range(nl)]
+    layers = [binding.Layer(cfg, hw[l]) for l in range(nl)]
+    st = binding.Stack(layers)
+    lmh = binding.LM(cfg, lw)
+    handles = [l.handle for l in layers]
+    prompt = torch.from_numpy(synth.tokens(cfg, V, T)).cuda()
+    runs = []
+    for native in (False, True):
+        caches = [l.new_cache(1, 0) for l in layers]
+        kcs, vcs = [c[0] for c in caches], [c[1] for c in caches]
+        x = torch.empty(T, cfg.hidden, device="cuda")
+        y = torch.empty_like(x)
+        lmh.embed(prompt, x)
+        st.prefill(x, torch.arange(T, dtype=torch.int32, device="cuda"), 0, kcs, vcs, y)
+        logits = torch.empty(1, V, device="cuda")
+        tok = torch.empty(1, dtype=torch.int32, device="cuda")
+        lmh.head(y[T - 1:T], logits, tok)
+        outs = []
+        max_ctx = T + D
+        n = binding.model_decode_workspace_size(handles, lmh.handle, 1, max_ctx)
+        assert n > 0
+        ws = torch.empty(n, dtype=torch.uint8, device="cuda")
+        x1, y1 = torch.empty(1, cfg.hidden, device="cuda"), torch.empty(1, cfg.hidden, device="cuda")
+        for s in range(D):
+            td = torch.tensor([T + s], dtype=torch.int32, device="cuda")
+            if native:
+                binding.check(binding.model_decode_greedy(handles, lmh.handle, tok, td, td, max_ctx, 1, kcs, vcs,
+                                                          logits, tok, ws, n))
+            else:
+                lmh.embed(tok, x1)
+                st.decode(x1, td, td, max_ctx, kcs, vcs, y1)
+                lmh.head(y1, logits, tok)
+            outs.append((logits.cpu().numpy().copy(), int(tok.item())))
+        runs.append(outs)
+    for s in range(D):
+        assert runs[0][s][1] == runs[1][s][1], f"step {s} tokens differ"
+        assert np.array_equal(runs[0][s][0], runs[1][s][0]), f"step {s} logits differ"
+    # argument checks happen before any launch
+    assert binding.model_decode_workspace_size(handles, lmh.handle, 1, cfg.max_seq) == 0
+    assert binding.model_decode_greedy(handles, lmh.handle, tok, td, td, cfg.max_seq, 1, kcs, vcs, logits, tok, ws,
+                                       n) == binding.W4_ECAPACITY
+    assert binding.model_decode_greedy(handles, lmh.handle, tok, td, td, T + D, 1, kcs, vcs, logits, tok, ws,
+                                       n - 1) == binding.W4_EWORKSPACE
+    assert binding.model_decode_greedy(handles, None, tok, td, td, T + D, 1, kcs, vcs, logits, tok, ws,
+                                       n) == binding.W4_EINVAL
+    lmh.close()
+    for l in layers:
+        l.close()
