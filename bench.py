@@ -400,8 +400,9 @@ def run_stack(args):
 def run_model_loop(cfg, st, kcs, vcs, P, S, layers_ms, binding, synth, vocab=128256, reps=30):
     """The whole-model greedy loop on the stack: embed the prompt, prefill it
     through every layer, LM head + greedy pick on its last row, then S steps
-    of embed(picked token) -> every layer's decode -> LM head + pick, with no
-    host round trip inside the timed region.  The ends use a Llama-3-8B
+    of the native loop step (model_decode_greedy: embed(picked token) ->
+    every layer's decode -> LM head + pick), with no host round trip inside
+    the timed region.  The ends use a Llama-3-8B
     vocabulary of 128256 tokens (seeded int4 head, bf16 embedding rows).
     Also the LM head + pick alone at B=1 (median of reps, HIP events)."""
     import numpy as np
@@ -425,11 +426,14 @@ def run_model_loop(cfg, st, kcs, vcs, P, S, layers_ms, binding, synth, vocab=128
     lm.embed(prompt, xp)
     st.prefill(xp, torch.arange(P, dtype=torch.int32, device="cuda"), 0, kcs, vcs, yp)
     lm.head(yp[P - 1:P], logits, picks[0:1])
+    handles = [l for l in st.handles]
+    max_ctx = P + S
+    n = binding.model_decode_workspace_size(handles, lm.handle, 1, max_ctx)
+    ws = torch.empty(n, dtype=torch.uint8, device="cuda")
     e1.record()
     for s in range(S):
-        lm.embed(picks[s:s + 1], x1)
-        st.decode(x1, slots[s:s + 1], slots[s:s + 1], P + s, kcs, vcs, y1)
-        lm.head(y1, logits, picks[s + 1:s + 2])
+        binding.check(binding.model_decode_greedy(handles, lm.handle, picks[s:s + 1], slots[s:s + 1], slots[s:s + 1],
+                                                  P + s, 1, kcs, vcs, logits, picks[s + 1:s + 2], ws, n))
     e2.record()
     torch.cuda.synchronize()
     assert lm.error() == 0
@@ -491,11 +495,13 @@ def run_model_loop_batch(cfg, layers, st, B, binding, synth, vocab=128256, P=256
         st.prefill(xp, pos, 0, [k[b:b + 1] for k in kcs], [v[b:b + 1] for v in vcs], yp)
         ylast[b] = yp[P - 1]
     lm.head(ylast, logits, picks[0])
+    handles = [l for l in st.handles]
+    n = binding.model_decode_workspace_size(handles, lm.handle, B, P + S)
+    ws = torch.empty(n, dtype=torch.uint8, device="cuda")
     e1.record()
     for s in range(S):
-        lm.embed(picks[s], x1)
-        st.decode(x1, ctxs[s], ctxs[s], P + s, kcs, vcs, y1)
-        lm.head(y1, logits, picks[s + 1])
+        binding.check(binding.model_decode_greedy(handles, lm.handle, picks[s], ctxs[s], ctxs[s], P + s, B, kcs, vcs,
+                                                  logits, picks[s + 1], ws, n))
     e2.record()
     torch.cuda.synchronize()
     assert lm.error() == 0
