@@ -290,6 +290,8 @@ def reports(binding, synth, stream, reps=20):
         out[name] = res
         torch.cuda.synchronize()
         for lay in layers:
+            if lay.error():
+                raise RuntimeError(f"{name}: a device error flag was raised")
             lay.close()
         del caches, ws
     return out
@@ -370,6 +372,7 @@ def run_stack(args):
     prefill_ms = e0.elapsed_time(e1)
     decode_ms = e1.elapsed_time(e2)
     assert torch.isfinite(yd).all() and torch.isfinite(yp).all()
+    assert all(l.error() == 0 for l in layers), "a device error flag was raised"
     tok_s = S / (decode_ms * 1e-3)
     # bytes a decode step reads: all weights plus the K/V of every layer (ctx P..P+S-1)
     wbytes = weight_bytes(cfg) * nl
@@ -394,6 +397,9 @@ def run_stack(args):
         del caches, kcs, vcs
         line["model_batch"] = run_model_loop_batch(cfg, layers, st, args.stack_batch, binding, synth)
     print(json.dumps(line), flush=True)
+    torch.cuda.synchronize()
+    for l in layers:
+        l.close()
     return 0
 
 
@@ -436,7 +442,7 @@ def run_model_loop(cfg, st, kcs, vcs, P, S, layers_ms, binding, synth, vocab=128
                                                   P + s, 1, kcs, vcs, logits, picks[s + 1:s + 2], ws, n))
     e2.record()
     torch.cuda.synchronize()
-    assert lm.error() == 0
+    assert lm.error() == 0 and all(binding.layer_error(h) == (0, 0) for h in handles)
     toks = picks.cpu().numpy()
     assert ((toks >= 0) & (toks < vocab)).all()
     loop_ms = e1.elapsed_time(e2)
@@ -504,7 +510,7 @@ def run_model_loop_batch(cfg, layers, st, B, binding, synth, vocab=128256, P=256
                                                   logits, picks[s + 1], ws, n))
     e2.record()
     torch.cuda.synchronize()
-    assert lm.error() == 0
+    assert lm.error() == 0 and all(binding.layer_error(h) == (0, 0) for h in handles)
     toks = picks.cpu().numpy()
     assert ((toks >= 0) & (toks < vocab)).all()
     loop_ms = e1.elapsed_time(e2)
@@ -633,6 +639,13 @@ def main():
         binding.layer_profile_kernel(lay.handle, 0, -1)
         binding.layer_profile_kernel(lay.handle, 2, -1)
 
+    # device error flags of the timed steps (a timed-out persistent-decode
+    # wait, an activation beyond the fp16 operand range): any raised flag
+    # makes the measurement invalid
+    flags = 0
+    for lay in layers:
+        flags |= lay.error()
+
     fl_p = stage_flops(cfg, Tp, Tp, 0, 1)
     fl_k = stage_flops(cfg, Tk, Tk, Lk, 1)
     by_d = stage_bytes(cfg, Bd, 1, ctx, Bd)
@@ -685,6 +698,8 @@ def main():
         "stages": stages,
         "roofline": roofline,
         "roofline_decode": roofline_decode,
+        "device_error_flags": flags,
+        "decode_wait_timeouts": int(bool(flags & binding.W4_FLAG_WAIT_TIMEOUT)),
     }
     if not args.no_extras:
         out["extras"] = extras(cfg, layers, caches, binding, synth, stream)
@@ -693,10 +708,19 @@ def main():
     if not args.no_cpu_baseline:
         log("bench: timing the CPU oracle (one decode layer-step)")
         out["cpu_baseline"] = cpu_baseline(cfg, w)
+    for lay in layers:
+        flags |= lay.error()
+    out["device_error_flags"] = flags
+    out["decode_wait_timeouts"] = int(bool(flags & binding.W4_FLAG_WAIT_TIMEOUT))
     print(json.dumps(out), flush=True)
+    torch.cuda.synchronize()
     for lay in layers:
         lay.close()
+    if flags:
+        log(f"bench: device error flags raised ({flags}): the measurement is not valid")
+        return 3
+    return 0
 
 
 if __name__ == "__main__":
-    main()
+    sys.exit(main())

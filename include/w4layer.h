@@ -39,6 +39,12 @@
  *     is the W4BF16 precision; the K/V cache holds bf16.
  *   - Weights are used exactly: W[k][n] = s[k/G][n] * (q[k][n] - z), sums in
  *     fp32.
+ *   - The matrix units take the bf16-rounded activations as fp16 operands.
+ *     Every bf16 value of magnitude 2^-17 .. 65280 is an fp16 value, so this
+ *     is exact there (below 2^-17 a value moves by less than 3e-8).  A
+ *     rounded activation beyond 65504 has no fp16 value: the kernel that
+ *     forms it raises W4_FLAG_F16_RANGE in the layer's device error flag
+ *     (layer_error) and the call's outputs are not valid.
  */
 #ifndef W4LAYER_H
 #define W4LAYER_H
@@ -57,6 +63,15 @@ extern "C" {
 #define W4_ECAPACITY     -3  /* would exceed max_seq or max_batch             */
 #define W4_EWORKSPACE    -4  /* workspace missing or smaller than required   */
 #define W4_EHIP          -5  /* a HIP runtime call or launch failed          */
+
+/* ---- device error flags (bits; layer_error / lm_error read and clear) ---- */
+#define W4_FLAG_WAIT_TIMEOUT 1  /* a wait of the persistent decode timed out: a
+                                   block of the launch never got its inputs
+                                   (e.g. other work held compute units)      */
+#define W4_FLAG_F16_RANGE    2  /* a bf16 activation exceeded 65504 in magnitude
+                                   (or was NaN) where an fp16 matrix operand is
+                                   formed                                      */
+#define W4_FLAG_TOKEN_ID     4  /* lm_embed saw a token id outside the vocabulary */
 
 /* ---- types ---------------------------------------------------------------- */
 
@@ -205,7 +220,10 @@ int layer_prefill_chunked(layer_t layer, const float* x, const int32_t* pos, int
  *   y         fp32 [B][hidden] out;
  *   ws        at least layer_workspace_size(layer, 2, B, 1, max_ctx).
  * Errors: W4_EINVAL, W4_ECAPACITY (B > max_batch or max_ctx + 1 > max_seq),
- * W4_EWORKSPACE, W4_EHIP. */
+ * W4_EUNSUPPORTED (B > 8, or decode path 2 selected and the persistent launch
+ * cannot serve the call), W4_EWORKSPACE, W4_EHIP.  Failures the host cannot
+ * see (a timed-out wait, an activation beyond the fp16 range) raise bits of
+ * the layer's error flag instead: read it with layer_error. */
 int layer_decode(layer_t layer, const float* x, const int32_t* pos, const int32_t* ctx_lens,
                  int32_t max_ctx, const float* attn_mask, int32_t B,
                  void* k_cache, void* v_cache, float* y,
@@ -228,7 +246,8 @@ int layer_decode(layer_t layer, const float* x, const int32_t* pos, const int32_
  * stack_decode: every layer runs layer_decode with the same pos, ctx_lens,
  * max_ctx, attn_mask and B.
  * Errors: those of the single-layer calls, and W4_EINVAL for a null or
- * mismatched layer list. */
+ * mismatched layer list.  Every layer's checks run before the first layer
+ * is enqueued, so a failed stack call has launched nothing. */
 size_t stack_workspace_size(const layer_t* layers, int32_t n_layers, int32_t stage, int32_t batch,
                             int32_t T, int32_t max_ctx);
 int stack_prefill(const layer_t* layers, int32_t n_layers, const float* x, const int32_t* pos,
@@ -304,9 +323,10 @@ size_t lm_head_workspace_size(lm_t lm, int32_t B);
 int lm_head(lm_t lm, const float* x, int32_t B, float* logits, int32_t* next_tokens,
             void* ws, size_t ws_bytes, void* stream);
 
-/* Reads and clears the error flag lm_embed sets: *flag = 1 if an
- * out-of-range token id was seen since the last call, else 0.  Waits for
- * the device.  Errors: W4_EINVAL, W4_EHIP. */
+/* Reads and clears the model ends' error flag: *flag holds W4_FLAG_TOKEN_ID
+ * if lm_embed saw an id outside the vocabulary, W4_FLAG_F16_RANGE if the
+ * final RMSNorm formed an activation beyond the fp16 range, since the last
+ * call; 0 if neither.  Waits for the device.  Errors: W4_EINVAL, W4_EHIP. */
 int lm_error(lm_t lm, int32_t* flag);
 
 /* One step of the runtime loop's greedy decode (Sec. 2, Sec. 4.5): embed
@@ -318,8 +338,14 @@ int lm_error(lm_t lm, int32_t* flag);
  * step without the host.  pos, ctx_lens, max_ctx, caches as for
  * stack_decode; logits fp32 [B][vocab] device out.  ws: at least
  * model_decode_workspace_size(layers, n_layers, lm, B, max_ctx) bytes (0 for
- * invalid arguments).  Arguments are checked before the first launch.
- * Errors: W4_EINVAL, W4_ECAPACITY, W4_EWORKSPACE, W4_EHIP. */
+ * invalid arguments).  Every check of every layer (capacity, B <= 8, a
+ * forced persistent path that cannot serve the call) runs before the first
+ * launch.  If the model ends' error flag or any layer's is set when the pick
+ * is done (by this step or an earlier one whose flags were not cleared),
+ * every next_tokens[b] is -1, so a loop that stays on the device sees the
+ * failure; the next step's embedding then flags the id -1 in turn.
+ * Errors: W4_EINVAL, W4_ECAPACITY, W4_EUNSUPPORTED, W4_EWORKSPACE,
+ * W4_EHIP. */
 size_t model_decode_workspace_size(const layer_t* layers, int32_t n_layers, lm_t lm, int32_t B, int32_t max_ctx);
 int model_decode_greedy(const layer_t* layers, int32_t n_layers, lm_t lm, const int32_t* tokens,
                         const int32_t* pos, const int32_t* ctx_lens, int32_t max_ctx, int32_t B,
@@ -362,6 +388,13 @@ int layer_debug_dequant(layer_t layer, int32_t which, float* out, void* stream);
  * kernels.  Errors: W4_EINVAL. */
 int layer_set_decode_path(layer_t layer, int32_t path);
 
+/* Poll budget of the persistent decode path (testing): the number of polls
+ * per thread and launch after which a wait for another block's data gives
+ * up, raises W4_FLAG_WAIT_TIMEOUT and lets the launch run to its end (the
+ * outputs are then not valid); 0 restores the default (2^20).  A small
+ * budget forces the timeout path from the host.  Errors: W4_EINVAL. */
+int layer_set_decode_spin_limit(layer_t layer, int32_t polls);
+
 /* Time stamps of the persistent decode path (diagnostics): with on != 0 its
  * launches record per-block wall-clock stamps for layer_decode_phase_times
  * and layer_debug_decode_stamps; off (the default) they record none (the
@@ -373,9 +406,9 @@ int layer_set_decode_trace(layer_t layer, int32_t on);
  * combine of its chunks, o_proj, gate/up, down), phase p measured from the
  * moment the last block finished phase p-1 (the kernel start for p = 0) to
  * the moment the last block finished phase p (stamps of the last call made
- * with layer_set_decode_trace on), into us_out[5]; and the error
- * flag raised by a wait that timed out (0 = none, sticky) into *error_flag
- * (nullable).  Waits for the device.  Errors: W4_EINVAL, W4_EHIP. */
+ * with layer_set_decode_trace on), into us_out[5]; and the layer's error
+ * flag (W4_FLAG_* bits, not cleared) into *error_flag (nullable).  Waits for
+ * the device.  Errors: W4_EINVAL, W4_EHIP. */
 int layer_decode_phase_times(layer_t layer, float* us_out, int32_t* error_flag);
 
 /* Raw wall-clock stamps of the last persistent decode call (diagnostics):
@@ -408,6 +441,13 @@ int layer_debug_decode_stamps(layer_t layer, uint64_t* out, int32_t n);
  * Errors: W4_EINVAL, W4_EHIP. */
 int layer_profile_kernel(layer_t layer, int32_t stage, int32_t kernel);
 int layer_profile_read(layer_t layer, int32_t stage, float* total_ms, int32_t* launches);
+
+/* Reads and clears the layer's device error flag: *flag is the OR of the
+ * W4_FLAG_* bits raised by its kernels since the last call (0: none).  Waits
+ * for the device first (no kernel of the layer is in flight when the flag is
+ * read); a call on another host thread that launches meanwhile may have its
+ * bits cleared.  Errors: W4_EINVAL, W4_EHIP. */
+int layer_error(layer_t layer, int32_t* flag);
 
 /* Message of the last failed call on this thread ("" if none). */
 const char* layer_last_error(void);

@@ -10,9 +10,12 @@ no fallback path.
 """
 from __future__ import annotations
 
+import atexit
 import ctypes
 import os
 import re
+import sys
+import weakref
 from typing import Optional
 
 import numpy as np
@@ -22,6 +25,7 @@ LIB_PATH = os.path.join(HERE, "libw4layer.so")
 HEADER = os.path.join(os.path.dirname(HERE), "include", "w4layer.h")
 
 W4_OK, W4_EINVAL, W4_EUNSUPPORTED, W4_ECAPACITY, W4_EWORKSPACE, W4_EHIP = 0, -1, -2, -3, -4, -5
+W4_FLAG_WAIT_TIMEOUT, W4_FLAG_F16_RANGE, W4_FLAG_TOKEN_ID = 1, 2, 4
 STAGE_PREFILL, STAGE_PREFILL_KV, STAGE_DECODE = 0, 1, 2
 LINEAR_INDEX = {"q": 0, "k": 1, "v": 2, "o": 3, "gate": 4, "up": 5, "down": 6}
 
@@ -91,9 +95,11 @@ _SIG = {
     "layer_decode_phase_times": (ctypes.c_int, [_P, _P, _P]),
     "layer_debug_decode_stamps": (ctypes.c_int, [_P, _P, _I]),
     "layer_set_decode_trace": (ctypes.c_int, [_P, _I]),
+    "layer_set_decode_spin_limit": (ctypes.c_int, [_P, _I]),
     "layer_profile_kernel": (ctypes.c_int, [_P, _I, _I]),
     "layer_profile_read": (ctypes.c_int, [_P, _I, ctypes.POINTER(ctypes.c_float), ctypes.POINTER(ctypes.c_int32)]),
     "layer_last_error": (ctypes.c_char_p, []),
+    "layer_error": (ctypes.c_int, [_P, ctypes.POINTER(ctypes.c_int32)]),
     "stack_workspace_size": (ctypes.c_size_t, [_P, _I, _I, _I, _I, _I]),
     "stack_prefill": (ctypes.c_int, [_P, _I, _P, _P, _I, _I, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "stack_decode": (ctypes.c_int, [_P, _I, _P, _P, _P, _I, _P, _I, _P, _P, _P, _P, ctypes.c_size_t, _P]),
@@ -264,6 +270,13 @@ def layer_debug_dequant(handle, which, out, stream=None) -> int:
     return _lib.layer_debug_dequant(handle, which, _ptr(out), _stream(stream))
 
 
+def layer_error(handle):
+    """(status, flag): the layer's W4_FLAG_* bits since the last call, cleared."""
+    f = ctypes.c_int32(0)
+    rc = _lib.layer_error(handle, ctypes.byref(f))
+    return rc, f.value
+
+
 def layer_decode_phase_times(handle):
     us = (ctypes.c_float * 5)()
     err = ctypes.c_int32()
@@ -279,6 +292,10 @@ def layer_debug_decode_stamps(handle, n: int = 8 + 32 * 1024):
 
 def layer_set_decode_trace(handle, on: int) -> int:
     return _lib.layer_set_decode_trace(handle, int(on))
+
+
+def layer_set_decode_spin_limit(handle, polls: int) -> int:
+    return _lib.layer_set_decode_spin_limit(handle, polls)
 
 
 def layer_set_decode_path(handle, path: int) -> int:
@@ -354,6 +371,22 @@ def model_decode_greedy(handles, lm_handle, tokens, pos, ctx_lens, max_ctx, B, k
                                     _ptr(logits), _ptr(next_tokens), _ptr(ws), ws_bytes, _stream(stream))
 
 
+# Handles still open when the interpreter exits are closed by an exit hook,
+# which runs before the interpreter and the HIP runtime tear down; the
+# finalisers of the owning objects make no library (HIP) call once the
+# interpreter is finalising.
+_live = weakref.WeakSet()
+
+
+@atexit.register
+def _close_all():
+    for obj in list(_live):
+        try:
+            obj.close()
+        except Exception:
+            pass
+
+
 class LM:
     """Owns a model-ends handle (embedding, LM head, greedy sampling) plus
     reusable workspace; methods raise W4Error."""
@@ -363,6 +396,7 @@ class LM:
         self.cfg, self.vocab = cfg, lm["vocab"]
         rc, self.handle = lm_create(self.vocab, cfg.hidden, cfg.group_size, cfg.rms_eps, max_batch, lm)
         check(rc)
+        _live.add(self)
         self._ws = torch.empty(0, dtype=torch.uint8, device="cuda")
 
     def close(self):
@@ -371,6 +405,8 @@ class LM:
             self.handle = None
 
     def __del__(self):
+        if sys.is_finalizing():
+            return
         try:
             self.close()
         except Exception:
@@ -403,6 +439,7 @@ class Layer:
         self.cfg = cfg
         rc, self.handle = layer_create(cfg, weights)
         check(rc)
+        _live.add(self)
         self._ws = torch.empty(0, dtype=torch.uint8, device="cuda")
 
     def close(self):
@@ -411,10 +448,18 @@ class Layer:
             self.handle = None
 
     def __del__(self):
+        if sys.is_finalizing():
+            return
         try:
             self.close()
         except Exception:
             pass
+
+    def error(self) -> int:
+        """The layer's W4_FLAG_* bits since the last call (read and cleared)."""
+        rc, f = layer_error(self.handle)
+        check(rc)
+        return f
 
     def workspace(self, stage, batch, T, max_ctx):
         import torch

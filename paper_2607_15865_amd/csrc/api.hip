@@ -10,6 +10,7 @@
 #include <cstdio>
 #include <cstdarg>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <thread>
 #include <vector>
@@ -152,6 +153,7 @@ struct Profiler {          // one timed kernel per stage
 };
 
 constexpr int kMaxBlocks = 1024;                    // persistent decode blocks (one per CU)
+constexpr int kSpinDefault = 1 << 20;               // polls per thread per persistent launch
 constexpr int kStampWords = 8 + 32 * kMaxBlocks;
 
 struct layer_s {
@@ -170,6 +172,7 @@ struct layer_s {
     unsigned long long* stamps = nullptr;
     int decode_path = 0;   // 0 auto, 1 separate kernels, 2 persistent
     bool decode_trace = false;   // persistent decode records its time stamps
+    int spin_max = kSpinDefault; // polls per thread per persistent launch before a wait gives up
 };
 
 namespace {
@@ -441,7 +444,9 @@ struct ProfScope {
     int stage;
     bool on = false;
     hipStream_t st;
+    // stage < 0: no timing (calls that must not allocate, even events)
     ProfScope(layer_s* L_, int stage_, int k, hipStream_t s) : L(L_), stage(stage_), st(s) {
+        if (stage < 0) return;
         Profiler& p = L->prof;
         if (p.kernel[stage] == k && p.used[stage] < Profiler::kMax) {
             auto& ev = p.ev[stage];
@@ -472,6 +477,7 @@ EpiArgs base_epi(const layer_s* L) {
     e.nkv = c.n_kv_heads;
     e.head_dim = c.head_dim;
     e.F_pad = L->F_pad;
+    e.err = L->err;
     return e;
 }
 
@@ -504,6 +510,7 @@ int launch_fused(layer_s* L, const FusedPlan& fp, const float* x, const int32_t*
     a.g = (uint64_t*)(base + fp.g);
     a.down_part = (uint64_t*)(base + fp.down_part);
     a.epoch = next_epoch();
+    a.spin_max = L->spin_max;
     a.err = L->err;
     a.stamps = L->decode_trace ? L->stamps : nullptr;
     a.S_qkv = fp.S_qkv; a.S_o = fp.S_o; a.S_down = fp.S_down;
@@ -569,7 +576,7 @@ int run_decode_seq(layer_s* L, const float* x, const int32_t* pos, const int32_t
     const bool prenorm = B >= 4;
     f16* xn = (f16*)(base + w.xn);
     if (prenorm) {
-        rc |= launch_rmsnorm(x, (const uint16_t*)L->attn_norm.p, c.rms_eps, B, H, xn, st);
+        rc |= launch_rmsnorm(x, (const uint16_t*)L->attn_norm.p, c.rms_eps, B, H, xn, L->err, st);
         a1.x_f16 = xn;
         a1.ldx = H;
     }
@@ -594,6 +601,7 @@ int run_decode_seq(layer_s* L, const float* x, const int32_t* pos, const int32_t
     ad.chunk = w.chunk;
     ad.nchunks = w.nchunks;
     ad.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)d));
+    ad.err = L->err;
     { ProfScope ps(L, ps_stage, ps_stage == 2 ? 1 : 2, st); rc |= launch_attn_decode(ad, st); }
 
     GemvArgs a2{};
@@ -619,7 +627,7 @@ int run_decode_seq(layer_s* L, const float* x, const int32_t* pos, const int32_t
     a3.copy_dst = y;
     a3.copy_n = B * H;
     if (prenorm) {
-        rc |= launch_rmsnorm(h, (const uint16_t*)L->mlp_norm.p, c.rms_eps, B, H, xn, st);
+        rc |= launch_rmsnorm(h, (const uint16_t*)L->mlp_norm.p, c.rms_eps, B, H, xn, L->err, st);
         a3.x_f16 = xn;
         a3.ldx = H;
     }
@@ -660,9 +668,9 @@ int run_prefill(layer_s* L, const float* x, const int32_t* pos, int T, int hist,
                 void* ws, size_t ws_bytes, void* stream_) {
     if (!L) return fail(W4_EINVAL, "null layer");
     if (!x || !pos || !kc || !vc || !y || !ws) return fail(W4_EINVAL, "null pointer argument");
-    if (T < 1 || hist < 0) return fail(W4_EINVAL, "T must be >= 1 and hist_len >= 0");
     if ((const void*)x == (const void*)y) return fail(W4_EINVAL, "x and y must not alias");
     const layer_config& c = L->cfg;
+    if (T < 1 || hist < 0) return fail(W4_EINVAL, "T must be >= 1 and hist_len >= 0");
     if ((long long)hist + T > c.max_seq) return fail(W4_ECAPACITY, "hist_len + T = %lld exceeds max_seq %d", (long long)hist + T, c.max_seq);
     hipStream_t st = (hipStream_t)stream_;
     const int stage = hist > 0 ? 1 : 0;
@@ -692,7 +700,7 @@ int run_prefill(layer_s* L, const float* x, const int32_t* pos, int T, int hist,
         if (gp->S > 1 && gp->tiles > kGemmCounters) return fail(W4_EUNSUPPORTED, "split-K tile count above %d", kGemmCounters);
 
     int rc = 0;
-    { ProfScope ps(L, stage, 0, st); rc |= launch_rmsnorm(x, (const uint16_t*)L->attn_norm.p, c.rms_eps, T, H, xn1, st); }
+    { ProfScope ps(L, stage, 0, st); rc |= launch_rmsnorm(x, (const uint16_t*)L->attn_norm.p, c.rms_eps, T, H, xn1, L->err, st); }
     EpiArgs e = base_epi(L);
     e.q_out = q;
     e.k_cache = (uint16_t*)kc;
@@ -715,12 +723,13 @@ int run_prefill(layer_s* L, const float* x, const int32_t* pos, int T, int hist,
     aa.d = d;
     aa.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)d));
     aa.part = part;
+    aa.err = L->err;
     { ProfScope ps(L, stage, 2, st); rc |= launch_attn_prefill(aa, w.at, st); }
     EpiArgs eo = base_epi(L);
     eo.resid = x;
     eo.out_f32 = h;
     { ProfScope ps(L, stage, 3, st); rc |= launch_gemm_w4(EPI_RESID, attn, qd, L->o.d, eo, w.o, T, part, cnt, next_epoch(), st); }
-    { ProfScope ps(L, stage, 4, st); rc |= launch_rmsnorm(h, (const uint16_t*)L->mlp_norm.p, c.rms_eps, T, H, xn2, st); }
+    { ProfScope ps(L, stage, 4, st); rc |= launch_rmsnorm(h, (const uint16_t*)L->mlp_norm.p, c.rms_eps, T, H, xn2, L->err, st); }
     EpiArgs eg = base_epi(L);
     eg.act_out = g;
     { ProfScope ps(L, stage, 5, st); rc |= launch_gemm_w4(EPI_SWIGLU, xn2, H, L->gu.d, eg, w.gu, T, part, cnt, next_epoch(), st); }
@@ -729,6 +738,55 @@ int run_prefill(layer_s* L, const float* x, const int32_t* pos, int T, int hist,
     ed.out_f32 = y;
     { ProfScope ps(L, stage, 6, st); rc |= launch_gemm_w4(EPI_RESID, g, L->F_pad, L->down.d, ed, w.down, T, part, cnt, next_epoch(), st); }
     if (rc) return fail(W4_EHIP, "kernel launch failed: %s", hipGetErrorString(hipGetLastError()));
+    return W4_OK;
+}
+
+FusedPlan decode_fused_choice(layer_s* L, int B, int max_ctx);
+
+// A checked decode call on workspace ws: the persistent launch or the kernel
+// sequence.  ps_stage: 2 (the decode stage's kernel timing) or -1 (none).
+int decode_run(layer_s* L, const float* x, const int32_t* pos, const int32_t* ctx_lens, int max_ctx,
+               const float* attn_mask, int B, void* kc, void* vc, float* y, void* ws, size_t ws_bytes,
+               hipStream_t st, int ps_stage) {
+    const FusedPlan fp = decode_fused_choice(L, B, max_ctx);
+    if (fp.ok) {
+        if (ws_bytes < fp.total) return fail(W4_EWORKSPACE, "workspace %zu bytes, need %zu", ws_bytes, fp.total);
+        int rc;
+        { ProfScope ps(L, ps_stage, 6, st); rc = launch_fused(L, fp, x, pos, ctx_lens, 0, false, attn_mask, B, kc, vc, y, ws, st); }
+        if (rc) return fail(W4_EHIP, "persistent decode launch failed: %s", hipGetErrorString(hipGetLastError()));
+        return W4_OK;
+    }
+    return run_decode_seq(L, x, pos, ctx_lens, 0, false, attn_mask, B, max_ctx, kc, vc, y, ws, ws_bytes, st, ps_stage);
+}
+
+// The persistent decode plan a decode call of B rows uses: forced by path 2,
+// automatic for at most 2 rows (from 3 rows on the kernel sequence is the
+// faster one); not ok means the kernel sequence.
+FusedPlan decode_fused_choice(layer_s* L, int B, int max_ctx) {
+    if (L->decode_path == 1 || (L->decode_path == 0 && B > 2)) return FusedPlan{};
+    return plan_fused(L, B, max_ctx, true);
+}
+
+// Every check of a decode call of B rows up to context max_ctx that does not
+// look at pointers, so a stack or model step can check all its layers
+// before it enqueues the first kernel.
+int decode_check(layer_s* L, int B, int max_ctx) {
+    const layer_config& c = L->cfg;
+    if (B < 1 || max_ctx < 0) return fail(W4_EINVAL, "B must be >= 1 and max_ctx >= 0");
+    if (B > c.max_batch) return fail(W4_ECAPACITY, "B = %d exceeds max_batch %d", B, c.max_batch);
+    if (B > 8) return fail(W4_EUNSUPPORTED, "decode batch above 8");
+    if ((long long)max_ctx + 1 > c.max_seq)
+        return fail(W4_ECAPACITY, "max_ctx + 1 = %lld exceeds max_seq %d", (long long)max_ctx + 1, c.max_seq);
+    if (L->decode_path == 2 && !plan_fused(L, B, max_ctx, true).ok)
+        return fail(W4_EUNSUPPORTED, "persistent decode not possible for this shape/batch");
+    return W4_OK;
+}
+
+// The same for a prefill / prefill_kv call of T tokens after hist_len.
+int prefill_check(layer_s* L, int T, int hist) {
+    if (T < 1 || hist < 0) return fail(W4_EINVAL, "T must be >= 1 and hist_len >= 0");
+    if ((long long)hist + T > L->cfg.max_seq)
+        return fail(W4_ECAPACITY, "hist_len + T = %lld exceeds max_seq %d", (long long)hist + T, L->cfg.max_seq);
     return W4_OK;
 }
 
@@ -942,27 +1000,10 @@ int layer_decode(layer_t L, const float* x, const int32_t* pos, const int32_t* c
                  void* stream) {
     if (!L) return fail(W4_EINVAL, "null layer");
     if (!x || !pos || !ctx_lens || !kc || !vc || !y || !ws) return fail(W4_EINVAL, "null pointer argument");
-    if (B < 1 || max_ctx < 0) return fail(W4_EINVAL, "B must be >= 1 and max_ctx >= 0");
     if ((const void*)x == (const void*)y) return fail(W4_EINVAL, "x and y must not alias");
-    const layer_config& c = L->cfg;
-    if (B > c.max_batch) return fail(W4_ECAPACITY, "B = %d exceeds max_batch %d", B, c.max_batch);
-    if (B > 8) return fail(W4_EUNSUPPORTED, "decode batch above 8");
-    if ((long long)max_ctx + 1 > c.max_seq) return fail(W4_ECAPACITY, "max_ctx + 1 = %lld exceeds max_seq %d", (long long)max_ctx + 1, c.max_seq);
-    hipStream_t st = (hipStream_t)stream;
-    // the persistent launch: forced by path 2, automatic for at most 2 rows
-    // (from 3 rows on the kernel sequence is the faster one)
-    const FusedPlan fp = L->decode_path == 1 || (L->decode_path == 0 && B > 2) ? FusedPlan{} : plan_fused(L, B, max_ctx, true);
-    if (L->decode_path == 2 && !fp.ok) return fail(W4_EUNSUPPORTED, "persistent decode not possible for this shape/batch");
-    if (fp.ok) {
-        if (ws_bytes < fp.total) return fail(W4_EWORKSPACE, "workspace %zu bytes, need %zu", ws_bytes, fp.total);
-        int rc;
-        { ProfScope ps(L, 2, 6, st); rc = launch_fused(L, fp, x, pos, ctx_lens, 0, false, attn_mask, B, kc, vc, y, ws, st); }
-        if (rc) return fail(W4_EHIP, "persistent decode launch failed: %s", hipGetErrorString(hipGetLastError()));
-        return W4_OK;
-    }
     int rc;
-    { rc = run_decode_seq(L, x, pos, ctx_lens, 0, false, attn_mask, B, max_ctx, kc, vc, y, ws, ws_bytes, st, 2); }
-    return rc;
+    if ((rc = decode_check(L, B, max_ctx))) return rc;
+    return decode_run(L, x, pos, ctx_lens, max_ctx, attn_mask, B, kc, vc, y, ws, ws_bytes, (hipStream_t)stream, 2);
 }
 
 int kv_append(const kv_desc* desc, void* kc, void* vc, const void* k_new, const void* v_new, int32_t B, int32_t T,
@@ -1038,7 +1079,8 @@ int stack_prefill(const layer_t* layers, int32_t n, const float* x, const int32_
     if ((rc = check_stack(layers, n))) return rc;
     if (!x || !y || !ws || !k_caches || !v_caches) return fail(W4_EINVAL, "null pointer argument");
     if ((const void*)x == (const void*)y) return fail(W4_EINVAL, "x and y must not alias");
-    if (T < 1 || hist_len < 0) return fail(W4_EINVAL, "T must be >= 1 and hist_len >= 0");
+    for (int i = 0; i < n; i++)
+        if ((rc = prefill_check(layers[i], T, hist_len))) return rc;
     const size_t need = stack_workspace_size(layers, n, hist_len > 0 ? 1 : 0, 1, T, hist_len);
     if (need == 0 || ws_bytes < need) return fail(W4_EWORKSPACE, "workspace %zu bytes, need %zu", ws_bytes, need);
     const size_t act = stack_act_offset(need - 2 * (size_t)T * layers[0]->cfg.hidden * sizeof(float));
@@ -1059,7 +1101,8 @@ int stack_decode(const layer_t* layers, int32_t n, const float* x, const int32_t
     if ((rc = check_stack(layers, n))) return rc;
     if (!x || !y || !ws || !k_caches || !v_caches) return fail(W4_EINVAL, "null pointer argument");
     if ((const void*)x == (const void*)y) return fail(W4_EINVAL, "x and y must not alias");
-    if (B < 1 || max_ctx < 0) return fail(W4_EINVAL, "B must be >= 1 and max_ctx >= 0");
+    for (int i = 0; i < n; i++)
+        if ((rc = decode_check(layers[i], B, max_ctx))) return rc;
     const size_t need = stack_workspace_size(layers, n, 2, B, 1, max_ctx);
     if (need == 0 || ws_bytes < need) return fail(W4_EWORKSPACE, "workspace %zu bytes, need %zu", ws_bytes, need);
     const size_t act = stack_act_offset(need - 2 * (size_t)B * layers[0]->cfg.hidden * sizeof(float));
@@ -1072,6 +1115,17 @@ int stack_decode(const layer_t* layers, int32_t n, const float* x, const int32_t
             return rc;
         in = out;
     }
+    return W4_OK;
+}
+
+int layer_error(layer_t L, int32_t* flag) {
+    if (!L || !flag) return fail(W4_EINVAL, "null argument");
+    int v = 0;
+    HIP_TRY(hipDeviceSynchronize());
+    HIP_TRY(hipMemcpy(&v, L->err, sizeof v, hipMemcpyDeviceToHost));
+    HIP_TRY(hipMemset(L->err, 0, sizeof v));
+    HIP_TRY(hipDeviceSynchronize());
+    *flag = v;
     return W4_OK;
 }
 
@@ -1108,6 +1162,13 @@ int layer_set_decode_path(layer_t L, int32_t path) {
     if (!L) return fail(W4_EINVAL, "null layer");
     if (path < 0 || path > 2) return fail(W4_EINVAL, "path must be 0, 1 or 2");
     L->decode_path = path;
+    return W4_OK;
+}
+
+int layer_set_decode_spin_limit(layer_t L, int32_t polls) {
+    if (!L) return fail(W4_EINVAL, "null layer");
+    if (polls < 0) return fail(W4_EINVAL, "polls must be >= 0");
+    L->spin_max = polls == 0 ? kSpinDefault : polls;
     return W4_OK;
 }
 
@@ -1251,7 +1312,7 @@ int lm_head(lm_t M, const float* x, int32_t B, float* logits, int32_t* next_toke
     const lm_config& c = M->cfg;
     const int H = c.hidden, V = c.vocab;
     f16* xn = (f16*)ws;
-    int rc = launch_rmsnorm(x, (const uint16_t*)M->final_norm.p, c.rms_eps, B, H, xn, st);
+    int rc = launch_rmsnorm(x, (const uint16_t*)M->final_norm.p, c.rms_eps, B, H, xn, (int*)M->err.p, st);
     for (int r0 = 0; r0 < B && !rc; r0 += kLmRows) {
         GemvArgs a{};
         a.W = M->head.d;
@@ -1272,6 +1333,7 @@ int lm_head(lm_t M, const float* x, int32_t B, float* logits, int32_t* next_toke
 int lm_error(lm_t M, int32_t* flag) {
     if (!M || !flag) return fail(W4_EINVAL, "null argument");
     int v = 0;
+    HIP_TRY(hipDeviceSynchronize());
     HIP_TRY(hipMemcpy(&v, M->err.p, 4, hipMemcpyDeviceToHost));
     HIP_TRY(hipMemset(M->err.p, 0, 4));
     HIP_TRY(hipDeviceSynchronize());
@@ -1283,17 +1345,21 @@ int lm_error(lm_t M, int32_t* flag) {
 
 namespace {
 size_t model_act_bytes(int B, int H) { return ((size_t)B * H * 4 + 255) / 256 * 256; }
-// every layer holds B sequences and a context of max_ctx + 1
-bool model_fits(const layer_t* layers, int n, int B, int max_ctx) {
-    for (int i = 0; i < n; i++)
-        if (!layers[i] || B > layers[i]->cfg.max_batch || max_ctx + 1 > layers[i]->cfg.max_seq) return false;
-    return true;
+// every layer can decode B sequences at a context up to max_ctx (the checks
+// of a decode call: capacity, the batch limit, a forced persistent path)
+int model_check(const layer_t* layers, int n, int B, int max_ctx) {
+    for (int i = 0; i < n; i++) {
+        if (!layers[i]) return fail(W4_EINVAL, "null layer %d", i);
+        const int rc = decode_check(layers[i], B, max_ctx);
+        if (rc) return rc;
+    }
+    return W4_OK;
 }
 }
 
 size_t model_decode_workspace_size(const layer_t* layers, int32_t n_layers, lm_t lm, int32_t B, int32_t max_ctx) {
     if (!layers || n_layers < 1 || !lm || !layers[0] || layers[0]->cfg.hidden != lm->cfg.hidden) return 0;
-    if (B < 1 || max_ctx < 0 || !model_fits(layers, n_layers, B, max_ctx)) return 0;
+    if (B < 1 || max_ctx < 0 || model_check(layers, n_layers, B, max_ctx) != W4_OK) return 0;
     const size_t st = stack_workspace_size(layers, n_layers, 2, B, 1, max_ctx);
     const size_t hd = lm_head_workspace_size(lm, B);
     if (!st || !hd) return 0;
@@ -1312,22 +1378,28 @@ int model_decode_greedy(const layer_t* layers, int32_t n_layers, lm_t lm, const 
     if (layers[0]->cfg.hidden != lm->cfg.hidden) return fail(W4_EINVAL, "layers and LM ends differ in hidden size");
     if (B < 1 || max_ctx < 0) return fail(W4_EINVAL, "B must be >= 1 and max_ctx >= 0");
     if (B > lm->cfg.max_batch) return fail(W4_ECAPACITY, "B %d > the LM ends' max_batch %d", B, lm->cfg.max_batch);
-    if (!model_fits(layers, n_layers, B, max_ctx))
-        return fail(W4_ECAPACITY, "B %d or max_ctx %d + 1 beyond a layer's max_batch / max_seq", B, max_ctx);
+    int rc;
+    if ((rc = model_check(layers, n_layers, B, max_ctx))) return rc;
     const size_t need = model_decode_workspace_size(layers, n_layers, lm, B, max_ctx);
     if (need == 0) return fail(W4_ECAPACITY, "B or max_ctx outside what the layers hold");
     if (!ws || ws_bytes < need) return fail(W4_EWORKSPACE, "workspace %zu bytes, need %zu", ws_bytes, need);
     const size_t act = model_act_bytes(B, lm->cfg.hidden);
     float* x = (float*)ws;
     float* y = (float*)((char*)ws + act);
-    void* scratch = (char*)ws + 2 * act;
+    void* rest = (char*)ws + 2 * act;
     const size_t sbytes = ws_bytes - 2 * act;
-    int rc;
     if ((rc = lm_embed(lm, tokens, B, x, stream))) return rc;
-    if ((rc = stack_decode(layers, n_layers, x, pos, ctx_lens, max_ctx, nullptr, B, k_caches, v_caches, y, scratch,
+    if ((rc = stack_decode(layers, n_layers, x, pos, ctx_lens, max_ctx, nullptr, B, k_caches, v_caches, y, rest,
                            sbytes, stream)))
         return rc;
-    return lm_head(lm, y, B, logits, next_tokens, scratch, sbytes, stream);
+    if ((rc = lm_head(lm, y, B, logits, next_tokens, rest, sbytes, stream))) return rc;
+    // a raised error flag (the LM's or any layer's) turns the picks into -1,
+    // so a loop that stays on the device sees the failure in its tokens
+    std::vector<const int*> flags{(const int*)lm->err.p};
+    for (int i = 0; i < n_layers; i++) flags.push_back(layers[i]->err);
+    if (launch_pick_guard(flags.data(), (int)flags.size(), next_tokens, B, (hipStream_t)stream))
+        return fail(W4_EHIP, "kernel launch failed: %s", hipGetErrorString(hipGetLastError()));
+    return W4_OK;
 }
 
 }  // extern "C"

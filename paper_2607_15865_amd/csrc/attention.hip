@@ -210,10 +210,12 @@ __global__ void __launch_bounds__(64 * PF_MAXHB) attn_prefill_kernel(AttnPrefill
         const float lt = l + __shfl_xor(l, 32, 64);
         const float inv = (lt > 0.f) ? 1.f / lt : 0.f;
         f16* out = a.out + ((size_t)qrow * a.nq + head) * D;
+        bool bad = false;
 #pragma unroll
         for (int i = 0; i < D / 32; i++)
 #pragma unroll
-            for (int e = 0; e < 16; e++) out[i * 32 + 8 * (e / 4) + 4 * h + (e % 4)] = act_f16(o[i][e] * inv);
+            for (int e = 0; e < 16; e++) out[i * 32 + 8 * (e / 4) + 4 * h + (e % 4)] = act_f16(o[i][e] * inv, bad);
+        flag_range(a.err, bad);
         return;
     }
     // partial state of this chunk: [row][item][wave][m, l, O registers][64 lanes]
@@ -282,8 +284,10 @@ __global__ void __launch_bounds__(64 * PF_MAXHB) attn_prefill_merge_kernel(AttnP
     if (qrow >= a.T) return;
     const float inv = (lt > 0.f) ? 1.f / lt : 0.f;
     f16* out = a.out + ((size_t)qrow * a.nq + g * r + hidx) * D;
+    bool bad = false;
 #pragma unroll
-    for (int e = 0; e < 16; e++) out[i * 32 + 8 * (e / 4) + 4 * h + (e % 4)] = act_f16(acc[e] * inv);
+    for (int e = 0; e < 16; e++) out[i * 32 + 8 * (e / 4) + 4 * h + (e % 4)] = act_f16(acc[e] * inv, bad);
+    flag_range(a.err, bad);
 }
 
 // ---------------------------------------------------------------- decode
@@ -493,7 +497,9 @@ __global__ void __launch_bounds__(D * DEC_CG) attn_decode_combine_kernel(AttnDec
         }
     }
     const float v = (Lt > 0.f) ? Ot / Lt : 0.f;
-    a.out[((size_t)b * a.nq + head) * D + dim] = act_f16(v);
+    bool bad = false;
+    a.out[((size_t)b * a.nq + head) * D + dim] = act_f16(v, bad);
+    flag_range(a.err, bad);
 }
 
 }  // namespace

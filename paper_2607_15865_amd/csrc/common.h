@@ -33,6 +33,8 @@
 #include <stdint.h>
 #include <mutex>
 
+#include "w4layer.h"
+
 typedef _Float16 f16;
 typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
@@ -93,10 +95,24 @@ __device__ __forceinline__ float bf16_bits_to_f32(uint16_t b) {
     return __uint_as_float(((uint32_t)b) << 16);
 }
 
-// Activation store: the value rounded to bf16 and held as fp16 (exact for
-// the bf16 values inside the fp16 range), the operand type of the W4 MFMA.
-__device__ __forceinline__ f16 act_f16(float x) {
-    return (f16)round_bf16(x);
+// Activation store: the value rounded to bf16 and held as fp16, the operand
+// type of the W4 MFMA.  Every bf16 value of magnitude 2^-17 .. 65280 is an
+// fp16 value, so the store is exact there; smaller magnitudes land on fp16's
+// 2^-24 grid (an absolute change below 3e-8).  A bf16 value beyond fp16's
+// range (65504) would become an infinity: `bad` records it (also NaN), and
+// the kernel raises W4_FLAG_F16_RANGE in the layer's error flag.
+__device__ __forceinline__ f16 act_f16(float x, bool& bad) {
+    const float r = round_bf16(x);
+    bad |= !(__builtin_fabsf(r) <= 65504.0f);
+    return (f16)r;
+}
+
+// Raise flag bits in a device error word (read and cleared by the host).
+__device__ __forceinline__ void raise_flag(int* err, int bits) {
+    if (err) atomicOr(err, bits);
+}
+__device__ __forceinline__ void flag_range(int* err, bool bad) {
+    if (bad) raise_flag(err, W4_FLAG_F16_RANGE);
 }
 
 // Dequantisation offsets of one zero point z: the fp16 pairs -(1024 + z) and
@@ -238,4 +254,5 @@ struct EpiArgs {
     // SWIGLU
     f16* act_out;             // fp16 [M][F_pad]
     int F_pad;
+    int* err;                 // the layer's error flag (W4_FLAG_F16_RANGE)
 };

@@ -30,7 +30,8 @@ struct DecodeFusedArgs {
     uint64_t* g;               // [B][F_pad / 2]         SwiGLU output, fp16 pairs
     uint64_t* down_part;       // [S_down][B][H]         fp32 partial sums (s >= 1)
     uint32_t epoch;            // tag of this launch (never 0)
-    int* err;                  // set when a wait times out
+    int spin_max;              // polls per thread per launch before a wait gives up
+    int* err;                  // the layer's error flag: W4_FLAG_WAIT_TIMEOUT, W4_FLAG_F16_RANGE
     unsigned long long* stamps;  // wall-clock stamps or null
     // work split
     const int* plan;           // per block: 16 ints (decode_fused_plan)

@@ -36,7 +36,6 @@ namespace {
 
 constexpr int NWAVE = 16;
 constexpr int NTHR = NWAVE * 64;
-constexpr int SPIN_MAX = 1 << 20;  // polls per thread per launch before the error flag is raised
 constexpr int RING = 4;            // weight tiles in flight per wave (gate/up, down)
 constexpr int RING_QKV = 4;        // q/k/v: its run is about 4 tiles per wave
 constexpr int RING_O = 4;          // o_proj: its run is 2 to 4 tiles per wave
@@ -77,7 +76,7 @@ __device__ __forceinline__ void settle_all(const uint64_t* const (&p)[N], uint64
         for (int i = 0; i < N; i++) late |= use[i] && (uint32_t)(v[i] >> 32) != ep;
         if (!late) return;
         if (--wt.left < 0) {
-            if (wt.left == -1) atomicExch(wt.err, 1);
+            if (wt.left == -1) raise_flag(wt.err, W4_FLAG_WAIT_TIMEOUT);
             return;
         }
         __builtin_amdgcn_s_sleep(1);
@@ -155,7 +154,7 @@ __device__ __forceinline__ void gather_raw(int n, uint32_t ep, Waiter& wt, Addr 
 // 128.  red8: 8 + NWAVE * B floats of LDS scratch.  Each thread takes 4
 // adjacent elements per pass, so the 16 lanes of a DPP row hold one 64-k tile.
 __device__ __forceinline__ void norm_prep_rows(const float* src, const uint16_t* gamma, float eps, int B, int K,
-                                               f16* xs, int ldx, float* c64, float* red8) {
+                                               f16* xs, int ldx, float* c64, float* red8, int* err) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     for (int b = 0; b < B; b++) {
         float ss = 0.f;
@@ -174,6 +173,7 @@ __device__ __forceinline__ void norm_prep_rows(const float* src, const uint16_t*
     }
     __syncthreads();
     const f16 sixteenth = (f16)0.0625f;
+    bool bad = false;
     for (int b = 0; b < B; b++) {
         const float rb = red8[b];
         for (int k0 = 0; k0 < K; k0 += 4 * NTHR) {          // uniform passes
@@ -183,10 +183,10 @@ __device__ __forceinline__ void norm_prep_rows(const float* src, const uint16_t*
                 // elements k % 8 = 0, 1 (or 4, 5) as they are, 2, 3 (or 6, 7) divided by 16
                 const float4 v = *reinterpret_cast<const float4*>(src + b * K + k);
                 const uint2 g = *reinterpret_cast<const uint2*>(gamma + k);
-                const f16 y0 = act_f16(v.x * rb * __uint_as_float(g.x << 16));
-                const f16 y1 = act_f16(v.y * rb * __uint_as_float(g.x & 0xFFFF0000u));
-                const f16 y2 = act_f16(v.z * rb * __uint_as_float(g.y << 16)) * sixteenth;
-                const f16 y3 = act_f16(v.w * rb * __uint_as_float(g.y & 0xFFFF0000u)) * sixteenth;
+                const f16 y0 = act_f16(v.x * rb * __uint_as_float(g.x << 16), bad);
+                const f16 y1 = act_f16(v.y * rb * __uint_as_float(g.x & 0xFFFF0000u), bad);
+                const f16 y2 = act_f16(v.z * rb * __uint_as_float(g.y << 16), bad) * sixteenth;
+                const f16 y3 = act_f16(v.w * rb * __uint_as_float(g.y & 0xFFFF0000u), bad) * sixteenth;
                 e = (float)y0 + (float)y1;
                 o = (float)y2 + (float)y3;
                 f16 q[4] = {y0, y1, y2, y3};
@@ -197,6 +197,7 @@ __device__ __forceinline__ void norm_prep_rows(const float* src, const uint16_t*
             if (k < K && (lane & 15) == 0) c64[(k >> 6) * GEMV_ROWS + b] = gemv_c64(e, o);
         }
     }
+    flag_range(err, bad);
     __syncthreads();
 }
 
@@ -245,7 +246,7 @@ __global__ void __launch_bounds__(NTHR) decode_fused_kernel(DecodeFusedArgs a) {
     const int B = a.B, H = a.H, nq = a.nq, nkv = a.nkv, r = nq / nkv;
     const int qd = nq * D, kd = nkv * D;
     const uint32_t ep = a.epoch;
-    Waiter wt{a.err, SPIN_MAX};
+    Waiter wt{a.err, a.spin_max};
     const int ldx = a.ldx;
     const int h = lane >> 5, c = lane & 31;
     f16* xs = reinterpret_cast<f16*>(smem);
@@ -367,7 +368,7 @@ __global__ void __launch_bounds__(NTHR) decode_fused_kernel(DecodeFusedArgs a) {
         const int t1 = pl[0], s1 = pl[3];
         const Run run1 = wave_run(1);
         // (the RMSNorm weights are in LDS unless the block's LDS has no room)
-        norm_prep_rows(hbuf, gam_lds ? gam : a.attn_norm, a.eps, B, H, xs, ldx, c64, red8);
+        norm_prep_rows(hbuf, gam_lds ? gam : a.attn_norm, a.eps, B, H, xs, ldx, c64, red8, a.err);
         stamp_done(6);
         clear_red();
         const GemvAct xa{xs, ldx, c64, nullptr, zero64};
@@ -644,6 +645,7 @@ __global__ void __launch_bounds__(NTHR) decode_fused_kernel(DecodeFusedArgs a) {
         const int v0 = min(V, blk * per), v1 = min(V, v0 + per), nv = v1 - v0;
         uint16_t* abuf = reinterpret_cast<uint16_t*>(smem);
         if (nv > 0) {
+            bool bad = false;
             const int LPV = a.comb_lpv, VPW = 64 / LPV;          // lanes per value (power of two)
             const int cpl = (NCH + LPV - 1) / LPV;                // chunks per lane (<= 4)
             for (int vb = wave * VPW; vb < nv; vb += NWAVE * VPW) {
@@ -700,8 +702,9 @@ __global__ void __launch_bounds__(NTHR) decode_fused_kernel(DecodeFusedArgs a) {
                     L += __shfl_xor(L, off, 64);
                     O += __shfl_xor(O, off, 64);
                 }
-                if (valid && cl == 0) abuf[j] = __builtin_bit_cast(uint16_t, act_f16(L > 0.f ? O / L : 0.f));
+                if (valid && cl == 0) abuf[j] = __builtin_bit_cast(uint16_t, act_f16(L > 0.f ? O / L : 0.f, bad));
             }
+            flag_range(a.err, bad);
             __syncthreads();
             stamp_done(10);
             for (int j = 2 * tid; j < nv; j += 2 * NTHR)
@@ -751,7 +754,7 @@ __global__ void __launch_bounds__(NTHR) decode_fused_kernel(DecodeFusedArgs a) {
         const int ta4 = pl[8], tb4 = pl[9];
         const Run run4 = wave_run(4);
         if (tid < 8) reinterpret_cast<u32x4*>(zero64)[tid] = u32x4{0u, 0u, 0u, 0u};   // (attention reused it)
-        norm_prep_rows(hbuf, gam_lds ? gam + H : a.mlp_norm, a.eps, B, H, xs, ldx, c64, red8);
+        norm_prep_rows(hbuf, gam_lds ? gam + H : a.mlp_norm, a.eps, B, H, xs, ldx, c64, red8, a.err);
         stamp_done(22);
         clear_red();
         const GemvAct xa{xs, ldx, c64, nullptr, zero64};
@@ -762,13 +765,15 @@ __global__ void __launch_bounds__(NTHR) decode_fused_kernel(DecodeFusedArgs a) {
         __syncthreads();
         stamp_done(24);
         const int np = (tb4 - ta4) / 2;
+        bool bad = false;
         for (int i = tid; i < np * B * 16; i += NTHR) {
             const int pp = i / (B * 16), rem = i - pp * B * 16, b = rem >> 4, cc = 2 * (rem & 15);
-            const f16 g0 = act_f16(silu(red_sum(2 * pp, b, cc)) * red_sum(2 * pp + 1, b, cc));
-            const f16 g1 = act_f16(silu(red_sum(2 * pp, b, cc + 1)) * red_sum(2 * pp + 1, b, cc + 1));
+            const f16 g0 = act_f16(silu(red_sum(2 * pp, b, cc)) * red_sum(2 * pp + 1, b, cc), bad);
+            const f16 g1 = act_f16(silu(red_sum(2 * pp, b, cc + 1)) * red_sum(2 * pp + 1, b, cc + 1), bad);
             const uint32_t word = (uint32_t)__builtin_bit_cast(uint16_t, g0) | ((uint32_t)__builtin_bit_cast(uint16_t, g1) << 16);
             put_tagged(a.g + ((size_t)b * a.F_pad + (ta4 / 2 + pp) * 32 + cc) / 2, word, ep);
         }
+        flag_range(a.err, bad);
     }
     prefetch(5);
     stamp_done(3);

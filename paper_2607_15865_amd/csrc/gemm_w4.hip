@@ -384,9 +384,11 @@ gemm_w4_kernel(const f16* __restrict__ X, int ldx, DevLinear W, EpiArgs ep, Gemm
             }
         } else if (EPI == EPI_SWIGLU) {
             const int f = (nt0 / 2) * 32 + c;          // tile pair (2j, 2j+1) = gate block j, up block j
+            bool bad = false;
 #pragma unroll
             for (int e = 0; e < 16; e++)
-                if (mr[e] >= 0) ep.act_out[(size_t)mr[e] * ep.F_pad + f] = act_f16(silu(v0[e]) * v1[e]);
+                if (mr[e] >= 0) ep.act_out[(size_t)mr[e] * ep.F_pad + f] = act_f16(silu(v0[e]) * v1[e], bad);
+            flag_range(ep.err, bad);
         } else {
             // q/k/v: the column pair (nt0 * 32 + c, + 32) holds dims dim0 and
             // dim1 of one head (see epi_qkv_pair); RoPE on q and k

@@ -82,18 +82,20 @@ __global__ void __launch_bounds__(NW * 64) gemv_w4_kernel(GemvArgs a) {
         __syncthreads();
         // the block's k slice, 4 elements per thread and pass
         const int k4n = klen / 4;
+        bool bad = false;
 #pragma unroll 4
         for (int i = tid; i < B * k4n; i += NW * 64) {
             const int b = i / k4n, k = 4 * (i - b * k4n);
             const float4 v = *reinterpret_cast<const float4*>(a.x_f32 + (size_t)b * K + klo + k);
             const uint2 g = *reinterpret_cast<const uint2*>(a.gamma + klo + k);
             const float rb = rinv[b];
-            f16 o[4] = {act_f16(v.x * rb * __uint_as_float(g.x << 16)),
-                        act_f16(v.y * rb * __uint_as_float(g.x & 0xFFFF0000u)),
-                        act_f16(v.z * rb * __uint_as_float(g.y << 16)),
-                        act_f16(v.w * rb * __uint_as_float(g.y & 0xFFFF0000u))};
+            f16 o[4] = {act_f16(v.x * rb * __uint_as_float(g.x << 16), bad),
+                        act_f16(v.y * rb * __uint_as_float(g.x & 0xFFFF0000u), bad),
+                        act_f16(v.z * rb * __uint_as_float(g.y << 16), bad),
+                        act_f16(v.w * rb * __uint_as_float(g.y & 0xFFFF0000u), bad)};
             *reinterpret_cast<uint2*>(xs + b * ldx + k) = *reinterpret_cast<const uint2*>(o);
         }
+        flag_range(a.ep.err, bad);
     } else {
         const int nv = klen / 8;
 #pragma unroll 4
@@ -155,11 +157,13 @@ __global__ void __launch_bounds__(NW * 64) gemv_w4_kernel(GemvArgs a) {
                 atomicAdd(o, tot[i]);
         }
     } else if (EPI == EPI_SWIGLU) {
+        bool bad = false;
         for (int i = tid; i < B * 32; i += NW * 64) {
             const int b = i / 32, cc = i % 32;
             const float gv = tot[b * 64 + cc], uv = tot[b * 64 + 32 + cc];
-            a.ep.act_out[(size_t)b * a.ep.F_pad + pair * 32 + cc] = act_f16(silu(gv) * uv);
+            a.ep.act_out[(size_t)b * a.ep.F_pad + pair * 32 + cc] = act_f16(silu(gv) * uv, bad);
         }
+        flag_range(a.ep.err, bad);
     } else {
         for (int i = tid; i < B * 32; i += NW * 64) {
             const int b = i / 32, cc = i % 32;

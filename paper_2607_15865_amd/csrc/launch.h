@@ -71,7 +71,7 @@ struct GemvArgs {
 };
 int launch_gemv_w4(int epi, bool norm, const GemvArgs& a, hipStream_t stream);
 
-int launch_rmsnorm(const float* x, const uint16_t* gamma, float eps, int M, int H, f16* out,
+int launch_rmsnorm(const float* x, const uint16_t* gamma, float eps, int M, int H, f16* out, int* err,
                    hipStream_t stream);
 
 struct AttnPrefillArgs {
@@ -84,6 +84,7 @@ struct AttnPrefillArgs {
     float scale_log2;        // log2(e) / sqrt(d)
     float* part;             // chunk partial states (plan.part_bytes)
     int chunk_keys, ngrp, items;   // set by the launcher from the plan
+    int* err;                // the layer's error flag (W4_FLAG_F16_RANGE)
 };
 // Prefill attention launch plan: key chunk length, work items per block
 // row, block size, workspace.
@@ -110,6 +111,7 @@ struct AttnDecodeArgs {
     f16* out;                // [B][nq*d]
     int B, nq, nkv, d, chunk, nchunks;
     float scale_log2;
+    int* err;                // the layer's error flag (W4_FLAG_F16_RANGE)
 };
 int launch_attn_decode(const AttnDecodeArgs& a, hipStream_t stream);
 

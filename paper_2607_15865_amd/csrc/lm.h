@@ -13,3 +13,6 @@ int launch_embed(const uint16_t* table, const int32_t* tokens, int V, int H, int
                  hipStream_t stream);
 int argmax_blocks(int V);
 int launch_argmax(const float* logits, int B, int V, float* pv, int* pi, int32_t* next, hipStream_t stream);
+// After a pick: next[0..B) = -1 if any of the n error words flags[i] (device
+// ints) is non-zero.
+int launch_pick_guard(const int* const* flags, int n, int32_t* next, int B, hipStream_t stream);

@@ -19,7 +19,7 @@ constexpr int AM_SPAN = 8192;   // logits per block of the first pass
 
 // out[b][:] = table[tokens[b]][:] as fp32 (exact: bf16 is the top half of
 // fp32).  One block per row; a token outside [0, V) gives a zero row and
-// sets *err to 1.
+// raises W4_FLAG_TOKEN_ID in *err.
 __global__ void __launch_bounds__(256) embed_kernel(const uint16_t* __restrict__ table,
                                                     const int32_t* __restrict__ tokens, int V, int H,
                                                     float* __restrict__ out, int* __restrict__ err) {
@@ -37,7 +37,7 @@ __global__ void __launch_bounds__(256) embed_kernel(const uint16_t* __restrict__
         }
         dst[i] = r;
     }
-    if (!ok && threadIdx.x == 0) atomicOr(err, 1);
+    if (!ok && threadIdx.x == 0) atomicOr(err, W4_FLAG_TOKEN_ID);
 }
 
 // (bv, bi) becomes (v, i) if v is larger, or equal with a lower index.  A
@@ -101,6 +101,20 @@ __global__ void __launch_bounds__(64) argmax_final_kernel(const float* __restric
     if (l == 0) next[b] = bi == INT_MAX ? 0 : bi;
 }
 
+// The guard after a greedy pick: if any of the error words is non-zero,
+// every pick of the step becomes -1.
+struct FlagList {
+    const int* p[32];
+    int n;
+};
+
+__global__ void __launch_bounds__(64) pick_guard_kernel(FlagList f, int32_t* __restrict__ next, int B) {
+    int any = 0;
+    for (int i = 0; i < f.n; i++) any |= f.p[i][0];
+    if (any)
+        for (int b = threadIdx.x; b < B; b += 64) next[b] = -1;
+}
+
 }  // namespace
 
 int launch_embed(const uint16_t* table, const int32_t* tokens, int V, int H, int B, float* out, int* err,
@@ -117,5 +131,15 @@ int launch_argmax(const float* logits, int B, int V, float* pv, int* pi, int32_t
     const int nblk = argmax_blocks(V);
     hipLaunchKernelGGL(argmax_partial_kernel, dim3(nblk, B), dim3(256), 0, stream, logits, V, nblk, pv, pi);
     hipLaunchKernelGGL(argmax_final_kernel, dim3(B), dim3(64), 0, stream, pv, pi, nblk, next);
+    return hipGetLastError() == hipSuccess ? 0 : -1;
+}
+
+int launch_pick_guard(const int* const* flags, int n, int32_t* next, int B, hipStream_t stream) {
+    for (int i0 = 0; i0 < n; i0 += 32) {
+        FlagList f{};
+        f.n = n - i0 < 32 ? n - i0 : 32;
+        for (int i = 0; i < f.n; i++) f.p[i] = flags[i0 + i];
+        hipLaunchKernelGGL(pick_guard_kernel, dim3(1), dim3(64), 0, stream, f, next, B);
+    }
     return hipGetLastError() == hipSuccess ? 0 : -1;
 }

@@ -10,7 +10,8 @@ namespace {
 // kept in registers between the sum of squares and the output.
 template <int NV>
 __global__ void __launch_bounds__(256) rmsnorm_kernel(const float* __restrict__ x, const uint16_t* __restrict__ gamma,
-                                                      float eps, int H, f16* __restrict__ out) {
+                                                      float eps, int H, f16* __restrict__ out,
+                                                      int* __restrict__ err) {
     __shared__ float part[4];
     const int row = blockIdx.x, tid = threadIdx.x;
     const float* xr = x + (size_t)row * H;
@@ -31,17 +32,19 @@ __global__ void __launch_bounds__(256) rmsnorm_kernel(const float* __restrict__ 
     const float tot = part[0] + part[1] + part[2] + part[3];
     const float rinv = 1.0f / sqrtf(tot / (float)H + eps);
     f16* orow = out + (size_t)row * H;
+    bool bad = false;
 #pragma unroll
     for (int j = 0; j < NV; j++) {
         const int k = (tid + 256 * j) * 4;
         if (k >= H) break;
         f16 o[4];
-        o[0] = act_f16(v[j].x * rinv * __uint_as_float(g[j].x << 16));
-        o[1] = act_f16(v[j].y * rinv * __uint_as_float(g[j].x & 0xFFFF0000u));
-        o[2] = act_f16(v[j].z * rinv * __uint_as_float(g[j].y << 16));
-        o[3] = act_f16(v[j].w * rinv * __uint_as_float(g[j].y & 0xFFFF0000u));
+        o[0] = act_f16(v[j].x * rinv * __uint_as_float(g[j].x << 16), bad);
+        o[1] = act_f16(v[j].y * rinv * __uint_as_float(g[j].x & 0xFFFF0000u), bad);
+        o[2] = act_f16(v[j].z * rinv * __uint_as_float(g[j].y << 16), bad);
+        o[3] = act_f16(v[j].w * rinv * __uint_as_float(g[j].y & 0xFFFF0000u), bad);
         *reinterpret_cast<uint2*>(orow + k) = *reinterpret_cast<const uint2*>(o);
     }
+    flag_range(err, bad);
 }
 
 struct SlotStarts { int32_t v[64]; };
@@ -95,14 +98,15 @@ __global__ void debug_dequant_kernel(DevLinear W, const int32_t* __restrict__ co
 
 }  // namespace
 
-int launch_rmsnorm(const float* x, const uint16_t* gamma, float eps, int M, int H, f16* out, hipStream_t stream) {
+int launch_rmsnorm(const float* x, const uint16_t* gamma, float eps, int M, int H, f16* out, int* err,
+                   hipStream_t stream) {
     if (H % 4 || H > 16 * 1024) return -1;
     const int nv = (H + 1023) / 1024;
-    if (nv <= 1) hipLaunchKernelGGL(rmsnorm_kernel<1>, dim3(M), dim3(256), 0, stream, x, gamma, eps, H, out);
-    else if (nv <= 2) hipLaunchKernelGGL(rmsnorm_kernel<2>, dim3(M), dim3(256), 0, stream, x, gamma, eps, H, out);
-    else if (nv <= 4) hipLaunchKernelGGL(rmsnorm_kernel<4>, dim3(M), dim3(256), 0, stream, x, gamma, eps, H, out);
-    else if (nv <= 8) hipLaunchKernelGGL(rmsnorm_kernel<8>, dim3(M), dim3(256), 0, stream, x, gamma, eps, H, out);
-    else hipLaunchKernelGGL(rmsnorm_kernel<16>, dim3(M), dim3(256), 0, stream, x, gamma, eps, H, out);
+    if (nv <= 1) hipLaunchKernelGGL(rmsnorm_kernel<1>, dim3(M), dim3(256), 0, stream, x, gamma, eps, H, out, err);
+    else if (nv <= 2) hipLaunchKernelGGL(rmsnorm_kernel<2>, dim3(M), dim3(256), 0, stream, x, gamma, eps, H, out, err);
+    else if (nv <= 4) hipLaunchKernelGGL(rmsnorm_kernel<4>, dim3(M), dim3(256), 0, stream, x, gamma, eps, H, out, err);
+    else if (nv <= 8) hipLaunchKernelGGL(rmsnorm_kernel<8>, dim3(M), dim3(256), 0, stream, x, gamma, eps, H, out, err);
+    else hipLaunchKernelGGL(rmsnorm_kernel<16>, dim3(M), dim3(256), 0, stream, x, gamma, eps, H, out, err);
     return hipGetLastError() == hipSuccess ? 0 : -1;
 }
 

@@ -26,3 +26,24 @@ def read_golden(name):
                 continue
             rows.append(line.split())
     return rows
+
+
+@pytest.fixture(autouse=True)
+def _device_error_flags_clear(request):
+    """After every GPU test: no library handle that is still open may hold a
+    raised device error flag (a timed-out wait of the persistent decode, an
+    activation beyond the fp16 range, an out-of-range token id).  Tests that
+    raise a flag on purpose read (and so clear) it themselves."""
+    yield
+    if request.node.get_closest_marker("gpu") is None:
+        return
+    b = sys.modules.get("paper_2607_15865_amd.binding")
+    if b is None:
+        return
+    raised = []
+    for obj in list(b._live):
+        if getattr(obj, "handle", None):
+            f = obj.error()
+            if f:
+                raised.append((type(obj).__name__, f))
+    assert not raised, f"device error flags raised: {raised}"

@@ -55,7 +55,7 @@ def test_embed_bitexact_and_out_of_range():
     lmh.embed(bad, xb)
     xbh = xb.cpu().numpy()
     assert np.array_equal(xbh[0], M.embed(lw["embed"], [3])[0]) and not xbh[1:].any()
-    assert lmh.error() == 1 and lmh.error() == 0
+    assert lmh.error() == binding.W4_FLAG_TOKEN_ID and lmh.error() == 0
     lmh.close()
 
 
@@ -334,6 +334,92 @@ def test_model_decode_greedy_matches_composed_calls():
                                        n - 1) == binding.W4_EWORKSPACE
     assert binding.model_decode_greedy(handles, None, tok, td, td, T + D, 1, kcs, vcs, logits, tok, ws,
                                        n) == binding.W4_EINVAL
+    lmh.close()
+    for l in layers:
+        l.close()
+
+
+def test_model_decode_greedy_batch_positions_not_slots():
+    """The native loop step at B = 4 (the layers' kernel-sequence decode,
+    a head launch over four rows), each sequence at its own context with
+    a position unrelated to it: every row's logits against the oracle
+    layers decoding that row on its own cache, and its pick."""
+    name, nl, V, B = "tiny", 2, 1024, 4
+    cfg = synth.CONFIGS[name]
+    _, lw = host_lm(name, V)
+    hw = [host_layer(name, layer=l)[1] for l in range(nl)]
+    W = [oracle_weights(name, layer=l) for l in range(nl)]
+    layers = [binding.Layer(cfg, hw[l]) for l in range(nl)]
+    lmh = binding.LM(cfg, lw)
+    handles = [l.handle for l in layers]
+    ctx = np.array([17, 0, 90, 55], dtype=np.int32)
+    pos = np.array([100, 31, 2, 127], dtype=np.int32)
+    fills = [synth.kv_fill(cfg, B, layer=l) for l in range(nl)]
+    kcs = [torch.from_numpy(f[0].view(np.int16).copy()).cuda() for f in fills]
+    vcs = [torch.from_numpy(f[1].view(np.int16).copy()).cuda() for f in fills]
+    toks = synth.tokens(cfg, V, B, seed=99)
+    tok = torch.from_numpy(toks.copy()).cuda()
+    logits = torch.empty(B, V, device="cuda")
+    max_ctx = int(ctx.max())
+    n = binding.model_decode_workspace_size(handles, lmh.handle, B, max_ctx)
+    ws = torch.empty(n, dtype=torch.uint8, device="cuda")
+    binding.check(binding.model_decode_greedy(handles, lmh.handle, tok, torch.from_numpy(pos).cuda(),
+                                              torch.from_numpy(ctx).cuda(), max_ctx, B, kcs, vcs, logits, tok,
+                                              ws, n))
+    gl, picks = logits.cpu().numpy(), tok.cpu().numpy()
+    xv = M.embed(lw["embed"], toks)
+    for l in range(nl):
+        xv = O.decode(hw[l], cfg, xv, pos, O.bf16_to_f64(fills[l][0]), O.bf16_to_f64(fills[l][1]), ctx, W=W[l])[0]
+    ol = M.lm_logits(xv, lw["final_norm"], lw["head"], cfg.group_size, cfg.rms_eps)
+    for b in range(B):
+        assert_parity(gl[b], ol[b], f"row {b} logits")
+        check_pick(gl[b], ol[b], int(picks[b]), f"row {b}")
+    lmh.close()
+    for l in layers:
+        l.close()
+
+
+def test_model_decode_greedy_rejects_before_launch():
+    """Rejected steps leave logits and tokens as they were: a batch above 8
+    (W4_EUNSUPPORTED), a forced persistent path that cannot serve the batch,
+    a context beyond max_seq, a short workspace."""
+    name, nl, V = "tiny", 2, 1024
+    cfg = synth.replace(synth.CONFIGS[name], max_batch=16)
+    _, lw = host_lm(name, V)
+    hw = [host_layer(name, layer=l)[1] for l in range(nl)]
+    layers = [binding.Layer(cfg, hw[l]) for l in range(nl)]
+    lmh = binding.LM(cfg, lw, max_batch=16)
+    handles = [l.handle for l in layers]
+    B = 9
+    kcs = [l.new_cache(B, 0)[0] for l in layers]
+    vcs = [l.new_cache(B, 0)[1] for l in layers]
+    tok = torch.full((B,), -7, dtype=torch.int32, device="cuda")
+    logits = torch.full((B, V), 5.0, device="cuda")
+    td = torch.full((B,), 3, dtype=torch.int32, device="cuda")
+    ws = torch.empty(1 << 24, dtype=torch.uint8, device="cuda")
+    assert binding.model_decode_workspace_size(handles, lmh.handle, B, 3) == 0
+    assert binding.model_decode_greedy(handles, lmh.handle, tok, td, td, 3, B, kcs, vcs, logits, tok, ws,
+                                       ws.numel()) == binding.W4_EUNSUPPORTED
+    layers[1].set_decode_path(2)       # the persistent launch takes at most 4 rows
+    assert binding.model_decode_workspace_size(handles, lmh.handle, 5, 3) == 0
+    assert binding.model_decode_greedy(handles, lmh.handle, tok, td, td, 3, 5, kcs, vcs, logits, tok, ws,
+                                       ws.numel()) == binding.W4_EUNSUPPORTED
+    layers[1].set_decode_path(0)
+    assert binding.model_decode_greedy(handles, lmh.handle, tok, td, td, cfg.max_seq, 2, kcs, vcs, logits, tok, ws,
+                                       ws.numel()) == binding.W4_ECAPACITY
+    need = binding.model_decode_workspace_size(handles, lmh.handle, 2, 3)
+    assert need > 0
+    assert binding.model_decode_greedy(handles, lmh.handle, tok, td, td, 3, 2, kcs, vcs, logits, tok, ws,
+                                       need - 1) == binding.W4_EWORKSPACE
+    # stack_decode checks every layer before the first one runs
+    x = torch.zeros(5, cfg.hidden, device="cuda")
+    y = torch.full_like(x, 3.0)
+    layers[1].set_decode_path(2)
+    assert binding.stack_decode(handles, x, td, td, 3, None, 5, kcs, vcs, y, ws, ws.numel()) == binding.W4_EUNSUPPORTED
+    layers[1].set_decode_path(0)
+    torch.cuda.synchronize()
+    assert bool((logits == 5.0).all()) and bool((tok == -7).all()) and bool((y == 3.0).all())
+    assert not kcs[0].any() and not vcs[0].any()
     lmh.close()
     for l in layers:
         l.close()

@@ -355,3 +355,114 @@ def test_chain_prefill_prefill_kv_decode():
     n = P + C + D
     assert_parity(cache_values(k)[0][:, :n], kc[:, :n], "cache K")
     assert_parity(cache_values(v)[0][:, :n], vc[:, :n], "cache V")
+
+
+# Position ids feed only RoPE; the cache slot of a token is fixed by the
+# history length (Table 1 lists the positions as an input of their own, and
+# the cos/sin table is gathered by them, Sec. 4.6.2).  These cases give
+# positions that differ from the slots (shifted, permuted, per row unrelated
+# to the context), so a kernel that rotated by slot, or wrote the cache at the
+# position, fails them.
+def _positions(kind, n, lo, hi, seed):
+    if kind == "shift":
+        return np.arange(lo, lo + n)
+    rng = np.random.default_rng(seed)
+    return rng.choice(np.arange(lo, hi), n, replace=False)
+
+
+POS_PREFILL_CASES = [("tiny", 32, "shift", 90), ("tiny", 20, "perm", 0), ("qwen05b", 256, "shift", 700),
+                     ("llama8b", 128, "perm", 0)]
+
+
+@pytest.mark.parametrize("name,T,kind,lo", POS_PREFILL_CASES)
+def test_prefill_positions_not_slots(name, T, kind, lo):
+    cfg, w = host_layer(name)
+    W = oracle_weights(name)
+    lay = device_layer(name)
+    pos = _positions(kind, T, lo, cfg.max_seq, 11 + T)
+    assert not np.array_equal(pos, np.arange(T))
+    log(f"prefill {name} T={T} positions {kind} {pos[:4]}...")
+    xb, xv = _x(cfg, synth.TID_X_PREFILL, T)
+    k, v = lay.new_cache(1, 0)
+    x = bits_to_torch_f32(xb)
+    y = torch.empty_like(x)
+    lay.prefill(x, torch.from_numpy(pos.astype(np.int32)).cuda(), k, v, y)
+    torch.cuda.synchronize()
+    yo, ko, vo = O.prefill(w, cfg, xv, pos, W=W)
+    assert_parity(y.cpu().numpy(), yo, "y")
+    _check_new_kv(k, v, ko, vo, 0, T)
+    # slots past T are untouched (the cache was zeros)
+    assert not k.cpu().numpy()[0][:, T:, :].any() and not v.cpu().numpy()[0][:, T:, :].any()
+
+
+# prefill_kv on the prefill kernels (T = 16, 128) and on the decode kernels
+# (T = 2: persistent launch; 4 with path 2: persistent; 6: kernel sequence)
+POS_PKV_CASES = [("tiny", 16, 32, 0), ("tiny", 2, 40, 0), ("tiny", 4, 40, 2), ("tiny", 6, 40, 0),
+                 ("llama8b", 128, 1024, 0), ("llama8b", 2, 1500, 0)]
+
+
+@pytest.mark.parametrize("name,T,L,path", POS_PKV_CASES)
+def test_prefill_kv_positions_not_slots(name, T, L, path):
+    cfg, w = host_layer(name)
+    W = oracle_weights(name)
+    lay = device_layer(name)
+    lay.set_decode_path(path)
+    pos = _positions("perm", T, 0, cfg.max_seq, 5 + T + L)
+    log(f"prefill_kv {name} T={T} L={L} path={path} positions {pos}")
+    kb, vb = synth.kv_fill(cfg, 1)
+    kc, vc = O.bf16_to_f64(kb)[0], O.bf16_to_f64(vb)[0]
+    k = torch.from_numpy(kb.view(np.int16).copy()).cuda()
+    v = torch.from_numpy(vb.view(np.int16).copy()).cuda()
+    xb, xv = _x(cfg, synth.TID_X_PREFILL_KV, T)
+    x = bits_to_torch_f32(xb)
+    y = torch.empty_like(x)
+    lay.prefill_kv(x, torch.from_numpy(pos.astype(np.int32)).cuda(), L, k, v, y)
+    torch.cuda.synchronize()
+    lay.set_decode_path(0)
+    yo, ko, vo = O.prefill_kv(w, cfg, xv, pos, kc, vc, L, W=W)
+    assert_parity(y.cpu().numpy(), yo, "y")
+    _check_new_kv(k, v, ko, vo, L, T)
+    kk = k.cpu().numpy()[0]
+    ref = kb.view(np.int16)[0]
+    assert np.array_equal(kk[:, :L, :], ref[:, :L, :]) and np.array_equal(kk[:, L + T:, :], ref[:, L + T:, :])
+
+
+POS_DECODE_CASES = [("tiny", 4, [0, 9, 64, 126], 0), ("tiny", 4, [0, 9, 64, 126], 1), ("tiny", 4, [0, 9, 64, 126], 2),
+                    ("tiny", 1, [48], 0), ("llama8b", 1, [2048], 0), ("llama8b", 2, [2048, 300], 0),
+                    ("llama8b", 4, [2048, 1, 4000, 700], 1), ("qwen7b", 2, [8192, 3000], 2)]
+
+
+@pytest.mark.parametrize("name,B,ctx,path", POS_DECODE_CASES)
+def test_decode_positions_not_slots(name, B, ctx, path):
+    """Decode rows whose positions are unrelated to their context lengths:
+    each row writes slot ctx[b] and attends slots 0..ctx[b], rotated by
+    pos[b]."""
+    cfg, w = host_layer(name)
+    W = oracle_weights(name)
+    lay = device_layer(name)
+    lay.set_decode_path(path)
+    ctx = np.array(ctx, dtype=np.int32)
+    rng = np.random.default_rng(B * 7 + int(ctx.sum()))
+    pos = rng.integers(0, cfg.max_seq, B).astype(np.int32)
+    pos = np.where(pos == ctx, (pos + 1) % cfg.max_seq, pos).astype(np.int32)
+    log(f"decode {name} B={B} ctx={ctx} pos={pos} path={path}")
+    kb, vb = synth.kv_fill(cfg, B)
+    kc, vc = O.bf16_to_f64(kb), O.bf16_to_f64(vb)
+    xb, xv = _x(cfg, synth.TID_X_DECODE, B)
+    k = torch.from_numpy(kb.view(np.int16).copy()).cuda()
+    v = torch.from_numpy(vb.view(np.int16).copy()).cuda()
+    x = bits_to_torch_f32(xb)
+    y = torch.empty_like(x)
+    lay.decode(x, torch.from_numpy(pos).cuda(), torch.from_numpy(ctx).cuda(), int(ctx.max()), k, v, y)
+    torch.cuda.synchronize()
+    lay.set_decode_path(0)
+    yo, ko, vo = O.decode(w, cfg, xv, pos, kc, vc, ctx, W=W)
+    assert_parity(y.cpu().numpy(), yo, "y")
+    gk, gv = cache_values(k), cache_values(v)
+    assert_parity(np.stack([gk[b][:, ctx[b], :] for b in range(B)]), ko, "new K")
+    assert_parity(np.stack([gv[b][:, ctx[b], :] for b in range(B)]), vo, "new V")
+    # only slot ctx[b] of each row changed
+    kk = k.cpu().numpy()
+    for b in range(B):
+        diff = np.argwhere((kk[b] != kb.view(np.int16)[b]).any(axis=(0, 2))).ravel()
+        assert set(diff.tolist()) <= {int(ctx[b])}, (b, diff[:8])
