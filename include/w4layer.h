@@ -229,6 +229,24 @@ int layer_decode(layer_t layer, const float* x, const int32_t* pos, const int32_
                  void* k_cache, void* v_cache, float* y,
                  void* ws, size_t ws_bytes, void* stream);
 
+/* Decode without allocation, for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * it): layer_decode with its workspace taken from a static device array of
+ * the library (layer_decode_noalloc_max_bytes() bytes, 32 MiB) instead of a
+ * caller buffer.  Each device holds the array from the first layer_create
+ * on it until the process ends, and every call on a device shares it, so
+ * calls that overlap on one device (other streams, other host threads)
+ * race: the caller serialises them.  The call allocates nothing (no
+ * hipMalloc, no events: kernel timing does not apply to it); no part of
+ * the array has to start at zero.  Arguments as for layer_decode, without
+ * ws.  Errors: those of layer_decode; W4_EWORKSPACE if the call needs more
+ * scratch than the array holds (the message states both sizes); W4_EHIP if
+ * the array was not set up on the layer's device. */
+int layer_decode_noalloc(layer_t layer, const float* x, const int32_t* pos, const int32_t* ctx_lens,
+                         int32_t max_ctx, const float* attn_mask, int32_t B,
+                         void* k_cache, void* v_cache, float* y, void* stream);
+size_t layer_decode_noalloc_max_bytes(void);
+
 /* ---- layer stacks (Sec. 4.5, runtime orchestration) ---------------------- */
 
 /* A stack of n_layers layers of one model run back to back on one stream:

@@ -89,6 +89,8 @@ _SIG = {
     "layer_prefill_chunked_workspace_size": (ctypes.c_size_t, [_P, _I, _I]),
     "layer_prefill_chunked": (ctypes.c_int, [_P, _P, _P, _I, _I, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "layer_decode": (ctypes.c_int, [_P, _P, _P, _P, _I, _P, _I, _P, _P, _P, _P, ctypes.c_size_t, _P]),
+    "layer_decode_noalloc": (ctypes.c_int, [_P, _P, _P, _P, _I, _P, _I, _P, _P, _P, _P]),
+    "layer_decode_noalloc_max_bytes": (ctypes.c_size_t, []),
     "kv_append": (ctypes.c_int, [ctypes.POINTER(kv_desc), _P, _P, _P, _P, _I, _I, _P, _P]),
     "layer_debug_dequant": (ctypes.c_int, [_P, _I, _P, _P]),
     "layer_set_decode_path": (ctypes.c_int, [_P, _I]),
@@ -234,6 +236,15 @@ def layer_decode(handle, x, pos, ctx_lens, max_ctx, attn_mask, B, k_cache, v_cac
                  stream=None) -> int:
     return _lib.layer_decode(handle, _ptr(x), _ptr(pos), _ptr(ctx_lens), max_ctx, _ptr(attn_mask), B,
                              _ptr(k_cache), _ptr(v_cache), _ptr(y), _ptr(ws), ws_bytes, _stream(stream))
+
+
+def layer_decode_noalloc(handle, x, pos, ctx_lens, max_ctx, attn_mask, B, k_cache, v_cache, y, stream=None) -> int:
+    return _lib.layer_decode_noalloc(handle, _ptr(x), _ptr(pos), _ptr(ctx_lens), max_ctx, _ptr(attn_mask), B,
+                                     _ptr(k_cache), _ptr(v_cache), _ptr(y), _stream(stream))
+
+
+def layer_decode_noalloc_max_bytes() -> int:
+    return _lib.layer_decode_noalloc_max_bytes()
 
 
 def _ptr_array(handles):

@@ -152,6 +152,17 @@ struct Profiler {          // one timed kernel per stage
     }
 };
 
+// Scratch memory of layer_decode_noalloc: a file-scope device array that each
+// device holds from the library's first layer_create on it until the process
+// ends.  Host code never passes the array's name to a kernel (on the host it
+// names a stand-in, not device memory); it uses the device address that
+// hipGetSymbolAddress returned for the current device.
+constexpr size_t kScratchBytes = (size_t)32 << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch[kMaxDevices] = {};
+
 constexpr int kMaxBlocks = 1024;                    // persistent decode blocks (one per CU)
 constexpr int kSpinDefault = 1 << 20;               // polls per thread per persistent launch
 constexpr int kStampWords = 8 + 32 * kMaxBlocks;
@@ -255,6 +266,21 @@ int check_device() {
     if (std::strncmp(prop.gcnArchName, "gfx950", 6) != 0)
         return fail(W4_EUNSUPPORTED, "device %d is %s, this library is built for gfx950", dev, prop.gcnArchName);
     return 0;
+}
+
+// Device address of `scratch` on the current device, looked up once per
+// device (with that device current) and kept.
+int scratch_setup() {
+    int dev = 0;
+    HIP_TRY(hipGetDevice(&dev));
+    if (dev < 0 || dev >= kMaxDevices) return fail(W4_EUNSUPPORTED, "device index %d above %d", dev, kMaxDevices - 1);
+    std::lock_guard<std::mutex> g(g_scratch_mu);
+    if (g_scratch[dev]) return W4_OK;
+    void* p = nullptr;
+    HIP_TRY(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    if (!p) return fail(W4_EHIP, "no device address for the scratch array");
+    g_scratch[dev] = p;
+    return W4_OK;
 }
 
 // ---- workspace plan
@@ -822,6 +848,7 @@ int layer_create(const layer_config* cfg, const layer_weights_host* w, layer_t* 
         if (!lins[i]->qweight || !lins[i]->scales) return fail(W4_EINVAL, "null weight pointer (linear %d)", i);
     if (!w->attn_norm || !w->mlp_norm) return fail(W4_EINVAL, "null norm weight");
     if ((rc = check_device())) return rc;
+    if ((rc = scratch_setup())) return rc;
     const bool zq = w->q.zeros || w->k.zeros || w->v.zeros || w->o.zeros || w->gate.zeros || w->up.zeros || w->down.zeros;
     if (zq && !(w->q.zeros && w->k.zeros && w->v.zeros && w->o.zeros && w->gate.zeros && w->up.zeros && w->down.zeros))
         return fail(W4_EINVAL, "zero points must be given for all seven linears or for none");
@@ -1005,6 +1032,25 @@ int layer_decode(layer_t L, const float* x, const int32_t* pos, const int32_t* c
     if ((rc = decode_check(L, B, max_ctx))) return rc;
     return decode_run(L, x, pos, ctx_lens, max_ctx, attn_mask, B, kc, vc, y, ws, ws_bytes, (hipStream_t)stream, 2);
 }
+
+int layer_decode_noalloc(layer_t L, const float* x, const int32_t* pos, const int32_t* ctx_lens, int32_t max_ctx,
+                         const float* attn_mask, int32_t B, void* kc, void* vc, float* y, void* stream) {
+    if (!L) return fail(W4_EINVAL, "null layer");
+    if (!x || !pos || !ctx_lens || !kc || !vc || !y) return fail(W4_EINVAL, "null pointer argument");
+    if ((const void*)x == (const void*)y) return fail(W4_EINVAL, "x and y must not alias");
+    int rc;
+    if ((rc = decode_check(L, B, max_ctx))) return rc;
+    if (L->device < 0 || L->device >= kMaxDevices || !g_scratch[L->device])
+        return fail(W4_EHIP, "scratch array not set up on device %d", L->device);
+    const size_t need = layer_workspace_size(L, 2, B, 1, max_ctx);
+    if (need == 0 || need > kScratchBytes)
+        return fail(W4_EWORKSPACE, "decode of B = %d at context %d needs %zu bytes of scratch; the static scratch "
+                    "array holds %zu", B, max_ctx, need, kScratchBytes);
+    return decode_run(L, x, pos, ctx_lens, max_ctx, attn_mask, B, kc, vc, y, g_scratch[L->device], kScratchBytes,
+                      (hipStream_t)stream, -1);
+}
+
+size_t layer_decode_noalloc_max_bytes(void) { return kScratchBytes; }
 
 int kv_append(const kv_desc* desc, void* kc, void* vc, const void* k_new, const void* v_new, int32_t B, int32_t T,
               const int32_t* slot_start, void* stream) {
