@@ -416,7 +416,7 @@ class LM:
             self.handle = None
 
     def __del__(self):
-        if sys.is_finalizing():
+        if sys is None or sys.is_finalizing():
             return
         try:
             self.close()
@@ -459,7 +459,7 @@ class Layer:
             self.handle = None
 
     def __del__(self):
-        if sys.is_finalizing():
+        if sys is None or sys.is_finalizing():
             return
         try:
             self.close()
