@@ -35,6 +35,11 @@ therefore holds bf16 values.  Everything else (weights after dequantisation,
 scores, softmax, sums, the residual stream h and the output y) is computed in
 fp64 and not rounded.
 
+Weight formats.  Besides the W4 format (4-bit codes, group scales), the
+paper's direct-through modes INT8 (symmetric or asymmetric) and BF16 are
+accepted per linear (``dequant``); the block's arithmetic does not depend on
+the format, only on the fp64 weights it yields.
+
 Pins: every function here is checked by tests/test_oracle_*.py against
 brute-force loops on tiny inputs, closed forms and the stage invariants the
 paper implies; none is "parity unpinned".
@@ -72,14 +77,43 @@ def unpack_int4(qweight, K: int) -> np.ndarray:
     return ((w[k // 8, :] >> shift[:, None]) & np.uint32(0xF)).astype(np.int64)
 
 
-def dequant(lin: dict, group_size: int) -> np.ndarray:
-    """W[k][n] = s[k // G][n] * (q[k][n] - z[k // G][n]) in fp64 (exact).
+def dequant_int8(lin: dict) -> np.ndarray:
+    """W[k][n] = s[n] * (q[k][n] - z[n]) in fp64 (exact) for an INT8 linear.
 
-    The W4A16 matmul carries the weight's quantisation scales (and zero
-    points) alongside the packed codes (Sec. 3.2).  Reading taken: groups
-    run along K, the last group may be shorter, the zero point is 8 unless
-    per-group zero points are supplied.
+    The paper compiles INT8 weights symmetric or asymmetric (Sec. 3.2).
+    Readings taken: one scale per output channel (fp16, ``scales[n]``);
+    symmetric weights hold signed codes -128 .. 127 (``q8`` as int8) with
+    zero point 0; asymmetric weights hold unsigned codes 0 .. 255 (``q8`` as
+    uint8) and a zero point per output channel (``zeros[n]``, 0 .. 255).
     """
+    s = f16_to_f64(lin["scales"]).reshape(-1)
+    if lin.get("zeros") is None:
+        q = np.asarray(lin["q8"]).view(np.int8).astype(F64)
+        return s[None, :] * q
+    q = np.asarray(lin["q8"]).view(np.uint8).astype(F64)
+    z = np.asarray(lin["zeros"], dtype=F64).reshape(-1)
+    return s[None, :] * (q - z[None, :])
+
+
+def dequant(lin: dict, group_size: int) -> np.ndarray:
+    """The fp64 weight W[K][N] of a linear in any of the layer's formats.
+
+    ``format`` "int4" (the default): W[k][n] = s[k // G][n] * (q[k][n] -
+    z[k // G][n]) (exact).  The W4A16 matmul carries the weight's
+    quantisation scales (and zero points) alongside the packed codes
+    (Sec. 3.2).  Reading taken: groups run along K, the last group may be
+    shorter, the zero point is 8 unless per-group zero points are supplied.
+    ``format`` "int8": dequant_int8.  ``format`` "bf16": the unquantised
+    weights of the paper's BF16 mode (Sec. 3.2), bf16 bit patterns
+    ``w16[K][N]`` taken exactly.
+    """
+    fmt = lin.get("format", "int4")
+    if fmt == "int8":
+        return dequant_int8(lin)
+    if fmt == "bf16":
+        return bf16_to_f64(lin["w16"])
+    if fmt != "int4":
+        raise ValueError(f"unknown weight format {fmt!r}")
     K, N = lin["K"], lin["N"]
     q = unpack_int4(lin["qweight"], K)
     g = np.arange(K) // group_size

@@ -16,6 +16,8 @@ paper passes straight through the lowering, Sec. 3.2):
     8r+j in bits 4j .. 4j+3;
   * ``scales[g][n]`` (fp16) is the scale of group g = k // group_size;
   * the zero point is 8 unless a ``zeros[g][n]`` array is given.
+The paper's other direct-through weight modes (Sec. 3.2) are drawn too:
+INT8 symmetric / asymmetric with per-channel scales, and BF16 (make_linear).
 """
 from __future__ import annotations
 
@@ -127,11 +129,39 @@ def pack_int4(q: np.ndarray) -> np.ndarray:
 
 # ---------------------------------------------------------------- draws
 
+WEIGHT_FORMATS = ("int4", "int8", "int8a", "bf16")
+
+
 def make_linear(cfg: LayerConfig, which: str, layer: int = 0,
-                with_zeros: bool = False) -> dict:
-    """Codes uniform in [0, 15], fp16 scales |N(0, 0.02)| / 8, zero point 8."""
+                with_zeros: bool = False, fmt: str = "int4") -> dict:
+    """One linear in weight format ``fmt``:
+
+    * "int4": codes uniform in [0, 15], fp16 scales |N(0, 0.02)| / 8 per
+      group, zero point 8 (or per-group zero points uniform in [0, 15]);
+    * "int8" (symmetric): signed codes uniform in [-128, 127], one fp16 scale
+      |N(0, 0.02)| / 128 per output channel;
+    * "int8a" (asymmetric): unsigned codes uniform in [0, 255], per-channel
+      zero points uniform in [96, 160] and scales as "int8";
+    * "bf16": N(0, 0.01) weights as bf16 bit patterns.
+    The 8-bit and bf16 draws give weights of about the magnitude of the
+    4-bit ones."""
     j = LINEARS.index(which)
     K, N = cfg.linear_shape(which)
+    if fmt in ("int8", "int8a"):
+        s = np.abs(rng_for(cfg.cfg_id, layer, TID_SCALES + j).normal(0.0, 0.02, size=N)) / 128.0
+        g = rng_for(cfg.cfg_id, layer, TID_QVALS + j)
+        if fmt == "int8":
+            q8 = g.integers(-128, 128, size=(K, N), dtype=np.int16).astype(np.int8)
+            zeros = None
+        else:
+            q8 = g.integers(0, 256, size=(K, N), dtype=np.int16).astype(np.uint8)
+            zeros = rng_for(cfg.cfg_id, layer, TID_ZEROS + j).integers(96, 161, size=N, dtype=np.int16).astype(np.uint8)
+        return dict(format="int8", K=K, N=N, q8=q8, scales=s.astype(np.float16), zeros=zeros)
+    if fmt == "bf16":
+        w16 = bf16_bits(rng_for(cfg.cfg_id, layer, TID_QVALS + j).normal(0.0, 0.01, size=(K, N)))
+        return dict(format="bf16", K=K, N=N, w16=w16)
+    if fmt != "int4":
+        raise ValueError(f"unknown weight format {fmt!r}")
     ng = -(-K // cfg.group_size)
     q = rng_for(cfg.cfg_id, layer, TID_QVALS + j).integers(0, 16, size=(K, N), dtype=np.uint8)
     s = (np.abs(rng_for(cfg.cfg_id, layer, TID_SCALES + j).normal(0.0, 0.02, size=(ng, N))) / 8.0)
@@ -142,9 +172,10 @@ def make_linear(cfg: LayerConfig, which: str, layer: int = 0,
     return dict(K=K, N=N, q=q, qweight=pack_int4(q), scales=scales, zeros=zeros)
 
 
-def make_layer(cfg: LayerConfig, layer: int = 0, with_zeros: bool = False) -> dict:
-    """All weights of one decoder layer in the canonical host format."""
-    w = {name: make_linear(cfg, name, layer, with_zeros) for name in LINEARS}
+def make_layer(cfg: LayerConfig, layer: int = 0, with_zeros: bool = False, fmt: str = "int4") -> dict:
+    """All weights of one decoder layer in the canonical host format (every
+    linear in weight format ``fmt``, see make_linear)."""
+    w = {name: make_linear(cfg, name, layer, with_zeros, fmt) for name in LINEARS}
     w["attn_norm"] = bf16_bits(rng_for(cfg.cfg_id, layer, TID_GAMMA1).uniform(0.5, 1.5, cfg.hidden))
     w["mlp_norm"] = bf16_bits(rng_for(cfg.cfg_id, layer, TID_GAMMA2).uniform(0.5, 1.5, cfg.hidden))
     return w
