@@ -73,6 +73,15 @@ extern "C" {
                                    formed                                      */
 #define W4_FLAG_TOKEN_ID     4  /* lm_embed saw a token id outside the vocabulary */
 
+/* ---- weight formats (layer_config.weight_format) -------------------------
+ * The paper compiles W4 group-quantised weights and, besides them, INT8
+ * (symmetric or asymmetric) and BF16 weights straight through (Sec. 3.2).
+ * All seven linears of a layer share the format.                            */
+#define W4_WEIGHTS_INT4 0   /* 4-bit codes, fp16 scales per group of group_size */
+#define W4_WEIGHTS_INT8 1   /* 8-bit codes, one fp16 scale (and, asymmetric,
+                               one zero point) per output column             */
+#define W4_WEIGHTS_BF16 2   /* unquantised bf16 weights                       */
+
 /* ---- types ---------------------------------------------------------------- */
 
 /* Shape of one decoder layer.  Supported: head_dim 64 or 128; n_heads a
@@ -92,19 +101,39 @@ typedef struct layer_config {
     float   rope_base;
     int32_t max_seq;     /* capacity of the KV cache and of the RoPE table */
     int32_t max_batch;   /* largest decode batch                            */
+    int32_t weight_format; /* W4_WEIGHTS_*; 0 (INT4) for zero-initialised
+                              configs.  group_size applies to INT4 only.  */
 } layer_config;
 
-/* One quantised linear y[M][N] = x[M][K] * W[K][N] in the canonical
- * GPTQ-style format that the paper compiles straight through (Sec. 3.2).
- * All pointers are host pointers, read only during layer_create.
+/* One linear y[M][N] = x[M][K] * W[K][N] in a format that the paper
+ * compiles straight through (Sec. 3.2).  All pointers are host pointers,
+ * read only during layer_create; the fields a format does not use are
+ * ignored.
+ * W4_WEIGHTS_INT4 (the canonical GPTQ-style format):
  *   qweight  int32 [K/8][N]: code k = 8r + j of column n in bits 4j..4j+3 of
  *            word [r][n];
  *   scales   fp16 bit patterns [ceil(K/G)][N]: scale of group g = k / G;
- *   zeros    uint8 [ceil(K/G)][N] zero points in 0..15, or NULL for 8. */
+ *   zeros    uint8 [ceil(K/G)][N] zero points in 0..15, or NULL for 8;
+ *   W[k][n] = scales[k/G][n] * (code - zero).
+ * W4_WEIGHTS_INT8 (per output column):
+ *   q8       [K][N] codes: with zeros == NULL (symmetric) signed int8 bytes
+ *            -128..127 and W[k][n] = scales[n] * q8[k][n]; with zeros
+ *            (asymmetric) unsigned bytes 0..255 and
+ *            W[k][n] = scales[n] * (q8[k][n] - zeros[n]);
+ *   scales   fp16 bit patterns [N];
+ *   zeros    uint8 [N] or NULL.
+ * W4_WEIGHTS_BF16:
+ *   w16      bf16 bit patterns [K][N]; every |W| must be finite and below
+ *            4096 (layer_create returns W4_EINVAL otherwise).  Numerics: the
+ *            device holds them as fp16 (the matrix cores' operand type of
+ *            the layer), which is exact for |W| >= 2^-17 and within 2^-24
+ *            below it. */
 typedef struct qlinear_host {
     const int32_t*  qweight;
     const uint16_t* scales;
     const uint8_t*  zeros;
+    const uint8_t*  q8;
+    const uint16_t* w16;
 } qlinear_host;
 
 /* All weights of one layer (host pointers).  K x N of each linear, with
@@ -386,15 +415,17 @@ int kv_append(const kv_desc* desc, void* k_cache, void* v_cache,
 
 /* Dequantise linear `which` (0..6 = q, k, v, o, gate, up, down) from the
  * device copy of the weights into out, fp32 [K][N] device, in the order of
- * the canonical format: out[k][n] = s[k/G][n] * (q[k][n] - z).  Exact (the
- * product fits fp32).  Uses the same unpacking code as the stage kernels.
+ * the canonical format: out[k][n] = s[k/G][n] * (q[k][n] - z) (INT4),
+ * s[n] * (q[k][n] - z[n]) (INT8), exact (the product fits fp32); for BF16
+ * layers the fp16 value the device holds.  Uses the same unpacking code as
+ * the stage kernels.
  * Errors: W4_EINVAL, W4_EHIP. */
 int layer_debug_dequant(layer_t layer, int32_t which, float* out, void* stream);
 
 /* Decode implementation (tuning / testing): 0 automatic (default), 1 a
  * sequence of kernels, 2 one persistent launch with one block per CU (B <=
- * 4, no zero points, groups of 64 or more, and the on-chip working set must
- * fit; chosen automatically for B <= 2).  Both compute the same result up to
+ * 4, INT4 weights without zero points in groups of 64 or more, and the
+ * on-chip working set must fit; chosen automatically for B <= 2).  Both compute the same result up to
  * rounding order; the persistent path is deterministic, the kernel sequence
  * adds k-split partials with atomics.  With 2, a decode call the persistent
  * path cannot serve fails with W4_EUNSUPPORTED.  The decode kernels also

@@ -26,6 +26,8 @@ HEADER = os.path.join(os.path.dirname(HERE), "include", "w4layer.h")
 
 W4_OK, W4_EINVAL, W4_EUNSUPPORTED, W4_ECAPACITY, W4_EWORKSPACE, W4_EHIP = 0, -1, -2, -3, -4, -5
 W4_FLAG_WAIT_TIMEOUT, W4_FLAG_F16_RANGE, W4_FLAG_TOKEN_ID = 1, 2, 4
+W4_WEIGHTS_INT4, W4_WEIGHTS_INT8, W4_WEIGHTS_BF16 = 0, 1, 2
+WEIGHT_FORMAT_CODE = {"int4": W4_WEIGHTS_INT4, "int8": W4_WEIGHTS_INT8, "bf16": W4_WEIGHTS_BF16}
 STAGE_PREFILL, STAGE_PREFILL_KV, STAGE_DECODE = 0, 1, 2
 LINEAR_INDEX = {"q": 0, "k": 1, "v": 2, "o": 3, "gate": 4, "up": 5, "down": 6}
 
@@ -50,11 +52,12 @@ class layer_config(ctypes.Structure):
     _fields_ = [("hidden", ctypes.c_int32), ("n_heads", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32),
                 ("head_dim", ctypes.c_int32), ("ffn", ctypes.c_int32), ("group_size", ctypes.c_int32),
                 ("rms_eps", ctypes.c_float), ("rope_base", ctypes.c_float),
-                ("max_seq", ctypes.c_int32), ("max_batch", ctypes.c_int32)]
+                ("max_seq", ctypes.c_int32), ("max_batch", ctypes.c_int32), ("weight_format", ctypes.c_int32)]
 
 
 class qlinear_host(ctypes.Structure):
-    _fields_ = [("qweight", ctypes.c_void_p), ("scales", ctypes.c_void_p), ("zeros", ctypes.c_void_p)]
+    _fields_ = [("qweight", ctypes.c_void_p), ("scales", ctypes.c_void_p), ("zeros", ctypes.c_void_p),
+                ("q8", ctypes.c_void_p), ("w16", ctypes.c_void_p)]
 
 
 class layer_weights_host(ctypes.Structure):
@@ -145,10 +148,10 @@ def check(rc: int) -> int:
     return rc
 
 
-def make_config(cfg) -> layer_config:
+def make_config(cfg, weight_format: int = W4_WEIGHTS_INT4) -> layer_config:
     """layer_config from any object with the LayerConfig attribute names."""
     return layer_config(cfg.hidden, cfg.n_heads, cfg.n_kv_heads, cfg.head_dim, cfg.ffn, cfg.group_size,
-                        cfg.rms_eps, cfg.rope_base, cfg.max_seq, cfg.max_batch)
+                        cfg.rms_eps, cfg.rope_base, cfg.max_seq, cfg.max_batch, weight_format)
 
 
 def _ptr(t) -> Optional[int]:
@@ -173,9 +176,13 @@ def _stream(stream) -> Optional[int]:
 # ------------------------------------------------------------ C-named calls
 
 def layer_create(cfg, weights: dict):
-    """weights: the canonical host format (numpy arrays): for each linear a
-    dict with qweight int32 [K/8][N], scales fp16 [ceil(K/G)][N], optional
-    zeros uint8; attn_norm / mlp_norm bf16 bit patterns (uint16)."""
+    """weights: the host format of qlinear_host (numpy arrays): for each
+    linear a dict with "format" ("int4" when absent, "int8" or "bf16"; all
+    seven alike) and, for int4, qweight int32 [K/8][N], scales fp16
+    [ceil(K/G)][N], optional zeros uint8; for int8, q8 [K][N] (int8 codes, or
+    uint8 codes with per-column zeros uint8 [N]) and scales fp16 [N]; for
+    bf16, w16 bf16 bit patterns [K][N]; attn_norm / mlp_norm bf16 bit
+    patterns (uint16)."""
     keep = []
 
     def arr(a, dtype):
@@ -188,12 +195,22 @@ def layer_create(cfg, weights: dict):
     wh = layer_weights_host()
     wh.attn_norm = arr(weights["attn_norm"], np.uint16)
     wh.mlp_norm = arr(weights["mlp_norm"], np.uint16)
+    fmts = {weights[n].get("format", "int4") for n in ("q", "k", "v", "o", "gate", "up", "down")}
+    if len(fmts) != 1:
+        raise ValueError(f"the seven linears of a layer share one weight format, got {sorted(fmts)}")
+    fmt = fmts.pop()
     for name in ("q", "k", "v", "o", "gate", "up", "down"):
         lin = weights[name]
         z = lin.get("zeros")
-        setattr(wh, name, qlinear_host(arr(lin["qweight"], np.int32), arr(lin["scales"], np.uint16),
-                                       None if z is None else arr(z, np.uint8)))
-    c = make_config(cfg)
+        zp = None if z is None else arr(z, np.uint8)
+        if fmt == "int4":
+            ql = qlinear_host(arr(lin["qweight"], np.int32), arr(lin["scales"], np.uint16), zp, None, None)
+        elif fmt == "int8":
+            ql = qlinear_host(None, arr(lin["scales"], np.uint16), zp, arr(lin["q8"], np.uint8), None)
+        else:
+            ql = qlinear_host(None, None, None, None, arr(lin["w16"], np.uint16))
+        setattr(wh, name, ql)
+    c = make_config(cfg, WEIGHT_FORMAT_CODE[fmt])
     h = _P()
     rc = _lib.layer_create(ctypes.byref(c), ctypes.byref(wh), ctypes.byref(h))
     return rc, h.value

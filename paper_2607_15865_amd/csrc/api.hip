@@ -56,6 +56,9 @@ struct HostLin {
     const uint16_t* sc;
     const uint8_t* z;
     int K, N;
+    int fmt = W4_WEIGHTS_INT4;
+    const uint8_t* q8 = nullptr;
+    const uint16_t* w16 = nullptr;
 };
 
 struct ColSrc {        // where a device column comes from
@@ -133,6 +136,102 @@ void repack_cols(const std::vector<ColSrc>& cols, int K_pad, int G, bool has_zer
     }
 }
 
+// fp16 bits of a double (round to nearest even, subnormals; the caller keeps
+// |v| within the finite range).
+uint16_t f16_bits(double v) {
+    uint16_t sign = std::signbit(v) ? 0x8000u : 0u;
+    double a = std::fabs(v);
+    if (a == 0.0) return sign;
+    int e;
+    std::frexp(a, &e);                     // a = m 2^e, 0.5 <= m < 1
+    const int ex = std::max(e - 1, -14);   // fp16 exponent (subnormals at -14)
+    const double q = std::nearbyint(std::ldexp(a, 10 - ex));   // significand on the 2^(ex-10) grid
+    const double r = std::ldexp(q, ex - 10);
+    if (r == 0.0) return sign;             // below half the smallest subnormal
+    if (r >= 65536.0) return sign | 0x7C00u;
+    // encode r exactly
+    int e2;
+    std::frexp(r, &e2);
+    const int ex2 = e2 - 1;
+    if (ex2 < -14) return sign | (uint16_t)std::ldexp(r, 24);                       // subnormal
+    const uint16_t mant = (uint16_t)(std::ldexp(r, 10 - ex2) - 1024.0);
+    return sign | (uint16_t)((ex2 + 15) << 10) | mant;
+}
+
+inline double bf16_value(uint16_t b) {
+    uint32_t u = (uint32_t)b << 16;
+    float f;
+    std::memcpy(&f, &u, 4);
+    return (double)f;
+}
+
+// Repack columns [c0, c1) of an INT8 (wf 1) or F16 (wf 2) device linear
+// (tile layouts of WeightFormat): INT8 codes as unsigned bytes (symmetric
+// ones + 128) with the column's scale and zero point in every group of 128;
+// F16 values from the bf16 weights, those at k % 8 in {2, 3, 6, 7} times 16.
+void repack_cols_x(const std::vector<ColSrc>& cols, int K_pad, int wf, Repacked& R, int c0, int c1) {
+    const int KG = K_pad / 128, KB = K_pad / 64;
+    const size_t N_dev = cols.size();
+    const size_t tile_words = wf == 1 ? 512 : 1024;
+    for (int nd = c0; nd < c1; nd++) {
+        const ColSrc& cs = cols[nd];
+        const HostLin* L = cs.lin;
+        uint16_t sc = 0x3C00;
+        uint8_t z = 128;
+        bool dead = L == nullptr;
+        if (wf == 1 && L) {
+            sc = L->sc[cs.n];
+            if (L->z) z = L->z[cs.n];
+            dead = f16_is_zero(sc);
+            if (dead) sc = 0x3C00;            // a zero column: codes at the zero point
+        }
+        const int nb = nd / 32, cc = nd % 32;
+        for (int kb = 0; kb < KB; kb++) {
+            uint32_t* tile = R.qw.data() + ((size_t)nb * KB + kb) * tile_words;
+            for (int hh = 0; hh < 2; hh++)
+                for (int si = 0; si < 4; si++) {
+                    const int k0 = kb * 64 + si * 16 + hh * 8, lane = hh * 32 + cc;
+                    if (wf == 1) {
+                        uint32_t wd[2] = {0, 0};
+                        for (int j = 0; j < 8; j++) {
+                            const int k = k0 + j;
+                            uint8_t u = z;
+                            if (!dead && k < L->K) {
+                                const uint8_t b = L->q8[(size_t)k * L->N + cs.n];
+                                u = L->z ? b : (uint8_t)(b ^ 0x80u);
+                            }
+                            wd[j / 4] |= (uint32_t)u << (8 * (j % 4));
+                        }
+                        const size_t o = ((size_t)(si / 2) * 64 + lane) * 4 + 2 * (si % 2);
+                        tile[o] = wd[0];
+                        tile[o + 1] = wd[1];
+                    } else {
+                        for (int pq = 0; pq < 4; pq++) {
+                            uint32_t wd = 0;
+                            for (int e = 0; e < 2; e++) {
+                                const int k = k0 + 2 * pq + e;
+                                double v = 0.0;
+                                if (L && k < L->K) v = bf16_value(L->w16[(size_t)k * L->N + cs.n]);
+                                if ((pq & 1) == 1) v *= 16.0;
+                                wd |= (uint32_t)f16_bits(v) << (16 * e);
+                            }
+                            tile[((size_t)si * 64 + lane) * 4 + pq] = wd;
+                        }
+                    }
+                }
+        }
+        for (int g = 0; g < KG; g++) {
+            const size_t gi = (size_t)g * N_dev + nd;
+            R.scales[gi] = sc;
+            R.ratios[gi] = 1.0f;
+            if (wf == 1) {
+                R.zeros[gi] = z;
+                R.sz[gi] = (uint32_t)sc | ((uint32_t)z << 16);
+            }
+        }
+    }
+}
+
 }  // namespace
 
 struct DevLinearOwned {
@@ -195,11 +294,17 @@ int upload(DevBuf& b, const void* src, size_t bytes) {
     return 0;
 }
 
-int build_linear(DevLinearOwned& out, const std::vector<ColSrc>& cols, int K, int K_pad, int G, bool has_zeros) {
+int build_linear(DevLinearOwned& out, const std::vector<ColSrc>& cols, int K, int K_pad, int G, bool has_zeros,
+                 int fmt = W4_WEIGHTS_INT4) {
     const int N_dev = (int)cols.size();
+    const int wf = fmt == W4_WEIGHTS_INT8 ? WF_INT8 : fmt == W4_WEIGHTS_BF16 ? WF_F16 : WF_INT4;
+    if (wf != WF_INT4) {
+        G = 128;
+        has_zeros = wf == WF_INT8;
+    }
     const int KG = K_pad / G;
     Repacked R;
-    R.qw.resize((size_t)N_dev * K_pad / 8);
+    R.qw.resize((size_t)N_dev * K_pad / 8 << wf);
     R.scales.resize((size_t)N_dev * KG);
     R.ratios.resize((size_t)N_dev * KG);
     if (has_zeros) {
@@ -212,7 +317,8 @@ int build_linear(DevLinearOwned& out, const std::vector<ColSrc>& cols, int K, in
     for (int i = 0; i < nth; i++) {
         const int c0 = i * per, c1 = std::min(N_dev, (i + 1) * per);
         if (c0 >= c1) break;
-        th.emplace_back(repack_cols, std::cref(cols), K_pad, G, has_zeros, std::ref(R), c0, c1);
+        if (wf == WF_INT4) th.emplace_back(repack_cols, std::cref(cols), K_pad, G, has_zeros, std::ref(R), c0, c1);
+        else th.emplace_back(repack_cols_x, std::cref(cols), K_pad, wf, std::ref(R), c0, c1);
     }
     for (auto& t : th) t.join();
     int rc;
@@ -234,6 +340,7 @@ int build_linear(DevLinearOwned& out, const std::vector<ColSrc>& cols, int K, in
     d.KG = KG;
     d.lgG = 0;
     while ((1 << d.lgG) < G) d.lgG++;
+    d.wf = wf;
     return 0;
 }
 
@@ -246,7 +353,10 @@ int validate_config(const layer_config* c) {
     if (c->head_dim != 64 && c->head_dim != 128) return fail(W4_EUNSUPPORTED, "head_dim must be 64 or 128");
     if (c->n_heads % c->n_kv_heads) return fail(W4_EUNSUPPORTED, "n_heads must be a multiple of n_kv_heads");
     if (c->n_heads / c->n_kv_heads > 8) return fail(W4_EUNSUPPORTED, "at most 8 query heads per kv head");
-    const int G = c->group_size;
+    if (c->weight_format < W4_WEIGHTS_INT4 || c->weight_format > W4_WEIGHTS_BF16)
+        return fail(W4_EINVAL, "unknown weight_format %d", c->weight_format);
+    // (the 8- and 16-bit formats keep one scale per column in groups of 128)
+    const int G = c->weight_format == W4_WEIGHTS_INT4 ? c->group_size : 128;
     if (G != 32 && G != 64 && G != 128 && G != 256) return fail(W4_EUNSUPPORTED, "group_size must be 32, 64, 128 or 256");
     const int KP = std::max(64, G);
     if (c->hidden % 128 || c->hidden % KP) return fail(W4_EUNSUPPORTED, "hidden must be a multiple of 128 and of group_size");
@@ -363,6 +473,7 @@ FusedPlan plan_fused(const layer_s* L, int B, int max_ctx, bool query_device) {
     FusedPlan p;
     const layer_config& c = L->cfg;
     if (B > 4 || L->decode_path == 1) return p;
+    if (L->qkv.d.wf != WF_INT4) return p;                                    // 8- and 16-bit weights: separate kernels
     if (L->qkv.d.sz || L->o.d.sz || L->gu.d.sz || L->down.d.sz) return p;   // zero points: separate kernels
     if (c.group_size < 64) return p;                                         // groups of 32: separate kernels
     const int d = c.head_dim, qd = c.n_heads * d, H = c.hidden, r = c.n_heads / c.n_kv_heads;
@@ -844,8 +955,13 @@ int layer_create(const layer_config* cfg, const layer_weights_host* w, layer_t* 
     if ((rc = validate_config(cfg))) return rc;
     if (!w || !out) return fail(W4_EINVAL, "null argument");
     const qlinear_host* lins[7] = {&w->q, &w->k, &w->v, &w->o, &w->gate, &w->up, &w->down};
-    for (int i = 0; i < 7; i++)
-        if (!lins[i]->qweight || !lins[i]->scales) return fail(W4_EINVAL, "null weight pointer (linear %d)", i);
+    const int fmt = cfg->weight_format;
+    for (int i = 0; i < 7; i++) {
+        const qlinear_host& q = *lins[i];
+        const bool ok = fmt == W4_WEIGHTS_INT4 ? (q.qweight && q.scales)
+                        : fmt == W4_WEIGHTS_INT8 ? (q.q8 && q.scales) : q.w16 != nullptr;
+        if (!ok) return fail(W4_EINVAL, "null weight pointer (linear %d)", i);
+    }
     if (!w->attn_norm || !w->mlp_norm) return fail(W4_EINVAL, "null norm weight");
     if ((rc = check_device())) return rc;
     if ((rc = scratch_setup())) return rc;
@@ -854,26 +970,44 @@ int layer_create(const layer_config* cfg, const layer_weights_host* w, layer_t* 
         return fail(W4_EINVAL, "zero points must be given for all seven linears or for none");
 
     const layer_config& c = *cfg;
-    const int H = c.hidden, d = c.head_dim, nq = c.n_heads, nkv = c.n_kv_heads, F = c.ffn, G = c.group_size;
+    const int H = c.hidden, d = c.head_dim, nq = c.n_heads, nkv = c.n_kv_heads, F = c.ffn;
+    const int G = fmt == W4_WEIGHTS_INT4 ? c.group_size : 128;   // (8/16-bit: per column, groups of 128 on device)
     const int qd = nq * d, kvd = nkv * d;
     // K of every linear a multiple of 128 (and of G): the prefill GEMM takes
     // its k range in pairs of 64-k tiles
     const int F_pad = round_up(F, std::max(128, G));
 
-    // scales must be finite
+    // scales must be finite; bf16 weights finite and below 4096 in magnitude
+    // (the device holds 16 W in fp16 at half of the k positions)
     auto finite_scales = [&](const qlinear_host& q, int K, int N) {
-        const size_t n = (size_t)((K + G - 1) / G) * N;
+        if (fmt == W4_WEIGHTS_BF16) {
+            const size_t n = (size_t)K * N;
+            for (size_t i = 0; i < n; i++) {
+                const uint16_t b = q.w16[i];
+                if (((b >> 7) & 0xFF) == 0xFF || !(std::fabs(bf16_value(b)) < 4096.0)) return false;
+            }
+            return true;
+        }
+        const size_t n = (size_t)(fmt == W4_WEIGHTS_INT8 ? 1 : (K + G - 1) / G) * N;
         for (size_t i = 0; i < n; i++)
             if (((q.scales[i] >> 10) & 0x1F) == 0x1F) return false;
         return true;
     };
-    HostLin hq{w->q.qweight, w->q.scales, w->q.zeros, H, qd}, hk{w->k.qweight, w->k.scales, w->k.zeros, H, kvd},
-        hv{w->v.qweight, w->v.scales, w->v.zeros, H, kvd}, ho{w->o.qweight, w->o.scales, w->o.zeros, qd, H},
-        hg{w->gate.qweight, w->gate.scales, w->gate.zeros, H, F}, hu{w->up.qweight, w->up.scales, w->up.zeros, H, F},
-        hd{w->down.qweight, w->down.scales, w->down.zeros, F, H};
+    auto host_lin = [&](const qlinear_host& q, int K, int N) {
+        HostLin h{q.qweight, q.scales, q.zeros, K, N};
+        h.fmt = fmt;
+        h.q8 = q.q8;
+        h.w16 = q.w16;
+        return h;
+    };
+    HostLin hq = host_lin(w->q, H, qd), hk = host_lin(w->k, H, kvd), hv = host_lin(w->v, H, kvd),
+            ho = host_lin(w->o, qd, H), hg = host_lin(w->gate, H, F), hu = host_lin(w->up, H, F),
+            hd = host_lin(w->down, F, H);
     const HostLin* all[7] = {&hq, &hk, &hv, &ho, &hg, &hu, &hd};
     for (int i = 0; i < 7; i++)
-        if (!finite_scales(*lins[i], all[i]->K, all[i]->N)) return fail(W4_EINVAL, "non-finite scale in linear %d", i);
+        if (!finite_scales(*lins[i], all[i]->K, all[i]->N))
+            return fail(W4_EINVAL, fmt == W4_WEIGHTS_BF16 ? "bf16 weight not finite or not below 4096 in linear %d"
+                                                           : "non-finite scale in linear %d", i);
 
     layer_s* L = new layer_s();
     L->cfg = c;
@@ -908,8 +1042,8 @@ int layer_create(const layer_config* cfg, const layer_weights_host* w, layer_t* 
             cgu[nd] = ColSrc{nullptr, 0};
         }
     }
-    if ((rc = build_linear(L->qkv, cq, H, H, G, zq)) || (rc = build_linear(L->o, co, qd, qd, G, zq)) ||
-        (rc = build_linear(L->gu, cgu, H, H, G, zq)) || (rc = build_linear(L->down, cd, F, F_pad, G, zq)) ||
+    if ((rc = build_linear(L->qkv, cq, H, H, G, zq, fmt)) || (rc = build_linear(L->o, co, qd, qd, G, zq, fmt)) ||
+        (rc = build_linear(L->gu, cgu, H, H, G, zq, fmt)) || (rc = build_linear(L->down, cd, F, F_pad, G, zq, fmt)) ||
         (rc = upload(L->qkv.colmap_a, mq.data(), mq.size() * 4)) || (rc = upload(L->qkv.colmap_b, mk.data(), mk.size() * 4)) ||
         (rc = upload(L->qkv.colmap_c, mv.data(), mv.size() * 4)) || (rc = upload(L->o.colmap_a, mo.data(), mo.size() * 4)) ||
         (rc = upload(L->gu.colmap_a, mg.data(), mg.size() * 4)) || (rc = upload(L->gu.colmap_b, mu.data(), mu.size() * 4)) ||

@@ -167,6 +167,33 @@ __device__ __forceinline__ f16x8 dequant8(uint32_t w, ZeroOff zo, const DqConst&
 }
 
 
+// INT8 fragment (codes of bytes lo[0..3], hi[0..3] in k order) -> the exact
+// fp16 values (code - zero): v_perm builds the pairs 0x64 | code = 1024 +
+// code, one packed add takes zneg = -(1024 + zero).  Six VALU operations.
+__device__ __forceinline__ f16x8 dequant8_u8(uint32_t lo, uint32_t hi, f16x2 zneg) {
+    const uint32_t m = 0x64646464u;
+    const f16x2 p0 = __builtin_bit_cast(f16x2, __builtin_amdgcn_perm(m, lo, 0x04010400u)) + zneg;
+    const f16x2 p1 = __builtin_bit_cast(f16x2, __builtin_amdgcn_perm(m, lo, 0x04030402u)) + zneg;
+    const f16x2 p2 = __builtin_bit_cast(f16x2, __builtin_amdgcn_perm(m, hi, 0x04010400u)) + zneg;
+    const f16x2 p3 = __builtin_bit_cast(f16x2, __builtin_amdgcn_perm(m, hi, 0x04030402u)) + zneg;
+    f16x8 r;
+    r[0] = p0[0]; r[1] = p0[1]; r[2] = p1[0]; r[3] = p1[1];
+    r[4] = p2[0]; r[5] = p2[1]; r[6] = p3[0]; r[7] = p3[1];
+    return r;
+}
+
+// F16 fragment (four words of fp16 pairs, the pairs at k % 8 in {2, 3} and
+// {6, 7} held times 16) -> the weights (exact: a power-of-two scaling).
+__device__ __forceinline__ f16x8 f16_frag(uint32_t w0, uint32_t w1, uint32_t w2, uint32_t w3) {
+    const f16x2 sixteenth = f16x2{(f16)0.0625f, (f16)0.0625f};
+    const f16x2 p0 = __builtin_bit_cast(f16x2, w0), p2 = __builtin_bit_cast(f16x2, w2);
+    const f16x2 p1 = __builtin_bit_cast(f16x2, w1) * sixteenth, p3 = __builtin_bit_cast(f16x2, w3) * sixteenth;
+    f16x8 r;
+    r[0] = p0[0]; r[1] = p0[1]; r[2] = p1[0]; r[3] = p1[1];
+    r[4] = p2[0]; r[5] = p2[1]; r[6] = p3[0]; r[7] = p3[1];
+    return r;
+}
+
 // Reinterpret a 32-bit word as a bf16 pair.  Always pass a scalar: clang
 // miscompiles __builtin_bit_cast applied directly to an ext_vector element
 // with a loop index (it reads element 0).
@@ -220,6 +247,23 @@ __device__ __forceinline__ float wave_max(float v) {
 
 // ---------------------------------------------------------------- layouts
 
+// Weight formats of a device linear.  Every format cuts the weight into
+// tiles of 64 k x 32 columns, tile (t, kb) at index t * (K_pad / 64) + kb;
+// lane l of a wave stands for column 32 t + l % 32 and k half l / 32, and
+// its fragment s (0..3) holds the 8 values of k = 64 kb + 16 s + 8 (l / 32)
+// + 0..7.
+//   WF_INT4: 1 KB tiles, [lane][4 words]: word s = fragment s, codes 0..15
+//            in the nibble order of dequant8; groups of 2^lgG along k.
+//   WF_INT8: 2 KB tiles, [j][lane][4 words]: half j holds fragments 2 j and
+//            2 j + 1, 8 unsigned byte codes each in k order (words 2 (s % 2)
+//            and 2 (s % 2) + 1 of the half); one scale and zero point per
+//            column, repeated in every group of 128 (symmetric weights hold
+//            code + 128 with zero point 128).
+//   WF_F16:  4 KB tiles, [s][lane][4 words]: fragment s as 8 fp16 values, k
+//            order, those at k % 8 in {2, 3, 6, 7} multiplied by 16 (the
+//            GEMV's activations take them divided by 16); scales 1.
+enum WeightFormat { WF_INT4 = 0, WF_INT8 = 1, WF_F16 = 2 };
+
 struct DevLinear {
     const uint32_t* qw;      // tiles
     const uint16_t* scales;  // fp16 bits [KG][N_dev]
@@ -229,6 +273,7 @@ struct DevLinear {
     int K, N;                // logical
     int K_pad, N_dev, KG;    // padded rows, device columns, groups
     int lgG;                 // log2 of the group size (a power of two)
+    int wf;                  // WeightFormat
 };
 
 // Epilogue kinds shared by the GEMM (prefill) and GEMV (decode).

@@ -90,8 +90,12 @@ __host__ __device__ inline void split_range(int sp, int S, int KB, int& lo, int&
 
 // GT: group size class, 0 = groups of 32 (two per 64-k tile), 1 = groups of
 // 64, 2 = groups of 128 or more (starting only at the first tile of an
-// iteration); ZP: the linear has zero points.
-template <int EPI, int TM, int GT, bool ZP>
+// iteration); ZP: the linear has zero points; WF: weight format
+// (WeightFormat).  The 8- and 16-bit formats differ only in the tile bytes
+// (2 or 4 quads of 16 bytes per lane) and the fragment unpack (dequant8_u8,
+// f16_frag); their scales (one per column, in groups of 128) ride the same
+// ratio scheme (every ratio 1).
+template <int EPI, int TM, int GT, bool ZP, int WF>
 __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2)))
 gemm_w4_kernel(const f16* __restrict__ X, int ldx, DevLinear W, EpiArgs ep, GemmShape gs) {
     constexpr int BM = 32 * TM;
@@ -161,7 +165,9 @@ gemm_w4_kernel(const f16* __restrict__ X, int ldx, DevLinear W, EpiArgs ep, Gemm
     // the deeper loads stay in flight; row tiles of 128 load X straight into
     // LDS one iteration ahead (their registers hold the accumulators).
     constexpr bool XREG = TM < 4;
-    constexpr int P = TM == 1 ? 4 : (TM == 2 && GT != 0) ? 3 : 2;
+    // (the 8- and 16-bit formats hold 2 or 4 times the weight registers per
+    // tile: the shallowest pipeline)
+    constexpr int P = WF != WF_INT4 ? 2 : TM == 1 ? 4 : (TM == 2 && GT != 0) ? 3 : 2;
     constexpr int U = P % 2 == 0 ? P : 2 * P;          // unroll: X stage (mod P) and LDS buffer (mod 2) static
     constexpr int XS = XREG ? P : 1;
     u32x4 xr[XS][XL];
@@ -196,17 +202,21 @@ gemm_w4_kernel(const f16* __restrict__ X, int ldx, DevLinear W, EpiArgs ep, Gemm
     // of their groups.  Loads past the range re-read the range's first tile
     // (never used).
     constexpr int NG = XREG ? P : 2;
+    constexpr int NQ = 1 << WF;                         // 16-byte quads per lane and tile
+    constexpr uint32_t TB = 1024u << WF;                // tile bytes
     const char* const Wb = reinterpret_cast<const char*>(W.qw);
-    const uint32_t woff0 = ((uint32_t)(wave_on ? nt0 : 0) * (uint32_t)KB * 64u + (uint32_t)lane) * 16u;
-    const uint32_t wcol1 = (uint32_t)KB * 1024u;
+    const uint32_t woff0 = (uint32_t)(wave_on ? nt0 : 0) * (uint32_t)KB * TB + (uint32_t)lane * 16u;
+    const uint32_t wcol1 = (uint32_t)KB * TB;
     const char* const Rb = reinterpret_cast<const char*>(W.ratios);
-    u32x4 rw[4 * NG];
+    u32x4 rw[4 * NG][NQ];
     float rr[4 * NG][NH];
     uint32_t rz[4 * NG][NH];
     auto load_w = [&](int q, int kb) __attribute__((always_inline)) {
         const int kk = kb < kb_hi ? kb : kb_lo;
         const int col = (q & 1) ? col1 : col0;
-        rw[q] = *reinterpret_cast<const u32x4*>(Wb + (woff0 + ((q & 1) ? wcol1 : 0u) + (uint32_t)kk * 1024u));
+#pragma unroll
+        for (int j = 0; j < NQ; j++)
+            rw[q][j] = *reinterpret_cast<const u32x4*>(Wb + (woff0 + ((q & 1) ? wcol1 : 0u) + (uint32_t)kk * TB + 1024u * j));
 #pragma unroll
         for (int hh = 0; hh < NH; hh++) {
             const uint32_t gi = (uint32_t)((kk * 64 + 32 * hh) >> W.lgG) * (uint32_t)W.N_dev + (uint32_t)col;
@@ -255,8 +265,16 @@ gemm_w4_kernel(const f16* __restrict__ X, int ldx, DevLinear W, EpiArgs ep, Gemm
 #pragma unroll
             for (int i = 0; i < TM; i++)
                 a[p][i] = *reinterpret_cast<const f16x8*>(As + (uint32_t)i * 8192u + arow + chunk);
-            b[p][0] = dequant8(rw[q][s], zo0, dq);
-            b[p][1] = dequant8(rw[q + 1][s], zo1, dq);
+            if constexpr (WF == WF_INT8) {
+                b[p][0] = dequant8_u8(rw[q][s >> 1][2 * (s & 1)], rw[q][s >> 1][2 * (s & 1) + 1], zo0.even);
+                b[p][1] = dequant8_u8(rw[q + 1][s >> 1][2 * (s & 1)], rw[q + 1][s >> 1][2 * (s & 1) + 1], zo1.even);
+            } else if constexpr (WF == WF_F16) {
+                b[p][0] = f16_frag(rw[q][s][0], rw[q][s][1], rw[q][s][2], rw[q][s][3]);
+                b[p][1] = f16_frag(rw[q + 1][s][0], rw[q + 1][s][1], rw[q + 1][s][2], rw[q + 1][s][3]);
+            } else {
+                b[p][0] = dequant8(rw[q][0][s], zo0, dq);
+                b[p][1] = dequant8(rw[q + 1][0][s], zo1, dq);
+            }
         };
         // After step t, if step t + 1 (step 0 of the next iteration for
         // t = 7) starts a group inside the range, the accumulators take
@@ -518,13 +536,13 @@ gemm_w4_kernel(const f16* __restrict__ X, int ldx, DevLinear W, EpiArgs ep, Gemm
     }
 }
 
-template <int EPI, int TM, int GT, bool ZP>
+template <int EPI, int TM, int GT, bool ZP, int WF = WF_INT4>
 int launch_v(const f16* X, int ldx, const DevLinear& W, const EpiArgs& ep, const GemmShape& gs, hipStream_t stream) {
     const int blocks = gs.nrb * gs.ncb * gs.S;
     const size_t lds = lds_bytes<TM>();
     static LdsLimit lim;
-    if (ensure_lds_limit(lim, (const void*)gemm_w4_kernel<EPI, TM, GT, ZP>, lds)) return -1;
-    hipLaunchKernelGGL((gemm_w4_kernel<EPI, TM, GT, ZP>), dim3(blocks), dim3(256), lds, stream, X, ldx, W, ep, gs);
+    if (ensure_lds_limit(lim, (const void*)gemm_w4_kernel<EPI, TM, GT, ZP, WF>, lds)) return -1;
+    hipLaunchKernelGGL((gemm_w4_kernel<EPI, TM, GT, ZP, WF>), dim3(blocks), dim3(256), lds, stream, X, ldx, W, ep, gs);
     return hipGetLastError() == hipSuccess ? 0 : -1;
 }
 
@@ -535,6 +553,17 @@ int launch_epi(int TM, const f16* X, int ldx, const DevLinear& W, const EpiArgs&
                hipStream_t stream) {
     const bool zp = W.zeros != nullptr;
     const int gt = W.lgG == 5 ? 0 : W.lgG == 6 ? 1 : 2;
+    // 8-bit: zero points, groups of 128 (row tiles of 32 or 64); 16-bit: neither
+    // (row tiles of 32)
+    if (W.wf == WF_INT8) {
+        if (!zp || gt != 2 || TM == 4) return -1;
+        return TM == 2 ? launch_v<EPI, 2, 2, true, WF_INT8>(X, ldx, W, ep, gs, stream)
+                       : launch_v<EPI, 1, 2, true, WF_INT8>(X, ldx, W, ep, gs, stream);
+    }
+    if (W.wf == WF_F16) {
+        if (zp || gt != 2 || TM != 1) return -1;
+        return launch_v<EPI, 1, 2, false, WF_F16>(X, ldx, W, ep, gs, stream);
+    }
     if (!zp && gt == 2) {
         if (TM == 4) return launch_v<EPI, 4, 2, false>(X, ldx, W, ep, gs, stream);
         if (TM == 2) return launch_v<EPI, 2, 2, false>(X, ldx, W, ep, gs, stream);
@@ -569,7 +598,9 @@ int launch_epi(int TM, const f16* X, int ldx, const DevLinear& W, const EpiArgs&
 GemmPlan gemm_w4_plan(int M, const DevLinear& W, int num_cus) {
     GemmPlan p;
     const int ncb = (W.N_dev + BN - 1) / BN, KB = W.K_pad / 64;
-    const int tm_max = (W.zeros || W.lgG == 5) ? 2 : 4;   // the kernel variants that exist
+    // the kernel variants that exist (the 16-bit format's weight registers
+    // leave room for row tiles of 32 only)
+    const int tm_max = W.wf == WF_F16 ? 1 : (W.zeros || W.lgG == 5 || W.wf != WF_INT4) ? 2 : 4;
     auto nrb = [&](int tm) { return (M + 32 * tm - 1) / (32 * tm); };
     p.TM = tm_max;
     while (p.TM > 1 && nrb(p.TM) * ncb * 4 < num_cus * 3) p.TM /= 2;

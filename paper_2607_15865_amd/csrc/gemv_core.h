@@ -50,6 +50,19 @@ __device__ __forceinline__ f16x8 dequant8_raw(uint32_t w, const DqConst& k) {
     return __builtin_bit_cast(f16x8, r);
 }
 
+// INT8 fragment for the GEMV: fp16 pairs 1024 + q at k % 8 in {0, 1, 4, 5}
+// and 16 (1024 + q) at {2, 3, 6, 7} (0x64 | q and 0x74 | q), from the codes
+// of bytes lo[0..3], hi[0..3] in k order: four v_perm.
+__device__ __forceinline__ f16x8 dequant8_u8_raw(uint32_t lo, uint32_t hi) {
+    const uint32_t m = 0x74746464u;
+    u32x4 r;
+    r[0] = __builtin_amdgcn_perm(m, lo, 0x04010400u);
+    r[1] = __builtin_amdgcn_perm(m, lo, 0x06030602u);
+    r[2] = __builtin_amdgcn_perm(m, hi, 0x04010400u);
+    r[3] = __builtin_amdgcn_perm(m, hi, 0x06030602u);
+    return __builtin_bit_cast(f16x8, r);
+}
+
 constexpr int GEMV_ROWS = 8;     // row stride of the correction tables
 
 // Activation rows prepared by gemv_prep, all indexed by the absolute k of the
@@ -119,9 +132,11 @@ __device__ __forceinline__ void gemv_prep(f16* xs, int ldx, float* c64, float2* 
     }
 }
 
-template <int D, bool G32>
+// D tiles of a lane: quad j of tile slot u in w[u][j] (1, 2 or 4 quads
+// for the 4-, 8- and 16-bit formats).
+template <int D, bool G32, int WF = WF_INT4>
 struct TileRing {
-    u32x4 w[D];
+    u32x4 w[D][1 << WF];
     uint32_t sa[D];
     uint32_t sb[G32 ? D : 1];
 };
@@ -134,14 +149,14 @@ struct Run {
 // Wave-uniform position in a run: the tile's byte offset in the tile array,
 // the element offset of its group parameters (group row + column), and kb.
 struct RunCursor {
-    uint32_t woff;     // ((t * KBf + kb) * 1024)
+    uint32_t woff;     // ((t * KBf + kb) * tile bytes (1024 << wf))
     uint32_t grow;     // (kb * 64 >> lgG) * N_dev
     uint32_t gcol;     // t * 32
     int kb;
 
     __device__ __forceinline__ void start(const DevLinear& W, const Run& run) {
         const int KBf = W.K_pad >> 6;
-        woff = (uint32_t)(run.t0 * KBf + run.ka) << 10;
+        woff = (uint32_t)(run.t0 * KBf + run.ka) << (10 + W.wf);
         grow = (uint32_t)((run.ka * 64) >> W.lgG) * (uint32_t)W.N_dev;
         gcol = (uint32_t)run.t0 * 32u;
         kb = run.ka;
@@ -150,12 +165,12 @@ struct RunCursor {
     __device__ __forceinline__ void next(const DevLinear& W, const Run& run) {
         const int KBf = W.K_pad >> 6;
         kb++;
-        woff += 1024u;
+        woff += 1024u << W.wf;
         if (W.lgG < 6) grow += (uint32_t)W.N_dev << (6 - W.lgG);   // groups of 32: two per tile
         else if (((kb * 64) & ((1 << W.lgG) - 1)) == 0) grow += (uint32_t)W.N_dev;
         if (kb == run.kz) {
             kb = run.ka;
-            woff += (uint32_t)(KBf - (run.kz - run.ka)) << 10;
+            woff += (uint32_t)(KBf - (run.kz - run.ka)) << (10 + W.wf);
             grow = (uint32_t)((run.ka * 64) >> W.lgG) * (uint32_t)W.N_dev;
             gcol += 32u;
         }
@@ -163,11 +178,13 @@ struct RunCursor {
 };
 
 // Load the tile at cursor q into slot u.
-template <int D, bool ZP, bool G32>
-__device__ __forceinline__ void ring_load(const DevLinear& W, TileRing<D, G32>& R, int u, const RunCursor& q) {
+template <int D, bool ZP, bool G32, int WF = WF_INT4>
+__device__ __forceinline__ void ring_load(const DevLinear& W, TileRing<D, G32, WF>& R, int u, const RunCursor& q) {
     const int lane = threadIdx.x & 63;
     const uint32_t lo = (uint32_t)lane * 16u;
-    R.w[u] = *reinterpret_cast<const u32x4*>(reinterpret_cast<const char*>(W.qw) + (q.woff + lo));
+#pragma unroll
+    for (int j = 0; j < (1 << WF); j++)
+        R.w[u][j] = *reinterpret_cast<const u32x4*>(reinterpret_cast<const char*>(W.qw) + (q.woff + 1024u * j + lo));
     const uint32_t gi = q.grow + q.gcol + (uint32_t)(lane & 31);
     if (ZP) R.sa[u] = W.sz[gi];
     else R.sa[u] = W.scales[gi];
@@ -184,15 +201,16 @@ __device__ __forceinline__ void ring_load(const DevLinear& W, TileRing<D, G32>& 
 // first tile again (a cache hit): ring slots are written unconditionally, so
 // no slot value has to be merged across branches (that would force a wait
 // for the load).
-template <int D, bool ZP, bool G32>
-__device__ __forceinline__ void ring_prefetch(const DevLinear& W, const Run& run, TileRing<D, G32>& R, RunCursor& q) {
+template <int D, bool ZP, bool G32, int WF = WF_INT4>
+__device__ __forceinline__ void ring_prefetch(const DevLinear& W, const Run& run, TileRing<D, G32, WF>& R,
+                                              RunCursor& q) {
     const int n = run.size();
     RunCursor first;
     first.start(W, run);
     q = first;
 #pragma unroll
     for (int u = 0; u < D; u++) {
-        ring_load<D, ZP, G32>(W, R, u, u < n ? q : first);
+        ring_load<D, ZP, G32, WF>(W, R, u, u < n ? q : first);
         q.next(W, run);
     }
 }
@@ -215,9 +233,17 @@ __device__ __forceinline__ float gzero(uint32_t v) {
 // The walk is rounded up to a multiple of D tiles; the steps past the end do
 // no arithmetic, but every step refills its slot (past the end with the
 // run's first tile) so that no load sits under a branch.
-template <int D, bool ZP, bool G32, typename Emit>
+//
+// The 8- and 16-bit formats (WF) take the same activations x'.  INT8: the B
+// fragment pairs are 0x64 | code = 1024 + q at k % 8 in {0, 1, 4, 5} and
+// 0x74 | code = 16 (1024 + q) at the divided elements, so the product over
+// a 64-k tile is sum x (1024 + q) = sum x (q - z) + (1024 + z) S with S the
+// tile's sum of x (E + 16 O over its two 32-k segments): one correction per
+// output with the column's zero point.  F16: the divided elements' weights
+// are held times 16, so the product is the exact-weight sum (scale 1).
+template <int D, bool ZP, bool G32, typename Emit, int WF = WF_INT4>
 __device__ __forceinline__ void gemv_run(const DevLinear& W, const Run& run, const GemvAct& xa, int B,
-                                         TileRing<D, G32>& R, RunCursor& q, Emit&& emit) {
+                                         TileRing<D, G32, WF>& R, RunCursor& q, Emit&& emit) {
     const int lane = threadIdx.x & 63, h = lane >> 5;
     const DqConst dq = dq_const();
     // A operand of this lane: MFMA row m = lane % 16 (batch row bm, column
@@ -242,8 +268,26 @@ __device__ __forceinline__ void gemv_run(const DevLinear& W, const Run& run, con
                 const f16x8 a2 = *reinterpret_cast<const f16x8*>(xk + 32);
                 const f16x8 a3 = *reinterpret_cast<const f16x8*>(xk + 48);
                 const float sa = gscale(R.sa[u]);
-                f32x4_t acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a0, dequant8_raw(R.w[u][0], dq), zero, 0, 0, 0);
-                acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a1, dequant8_raw(R.w[u][1], dq), acc, 0, 0, 0);
+                if constexpr (WF == WF_INT8) {
+                    f32x4_t acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a0, dequant8_u8_raw(R.w[u][0][0], R.w[u][0][1]), zero, 0, 0, 0);
+                    acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a1, dequant8_u8_raw(R.w[u][0][2], R.w[u][0][3]), acc, 0, 0, 0);
+                    acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a2, dequant8_u8_raw(R.w[u][1][0], R.w[u][1][1]), acc, 0, 0, 0);
+                    acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a3, dequant8_u8_raw(R.w[u][1][2], R.w[u][1][3]), acc, 0, 0, 0);
+                    const float zc = 1024.0f + gzero<true>(R.sa[u]);
+                    const float2* uv = xa.uv32 + (2 * pkb) * GEMV_ROWS + 4 * h;
+                    const float2* uw = uv + GEMV_ROWS;
+#pragma unroll
+                    for (int r = 0; r < 4; r++) out[r] = __builtin_fmaf(sa, acc[r] - zc * (uv[r].y + uw[r].y), out[r]);
+                } else if constexpr (WF == WF_F16) {
+                    f32x4_t acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a0, __builtin_bit_cast(f16x8, R.w[u][0]), zero, 0, 0, 0);
+                    acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a1, __builtin_bit_cast(f16x8, R.w[u][1]), acc, 0, 0, 0);
+                    acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a2, __builtin_bit_cast(f16x8, R.w[u][2]), acc, 0, 0, 0);
+                    acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a3, __builtin_bit_cast(f16x8, R.w[u][3]), acc, 0, 0, 0);
+#pragma unroll
+                    for (int r = 0; r < 4; r++) out[r] += acc[r];
+                } else {
+                f32x4_t acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a0, dequant8_raw(R.w[u][0][0], dq), zero, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a1, dequant8_raw(R.w[u][0][1], dq), acc, 0, 0, 0);
                 if (G32) {
                     // k 0..31 and k 32..63 are two groups
                     const float za = gzero<ZP>(R.sa[u]);
@@ -252,15 +296,15 @@ __device__ __forceinline__ void gemv_run(const DevLinear& W, const Run& run, con
 #pragma unroll
                     for (int r = 0; r < 4; r++)
                         out[r] = __builtin_fmaf(sa, acc[r] - __builtin_fmaf(za, uv[r].y, 1024.0f * uv[r].x), out[r]);
-                    acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a2, dequant8_raw(R.w[u][2], dq), zero, 0, 0, 0);
-                    acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a3, dequant8_raw(R.w[u][3], dq), acc, 0, 0, 0);
+                    acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a2, dequant8_raw(R.w[u][0][2], dq), zero, 0, 0, 0);
+                    acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a3, dequant8_raw(R.w[u][0][3], dq), acc, 0, 0, 0);
                     const float2* uw = uv + GEMV_ROWS;
 #pragma unroll
                     for (int r = 0; r < 4; r++)
                         out[r] = __builtin_fmaf(sb, acc[r] - __builtin_fmaf(zb, uw[r].y, 1024.0f * uw[r].x), out[r]);
                 } else {
-                    acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a2, dequant8_raw(R.w[u][2], dq), acc, 0, 0, 0);
-                    acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a3, dequant8_raw(R.w[u][3], dq), acc, 0, 0, 0);
+                    acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a2, dequant8_raw(R.w[u][0][2], dq), acc, 0, 0, 0);
+                    acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a3, dequant8_raw(R.w[u][0][3], dq), acc, 0, 0, 0);
                     if (ZP) {
                         const float za = gzero<ZP>(R.sa[u]);
                         const float2* uv = xa.uv32 + (2 * pkb) * GEMV_ROWS + 4 * h;
@@ -276,6 +320,7 @@ __device__ __forceinline__ void gemv_run(const DevLinear& W, const Run& run, con
                         for (int r = 0; r < 4; r++) out[r] = __builtin_fmaf(sa, acc[r] - cc[r], out[r]);
                     }
                 }
+                }
                 if (pkb == run.kz - 1) {
                     emit(pt, out);
 #pragma unroll
@@ -287,7 +332,7 @@ __device__ __forceinline__ void gemv_run(const DevLinear& W, const Run& run, con
                 }
             }
             // refill the slot with tile base + u + D (or the first tile)
-            ring_load<D, ZP, G32>(W, R, u, base + u + D < n ? q : first);
+            ring_load<D, ZP, G32, WF>(W, R, u, base + u + D < n ? q : first);
             q.next(W, run);
         }
     }

@@ -1,5 +1,6 @@
 // W4A16 GEMV for the decode stage, one kernel per linear (B <= 8 rows):
-// y[b][n] = sum_k x[b][k] W[k][n].
+// y[b][n] = sum_k x[b][k] W[k][n].  The INT8 and F16 weight formats go
+// through the same kernel with their own fragment unpack (gemv_core.h).
 //
 // Block: 512 threads = 8 waves on a pair of column tiles (64 device columns:
 // a RoPE pair of q/k blocks, a gate/up pair, or two residual tiles) and the
@@ -22,9 +23,11 @@ namespace {
 
 constexpr int NW = 8;            // waves per block
 constexpr int MAXB = 8;
-constexpr int RING = 8;          // tiles in flight per wave
+constexpr int RING = 8;          // 1 KB tiles in flight per wave (the 8- and 16-bit formats' larger
+                                 // tiles: the same bytes in flight)
 
-template <int EPI, bool NORM, bool ZP, bool G32>
+// WF: weight format (WeightFormat); the 8-bit format always has zero points (ZP)
+template <int EPI, bool NORM, bool ZP, bool G32, int WF>
 __global__ void __launch_bounds__(NW * 64) gemv_w4_kernel(GemvArgs a) {
     extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
     const DevLinear& W = a.W;
@@ -51,9 +54,10 @@ __global__ void __launch_bounds__(NW * 64) gemv_w4_kernel(GemvArgs a) {
 
     // this wave's k-tiles of both column tiles
     const Run run{pair * 2, pair * 2 + 2, kb_lo + wave * nkb / NW, kb_lo + (wave + 1) * nkb / NW};
-    TileRing<RING, G32> R;
+    constexpr int RD = RING >> WF;
+    TileRing<RD, G32, WF> R;
     RunCursor q;
-    if (run.ka < run.kz) ring_prefetch<RING, ZP, G32>(W, run, R, q);
+    if (run.ka < run.kz) ring_prefetch<RD, ZP, G32>(W, run, R, q);
 
     // side copy (e.g. residual initialisation of the next accumulation)
     if (a.copy_n > 0) {
@@ -116,7 +120,7 @@ __global__ void __launch_bounds__(NW * 64) gemv_w4_kernel(GemvArgs a) {
     const GemvAct xa{xs - klo, ldx, c64 - kb_lo * GEMV_ROWS, uv32 - 2 * kb_lo * GEMV_ROWS, zero};
     float p0[4] = {0.f, 0.f, 0.f, 0.f}, p1[4] = {0.f, 0.f, 0.f, 0.f};
     if (run.ka < run.kz) {
-        gemv_run<RING, ZP, G32>(W, run, xa, B, R, q, [&](int t, const float (&out)[4]) {
+        gemv_run<RD, ZP, G32>(W, run, xa, B, R, q, [&](int t, const float (&out)[4]) {
             if (t == pair * 2) {
 #pragma unroll
                 for (int r = 0; r < 4; r++) p0[r] = out[r];
@@ -173,7 +177,7 @@ __global__ void __launch_bounds__(NW * 64) gemv_w4_kernel(GemvArgs a) {
     }
 }
 
-template <int EPI, bool NORM, bool ZP, bool G32>
+template <int EPI, bool NORM, bool ZP, bool G32, int WF>
 int launch_t(const GemvArgs& a, hipStream_t stream) {
     const int KB = a.W.K_pad / 64;
     const int kmax = (KB + a.ksplit - 1) / a.ksplit * 64;
@@ -181,18 +185,20 @@ int launch_t(const GemvArgs& a, hipStream_t stream) {
                         (size_t)(kmax / 64) * GEMV_ROWS * ((ZP || G32) ? 20 : 4) + (MAXB + MAXB * 64) * sizeof(float);
     if (smem > 160 * 1024) return -1;
     static LdsLimit lim;
-    if (ensure_lds_limit(lim, (const void*)gemv_w4_kernel<EPI, NORM, ZP, G32>, smem)) return -1;
+    if (ensure_lds_limit(lim, (const void*)gemv_w4_kernel<EPI, NORM, ZP, G32, WF>, smem)) return -1;
     dim3 grid(a.W.N_dev / 64, a.ksplit);
-    hipLaunchKernelGGL((gemv_w4_kernel<EPI, NORM, ZP, G32>), grid, dim3(NW * 64), smem, stream, a);
+    hipLaunchKernelGGL((gemv_w4_kernel<EPI, NORM, ZP, G32, WF>), grid, dim3(NW * 64), smem, stream, a);
     return hipGetLastError() == hipSuccess ? 0 : -1;
 }
 
-template <bool ZP, bool G32>
+template <bool ZP, bool G32, int WF = WF_INT4>
 int launch_zp(int epi, bool norm, const GemvArgs& a, hipStream_t stream) {
-    if (epi == EPI_QKV) return norm ? launch_t<EPI_QKV, true, ZP, G32>(a, stream) : launch_t<EPI_QKV, false, ZP, G32>(a, stream);
+    if (epi == EPI_QKV)
+        return norm ? launch_t<EPI_QKV, true, ZP, G32, WF>(a, stream) : launch_t<EPI_QKV, false, ZP, G32, WF>(a, stream);
     if (epi == EPI_SWIGLU)
-        return norm ? launch_t<EPI_SWIGLU, true, ZP, G32>(a, stream) : launch_t<EPI_SWIGLU, false, ZP, G32>(a, stream);
-    if (epi == EPI_RESID && !norm) return launch_t<EPI_RESID, false, ZP, G32>(a, stream);
+        return norm ? launch_t<EPI_SWIGLU, true, ZP, G32, WF>(a, stream)
+                    : launch_t<EPI_SWIGLU, false, ZP, G32, WF>(a, stream);
+    if (epi == EPI_RESID && !norm) return launch_t<EPI_RESID, false, ZP, G32, WF>(a, stream);
     return -1;
 }
 
@@ -200,6 +206,8 @@ int launch_zp(int epi, bool norm, const GemvArgs& a, hipStream_t stream) {
 
 int launch_gemv_w4(int epi, bool norm, const GemvArgs& a, hipStream_t stream) {
     if (a.B < 1 || a.B > MAXB) return -1;
+    if (a.W.wf == WF_INT8) return a.W.sz ? launch_zp<true, false, WF_INT8>(epi, norm, a, stream) : -1;
+    if (a.W.wf == WF_F16) return launch_zp<false, false, WF_F16>(epi, norm, a, stream);
     const bool g32 = a.W.lgG == 5;
     if (a.W.sz) return g32 ? launch_zp<true, true>(epi, norm, a, stream) : launch_zp<true, false>(epi, norm, a, stream);
     return g32 ? launch_zp<false, true>(epi, norm, a, stream) : launch_zp<false, false>(epi, norm, a, stream);

@@ -84,10 +84,21 @@ __global__ void debug_dequant_kernel(DevLinear W, const int32_t* __restrict__ co
         const int kb = k / 64, kr = k % 64;
         const int s = kr / 16, hh = (kr % 16) / 8, j = kr % 8;
         const int lane = hh * 32 + cc;
-        const uint32_t w = W.qw[(((size_t)nt * KB + kb) * 64 + lane) * 4 + s];
         const int g = k >> W.lgG;
         const size_t gi = (size_t)g * W.N_dev + nd;
-        const f16x8 v8 = dequant8(w, zero_off(W.zeros ? (float)W.zeros[gi] : 8.0f), dq_const());
+        const size_t tile = ((size_t)nt * KB + kb) * (256u << W.wf);      // words
+        f16x8 v8;
+        if (W.wf == WF_INT8) {
+            const uint32_t* w = W.qw + tile + ((size_t)(s / 2) * 64 + lane) * 4 + 2 * (s % 2);
+            const f16 zn = (f16)(-(1024.0f + (float)W.zeros[gi]));
+            v8 = dequant8_u8(w[0], w[1], f16x2{zn, zn});
+        } else if (W.wf == WF_F16) {
+            const uint32_t* w = W.qw + tile + ((size_t)s * 64 + lane) * 4;
+            v8 = f16_frag(w[0], w[1], w[2], w[3]);
+        } else {
+            const uint32_t w = W.qw[tile + (size_t)lane * 4 + s];
+            v8 = dequant8(w, zero_off(W.zeros ? (float)W.zeros[gi] : 8.0f), dq_const());
+        }
         f16 vals[8];
         __builtin_memcpy(vals, &v8, sizeof vals);
         const float qz = (float)vals[j];

@@ -115,3 +115,37 @@ def test_lm_validation_before_any_hip_call():
     assert B.lm_head_workspace_size(None, 1) == 0
     assert B.lm_error(None)[0] == B.W4_EINVAL
     assert B.lm_destroy(None) == B.W4_EINVAL
+
+
+def test_layer_create_weight_format_checks_before_any_hip_call():
+    """An unknown weight format, and a format whose weight pointers are
+    missing, are rejected on the host (no device needed)."""
+    import ctypes
+    cfg = synth.CONFIGS["tiny"]
+    for fmt, code in ((7, B.W4_EINVAL), (-1, B.W4_EINVAL)):
+        c = B.make_config(cfg, fmt)
+        wh = B.layer_weights_host()
+        h = ctypes.c_void_p()
+        assert B._lib.layer_create(ctypes.byref(c), ctypes.byref(wh), ctypes.byref(h)) == code
+        assert not h.value
+    w8 = synth.make_layer(cfg, fmt="int8")
+    for fmt in (B.W4_WEIGHTS_INT8, B.W4_WEIGHTS_BF16):
+        c = B.make_config(cfg, fmt)
+        wh = B.layer_weights_host()
+        keep = []
+        for name in synth.LINEARS:          # only the INT4 fields set: the format's own are missing
+            q = np.zeros((cfg.linear_shape(name)[0] // 8, cfg.linear_shape(name)[1]), np.int32)
+            s = np.ascontiguousarray(w8[name]["scales"]).view(np.uint16)
+            keep += [q, s]
+            setattr(wh, name, B.qlinear_host(q.ctypes.data, s.ctypes.data, None, None, None))
+        h = ctypes.c_void_p()
+        assert B._lib.layer_create(ctypes.byref(c), ctypes.byref(wh), ctypes.byref(h)) == B.W4_EINVAL
+        assert "null weight pointer" in B.layer_last_error()
+
+
+def test_binding_rejects_mixed_formats():
+    cfg = synth.CONFIGS["tiny"]
+    w = synth.make_layer(cfg, fmt="int8")
+    w["down"] = synth.make_linear(cfg, "down", fmt="bf16")
+    with pytest.raises(ValueError):
+        B.layer_create(cfg, w)
