@@ -101,12 +101,20 @@ def linear_shapes(cfg):
     return [cfg.linear_shape(n) for n in synth.LINEARS]
 
 
-def weight_bytes(cfg, names=None):
+def weight_bytes(cfg, names=None, fmt="int4"):
+    """Bytes of the linears' weights in a storage format: int4 codes + fp16
+    group scales; int8 codes + one fp16 scale (and, "int8a", one zero point)
+    per column; bf16 values."""
     from paper_2607_15865_amd import synth
     tot = 0
     for n in (names or synth.LINEARS):
         K, N = cfg.linear_shape(n)
-        tot += N * K // 2 + 2 * N * math.ceil(K / cfg.group_size)
+        if fmt == "int4":
+            tot += N * K // 2 + 2 * N * math.ceil(K / cfg.group_size)
+        elif fmt in ("int8", "int8a"):
+            tot += N * K + 2 * N + (N if fmt == "int8a" else 0)
+        else:
+            tot += 2 * N * K
     return tot
 
 
@@ -117,11 +125,12 @@ def stage_flops(cfg, M, T, L, B):
     return 2 * M * params + attn
 
 
-def stage_bytes(cfg, M, T, L, B):
-    """Weights (int4 + fp16 scales) + norm weights + KV read of the history
-    and the new entries + KV write + fp32 hidden states in and out."""
+def stage_bytes(cfg, M, T, L, B, fmt="int4"):
+    """Weights (int4 + fp16 scales, or the other formats') + norm weights + KV
+    read of the history and the new entries + KV write + fp32 hidden states
+    in and out."""
     kv_row = 2 * 2 * cfg.n_kv_heads * cfg.head_dim          # K and V, bf16
-    return (weight_bytes(cfg) + 4 * cfg.hidden + kv_row * B * (L + T) + kv_row * B * T
+    return (weight_bytes(cfg, fmt=fmt) + 4 * cfg.hidden + kv_row * B * (L + T) + kv_row * B * T
             + 8 * M * cfg.hidden)
 
 
@@ -294,6 +303,94 @@ def reports(binding, synth, stream, reps=20):
                 raise RuntimeError(f"{name}: a device error flag was raised")
             lay.close()
         del caches, ws
+    return out
+
+
+# ---------------------------------------------------------------- weight formats
+
+def formats(binding, synth, stream, reps=20):
+    """The paper's other direct-through weight modes on the Llama-3-8B-shaped
+    layer, timed after the bench steps (outside them): INT8 symmetric, INT8
+    asymmetric (per-column scales) and BF16 weights, each through prefill
+    T = 512, prefill_kv T = 128 over 1024 and decode B = 1 at context 2048
+    (the decode kernel sequence: the persistent launch takes INT4 only).
+    Rotation over 2 device copies (440 MB or 872 MB, beyond the 256 MB
+    last-level cache).  Median of `reps` calls, HIP events on the library's
+    stream; synthetic seeded weights, N(0,1) cache."""
+    import numpy as np
+    import torch
+    sp = stream.cuda_stream
+    cfg = synth.CONFIGS[WORKLOAD["name"]]
+    Tp, Tk, Lk, ctx = WORKLOAD["prefill_T"], WORKLOAD["pkv_T"], WORKLOAD["pkv_L"], WORKLOAD["decode_ctx"]
+
+    def f32(bits):
+        u = bits.astype(np.uint32) << 16
+        return torch.from_numpy(u.view(np.float32).copy()).cuda()
+
+    def median_us(call):
+        ts = []
+        for i in range(reps + 2):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            call(i)
+            e1.record(stream)
+            e1.synchronize()
+            if i >= 2:
+                ts.append(e0.elapsed_time(e1) * 1e3)
+        return float(np.median(ts))
+
+    kb, vb = synth.kv_fill(cfg, 1)
+    xp = f32(synth.activations(cfg, synth.TID_X_PREFILL, Tp))
+    xk = f32(synth.activations(cfg, synth.TID_X_PREFILL_KV, Tk))
+    xd = f32(synth.activations(cfg, synth.TID_X_DECODE, 1))
+    yp, yk, yd = torch.empty_like(xp), torch.empty_like(xk), torch.empty_like(xd)
+    pp = torch.arange(Tp, dtype=torch.int32, device="cuda")
+    pk = torch.arange(Lk, Lk + Tk, dtype=torch.int32, device="cuda")
+    cd = torch.full((1,), ctx, dtype=torch.int32, device="cuda")
+    out = {}
+    for fmt in ("int8", "int8a", "bf16"):
+        log(f"bench: {fmt} weights")
+        w = synth.make_layer(cfg, fmt=fmt)
+        ncp = 2
+        layers = [binding.Layer(cfg, w) for _ in range(ncp)]
+        del w
+        caches = [(torch.from_numpy(kb.view(np.int16)).cuda(), torch.from_numpy(vb.view(np.int16)).cuda())
+                  for _ in range(ncp)]
+        h0 = layers[0].handle
+        ws_bytes = max(binding.layer_workspace_size(h0, 0, 1, Tp, 0), binding.layer_workspace_size(h0, 1, 1, Tk, Lk),
+                       binding.layer_workspace_size(h0, 2, 1, 1, ctx))
+        ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
+
+        def pre(i):
+            k, v = caches[i % ncp]
+            binding.check(binding.layer_prefill(layers[i % ncp].handle, xp, pp, Tp, k, v, yp, ws, ws_bytes, sp))
+
+        def pkv(i):
+            k, v = caches[i % ncp]
+            binding.check(binding.layer_prefill_kv(layers[i % ncp].handle, xk, pk, Tk, Lk, k, v, yk, ws, ws_bytes, sp))
+
+        def dec(i):
+            k, v = caches[i % ncp]
+            binding.check(binding.layer_decode(layers[i % ncp].handle, xd, cd, cd, ctx, None, 1, k, v, yd, ws,
+                                               ws_bytes, sp))
+        res = {"weight_mbytes": round(weight_bytes(cfg, fmt=fmt) / 1e6, 1)}
+        for name, call, M, T, L in (("prefill", pre, Tp, Tp, 0), ("prefill_kv", pkv, Tk, Tk, Lk)):
+            us = median_us(call)
+            fl = stage_flops(cfg, M, T, L, 1)
+            res[name] = {"us": round(us, 2), "tflops": round(fl / (us * 1e-6) / 1e12, 1),
+                         "frac_mfma": round(fl / (us * 1e-6) / 1e12 / PEAK_MFMA_TFLOPS, 4)}
+        us = median_us(dec)
+        by = stage_bytes(cfg, 1, 1, ctx, 1, fmt=fmt)
+        res["decode"] = {"us": round(us, 2), "layer_steps_per_s": round(1e6 / us, 1), "mbytes": round(by / 1e6, 2),
+                         "gbps": round(by / (us * 1e-6) / 1e9, 1),
+                         "frac_hbm": round(by / (us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)}
+        torch.cuda.synchronize()
+        for lay in layers:
+            if lay.error():
+                raise RuntimeError(f"{fmt}: a device error flag was raised")
+            lay.close()
+        del caches, ws, layers
+        out[fmt] = res
     return out
 
 
@@ -532,6 +629,8 @@ def main():
                     help="skip the verification and long-prompt timings done after the steps")
     ap.add_argument("--no-reports", action="store_true",
                     help="skip the other workloads (Qwen-7B- and Qwen-0.5B-shaped layers) timed after the steps")
+    ap.add_argument("--no-formats", action="store_true",
+                    help="skip the INT8 / BF16 weight layers timed after the steps")
     ap.add_argument("--stack", action="store_true",
                     help="instead: the 32-layer stack, 1024-token prefill then 256 decode steps")
     ap.add_argument("--stack-layers", type=int, default=32)
@@ -705,6 +804,8 @@ def main():
         out["extras"] = extras(cfg, layers, caches, binding, synth, stream)
     if not args.no_reports:
         out["reports"] = reports(binding, synth, stream)
+    if not args.no_formats:
+        out["weight_formats"] = formats(binding, synth, stream)
     if not args.no_cpu_baseline:
         log("bench: timing the CPU oracle (one decode layer-step)")
         out["cpu_baseline"] = cpu_baseline(cfg, w)
