@@ -397,31 +397,117 @@ def formats(binding, synth, stream, reps=20):
 # ---------------------------------------------------------------- CPU baseline
 
 def cpu_baseline(cfg, w):
-    """The oracle as it stands, one decode layer-step on this workload."""
+    """The oracle as it stands, timed on this host on a bounded sample of the
+    workload: one decode layer-step (B = 1, context 2048) repeated for about
+    5 s, one prefill of 512 tokens and one prefill_kv of 128 over 1024, in
+    the oracle's fp64 and in its fp32 working precision (oracle.layer.
+    working_precision, timing only).  The weights are dequantised once,
+    outside the timed calls (the oracle's W argument).  Records the host's
+    core count, this process's affinity and the BLAS thread count."""
     import numpy as np
     from oracle import layer as O
     from paper_2607_15865_amd import synth
-    threads = None
+    blas = None
     try:
         import threadpoolctl
         info = threadpoolctl.threadpool_info()
-        threads = max([i.get("num_threads", 1) for i in info] or [1])
+        blas = max([i.get("num_threads", 1) for i in info] or [1])
     except Exception:
         pass
-    ctx = WORKLOAD["decode_ctx"]
+    try:
+        affinity = len(os.sched_getaffinity(0))
+    except Exception:
+        affinity = None
+    Tp, Tk, Lk, ctx = WORKLOAD["prefill_T"], WORKLOAD["pkv_T"], WORKLOAD["pkv_L"], WORKLOAD["decode_ctx"]
     rng = np.random.default_rng(0)
-    kc = O.bf16_to_f64(synth.bf16_bits(rng.standard_normal((1, cfg.n_kv_heads, ctx + 1, cfg.head_dim))))
-    vc = O.bf16_to_f64(synth.bf16_bits(rng.standard_normal((1, cfg.n_kv_heads, ctx + 1, cfg.head_dim))))
-    x = O.bf16_to_f64(synth.activations(cfg, synth.TID_X_DECODE, 1))
-    n, t0 = 0, time.perf_counter()
-    while n == 0 or time.perf_counter() - t0 < 10.0:
-        O.decode(w, cfg, x, [ctx], kc, vc, [ctx])
-        n += 1
-    dt = time.perf_counter() - t0
-    return {"value": n / dt, "unit": "layer-steps/s", "cores": threads or os.cpu_count(),
-            "kind": "oracle",
-            "sample": f"{n} decode layer-steps of the {WORKLOAD['name']}-shaped layer at context {ctx}, B=1, "
-                      f"fp64 numpy including the oracle's per-call weight dequantisation ({dt:.1f} s)"}
+    kb = synth.bf16_bits(rng.standard_normal((1, cfg.n_kv_heads, ctx + 1, cfg.head_dim)))
+    vb = synth.bf16_bits(rng.standard_normal((1, cfg.n_kv_heads, ctx + 1, cfg.head_dim)))
+    xd_b = synth.activations(cfg, synth.TID_X_DECODE, 1)
+    xp_b = synth.activations(cfg, synth.TID_X_PREFILL, Tp)
+    xk_b = synth.activations(cfg, synth.TID_X_PREFILL_KV, Tk)
+    modes = {}
+    for name, dt in (("fp64", np.float64), ("fp32", np.float32)):
+        with O.working_precision(dt):
+            W = O.dequant_layer(w, cfg)
+            kc, vc = O.bf16_to_f64(kb), O.bf16_to_f64(vb)
+            xd, xp, xk = O.bf16_to_f64(xd_b), O.bf16_to_f64(xp_b), O.bf16_to_f64(xk_b)
+            n, t0 = 0, time.perf_counter()
+            while n == 0 or time.perf_counter() - t0 < 5.0:
+                O.decode(w, cfg, xd, [ctx], kc, vc, [ctx], W=W)
+                n += 1
+            dt_d = (time.perf_counter() - t0) / n
+            t0 = time.perf_counter()
+            O.prefill(w, cfg, xp, np.arange(Tp), W=W)
+            dt_p = time.perf_counter() - t0
+            t0 = time.perf_counter()
+            O.prefill_kv(w, cfg, xk, np.arange(Lk, Lk + Tk), kc[0], vc[0], Lk, W=W)
+            dt_k = time.perf_counter() - t0
+        fl_p, fl_k = stage_flops(cfg, Tp, Tp, 0, 1), stage_flops(cfg, Tk, Tk, Lk, 1)
+        modes[name] = {"decode_layer_steps_per_s": round(1.0 / dt_d, 3), "decode_calls": n,
+                       "prefill_s": round(dt_p, 3), "prefill_gflops": round(fl_p / dt_p / 1e9, 1),
+                       "prefill_kv_s": round(dt_k, 3), "prefill_kv_gflops": round(fl_k / dt_k / 1e9, 1)}
+        del W
+    return {"value": modes["fp64"]["decode_layer_steps_per_s"], "unit": "layer-steps/s",
+            "cores": blas or affinity or os.cpu_count(), "kind": "oracle",
+            "sample": f"decode layer-steps of the {WORKLOAD['name']}-shaped layer at context {ctx}, B=1, repeated "
+                      f"for 5 s, fp64 numpy, weights dequantised outside the timing; also one prefill of {Tp} "
+                      f"and one prefill_kv of {Tk} over {Lk}, and the same in the fp32 working precision",
+            "os_cpu_count": os.cpu_count(), "affinity_cpus": affinity, "blas_threads": blas, "modes": modes}
+
+
+# ---------------------------------------------------------------- ceilings
+
+def ceilings(binding, stream, reps=5):
+    """What the device sustains on the two bounding resources, measured with
+    the library's ceiling kernels beside the published peaks: a pure streaming
+    read of 2 GiB (best grid of 1024 / 2048 / 4096 blocks of 256 threads) and a
+    pure fp16 MFMA loop (the GEMV's 16x16x32 and the GEMM's 32x32x16, 2 blocks
+    of 4 waves per CU).  Median of `reps` launches, HIP events."""
+    import numpy as np
+    import torch
+    nbytes = 2 << 30
+    buf = torch.empty(nbytes, dtype=torch.uint8, device="cuda").fill_(7)
+    sink = torch.empty(4096 * 256, dtype=torch.int32, device="cuda")
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+
+    def timed(call):
+        ts = []
+        for _ in range(reps + 1):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            call()
+            e1.record(stream)
+            e1.synchronize()
+            ts.append(e0.elapsed_time(e1) * 1e-3)
+        return float(np.median(ts[1:]))
+
+    best = None
+    for blocks in (1024, 2048, 4096):
+        t = timed(lambda: binding.check(binding.w4_ceiling_read(buf, nbytes, sink, blocks, stream)))
+        gbs = nbytes / t / 1e9
+        if best is None or gbs > best[0]:
+            best = (gbs, blocks)
+    out = {"hbm_read": {"gbps": round(best[0], 1), "frac_of_peak": round(best[0] / PEAK_HBM_GBS, 4),
+                        "bytes": nbytes, "blocks": best[1]}}
+    del buf
+    fsink = torch.empty(2 * cus * 256, dtype=torch.float32, device="cuda")
+    for key, big in (("mfma_f16_16x16x32", False), ("mfma_f16_32x32x16", True)):
+        iters = 20000 if big else 40000
+        rc, fl = binding.w4_ceiling_mfma(fsink, 2 * cus, iters, big, stream)
+        binding.check(rc)
+        t = timed(lambda: binding.check(binding.w4_ceiling_mfma(fsink, 2 * cus, iters, big, stream)[0]))
+        out[key] = {"tflops": round(fl / t / 1e12, 1), "frac_of_peak": round(fl / t / 1e12 / PEAK_MFMA_TFLOPS, 4)}
+    return out
+
+
+# The paper's own decode figures (Table 2, Sec. 5.2): whole-model decode of
+# W4BF16 Qwen3.5 models at 2K context on a Sophgo BM1684X (64 GB/s DDR),
+# bandwidth utilisation = tokens/s x model size / peak bandwidth (Sec. 5.1).
+# Another device and whole models: context for the per-layer figures here,
+# not a baseline.
+PAPER_TABLE2 = [{"model": "Qwen3.5-2B", "size_gb": 1.67, "tokens_per_s": 30.00, "bw_util": 0.780},
+                {"model": "Qwen3.5-4B", "size_gb": 3.00, "tokens_per_s": 16.77, "bw_util": 0.786},
+                {"model": "Qwen3.5-9B", "size_gb": 5.39, "tokens_per_s": 9.84, "bw_util": 0.830}]
 
 
 # ---------------------------------------------------------------- main
@@ -629,6 +715,8 @@ def main():
                     help="skip the verification and long-prompt timings done after the steps")
     ap.add_argument("--no-reports", action="store_true",
                     help="skip the other workloads (Qwen-7B- and Qwen-0.5B-shaped layers) timed after the steps")
+    ap.add_argument("--no-ceilings", action="store_true",
+                    help="skip the streaming-read and MFMA-loop ceiling kernels timed after the steps")
     ap.add_argument("--no-formats", action="store_true",
                     help="skip the INT8 / BF16 weight layers timed after the steps")
     ap.add_argument("--stack", action="store_true",
@@ -806,8 +894,14 @@ def main():
         out["reports"] = reports(binding, synth, stream)
     if not args.no_formats:
         out["weight_formats"] = formats(binding, synth, stream)
+    if not args.no_ceilings:
+        out["ceilings"] = ceilings(binding, stream)
+    out["paper_context"] = {"table2": PAPER_TABLE2,
+                            "note": "Sec. 5.2 Table 2: whole-model W4BF16 decode at 2K context on a Sophgo BM1684X "
+                                    "(64 GB/s DDR), bandwidth utilisation 0.78-0.83 of peak; per-layer decode here "
+                                    "is reported as a fraction of MI355X HBM (stages.decode.frac_hbm)"}
     if not args.no_cpu_baseline:
-        log("bench: timing the CPU oracle (one decode layer-step)")
+        log("bench: timing the CPU oracle (decode, prefill, prefill_kv; fp64 and fp32)")
         out["cpu_baseline"] = cpu_baseline(cfg, w)
     for lay in layers:
         flags |= lay.error()

@@ -498,6 +498,20 @@ int layer_profile_read(layer_t layer, int32_t stage, float* total_ms, int32_t* l
  * bits cleared.  Errors: W4_EINVAL, W4_EHIP. */
 int layer_error(layer_t layer, int32_t* flag);
 
+/* Ceiling kernels (measurement): what the device sustains on the two
+ * resources the stages are bound by (HBM bandwidth for decode, matrix-core
+ * throughput for prefill), to report beside the published peaks.
+ * w4_ceiling_read streams `bytes` (a multiple of 16, buf 16-byte aligned) of
+ * device memory once with 16-byte loads on a grid of `blocks` blocks of 256
+ * threads; sink: device memory for blocks * 256 words (a fold of the data).
+ * w4_ceiling_mfma runs `iters` (even) iterations of 4 independent fp16 MFMAs on
+ * each of 4 waves of `blocks` blocks (big != 0: the GEMM's 32x32x16, else the
+ * GEMV's 16x16x32), operands changing every iteration; sink: device memory
+ * for blocks * 256 floats; *flop: the floating-point operations of the
+ * launch.  Both only enqueue on `stream`.  Errors: W4_EINVAL, W4_EHIP. */
+int w4_ceiling_read(const void* buf, size_t bytes, uint32_t* sink, int32_t blocks, void* stream);
+int w4_ceiling_mfma(float* sink, int32_t blocks, int32_t iters, int32_t big, double* flop, void* stream);
+
 /* Message of the last failed call on this thread ("" if none). */
 const char* layer_last_error(void);
 

@@ -46,9 +46,25 @@ paper implies; none is "parity unpinned".
 """
 from __future__ import annotations
 
+import contextlib
+
 import numpy as np
 
-F64 = np.float64
+F64 = np.float64      # the working precision (fp64; see working_precision)
+
+
+@contextlib.contextmanager
+def working_precision(dtype):
+    """Timing only: run the oracle's arithmetic in ``dtype`` (np.float32 is
+    the fp32 mode timed as a CPU baseline).  Every comparison with the GPU
+    path and every pin uses the default fp64."""
+    global F64
+    old = F64
+    F64 = dtype
+    try:
+        yield
+    finally:
+        F64 = old
 
 
 # ------------------------------------------------------------ storage formats

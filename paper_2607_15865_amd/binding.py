@@ -105,6 +105,8 @@ _SIG = {
     "layer_profile_read": (ctypes.c_int, [_P, _I, ctypes.POINTER(ctypes.c_float), ctypes.POINTER(ctypes.c_int32)]),
     "layer_last_error": (ctypes.c_char_p, []),
     "layer_error": (ctypes.c_int, [_P, ctypes.POINTER(ctypes.c_int32)]),
+    "w4_ceiling_read": (ctypes.c_int, [_P, ctypes.c_size_t, _P, _I, _P]),
+    "w4_ceiling_mfma": (ctypes.c_int, [_P, _I, _I, _I, ctypes.POINTER(ctypes.c_double), _P]),
     "stack_workspace_size": (ctypes.c_size_t, [_P, _I, _I, _I, _I, _I]),
     "stack_prefill": (ctypes.c_int, [_P, _I, _P, _P, _I, _I, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "stack_decode": (ctypes.c_int, [_P, _I, _P, _P, _P, _I, _P, _I, _P, _P, _P, _P, ctypes.c_size_t, _P]),
@@ -296,6 +298,17 @@ def layer_debug_dequant(handle, which, out, stream=None) -> int:
     if isinstance(which, str):
         which = LINEAR_INDEX[which]
     return _lib.layer_debug_dequant(handle, which, _ptr(out), _stream(stream))
+
+
+def w4_ceiling_read(buf, nbytes: int, sink, blocks: int, stream=None) -> int:
+    return _lib.w4_ceiling_read(_ptr(buf), nbytes, _ptr(sink), blocks, _stream(stream))
+
+
+def w4_ceiling_mfma(sink, blocks: int, iters: int, big: bool, stream=None):
+    """Returns (rc, flop of the launch)."""
+    f = ctypes.c_double()
+    rc = _lib.w4_ceiling_mfma(_ptr(sink), blocks, iters, int(big), ctypes.byref(f), _stream(stream))
+    return rc, f.value
 
 
 def layer_error(handle):

@@ -19,7 +19,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "libw4layer.so")
 BUILD_DIR = os.path.join(ROOT, "_build")
-SOURCES = ["api.hip", "gemm_w4.hip", "gemv_w4.hip", "attention.hip", "misc.hip", "decode_fused.hip", "lm.hip"]
+SOURCES = ["api.hip", "gemm_w4.hip", "gemv_w4.hip", "attention.hip", "misc.hip", "decode_fused.hip", "lm.hip", "ceilings.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc" if os.path.exists("/opt/rocm/bin/hipcc") else "hipcc")
 FLAGS = [
