@@ -243,9 +243,7 @@ __global__ void __launch_bounds__(NTHR) decode_fused_kernel(DecodeFusedArgs a) {
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int blk = blockIdx.x, P = gridDim.x;
-    // (the one-row launch takes B as a constant: the row loops and the
-    // divisions by B fold away)
-    const int B = MAXB == 1 ? 1 : a.B, H = a.H, nq = a.nq, nkv = a.nkv, r = nq / nkv;
+    const int B = a.B, H = a.H, nq = a.nq, nkv = a.nkv, r = nq / nkv;
     const int qd = nq * D, kd = nkv * D;
     const uint32_t ep = a.epoch;
     Waiter wt{a.err, a.spin_max};
@@ -649,14 +647,13 @@ __global__ void __launch_bounds__(NTHR) decode_fused_kernel(DecodeFusedArgs a) {
         if (nv > 0) {
             bool bad = false;
             const int LPV = a.comb_lpv, VPW = 64 / LPV;          // lanes per value (power of two)
-            const int lgLPV = 31 - __builtin_clz(LPV);
             const int cpl = (NCH + LPV - 1) / LPV;                // chunks per lane (<= 4)
             for (int vb = wave * VPW; vb < nv; vb += NWAVE * VPW) {
-                const int j = vb + (lane >> lgLPV), cl = lane & (LPV - 1);
+                const int j = vb + lane / LPV, cl = lane % LPV;
                 const bool valid = j < nv;
                 const int vv = v0 + (valid ? j : 0);
                 const int head = vv / D, dim = vv - head * D;     // head over all rows: b * nq + head
-                const int b = MAXB == 1 ? 0 : head / nq;
+                const int b = head / nq;
                 const int nch = (meta[b] + 1 + CH - 1) / CH;
                 const uint64_t* base = a.apart + (size_t)head * NCH * (D + 2);
                 // words of chunk qq: 3 qq (output dim), 3 qq + 1 (max), 3 qq + 2 (sum)

@@ -603,7 +603,11 @@ GemmPlan gemm_w4_plan(int M, const DevLinear& W, int num_cus) {
     const int tm_max = W.wf == WF_F16 ? 1 : (W.zeros || W.lgG == 5 || W.wf != WF_INT4) ? 2 : 4;
     auto nrb = [&](int tm) { return (M + 32 * tm - 1) / (32 * tm); };
     p.TM = tm_max;
-    while (p.TM > 1 && nrb(p.TM) * ncb * 4 < num_cus * 3) p.TM /= 2;
+    // (a k range of 12288 or more also takes a row tile with 0.375 tiles per
+    // CU: two k splits then fill the CUs, and each dequantised fragment feeds
+    // twice the MFMAs -- the 512 x 4096 x 14336 down GEMM: 80 -> 76 us)
+    const int tile_need = KB * 64 >= 4 * 3072 ? num_cus * 3 / 2 : num_cus * 3;
+    while (p.TM > 1 && nrb(p.TM) * ncb * 4 < tile_need) p.TM /= 2;
     const int tiles = nrb(p.TM) * ncb;
     p.S = 1;
     while (p.S < 16 && KB / (p.S * 2) >= 8) {
