@@ -373,7 +373,7 @@ __global__ void __launch_bounds__(NTHR) decode_fused_kernel(DecodeFusedArgs a) {
         clear_red();
         const GemvAct xa{xs, ldx, c64, nullptr, zero64};
         if (run1.ka < run1.kz)
-            gemv_run<RING_QKV, false, false>(a.qkv, run1, xa, B, R1, q1, [&](int, const float (&out)[4]) { to_red(0, out); });
+            gemv_run<RING_QKV, false, false, MAXB == 1>(a.qkv, run1, xa, B, R1, q1, [&](int, const float (&out)[4]) { to_red(0, out); });
         stamp_done(7);
         __syncthreads();
         for (int i = tid; i < B * 32; i += NTHR) {
@@ -733,7 +733,7 @@ __global__ void __launch_bounds__(NTHR) decode_fused_kernel(DecodeFusedArgs a) {
         stamp_done(19);
         const GemvAct xa{xs - klo, ldx, c64 - ka3 * GEMV_ROWS, nullptr, zero64};
         if (run3.ka < run3.kz)
-            gemv_run<RING_O, false, false>(a.o, run3, xa, B, R3, q3, [&](int, const float (&out)[4]) { to_red(0, out); });
+            gemv_run<RING_O, false, false, MAXB == 1>(a.o, run3, xa, B, R3, q3, [&](int, const float (&out)[4]) { to_red(0, out); });
         stamp_done(20);
         __syncthreads();
         stamp_done(21);
@@ -759,7 +759,7 @@ __global__ void __launch_bounds__(NTHR) decode_fused_kernel(DecodeFusedArgs a) {
         clear_red();
         const GemvAct xa{xs, ldx, c64, nullptr, zero64};
         if (run4.ka < run4.kz)
-            gemv_run<RING, false, false>(a.gu, run4, xa, B, R4, q4,
+            gemv_run<RING, false, false, MAXB == 1>(a.gu, run4, xa, B, R4, q4,
                                          [&](int t, const float (&out)[4]) { to_red(t - ta4, out); });
         stamp_done(13);
         __syncthreads();
@@ -796,7 +796,7 @@ __global__ void __launch_bounds__(NTHR) decode_fused_kernel(DecodeFusedArgs a) {
         __syncthreads();
         const GemvAct xa{xs - klo, ldx, c64 - ka5 * GEMV_ROWS, nullptr, zero64};
         if (run5.ka < run5.kz)
-            gemv_run<RING, false, false>(a.down, run5, xa, B, R5, q5, [&](int, const float (&out)[4]) { to_red(0, out); });
+            gemv_run<RING, false, false, MAXB == 1>(a.down, run5, xa, B, R5, q5, [&](int, const float (&out)[4]) { to_red(0, out); });
         stamp_done(15);
         __syncthreads();
         if (s5 > 0) {

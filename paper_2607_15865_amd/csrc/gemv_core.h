@@ -232,7 +232,13 @@ __device__ __forceinline__ float gzero(uint32_t v) {
 //
 // The walk is rounded up to a multiple of D tiles; the steps past the end do
 // no arithmetic, but every step refills its slot (past the end with the
-// run's first tile) so that no load sits under a branch.
+// run's first tile) so that no load sits under a branch.  With DRAIN (the
+// persistent decode) no tile past the end is requested and the run returns
+// with all its loads complete.  A wave's memory counter counts loads and
+// stores together, in issue order, so a load still in flight when the wave
+// stores its results would make any later wait that covers it (the wait
+// before the ring's registers are reused) also wait for those stores to
+// complete.
 //
 // The 8- and 16-bit formats (WF) take the same activations x'.  INT8: the B
 // fragment pairs are 0x64 | code = 1024 + q at k % 8 in {0, 1, 4, 5} and
@@ -241,7 +247,7 @@ __device__ __forceinline__ float gzero(uint32_t v) {
 // tile's sum of x (E + 16 O over its two 32-k segments): one correction per
 // output with the column's zero point.  F16: the divided elements' weights
 // are held times 16, so the product is the exact-weight sum (scale 1).
-template <int D, bool ZP, bool G32, typename Emit, int WF = WF_INT4>
+template <int D, bool ZP, bool G32, bool DRAIN = false, typename Emit, int WF = WF_INT4>
 __device__ __forceinline__ void gemv_run(const DevLinear& W, const Run& run, const GemvAct& xa, int B,
                                          TileRing<D, G32, WF>& R, RunCursor& q, Emit&& emit) {
     const int lane = threadIdx.x & 63, h = lane >> 5;
@@ -332,8 +338,13 @@ __device__ __forceinline__ void gemv_run(const DevLinear& W, const Run& run, con
                 }
             }
             // refill the slot with tile base + u + D (or the first tile)
-            ring_load<D, ZP, G32, WF>(W, R, u, base + u + D < n ? q : first);
+            if constexpr (DRAIN) {
+                if (base + u + D < n) ring_load<D, ZP, G32, WF>(W, R, u, q);
+            } else {
+                ring_load<D, ZP, G32, WF>(W, R, u, base + u + D < n ? q : first);
+            }
             q.next(W, run);
         }
     }
+    if constexpr (DRAIN) __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
 }
