@@ -729,7 +729,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU: the layer's single-GPU kernels; --gpus {args.gpus} is not supported "
-              "(multi-GPU sharding is described in DESIGN.md, not built)", file=sys.stderr)
+              "(the path runs on one GPU; sharding it over several is not built)", file=sys.stderr)
         sys.exit(2)
 
     if args.copy_calibration:
