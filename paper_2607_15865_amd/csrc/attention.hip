@@ -165,11 +165,14 @@ __global__ void __launch_bounds__(64 * PF_MAXHB) attn_prefill_kernel(AttnPrefill
             }
             mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
             const float m_new = fmaxf(m, mt);
-            const float alpha = (m_new == -INFINITY) ? 1.f : exp2f(m - m_new);
+            // (while every key so far is masked, m_new is -inf: the weights
+            // and alpha are then 0, and o and l are still 0)
+            const float mb = m_new == -INFINITY ? 0.f : m_new;
+            const float alpha = exp2_hw(m - mb);
             float ls = 0.f;
 #pragma unroll
             for (int e = 0; e < 32; e++) {
-                p[e] = (p[e] == -INFINITY) ? 0.f : exp2f(p[e] - m_new);
+                p[e] = exp2_hw(p[e] - mb);
                 ls += p[e];
             }
             l = l * alpha + ls;

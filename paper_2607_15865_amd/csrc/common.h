@@ -205,6 +205,12 @@ __device__ __forceinline__ bf16x2 as_bf16x2(uint32_t u) {
 
 __device__ __forceinline__ float silu(float z) { return z / (1.0f + __expf(-z)); }
 
+// 2^x on the hardware exponential (v_exp_f32).  The library exp2f adds a
+// rescaling step that keeps results below 2^-126 exact as denormals; the
+// softmax weights that small add nothing to sums whose largest term is 1.
+// exp2_hw(-inf) = 0.
+__device__ __forceinline__ float exp2_hw(float x) { return __builtin_amdgcn_exp2f(x); }
+
 // wave-level reductions (64 lanes): DPP within each row of 16 lanes (swap
 // lane pairs, swap pairs of pairs, mirror within 8, mirror within 16), then
 // the four row results are read from lanes 0, 16, 32 and 48.
