@@ -192,12 +192,14 @@ __global__ void __launch_bounds__(64 * PF_MAXHB) attn_prefill_kernel(AttnPrefill
                     phi[j] = hi;
                     plo[j] = (__bf16)(pv - (float)hi);
                 }
-                const int key0 = 16 * ks + 8 * h;       // this lane's 8 keys of the group
+                // this lane's 8 keys 16 ks + 8 h .. + 7, dim i * 32 + c, by two
+                // transposing reads: lane s of its 16-lane group points at key
+                // 16 ks + 8 h + s / 4 (+ 4), dims 16 (c / 16) + 4 (s % 4) .. + 3
+                const __bf16* vrow = V + (16 * ks + 8 * h + ((lane & 15) >> 2)) * D + 16 * (c >> 4) + 4 * (lane & 3);
 #pragma unroll
                 for (int i = 0; i < D / 32; i++) {
-                    bf16x8 vf;
-#pragma unroll
-                    for (int j = 0; j < 8; j++) vf[j] = V[(key0 + j) * D + i * 32 + c];
+                    const i16x4 v0 = lds_read_tr16(vrow + i * 32), v1 = lds_read_tr16(vrow + 4 * D + i * 32);
+                    const bf16x8 vf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7));
                     o[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, phi, o[i], 0, 0, 0);
                     o[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, plo, o[i], 0, 0, 0);
                 }

@@ -39,6 +39,19 @@ typedef _Float16 f16;
 typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+
+// Transposing LDS read (gfx950 ds_read_b64_tr_b16).  In each group of 16
+// lanes, source lane s reads the four 16-bit values at its own address p_s;
+// output lane t receives, as element k, value t % 4 of source lane
+// 4 k + t / 4.  So when lane s of a group points at row r0 + s / 4, columns
+// c0 + 4 (s % 4) .. + 3 of a row-major 16-bit matrix, output lane t holds
+// column c0 + t of rows r0 .. r0 + 3: a column segment, as the MFMA takes
+// its operand.  p: 8-byte aligned, in LDS.
+__device__ __forceinline__ i16x4 lds_read_tr16(const void* p) {
+    return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (__attribute__((address_space(3))) i16x4*)(const_cast<void*>(p)));
+}
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
