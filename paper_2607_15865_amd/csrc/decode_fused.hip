@@ -579,9 +579,10 @@ __global__ void __launch_bounds__(NTHR) decode_fused_kernel(DecodeFusedArgs a) {
                 mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
                 bf16x8 phi, plo;
                 float ls = 0.f;
+                const float mb = mx == -INFINITY ? 0.f : mx;     // (every key masked: all weights 0)
 #pragma unroll
                 for (int e = 0; e < 8; e++) {
-                    const float pv = (mx == -INFINITY) ? 0.f : exp2f(sv[e] - mx);
+                    const float pv = exp2_hw(sv[e] - mb);
                     ls += pv;
                     const __bf16 hi = (__bf16)pv;
                     phi[e] = hi;
@@ -591,18 +592,18 @@ __global__ void __launch_bounds__(NTHR) decode_fused_kernel(DecodeFusedArgs a) {
                 ls += __shfl_xor(ls, 32, 64);
                 // O^T += V^T P^T per 16-dim block: lane (n16, q4) holds V of keys
                 // 8 q4 .. + 7, dim 16 db + n16 (16-bit reads of the V stage)
-                const uint16_t* Vw = reinterpret_cast<const uint16_t*>(Vst + (size_t)(32 * gw + 8 * q4) * D * 2);
+                // (two transposing reads: lane n16 of its group points at key
+                // 8 q4 + n16 / 4 (+ 4), dims 16 db + 4 (n16 % 4) .. + 3, in
+                // their swizzled chunk)
+                const uint16_t* Vw = reinterpret_cast<const uint16_t*>(Vst + (size_t)(32 * gw + 8 * q4 + (n16 >> 2)) * D * 2);
                 const int nb = D / 16 / ns;
 #pragma unroll
                 for (int d0 = 0; d0 < D / 16; d0++) {
                     if (d0 >= nb) break;
                     const int db = part * nb + d0;
-                    const int pos = ((((2 * db + (n16 >> 3)) ^ (2 * q4)) << 3) | (n16 & 7));
-                    u32x4 vw;
-#pragma unroll
-                    for (int j = 0; j < 4; j++)
-                        vw[j] = (uint32_t)Vw[2 * j * D + pos] | ((uint32_t)Vw[(2 * j + 1) * D + pos] << 16);
-                    const bf16x8 vf = __builtin_bit_cast(bf16x8, vw);
+                    const int off = (((2 * db + ((n16 & 3) >> 1)) ^ (2 * q4)) << 3) | (4 * (n16 & 1));
+                    const i16x4 v0 = lds_read_tr16(Vw + off), v1 = lds_read_tr16(Vw + 4 * D + off);
+                    const bf16x8 vf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7));
                     f32x4 o = f32x4{0.f, 0.f, 0.f, 0.f};
                     o = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, phi, o, 0, 0, 0);
                     o = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, plo, o, 0, 0, 0);
