@@ -154,43 +154,53 @@ __global__ void __launch_bounds__(64 * PF_MAXHB) attn_prefill_kernel(AttnPrefill
             const int kbase = k0 + st * PF_KST;
             const bool diag = kbase + PF_KST - 1 > a.L + q0;
             float p[32];
+#pragma unroll
+            for (int e = 0; e < 32; e++) p[e] = (e < 16 ? sa[e] : sb[e - 16]) * a.scale_log2;
+            if (diag) {            // (only the stages that straddle the diagonal)
+#pragma unroll
+                for (int e = 0; e < 32; e++) {
+                    const int kslot = kbase + 32 * (e / 16) + 16 * ((e % 16) / 8) + 8 * h + (e % 8);
+                    if (kslot > qslot) p[e] = -INFINITY;
+                }
+            }
             float mt = -INFINITY;
 #pragma unroll
-            for (int e = 0; e < 32; e++) {
-                const int kslot = kbase + 32 * (e / 16) + 16 * ((e % 16) / 8) + 8 * h + (e % 8);
-                float v = (e < 16 ? sa[e] : sb[e - 16]) * a.scale_log2;
-                if (diag && kslot > qslot) v = -INFINITY;
-                p[e] = v;
-                mt = fmaxf(mt, v);
-            }
+            for (int e = 0; e < 32; e++) mt = fmaxf(mt, p[e]);
             mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
             const float m_new = fmaxf(m, mt);
-            // (while every key so far is masked, m_new is -inf: the weights
-            // and alpha are then 0, and o and l are still 0)
-            const float mb = m_new == -INFINITY ? 0.f : m_new;
-            const float alpha = exp2_hw(m - mb);
+            // The running max m moves (and o, l are rescaled) only when some
+            // lane's scores pass it by more than 8 (log2 units); until then the
+            // weights are taken against the older m and stay below 2^8, which
+            // the hi + lo split of P carries as well as weights below 1.  While
+            // every key so far is masked, m is -inf and the weights are 0.
+            if (__builtin_amdgcn_ballot_w64(m_new > m + 8.0f) != 0) {
+                const float alpha = exp2_hw(m - (m_new == -INFINITY ? 0.f : m_new));
+                l *= alpha;
+#pragma unroll
+                for (int i = 0; i < D / 32; i++)
+#pragma unroll
+                    for (int e = 0; e < 16; e++) o[i][e] *= alpha;
+                m = m_new;
+            }
+            const float mb = m == -INFINITY ? 0.f : m;
             float ls = 0.f;
 #pragma unroll
             for (int e = 0; e < 32; e++) {
                 p[e] = exp2_hw(p[e] - mb);
                 ls += p[e];
             }
-            l = l * alpha + ls;
-            m = m_new;
-#pragma unroll
-            for (int i = 0; i < D / 32; i++)
-#pragma unroll
-                for (int e = 0; e < 16; e++) o[i][e] *= alpha;
+            l += ls;
             // O^T += V^T P^T over the 4 key groups of 16 (tile, step)
 #pragma unroll
             for (int ks = 0; ks < 4; ks++) {
                 bf16x8 phi, plo;
 #pragma unroll
-                for (int j = 0; j < 8; j++) {
-                    const float pv = p[8 * ks + j];
-                    const __bf16 hi = (__bf16)pv;
-                    phi[j] = hi;
-                    plo[j] = (__bf16)(pv - (float)hi);
+                for (int j = 0; j < 8; j += 2) {          // pairs: one packed conversion each
+                    const bf16x2 hi = __builtin_convertvector(f32x2{p[8 * ks + j], p[8 * ks + j + 1]}, bf16x2);
+                    const bf16x2 lo = __builtin_convertvector(
+                        f32x2{p[8 * ks + j] - (float)hi[0], p[8 * ks + j + 1] - (float)hi[1]}, bf16x2);
+                    phi[j] = hi[0]; phi[j + 1] = hi[1];
+                    plo[j] = lo[0]; plo[j + 1] = lo[1];
                 }
                 // this lane's 8 keys 16 ks + 8 h .. + 7, dim i * 32 + c, by two
                 // transposing reads: lane s of its 16-lane group points at key
