@@ -41,6 +41,8 @@
 
 namespace {
 
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
 __device__ __forceinline__ int key_perm(int r) {  // swap bits 2 and 3
     return (r & ~12) | ((r & 4) << 1) | ((r & 8) >> 1);
 }

@@ -40,7 +40,6 @@ typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
-typedef float f32x2 __attribute__((ext_vector_type(2)));
 
 // Transposing LDS read (gfx950 ds_read_b64_tr_b16).  In each group of 16
 // lanes, source lane s reads the four 16-bit values at its own address p_s;
