@@ -1086,7 +1086,9 @@ int layer_create(const layer_config* cfg, const layer_weights_host* w, layer_t* 
             };
             if (L->qkv.d.N_dev / 32 <= cus && L->o.d.N_dev / 32 <= cus && L->down.d.N_dev / 32 <= cus) {
                 L->S_qkv = parts(L->qkv.d);
-                L->S_o = parts(L->o.d);
+                // o_proj stays whole: its sums go to every block (the RMSNorm of
+                // h needs all of them), and a second k part doubles that hand-off
+                L->S_o = 1;
                 L->S_down = parts(L->down.d);
                 std::vector<int> tab((size_t)cus * 16);
                 decode_fused_plan(cus, L->qkv.d, L->o.d, L->gu.d, L->down.d, L->S_qkv, L->S_o, L->S_down, tab.data());
