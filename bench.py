@@ -43,7 +43,7 @@ TRAFFIC = {
     "prefill_gate_up": {"bytes": 134249614,
                        "sha256": "3119df97525e1e8e7c849f973de5815f75236794bdbda82d2c4454db805300fa"},
     "decode_fused": {"bytes": 129672696,
-                    "sha256": "ba82fc2613a0800e0e30794c72163adf64368c3ab9f100dfcc687a008779776a"},
+                    "sha256": "3d35689a326b5e48b71fe0481fe5ed4a457dbe11ac9d1e3ee02ad2ce89ecc927"},
 }
 CSRC = os.path.join(ROOT, "paper_2607_15865_amd", "csrc")
 

@@ -13,13 +13,14 @@
 // from memory to LDS (direct-to-LDS loads), double buffered: one memory round
 // trip per 64 keys, one barrier.  K rows are 16-byte-chunk XOR-swizzled by
 // row (conflict-free fragment reads); V stays in its natural [key][dim]
-// layout and the V^T fragments of O^T = V^T P^T are gathered with 16-bit LDS
-// reads.  Scores are formed transposed, S^T = K Q^T, with the 32 key rows
+// layout and the V^T fragments of O^T = V^T P^T come from it by transposing
+// LDS reads (lds_read_tr16).  Scores are formed transposed, S^T = K Q^T, with the 32 key rows
 // of a tile fed in a permuted order (bits 2 and 3 of the row index swapped)
 // so that register e of the score tile holds key 16*(e/8) + 8*(lane/32) +
 // e%8 of query lane%32: exactly the operand layout of P^T.  Every lane
 // therefore owns one query: the online softmax (running max and sum) lives
-// in registers and is updated once per 64 keys.  P is fed to the MFMA as a
+// in registers; the max moves only when a score passes it by more than 8
+// (log2 units), so the weights stay below 2^8.  P is fed to the MFMA as a
 // bf16 pair hi + lo (P - hi), which keeps P V at near-fp32 accuracy.  The
 // causal mask is computed from indices, only on tiles that straddle the
 // diagonal; tiles past it are never visited (the role the paper's small

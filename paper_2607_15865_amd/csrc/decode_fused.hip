@@ -591,7 +591,7 @@ __global__ void __launch_bounds__(NTHR) decode_fused_kernel(DecodeFusedArgs a) {
                 ls += __shfl_xor(ls, 16, 64);
                 ls += __shfl_xor(ls, 32, 64);
                 // O^T += V^T P^T per 16-dim block: lane (n16, q4) holds V of keys
-                // 8 q4 .. + 7, dim 16 db + n16 (16-bit reads of the V stage)
+                // 8 q4 .. + 7, dim 16 db + n16
                 // (two transposing reads: lane n16 of its group points at key
                 // 8 q4 + n16 / 4 (+ 4), dims 16 db + 4 (n16 % 4) .. + 3, in
                 // their swizzled chunk)
