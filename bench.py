@@ -849,6 +849,25 @@ def main():
                    "gbps": round(by_d / dec_s / 1e9, 1),
                    "frac_hbm": round(by_d / dec_s / 1e9 / PEAK_HBM_GBS, 4)},
     }
+    # the same decode step run back to back over the rotating layer copies
+    # (as a stack's layers run): one event pair around the whole run, so no
+    # per-launch event or dispatch gap is counted; outside the timed steps
+    nb2b = 8 * len(layers)
+    torch.cuda.synchronize()
+    b0, b1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    b0.record(stream)
+    for i in range(nb2b):
+        k, v = caches[i % len(layers)]
+        binding.check(binding.layer_decode(layers[i % len(layers)].handle, xd, pd, cd, ctx, None, Bd, k, v, yd,
+                                           ws, ws_bytes, sp))
+    b1.record(stream)
+    torch.cuda.synchronize()
+    b2b_us = b0.elapsed_time(b1) * 1e3 / nb2b
+    for lay in layers:
+        flags |= lay.error()
+    stages["decode"]["back_to_back"] = {"us": round(b2b_us, 2), "layer_steps_per_s": round(1e6 / b2b_us, 1),
+                                        "frac_hbm": round(by_d / (b2b_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4),
+                                        "calls": nb2b}
     gu_flop = 2.0 * Tp * cfg.hidden * 2 * cfg.ffn
     gu_avg = gu_ms / max(gu_n, 1)
     roofline = {"kernel": "prefill gate/up W4 GEMM (512 x 28672 x 4096, SwiGLU epilogue)",
