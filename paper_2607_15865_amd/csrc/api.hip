@@ -275,8 +275,7 @@ struct layer_s {
     Profiler prof;
     // persistent decode: error flag and optional per-block time stamps (zeroed)
     DevBuf sync;
-    DevBuf fplan;                 // work table of the persistent decode (decode_fused_plan)
-    int fplan_blocks = 0, S_qkv = 1, S_o = 1, S_down = 1;
+    int fused_blocks = 0, S_qkv = 1, S_o = 1, S_down = 1;   // persistent decode: blocks, k parts
     int num_cus = 256;
     int* err = nullptr;
     unsigned long long* stamps = nullptr;
@@ -487,7 +486,7 @@ FusedPlan plan_fused(const layer_s* L, int B, int max_ctx, bool query_device) {
         p.nblocks = cus;
     }
     const int P = p.nblocks;
-    if (P > kMaxBlocks || r > MAXR || P != L->fplan_blocks) return p;
+    if (P > kMaxBlocks || r > MAXR || P != L->fused_blocks) return p;
     const int gu_pairs = L->gu.d.N_dev / 64;                                 // whole gate/up pairs per block
     p.slots = 2 * std::max(1, (gu_pairs + P - 1) / P);
     if (p.slots > 8) return p;
@@ -651,7 +650,6 @@ int launch_fused(layer_s* L, const FusedPlan& fp, const float* x, const int32_t*
     a.err = L->err;
     a.stamps = L->decode_trace ? L->stamps : nullptr;
     a.S_qkv = fp.S_qkv; a.S_o = fp.S_o; a.S_down = fp.S_down;
-    a.plan = (const int*)L->fplan.p;
     a.comb_per = fp.comb_per; a.comb_lpv = fp.comb_lpv;
     a.slots = fp.slots;
     a.gam_lds = fp.gam_lds;
@@ -1072,7 +1070,7 @@ int layer_create(const layer_config* cfg, const layer_weights_host* w, layer_t* 
         L->err = (int*)L->sync.p;
         L->stamps = (unsigned long long*)((char*)L->sync.p + 64);
     }
-    // work table of the persistent decode: one block per CU; a product with
+    // work split of the persistent decode: one block per CU; a product with
     // fewer column tiles than blocks is also cut along k (at most 2 parts)
     {
         int dev = 0, cus = 0;
@@ -1090,10 +1088,7 @@ int layer_create(const layer_config* cfg, const layer_weights_host* w, layer_t* 
                 // h needs all of them), and a second k part doubles that hand-off
                 L->S_o = 1;
                 L->S_down = parts(L->down.d);
-                std::vector<int> tab((size_t)cus * 16);
-                decode_fused_plan(cus, L->qkv.d, L->o.d, L->gu.d, L->down.d, L->S_qkv, L->S_o, L->S_down, tab.data());
-                if ((rc = upload(L->fplan, tab.data(), tab.size() * 4))) { delete L; return rc; }
-                L->fplan_blocks = cus;
+                L->fused_blocks = cus;
             }
         }
     }

@@ -33,9 +33,8 @@ struct DecodeFusedArgs {
     int spin_max;              // polls per thread per launch before a wait gives up
     int* err;                  // the layer's error flag: W4_FLAG_WAIT_TIMEOUT, W4_FLAG_F16_RANGE
     unsigned long long* stamps;  // wall-clock stamps or null
-    // work split
-    const int* plan;           // per block: 16 ints (decode_fused_plan)
-    int S_qkv, S_o, S_down;    // k-parts per column tile
+    // work split (each block derives its share from these and its index)
+    int S_qkv, S_o, S_down;    // k-parts per column tile (1 or 2)
     int comb_per, comb_lpv;    // attention outputs combined per block, lanes per output
     int slots;                 // column tiles per block in one product (LDS partial slots)
     int chunk, nchunk;         // attention keys per unit, units per (row, kv head)
@@ -50,14 +49,6 @@ struct DecodeFusedArgs {
 };
 
 int launch_decode_fused(const DecodeFusedArgs& a, hipStream_t stream);
-// Work table of the persistent decode for nblocks blocks, 16 ints per block:
-//   [0..3]   q/k/v:  column tile (-1: none), k-tile range [ka, kz), k-part s
-//   [4..7]   o_proj: the same
-//   [8..9]   gate/up: column tile range [t0, t1) (whole gate/up pairs)
-//   [10..13] down:   column tile, k-tile range, k-part
-// S_* are the k-parts per column tile of the three products.
-void decode_fused_plan(int nblocks, const DevLinear& qkv, const DevLinear& o, const DevLinear& gu,
-                       const DevLinear& down, int S_qkv, int S_o, int S_down, int* out);
 // Blocks of the persistent launch (one per CU) or 0 if it cannot be resident.
 int decode_fused_blocks(int head_dim, int B, size_t lds_bytes);
 // Largest attention chunk (keys per unit) the kernel supports for head_dim.

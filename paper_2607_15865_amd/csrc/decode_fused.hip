@@ -271,15 +271,32 @@ __global__ void __launch_bounds__(NTHR) decode_fused_kernel(DecodeFusedArgs a) {
     };
     stamp_done(5);
 
-    // ---- this block's work (host plan): column tiles and k ranges per product.
-    // The row is read once, through the scalar cache (the table is read-only):
-    // a vector load here would wait behind the weight prefetches in flight.
+    // ---- this block's work: column tiles and k ranges per product, computed
+    // here (a table in memory would put a dependent load before the first
+    // weight request).  pl[0..3] q/k/v, pl[4..7] o_proj: column tile (-1:
+    // none), k-tile range [ka, kz), k part; pl[8..9] gate/up: column tiles
+    // [t0, t1) (whole gate/up pairs); pl[10..13] down.  A product of nt column
+    // tiles cut into S k parts (S <= 2) gives block blk tile blk / S, part
+    // blk % S, if blk < nt S.
+    static_assert(MAXS == 2, "k parts: 1 or 2");
     int pl[16];
     {
-        const __attribute__((address_space(4))) int* row =
-            (const __attribute__((address_space(4))) int*)(a.plan + blk * 16);
-#pragma unroll
-        for (int i = 0; i < 16; i++) pl[i] = row[i];
+        auto part = [&](const DevLinear& W, int S, int* e) {
+            const int nt = W.N_dev / 32, kb = W.K_pad / 64;
+            const bool on = blk < nt * S;
+            const int s = S == 1 ? 0 : blk & 1;
+            e[0] = on ? (S == 1 ? blk : blk >> 1) : -1;
+            e[1] = on ? s * kb / S : 0;
+            e[2] = on ? (s + 1) * kb / S : 0;
+            e[3] = on ? s : 0;
+        };
+        part(a.qkv, a.S_qkv, pl);
+        part(a.o, a.S_o, pl + 4);
+        const unsigned np = (unsigned)a.gu.N_dev / 64;
+        pl[8] = 2 * (int)((unsigned)blk * np / (unsigned)P);
+        pl[9] = 2 * (int)((unsigned)(blk + 1) * np / (unsigned)P);
+        part(a.down, a.S_down, pl + 10);
+        pl[14] = pl[15] = 0;
     }
     const int Nq = a.qkv.N_dev;
     // this wave's run of product ph (1 q/k/v, 3 o_proj, 4 gate/up, 5 down)
@@ -838,29 +855,6 @@ int launch_t(const DecodeFusedArgs& a, hipStream_t stream) {
 
 }  // namespace
 
-void decode_fused_plan(int P, const DevLinear& qkv, const DevLinear& o, const DevLinear& gu, const DevLinear& down,
-                       int S_qkv, int S_o, int S_down, int* out) {
-    auto part = [&](int blk, const DevLinear& W, int S, int* e) {
-        const int nt = W.N_dev / 32, kb = W.K_pad / 64;
-        if (blk >= nt * S) { e[0] = -1; e[1] = e[2] = e[3] = 0; return; }
-        const int t = blk / S, s = blk % S;
-        e[0] = t;
-        e[1] = s * kb / S;
-        e[2] = (s + 1) * kb / S;
-        e[3] = s;
-    };
-    const int np = gu.N_dev / 64;
-    for (int blk = 0; blk < P; blk++) {
-        int* e = out + (size_t)blk * 16;
-        part(blk, qkv, S_qkv, e);
-        part(blk, o, S_o, e + 4);
-        e[8] = 2 * (int)((long long)blk * np / P);
-        e[9] = 2 * (int)((long long)(blk + 1) * np / P);
-        part(blk, down, S_down, e + 10);
-        e[14] = e[15] = 0;
-    }
-}
-
 int decode_fused_max_chunk(int) { return 256; }   // 8 key groups
 
 int decode_fused_blocks(int head_dim, int B, size_t lds_bytes) {
@@ -883,6 +877,7 @@ int decode_fused_blocks(int head_dim, int B, size_t lds_bytes) {
 
 int launch_decode_fused(const DecodeFusedArgs& a, hipStream_t stream) {
     if (a.B > 4 || a.S_qkv > MAXS || a.S_o > MAXS || a.S_down > MAXS) return -1;
+    if (a.S_qkv < 1 || a.S_o < 1 || a.S_down < 1 || a.nblocks < 1) return -1;
     if (a.shared ? (a.ctx_lens != nullptr || a.sb != 0 || a.ctx_base < 0) : a.ctx_lens == nullptr) return -1;
     if (a.slots < 1 || (a.B == 1 && !a.gam_lds)) return -1;
     if (a.chunk < 1 || a.chunk > decode_fused_max_chunk(a.d) || a.nkv < 1 || a.nq % a.nkv || a.nq / a.nkv > MAXR)
