@@ -102,17 +102,19 @@ __global__ void __launch_bounds__(64) argmax_final_kernel(const float* __restric
 }
 
 // The guard after a greedy pick: if any of the error words is non-zero,
-// every pick of the step becomes -1.
+// every pick of the step becomes -1.  Lane i reads word i (all in one memory
+// round trip) and the wave ORs them.
+constexpr int kGuardFlags = 64;
 struct FlagList {
-    const int* p[32];
+    const int* p[kGuardFlags];
     int n;
 };
 
 __global__ void __launch_bounds__(64) pick_guard_kernel(FlagList f, int32_t* __restrict__ next, int B) {
-    int any = 0;
-    for (int i = 0; i < f.n; i++) any |= f.p[i][0];
-    if (any)
-        for (int b = threadIdx.x; b < B; b += 64) next[b] = -1;
+    const int lane = threadIdx.x;
+    const int v = lane < f.n ? f.p[lane][0] : 0;
+    if (__ballot(v != 0) == 0) return;
+    for (int b = lane; b < B; b += 64) next[b] = -1;
 }
 
 }  // namespace
@@ -135,9 +137,9 @@ int launch_argmax(const float* logits, int B, int V, float* pv, int* pi, int32_t
 }
 
 int launch_pick_guard(const int* const* flags, int n, int32_t* next, int B, hipStream_t stream) {
-    for (int i0 = 0; i0 < n; i0 += 32) {
+    for (int i0 = 0; i0 < n; i0 += kGuardFlags) {
         FlagList f{};
-        f.n = n - i0 < 32 ? n - i0 : 32;
+        f.n = n - i0 < kGuardFlags ? n - i0 : kGuardFlags;
         for (int i = 0; i < f.n; i++) f.p[i] = flags[i0 + i];
         hipLaunchKernelGGL(pick_guard_kernel, dim3(1), dim3(64), 0, stream, f, next, B);
     }
