@@ -208,8 +208,18 @@ gemm_w4_kernel(const f16* __restrict__ X, int ldx, DevLinear W, EpiArgs ep, Gemm
     const uint32_t woff0 = (uint32_t)(wave_on ? nt0 : 0) * (uint32_t)KB * TB + (uint32_t)lane * 16u;
     const uint32_t wcol1 = (uint32_t)KB * TB;
     const char* const Rb = reinterpret_cast<const char*>(W.ratios);
+    // FS (INT4, 128-row tiles, SwiGLU and residual epilogues): a weight
+    // fragment is multiplied by its group's fp16 scale (4 packed multiplies,
+    // which the fragment's 8 MFMAs share) instead of the accumulators by the
+    // running ratio at each group boundary (128 multiplies per group); the
+    // product (q - z) s is rounded to fp16.  With fewer row tiles a fragment
+    // serves fewer MFMAs and the ratio costs less, so those keep it; so does
+    // the q/k/v GEMM, whose exact sums decide the bf16 rounding of the
+    // cached keys and values.
+    constexpr bool FS = WF == WF_INT4 && TM == 4 && EPI != EPI_QKV;
     u32x4 rw[4 * NG][NQ];
     float rr[4 * NG][NH];
+    f16 rs[4 * NG][NH];
     uint32_t rz[4 * NG][NH];
     auto load_w = [&](int q, int kb) __attribute__((always_inline)) {
         const int kk = kb < kb_hi ? kb : kb_lo;
@@ -220,7 +230,8 @@ gemm_w4_kernel(const f16* __restrict__ X, int ldx, DevLinear W, EpiArgs ep, Gemm
 #pragma unroll
         for (int hh = 0; hh < NH; hh++) {
             const uint32_t gi = (uint32_t)((kk * 64 + 32 * hh) >> W.lgG) * (uint32_t)W.N_dev + (uint32_t)col;
-            rr[q][hh] = *reinterpret_cast<const float*>(Rb + gi * 4u);
+            if constexpr (FS) rs[q][hh] = __builtin_bit_cast(f16, W.scales[gi]);
+            else rr[q][hh] = *reinterpret_cast<const float*>(Rb + gi * 4u);
             if (ZP) rz[q][hh] = (uint32_t)W.zeros[gi];
         }
     };
@@ -231,6 +242,7 @@ gemm_w4_kernel(const f16* __restrict__ X, int ldx, DevLinear W, EpiArgs ep, Gemm
     // iteration it + 2 from the start of iteration it on).
     float rn[2][2];
     auto load_rn = [&](int slot, int kb) __attribute__((always_inline)) {
+        if constexpr (FS) return;
         const int kk = kb < kb_hi ? kb : kb_lo;
         const uint32_t g0 = (uint32_t)((kk * 64) >> W.lgG) * (uint32_t)W.N_dev;
         rn[slot][0] = *reinterpret_cast<const float*>(Rb + (g0 + (uint32_t)col0) * 4u);
@@ -274,6 +286,11 @@ gemm_w4_kernel(const f16* __restrict__ X, int ldx, DevLinear W, EpiArgs ep, Gemm
             } else {
                 b[p][0] = dequant8(rw[q][0][s], zo0, dq);
                 b[p][1] = dequant8(rw[q + 1][0][s], zo1, dq);
+                if constexpr (FS) {
+                    const f16 s0 = rs[q][hh], s1 = rs[q + 1][hh];
+                    b[p][0] = b[p][0] * f16x8{s0, s0, s0, s0, s0, s0, s0, s0};
+                    b[p][1] = b[p][1] * f16x8{s1, s1, s1, s1, s1, s1, s1, s1};
+                }
             }
         };
         // After step t, if step t + 1 (step 0 of the next iteration for
@@ -292,7 +309,7 @@ gemm_w4_kernel(const f16* __restrict__ X, int ldx, DevLinear W, EpiArgs ep, Gemm
                 acc[i][0] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a[p][i], b[p][0], acc[i][0], 0, 0, 0);
                 acc[i][1] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a[p][i], b[p][1], acc[i][1], 0, 0, 0);
             }
-            if (next_group(t)) {
+            if (!FS && next_group(t)) {
                 const int tn = (t + 1) & 7;                       // the next step
                 const int half = tn >> 2, hh = NH == 2 ? ((tn & 3) >> 1) : 0;
                 const int q = (t == 7 ? qn : qb) + 2 * half;
@@ -367,10 +384,10 @@ gemm_w4_kernel(const f16* __restrict__ X, int ldx, DevLinear W, EpiArgs ep, Gemm
         }
     }
 
-    // ---- scale of the range's last group
+    // ---- scale of the range's last group (1 with fragment scales)
     const int glast = ((kb_hi * 64) - 1) >> W.lgG;
-    const float sl0 = (float)__builtin_bit_cast(f16, W.scales[(size_t)glast * W.N_dev + col0]);
-    const float sl1 = (float)__builtin_bit_cast(f16, W.scales[(size_t)glast * W.N_dev + col1]);
+    const float sl0 = FS ? 1.0f : (float)__builtin_bit_cast(f16, W.scales[(size_t)glast * W.N_dev + col0]);
+    const float sl1 = FS ? 1.0f : (float)__builtin_bit_cast(f16, W.scales[(size_t)glast * W.N_dev + col1]);
 
     // Epilogue of row tile i: v0[e], v1[e] are the sums of columns col0 and
     // col1 for row m0 + 32 i + 8 (e / 4) + 4 h + e % 4.  Every value the
