@@ -156,6 +156,46 @@ def test_wait_timeout_flag_and_sentinel_picks():
     lay.close()
 
 
+def test_sentinel_picks_past_the_first_64_flags():
+    """The pick guard reads up to 64 error words per launch; a model of 70
+    layers needs a second launch.  Only the last layer (the 71st word after
+    the LM's) times out: the picks still turn into -1, and a clean step over
+    the same layers picks valid tokens."""
+    cfg, w = host_layer("tiny")
+    n_layers, V, B, ctx = 70, 1024, 1, 12
+    lays = [binding.Layer(cfg, w) for _ in range(n_layers)]
+    lmh = binding.LM(cfg, synth.make_lm(cfg, V), max_batch=B)
+    caches = [l.new_cache(B, 0) for l in lays]
+    logits = torch.empty(B, V, device="cuda")
+    c = torch.full((B,), ctx, dtype=torch.int32, device="cuda")
+    hs = [l.handle for l in lays]
+    n = binding.model_decode_workspace_size(hs, lmh.handle, B, ctx)
+    ws = torch.empty(n, dtype=torch.uint8, device="cuda")
+
+    def step():
+        tok = torch.from_numpy(synth.tokens(cfg, V, B)).cuda()
+        binding.check(binding.model_decode_greedy(hs, lmh.handle, tok, c, c, ctx, B, [k for k, _ in caches],
+                                                  [v for _, v in caches], logits, tok, ws, n))
+        torch.cuda.synchronize()
+        return tok.cpu().numpy()
+
+    picks = step()
+    assert (picks >= 0).all() and all(l.error() == 0 for l in lays) and lmh.error() == 0
+    binding.check(binding.layer_set_decode_spin_limit(lays[-1].handle, 1))
+    picks = step()
+    log(f"  70 layers, the last one timed out: picks {picks}")
+    assert (picks == -1).all()
+    assert lays[-1].error() & binding.W4_FLAG_WAIT_TIMEOUT
+    assert all(l.error() == 0 for l in lays[:-1])
+    lmh.error()      # (the outputs of the timed-out step are not valid)
+    binding.check(binding.layer_set_decode_spin_limit(lays[-1].handle, 0))
+    picks = step()
+    assert (picks >= 0).all() and lays[-1].error() == 0 and lmh.error() == 0
+    lmh.close()
+    for l in lays:
+        l.close()
+
+
 def test_range_flag_turns_picks_into_minus_one():
     cfg, lay = scaled_layer("attn_norm")
     V, B, ctx = 1024, 1, 10
